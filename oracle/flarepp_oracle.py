@@ -1,0 +1,240 @@
+"""Float64 CPU oracle for the FLARE++ mixer forward.
+
+TEST INFRASTRUCTURE ONLY.  This module is the correctness reference that the
+HIP path is compared against.  Only the tests, the package's ``smoke()`` and
+the CPU-baseline leg of the benchmark may import it; the product path never
+calls it and shares no code with it.
+
+It computes the plain definitions, in float64, in the paper's order:
+
+* ``project``     K = X W per weight, heads are contiguous D-wide column
+                  blocks (Sec. 2.1, Eq. (4); Sec. 2.2, Eqs. (7), (9)).
+* ``sdpa``        rectangular scaled dot-product attention, softmax over the
+                  keys, scale 1/sqrt(D) (Sec. 2.1, Eq. (3)).  Also returns the
+                  row log-normaliser L = logsumexp of the scaled scores
+                  (App. A.2, Eq. (20)).
+* ``mixer_forward`` project; Q = SDPA(Q~, K~, V~) (Eq. (8));
+                  Z = SDPA(Q, K, V) (Eq. (10)); Y = SDPA(K, Q, Z) (Eq. (11));
+                  heads merged and multiplied by W_O (Sec. 2.1 after Eq. (2);
+                  Fig. 1 "merge(Y) @ Wo").
+* ``split_merge`` the exact split-key merge of partial results
+                  (App. A.2, Eqs. (22)-(23); stable form App. A.3,
+                  Eqs. (24)-(28), including the empty-row convention).
+* ``materialised_operator`` W_eff = W_dec W_enc per head (Sec. 2.1, Eq. (6);
+                  Sec. 2.2, Eq. (12)), for small N only.
+
+Readings of points the paper leaves open (all fixed here, in the same way as
+in the input generator):
+
+* head h owns channels [h D, (h+1) D) of every projection;
+* weights are [C_in][C_out] and applied as X @ W; there are no biases;
+* the scale is 1/sqrt(D) in all three calls, including the decode whose keys
+  are the M routes;
+* seeds are shared across the batch; Q(X) is per batch element;
+* an empty key set gives L = -inf and a zero output (App. A.3).
+
+The softmax over a long key axis is evaluated in key chunks as a plain
+two-pass computation (pass 1: the exact row maximum; pass 2: exponentials,
+their sum and the weighted sum of values).  Chunking only bounds memory; the
+arithmetic is the textbook max-shifted softmax.
+
+Every function here is pinned by CPU tests against facts independent of this
+code (closed forms, brute force, a library SDPA, the structural invariants the
+paper states); no function is "parity unpinned".
+"""
+
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+__all__ = [
+    "project",
+    "sdpa",
+    "mixer_forward",
+    "flare_forward",
+    "split_merge",
+    "partial_encode",
+    "materialised_operator",
+    "merge_heads",
+]
+
+# Key chunk for the two-pass softmax and query chunk for independent rows;
+# only bounds memory.
+_KEY_CHUNK = 8192
+_QUERY_CHUNK = 16384
+
+
+def _f64(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64)
+
+
+def project(X: np.ndarray, W: np.ndarray, H: int) -> np.ndarray:
+    """Head-split projection ``X W`` (Sec. 2.1, Eq. (4); Sec. 2.2, Eq. (7)).
+
+    X: [B, N, C]; W: [C, C] (out = X @ W).  Returns [B, H, N, D] where head h
+    holds output channels [h D, (h+1) D).
+    """
+    X = _f64(X)
+    W = _f64(W)
+    B, N, C = X.shape
+    if C % H:
+        raise ValueError("C must be divisible by H")
+    D = C // H
+    Y = X @ W  # [B, N, C]
+    return Y.reshape(B, N, H, D).transpose(0, 2, 1, 3).copy()
+
+
+def merge_heads(Yh: np.ndarray) -> np.ndarray:
+    """Concatenate heads: [B, H, N, D] -> [B, N, H*D] (Sec. 2.1, after Eq. (2))."""
+    B, H, N, D = Yh.shape
+    return Yh.transpose(0, 2, 1, 3).reshape(B, N, H * D).copy()
+
+
+def sdpa(Q: np.ndarray, K: np.ndarray, V: np.ndarray,
+         scale: float | None = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Rectangular SDPA, softmax over the keys (Sec. 2.1, Eq. (3)).
+
+    Q: [..., Nq, D]; K: [..., Nk, D]; V: [..., Nk, Dv]; leading dimensions
+    broadcast.  Returns ``(out [..., Nq, Dv], L [..., Nq])`` where
+    ``L = log sum_j exp(scale * q . k_j)`` (App. A.2, Eq. (20)).
+    With no keys (Nk = 0) the output is zero and L = -inf (App. A.3).
+    """
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    D = Q.shape[-1]
+    s = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    Nq, Nk, Dv = Q.shape[-2], K.shape[-2], V.shape[-1]
+    lead = np.broadcast_shapes(Q.shape[:-2], K.shape[:-2], V.shape[:-2])
+    out = np.zeros(lead + (Nq, Dv))
+    L = np.full(lead + (Nq,), -np.inf)
+    if Nk == 0 or Nq == 0:
+        return out, L
+    for q0 in range(0, Nq, _QUERY_CHUNK):
+        q = Q[..., q0:q0 + _QUERY_CHUNK, :]
+        # pass 1: exact row maximum of the scaled scores
+        mx = None
+        for k0 in range(0, Nk, _KEY_CHUNK):
+            S = s * (q @ np.swapaxes(K[..., k0:k0 + _KEY_CHUNK, :], -1, -2))
+            cm = S.max(axis=-1)
+            mx = cm if mx is None else np.maximum(mx, cm)
+        # pass 2: exponentials, normaliser and weighted values
+        den = 0.0
+        num = 0.0
+        for k0 in range(0, Nk, _KEY_CHUNK):
+            S = s * (q @ np.swapaxes(K[..., k0:k0 + _KEY_CHUNK, :], -1, -2))
+            E = np.exp(S - mx[..., None])
+            den = den + E.sum(axis=-1)
+            num = num + E @ V[..., k0:k0 + _KEY_CHUNK, :]
+        out[..., q0:q0 + _QUERY_CHUNK, :] = num / den[..., None]
+        L[..., q0:q0 + _QUERY_CHUNK] = mx + np.log(den)
+    return out, L
+
+
+def mixer_forward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int) -> Dict[str, np.ndarray]:
+    """The FLARE++ mixer forward (Fig. 1; Sec. 2.2, Eqs. (7)-(11)).
+
+    X: [B, N, C]; W*: [C, C]; seeds: [H, M, D].  Returns a dict with
+    ``O [B,N,C]`` and the intermediates ``Q, Z [B,H,M,D]``, ``Y [B,N,C]``
+    (heads merged, before W_O), ``L1, L2 [B,H,M]`` (log-normalisers of the
+    two encode calls) and ``K, V, Kt, Vt [B,H,N,D]``.
+    """
+    X = _f64(X)
+    seeds = _f64(seeds)
+    B, N, C = X.shape
+    if seeds.shape[0] != H or seeds.shape[2] * H != C:
+        raise ValueError("seeds must be [H, M, C/H]")
+    # project step (Fig. 1; Eqs. (7), (9))
+    K = project(X, Wk, H)
+    V = project(X, Wv, H)
+    Kt = project(X, Wkt, H)
+    Vt = project(X, Wvt, H)
+    # call 1: query synthesis, softmax over the N tokens (Eq. (8));
+    # the seeds are shared across the batch
+    Q, L1 = sdpa(seeds[None], Kt, Vt)
+    # call 2: encode, softmax over the N tokens (Eq. (10))
+    Z, L2 = sdpa(Q, K, V)
+    # call 3: decode, the tokens' keys query the M routes; softmax over M
+    # (Eq. (11))
+    Yh, _ = sdpa(K, Q, Z)
+    Y = merge_heads(Yh)
+    # merge: concatenated heads times W_O
+    O = Y @ _f64(Wo)
+    return {"O": O, "Q": Q, "Z": Z, "Y": Y, "L1": L1, "L2": L2,
+            "K": K, "V": V, "Kt": Kt, "Vt": Vt}
+
+
+def flare_forward(X, Wk, Wv, Wo, Qlat, H: int) -> Dict[str, np.ndarray]:
+    """Fixed-query FLARE mixer (Sec. 2.1, Eqs. (4)-(5)): Z = SDPA(Q, K, V),
+    Y = SDPA(K, Q, Z) with learned per-head queries Q [H, M, D]."""
+    X = _f64(X)
+    K = project(X, Wk, H)
+    V = project(X, Wv, H)
+    Qb = _f64(Qlat)[None]
+    Z, L = sdpa(Qb, K, V)
+    Yh, _ = sdpa(K, Qb, Z)
+    Y = merge_heads(Yh)
+    return {"O": Y @ _f64(Wo), "Z": Z, "Y": Y, "L": L}
+
+
+def partial_encode(Qr, K, V, bounds: Sequence[int]) -> List[Tuple[np.ndarray, np.ndarray]]:
+    """Per-part encode on a split of the key axis (App. A.2, Eqs. (19)-(21)).
+
+    ``bounds`` are the cut points [0 = b_0 <= b_1 <= ... <= b_R = N]; part r
+    holds keys [b_r, b_{r+1}).  Returns ``[(O_r, L_r)]``; an empty part gives
+    ``O_r = 0`` and ``L_r = -inf`` (App. A.3).
+    """
+    parts = []
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        parts.append(sdpa(Qr, K[..., a:b, :], V[..., a:b, :]))
+    return parts
+
+
+def split_merge(parts: Sequence[Tuple[np.ndarray, np.ndarray]]) -> Tuple[np.ndarray, np.ndarray]:
+    """Exact merge of per-part SDPA results (App. A.3, Eqs. (24)-(28)).
+
+    ``parts`` is a sequence of ``(O_r [..., M, D], L_r [..., M])``.  Uses the
+    stable form: L_max = max_r L_r; a_r = exp(L_r - L_max); a = sum_r a_r;
+    U = sum_r a_r O_r; L = L_max + log a; Z = U / a.  Parts with L_r = -inf
+    contribute nothing; at least one part must be non-empty for every row.
+    """
+    Ls = np.stack([_f64(L) for _, L in parts])  # [R, ..., M]
+    Os = np.stack([_f64(O) for O, _ in parts])  # [R, ..., M, D]
+    Lmax = Ls.max(axis=0)
+    if not np.all(np.isfinite(Lmax)):
+        raise ValueError("every row needs at least one non-empty part")
+    a_r = np.exp(Ls - Lmax[None])
+    a = a_r.sum(axis=0)
+    U = (a_r[..., None] * Os).sum(axis=0)
+    return U / a[..., None], Lmax + np.log(a)
+
+
+def materialised_operator(X, Wk, Wv, Wkt, Wvt, seeds, H: int) -> Dict[str, np.ndarray]:
+    """Materialise the per-head rank-<=M token operator for small N.
+
+    W_enc = softmax over N of S = s Q K^T (rows are routes), W_dec = softmax
+    over M of S^T (rows are tokens), W_eff = W_dec W_enc in R^{N x N}
+    (Sec. 2.1, Eq. (6); Sec. 2.2, Eq. (12)).  Q is the synthesised query set
+    Q(X) (Eq. (8)).  Returns ``W_enc [B,H,M,N]``, ``W_dec [B,H,N,M]``,
+    ``W_eff [B,H,N,N]`` and ``V [B,H,N,D]``; the mixer's per-head output
+    before merging is ``W_eff @ V``.
+    """
+    X = _f64(X)
+    K = project(X, Wk, H)
+    V = project(X, Wv, H)
+    Kt = project(X, Wkt, H)
+    Vt = project(X, Wvt, H)
+    D = K.shape[-1]
+    s = 1.0 / math.sqrt(D)
+
+    def softmax_last(S):
+        E = np.exp(S - S.max(axis=-1, keepdims=True))
+        return E / E.sum(axis=-1, keepdims=True)
+
+    Wq = softmax_last(s * (_f64(seeds)[None] @ np.swapaxes(Kt, -1, -2)))  # [B,H,M,N]
+    Q = Wq @ Vt
+    S = s * (Q @ np.swapaxes(K, -1, -2))  # [B,H,M,N]
+    W_enc = softmax_last(S)
+    W_dec = softmax_last(np.swapaxes(S, -1, -2))  # [B,H,N,M]
+    return {"W_enc": W_enc, "W_dec": W_dec, "W_eff": W_dec @ W_enc, "V": V, "Q": Q}
