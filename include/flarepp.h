@@ -1,0 +1,149 @@
+/*
+ * flarepp.h -- C ABI of libflarepp.so, the FLARE++ mixer forward on AMD
+ * MI355X (gfx950).
+ *
+ * The operations follow "FLARE++: Low-rank attention with dynamic attention
+ * routing" (arXiv 2608.11519):
+ *
+ *   project   K = X W_K, V = X W_V, K~ = X W~_K, V~ = X W~_V, each split into
+ *             H heads of width D = C / H                (Sec. 2.1 Eq. (4);
+ *                                                         Sec. 2.2 Eqs. (7), (9))
+ *   route     rectangular SDPA, softmax(Q K^T / sqrt(D)) V, with the softmax
+ *             over the keys (Sec. 2.1 Eq. (3)).  ENCODE: M route queries over
+ *             N token keys (Eqs. (8), (10)); DECODE: N token queries over the
+ *             M routes (Eq. (11)).
+ *   mixer     project; Q = SDPA(Q~, K~, V~); Z = SDPA(Q, K, V);
+ *             Y = SDPA(K, Q, Z); O = [Y_1 .. Y_H] W_O  (Fig. 1; Sec. 2.2)
+ *
+ * Conventions shared by every entry point:
+ *   - All tensors are dense, row-major, in device memory (hipMalloc or any
+ *     allocation the device can address), 16-byte aligned.
+ *   - dtype selects the storage type of X, the weights, the seeds, the
+ *     token-side tensors and the outputs: FLAREPP_F32 (float) or FLAREPP_BF16
+ *     (bfloat16 bits).  Accumulation and softmax are always fp32.  With bf16,
+ *     MFMA operands (including the softmax numerators and the synthesised
+ *     queries / latents) are rounded to bf16; with f32 they stay fp32.
+ *   - Head h owns channels [h*D, (h+1)*D).  Weights are [C_in][C_out] and act
+ *     as out = X W (no biases).  The softmax scale is 1/sqrt(D) in every call.
+ *   - D must be 16, 32 or 64, and C = H*D a multiple of 32 for the project
+ *     and mixer entry points.  Every size must be >= 1.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ *     The library never allocates, frees or synchronises; the caller owns
+ *     every buffer, including the workspace, which must stay alive until the
+ *     enqueued work has finished.  Calls that share a workspace must not
+ *     overlap.
+ *   - Results are deterministic: the same inputs on the same device give
+ *     bitwise identical outputs (fixed reduction orders, no float atomics).
+ *   - Return value: FLAREPP_OK (0) or a negative FLAREPP_ERR_* code.
+ *     Arguments are validated before anything is enqueued: on an error
+ *     nothing is launched.  flarepp_last_error() describes the last failure
+ *     of the calling thread.  Faults inside kernels surface at the caller's
+ *     next synchronisation.
+ */
+#ifndef FLAREPP_H_
+#define FLAREPP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define FLAREPP_API __attribute__((visibility("default")))
+#else
+#define FLAREPP_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FLAREPP_OK 0
+#define FLAREPP_ERR_INVALID_ARG (-1) /* size < 1, C % H != 0, null or misaligned pointer */
+#define FLAREPP_ERR_UNSUPPORTED (-2) /* D not in {16,32,64}, unknown dtype/kind, too large */
+#define FLAREPP_ERR_WORKSPACE (-3)   /* workspace null or smaller than required */
+#define FLAREPP_ERR_HIP (-4)         /* a kernel launch failed */
+
+#define FLAREPP_F32 0
+#define FLAREPP_BF16 1
+
+#define FLAREPP_ENCODE 0 /* softmax over the N token keys (routes gather tokens) */
+#define FLAREPP_DECODE 1 /* softmax over the M route keys (tokens read routes) */
+
+/* Description of the last error on the calling thread ("" if none). */
+FLAREPP_API const char* flarepp_last_error(void);
+
+/* Library version string. */
+FLAREPP_API const char* flarepp_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Project (Sec. 2.1 Eq. (4); Sec. 2.2 Eqs. (7), (9)).
+ *
+ * X [B][N][C] and W* [C][C] in dtype.  For each non-null (W, out) pair,
+ * out [B][H][N][D] = X W split into heads.  At least one pair must be given;
+ * a pair with exactly one null pointer is INVALID_ARG.  The workspace holds
+ * the weights re-laid out as MFMA fragments.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_project_workspace_bytes(int dtype, int64_t C);
+FLAREPP_API int flarepp_project(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                    const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                    const void* Wvt, void* K, void* V, void* Kt, void* Vt,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Route: one rectangular SDPA call with M routes and N tokens per (b, h)
+ * (Sec. 2.1 Eq. (3)).
+ *
+ * FLAREPP_ENCODE (Eqs. (8), (10)):
+ *   q    route queries, float32 [B][H][M][D]; route_batch_stride is the
+ *        element stride between batch entries: H*M*D, or 0 when one [H][M][D]
+ *        set is shared by the whole batch (the learned seeds, App. A.1).
+ *   k, v token keys and values, dtype [B][H][N][D].
+ *   out  float32 [B][H][M][D] = softmax_N(q k^T / sqrt(D)) v.
+ *   lse  float32 [B][H][M] natural-log normaliser
+ *        log sum_n exp(q . k_n / sqrt(D)) (App. A.2 Eq. (20)), or NULL.
+ * FLAREPP_DECODE (Eq. (11)):
+ *   q    token queries, dtype [B][H][N][D] (the keys K of the mixer).
+ *   k, v route keys and values, float32 [B][H][M][D] (Q(X) and Z);
+ *        route_batch_stride as above applies to both.
+ *   out  dtype [B][N][H*D]: token n, head h at channels [h*D, (h+1)*D) =
+ *        softmax_M(q_n k^T / sqrt(D)) v (heads merged, Sec. 2.1).
+ *   lse  must be NULL.
+ * Route-side inputs are rounded to the MFMA operand type inside the call.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_route_workspace_bytes(int kind, int dtype, int64_t B, int64_t H,
+                                     int64_t N, int64_t M, int64_t D);
+FLAREPP_API int flarepp_route(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M,
+                  int64_t D, const void* q, int64_t route_batch_stride,
+                  const void* k, const void* v, void* out, float* lse,
+                  void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Whole mixer forward (Fig. 1; Sec. 2.2 Eqs. (7)-(11)).
+ *
+ * X [B][N][C]; Wk, Wv, Wkt (W~_K), Wvt (W~_V), Wo [C][C]; seeds (the learned
+ * Q~, shared by the batch) [H][M][D]; O [B][N][C] -- all in dtype.
+ * M may exceed N.  The workspace holds the projections, the split-key
+ * partials, Q(X), Z and Y; size it with flarepp_mixer_workspace_bytes.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_mixer_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C,
+                                     int64_t H, int64_t M);
+FLAREPP_API int flarepp_mixer_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                          int64_t M, const void* X, const void* Wk, const void* Wv,
+                          const void* Wkt, const void* Wvt, const void* Wo,
+                          const void* seeds, void* O, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* As flarepp_mixer_forward, and also copies the stage results for checking:
+ * Q_out, Z_out float32 [B][H][M][D] (the synthesised queries Q(X) and the
+ * latents Z), Y_out dtype [B][N][C] (decoded tokens, heads merged, before
+ * W_O).  Each may be NULL. */
+FLAREPP_API int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                int64_t M, const void* X, const void* Wk, const void* Wv,
+                                const void* Wkt, const void* Wvt, const void* Wo,
+                                const void* seeds, void* O, float* Q_out, float* Z_out,
+                                void* Y_out, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLAREPP_H_ */

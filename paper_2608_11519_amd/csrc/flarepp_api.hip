@@ -1,0 +1,511 @@
+// C ABI of libflarepp.so: argument validation, workspace layout and launch
+// sequencing for the FLARE++ mixer forward.  Declarations and the contract
+// of every entry point are in include/flarepp.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <string>
+
+#include "../../include/flarepp.h"
+#include "flarepp_internal.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return FLAREPP_OK;
+}
+
+constexpr int64_t kMaxTokens = int64_t(1) << 30;  // per batch entry
+constexpr int64_t kMaxRoutes = 1 << 16;
+constexpr int64_t kMaxWidth = 4096;
+constexpr int64_t kTargetUnits = 2048;  // waves per encode launch (8 per CU)
+constexpr int kMinChunk = 128;          // tokens per encode unit
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int dtype_bytes(int dtype) { return dtype == FLAREPP_F32 ? 4 : 2; }
+
+int check_dtype(int dtype) {
+  if (dtype != FLAREPP_F32 && dtype != FLAREPP_BF16)
+    return fail(FLAREPP_ERR_UNSUPPORTED, "unknown dtype %d (expected FLAREPP_F32=0 or FLAREPP_BF16=1)", dtype);
+  return FLAREPP_OK;
+}
+
+int check_head_width(int64_t D) {
+  if (D != 16 && D != 32 && D != 64)
+    return fail(FLAREPP_ERR_UNSUPPORTED, "head width D=%lld is not supported (16, 32 or 64)", (long long)D);
+  return FLAREPP_OK;
+}
+
+int check_ptr(const void* p, const char* name, bool may_be_null = false) {
+  if (!p) {
+    if (may_be_null) return FLAREPP_OK;
+    return fail(FLAREPP_ERR_INVALID_ARG, "%s is NULL", name);
+  }
+  if (reinterpret_cast<uintptr_t>(p) & 15)
+    return fail(FLAREPP_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return FLAREPP_OK;
+}
+
+int check_positive(int64_t v, const char* name) {
+  if (v < 1) return fail(FLAREPP_ERR_INVALID_ARG, "%s=%lld must be >= 1", name, (long long)v);
+  return FLAREPP_OK;
+}
+
+#define TRY(x) do { int _rc = (x); if (_rc != FLAREPP_OK) return _rc; } while (0)
+#define HIPTRY(x) do { hipError_t _e = (x); if (_e != hipSuccess) \
+    return fail(FLAREPP_ERR_HIP, "%s: %s", #x, hipGetErrorString(_e)); } while (0)
+
+int check_mixer_shape(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  TRY(check_dtype(dtype));
+  TRY(check_positive(B, "B"));
+  TRY(check_positive(N, "N"));
+  TRY(check_positive(C, "C"));
+  TRY(check_positive(H, "H"));
+  TRY(check_positive(M, "M"));
+  if (C % H) return fail(FLAREPP_ERR_INVALID_ARG, "C=%lld is not divisible by H=%lld", (long long)C, (long long)H);
+  TRY(check_head_width(C / H));
+  if (C % 32) return fail(FLAREPP_ERR_UNSUPPORTED, "C=%lld must be a multiple of 32", (long long)C);
+  if (N > kMaxTokens) return fail(FLAREPP_ERR_UNSUPPORTED, "N=%lld exceeds %lld", (long long)N, (long long)kMaxTokens);
+  if (M > kMaxRoutes) return fail(FLAREPP_ERR_UNSUPPORTED, "M=%lld exceeds %lld", (long long)M, (long long)kMaxRoutes);
+  if (C > kMaxWidth) return fail(FLAREPP_ERR_UNSUPPORTED, "C=%lld exceeds %lld", (long long)C, (long long)kMaxWidth);
+  if (B * H > (int64_t(1) << 24)) return fail(FLAREPP_ERR_UNSUPPORTED, "B*H too large");
+  if (B * round_up(N, 32) * C > (int64_t(1) << 40)) return fail(FLAREPP_ERR_UNSUPPORTED, "B*N*C too large");
+  return FLAREPP_OK;
+}
+
+// ---- encode work split ----------------------------------------------------
+struct EncPlan {
+  int nq, nqb, qgroups, nchunks, chunk;
+};
+
+EncPlan encode_plan(int64_t B, int64_t H, int64_t N, int64_t Mp, int64_t D) {
+  EncPlan e;
+  e.nq = flarepp::route_nq((int)D, false);
+  e.nqb = (int)(Mp / 32);
+  e.qgroups = (int)cdiv(e.nqb, e.nq);
+  const int64_t per = B * H * e.qgroups;
+  int64_t R;
+  const char* force = std::getenv("FLAREPP_FORCE_CHUNKS");
+  const int64_t forced = force ? std::atoll(force) : 0;
+  if (forced > 0) {
+    R = forced > 65536 ? 65536 : forced;
+    e.chunk = (int)round_up(cdiv(N, R), 32);
+  } else {
+    R = cdiv(kTargetUnits, per);
+    R = std::max<int64_t>(1, std::min<int64_t>(R, cdiv(N, kMinChunk)));
+    e.chunk = (int)round_up(cdiv(N, R), 32);
+    R = cdiv(N, e.chunk);
+  }
+  e.nchunks = (int)R;
+  return e;
+}
+
+// Squared score bound of the shift-free softmax path (2% below kFastRange^2
+// for the rounding of the norms); FLAREPP_NO_FAST_PATH=1 disables the path.
+float fast_limit() {
+  const char* off = std::getenv("FLAREPP_NO_FAST_PATH");
+  if (off && std::atoi(off) != 0) return -1.f;
+  return flarepp::kFastRangeSq * 0.98f;
+}
+
+flarepp::RouteParams encode_params(const EncPlan& e, int64_t B, int64_t H, int64_t N, int64_t Mp,
+                                   int64_t D) {
+  flarepp::RouteParams p{};
+  p.B = (int)B;
+  p.H = (int)H;
+  p.key_len = (int)N;
+  p.key_chunk = e.chunk;
+  p.nchunks = e.nchunks;
+  p.nqb = e.nqb;
+  p.qgroups = e.qgroups;
+  p.Mp = (int)Mp;
+  p.fast_lim = fast_limit();
+  (void)D;
+  return p;
+}
+
+flarepp::RouteParams decode_params(int64_t B, int64_t H, int64_t N, int64_t M, int64_t D) {
+  flarepp::RouteParams p{};
+  const int nq = flarepp::route_nq((int)D, true);
+  p.B = (int)B;
+  p.H = (int)H;
+  p.key_len = (int)M;
+  p.key_chunk = (int)round_up(M, 32);
+  p.nchunks = 1;
+  p.nqb = (int)cdiv(N, 32);
+  p.qgroups = (int)cdiv(p.nqb, nq);
+  p.fast_lim = fast_limit();
+  return p;
+}
+
+// ---- workspace carving ----------------------------------------------------
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off += align256(bytes);
+    return p;
+  }
+};
+
+struct MixerWs {
+  void *wf[5], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *q_op, *z_op, *Y;
+  float *part_ml, *part_acc;
+  size_t bytes;
+};
+
+MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
+  const size_t bs = dtype_bytes(dtype);
+  const EncPlan e = encode_plan(B, H, N, Mp, D);
+  Carver cv(base);
+  MixerWs w;
+  for (int i = 0; i < 5; ++i) w.wf[i] = cv.take(bs * C * C);
+  w.seeds_op = cv.take(bs * H * Mp * D);
+  w.K = cv.take(bs * B * H * N * D);
+  w.Kt = cv.take(bs * B * H * N * D);
+  w.Vdm = cv.take(bs * B * H * D * Np);
+  w.Vtdm = cv.take(bs * B * H * D * Np);
+  w.part_ml = (float*)cv.take(sizeof(float) * e.nchunks * B * H * Mp * 2);
+  w.part_acc = (float*)cv.take(sizeof(float) * e.nchunks * B * H * Mp * D);
+  w.q_op = cv.take(bs * B * H * Mp * D);
+  w.z_op = cv.take(bs * B * H * D * Mp);
+  w.Y = cv.take(bs * B * N * C);
+  w.bytes = cv.off;
+  return w;
+}
+
+float route_qscale(int64_t D) { return (float)(1.4426950408889634 / std::sqrt((double)D)); }
+
+template <typename T>
+int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
+               const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
+               const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
+               size_t ws_bytes, hipStream_t s) {
+  using namespace flarepp;
+  const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
+  const MixerWs w = mixer_ws(ws, dtype, B, N, C, H, M);
+  if (ws_bytes < w.bytes)
+    return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
+  const float qscale = route_qscale(D);
+
+  // 1. weights as MFMA fragments
+  WeightFragParams wp{};
+  wp.C = (int)C;
+  wp.nw = 5;
+  const void* ws_in[5] = {Wk, Wv, Wkt, Wvt, Wo};
+  for (int i = 0; i < 5; ++i) { wp.w[i] = ws_in[i]; wp.out[i] = w.wf[i]; }
+  HIPTRY(launch_weight_frags<T>(wp, s));
+
+  // 2. seeds -> scaled route operand (shared by the batch)
+  RoutePrepParams sp{};
+  sp.src = seeds; sp.src_bstride = 0; sp.B = 1; sp.H = (int)H; sp.M = (int)M; sp.Mp = (int)Mp;
+  sp.D = (int)D; sp.qscale = qscale; sp.q_op = w.seeds_op; sp.z_op = nullptr;
+  HIPTRY((launch_route_prep<T, T>(sp, s)));
+
+  // 3. project: K, K~ token-major; V, V~ d-major (value operands)
+  ProjParams pp{};
+  pp.x = X; pp.B = (int)B; pp.N = (int)N; pp.Np = (int)Np; pp.C = (int)C; pp.H = (int)H; pp.D = (int)D;
+  pp.nw = 4;
+  pp.wf[0] = w.wf[0]; pp.out[0] = w.K;    pp.layout[0] = kHeadsTokenMajor;
+  pp.wf[1] = w.wf[1]; pp.out[1] = w.Vdm;  pp.layout[1] = kHeadsDMajor;
+  pp.wf[2] = w.wf[2]; pp.out[2] = w.Kt;   pp.layout[2] = kHeadsTokenMajor;
+  pp.wf[3] = w.wf[3]; pp.out[3] = w.Vtdm; pp.layout[3] = kHeadsDMajor;
+  HIPTRY(launch_project<T>(pp, s));
+
+  const EncPlan e = encode_plan(B, H, N, Mp, D);
+  const int64_t tokHS = N * D, tokBS = H * N * D;          // token-major strides
+  const int64_t dmHS = D * Np, dmBS = H * D * Np;          // d-major token strides
+  const int64_t rtHS = Mp * D, rtBS = H * Mp * D;          // route operand strides
+
+  // 4. call 1: Q = SDPA(Q~, K~, V~), softmax over tokens
+  RouteParams r1 = encode_params(e, B, H, N, Mp, D);
+  r1.ka = w.Kt; r1.ka_sb = tokBS; r1.ka_sh = tokHS; r1.ka_rows = (int)N;
+  r1.va = w.Vtdm; r1.va_sb = dmBS; r1.va_sh = dmHS; r1.va_ld = (int)Np;
+  r1.qs = w.seeds_op; r1.qs_sb = 0; r1.qs_sh = rtHS; r1.qs_rows = (int)Mp;
+  r1.part_ml = w.part_ml; r1.part_acc = w.part_acc;
+  HIPTRY(launch_route<T>(r1, (int)D, false, s));
+  CombineParams c1{};
+  c1.part_ml = w.part_ml; c1.part_acc = w.part_acc; c1.BH = B * H; c1.R = e.nchunks;
+  c1.M = (int)M; c1.Mp = (int)Mp; c1.D = (int)D; c1.qscale = qscale;
+  c1.out32 = Q_out; c1.lse = nullptr; c1.q_op = w.q_op; c1.z_op = nullptr;
+  HIPTRY(launch_combine<T>(c1, s));
+
+  // 5. call 2: Z = SDPA(Q, K, V), softmax over tokens
+  RouteParams r2 = r1;
+  r2.ka = w.K; r2.va = w.Vdm;
+  r2.qs = w.q_op; r2.qs_sb = rtBS; r2.qs_sh = rtHS; r2.qs_rows = (int)Mp;
+  HIPTRY(launch_route<T>(r2, (int)D, false, s));
+  CombineParams c2 = c1;
+  c2.out32 = Z_out; c2.q_op = nullptr; c2.z_op = w.z_op;
+  HIPTRY(launch_combine<T>(c2, s));
+
+  // 6. call 3: Y = SDPA(K, Q, Z), softmax over routes, heads merged
+  void* Y = Y_out ? Y_out : w.Y;
+  RouteParams r3 = decode_params(B, H, N, M, D);
+  r3.ka = w.q_op; r3.ka_sb = rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
+  r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;
+  r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
+  r3.y = Y; r3.y_sb = N * C; r3.y_row = C;
+  HIPTRY(launch_route<T>(r3, (int)D, true, s));
+
+  // 7. merge: O = Y W_O
+  ProjParams mp{};
+  mp.x = Y; mp.B = (int)B; mp.N = (int)N; mp.Np = (int)Np; mp.C = (int)C; mp.H = (int)H; mp.D = (int)D;
+  mp.nw = 1; mp.wf[0] = w.wf[4]; mp.out[0] = O; mp.layout[0] = kPlain;
+  HIPTRY(launch_project<T>(mp, s));
+  return ok();
+}
+
+int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
+                const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
+                const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
+                size_t ws_bytes, void* stream) {
+  TRY(check_mixer_shape(dtype, B, N, C, H, M));
+  TRY(check_ptr(X, "X"));
+  TRY(check_ptr(Wk, "Wk"));
+  TRY(check_ptr(Wv, "Wv"));
+  TRY(check_ptr(Wkt, "Wkt"));
+  TRY(check_ptr(Wvt, "Wvt"));
+  TRY(check_ptr(Wo, "Wo"));
+  TRY(check_ptr(seeds, "seeds"));
+  TRY(check_ptr(O, "O"));
+  TRY(check_ptr(Q_out, "Q_out", true));
+  TRY(check_ptr(Z_out, "Z_out", true));
+  TRY(check_ptr(Y_out, "Y_out", true));
+  if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
+  TRY(check_ptr(ws, "ws"));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FLAREPP_F32)
+    return mixer_impl<float>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
+                             Y_out, ws, ws_bytes, s);
+  return mixer_impl<__bf16>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
+                            Y_out, ws, ws_bytes, s);
+}
+
+// ---- route ------------------------------------------------------------------
+struct RouteWs {
+  void *q_op, *z_op, *Vdm;
+  float *part_ml, *part_acc;
+  size_t bytes;
+};
+
+RouteWs route_ws(void* base, int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M, int64_t D,
+                 bool shared_routes) {
+  const int64_t Mp = round_up(M, 32), Np = round_up(N, 32);
+  const size_t bs = dtype_bytes(dtype);
+  const int64_t Br = shared_routes ? 1 : B;
+  Carver cv(base);
+  RouteWs w{};
+  w.q_op = cv.take(bs * Br * H * Mp * D);
+  if (kind == FLAREPP_ENCODE) {
+    const EncPlan e = encode_plan(B, H, N, Mp, D);
+    w.Vdm = cv.take(bs * B * H * D * Np);
+    w.part_ml = (float*)cv.take(sizeof(float) * e.nchunks * B * H * Mp * 2);
+    w.part_acc = (float*)cv.take(sizeof(float) * e.nchunks * B * H * Mp * D);
+  } else {
+    w.z_op = cv.take(bs * Br * H * D * Mp);
+  }
+  w.bytes = cv.off;
+  return w;
+}
+
+int check_route_shape(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M, int64_t D) {
+  if (kind != FLAREPP_ENCODE && kind != FLAREPP_DECODE)
+    return fail(FLAREPP_ERR_UNSUPPORTED, "unknown route kind %d", kind);
+  TRY(check_dtype(dtype));
+  TRY(check_positive(B, "B"));
+  TRY(check_positive(H, "H"));
+  TRY(check_positive(N, "N"));
+  TRY(check_positive(M, "M"));
+  TRY(check_positive(D, "D"));
+  TRY(check_head_width(D));
+  if (N > kMaxTokens) return fail(FLAREPP_ERR_UNSUPPORTED, "N too large");
+  if (M > kMaxRoutes) return fail(FLAREPP_ERR_UNSUPPORTED, "M too large");
+  if (B * H > (int64_t(1) << 24)) return fail(FLAREPP_ERR_UNSUPPORTED, "B*H too large");
+  return FLAREPP_OK;
+}
+
+template <typename T>
+int route_impl(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M, int64_t D,
+               const void* q, int64_t rstride, const void* k, const void* v, void* out, float* lse,
+               void* ws, size_t ws_bytes, hipStream_t s) {
+  using namespace flarepp;
+  const bool shared = rstride == 0;
+  const int64_t Mp = round_up(M, 32), Np = round_up(N, 32);
+  const RouteWs w = route_ws(ws, kind, dtype, B, H, N, M, D, shared);
+  if (ws_bytes < w.bytes)
+    return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
+  const float qscale = route_qscale(D);
+  const int64_t rtHS = Mp * D, rtBS = shared ? 0 : H * Mp * D;
+  const int64_t tokHS = N * D, tokBS = H * N * D;
+  RoutePrepParams rp{};
+  rp.src_bstride = rstride; rp.B = shared ? 1 : (int)B; rp.H = (int)H; rp.M = (int)M; rp.Mp = (int)Mp;
+  rp.D = (int)D; rp.qscale = qscale;
+  if (kind == FLAREPP_ENCODE) {
+    rp.src = q; rp.q_op = w.q_op; rp.z_op = nullptr;
+    HIPTRY((launch_route_prep<float, T>(rp, s)));
+    DmajorParams dp{};
+    dp.src = v; dp.dst = w.Vdm; dp.BH = B * H; dp.N = (int)N; dp.Np = (int)Np; dp.D = (int)D;
+    HIPTRY(launch_dmajor<T>(dp, s));
+    const EncPlan e = encode_plan(B, H, N, Mp, D);
+    RouteParams r = encode_params(e, B, H, N, Mp, D);
+    r.ka = k; r.ka_sb = tokBS; r.ka_sh = tokHS; r.ka_rows = (int)N;
+    r.va = w.Vdm; r.va_sb = H * D * Np; r.va_sh = D * Np; r.va_ld = (int)Np;
+    r.qs = w.q_op; r.qs_sb = rtBS; r.qs_sh = rtHS; r.qs_rows = (int)Mp;
+    r.part_ml = w.part_ml; r.part_acc = w.part_acc;
+    HIPTRY(launch_route<T>(r, (int)D, false, s));
+    CombineParams c{};
+    c.part_ml = w.part_ml; c.part_acc = w.part_acc; c.BH = B * H; c.R = e.nchunks; c.M = (int)M;
+    c.Mp = (int)Mp; c.D = (int)D; c.qscale = qscale; c.out32 = (float*)out; c.lse = lse;
+    HIPTRY(launch_combine<T>(c, s));
+  } else {
+    rp.src = k; rp.q_op = w.q_op; rp.z_op = nullptr;
+    HIPTRY((launch_route_prep<float, T>(rp, s)));
+    rp.src = v; rp.q_op = nullptr; rp.z_op = w.z_op;
+    HIPTRY((launch_route_prep<float, T>(rp, s)));
+    RouteParams r = decode_params(B, H, N, M, D);
+    r.ka = w.q_op; r.ka_sb = rtBS; r.ka_sh = rtHS; r.ka_rows = (int)Mp;
+    r.va = w.z_op; r.va_sb = shared ? 0 : H * D * Mp; r.va_sh = D * Mp; r.va_ld = (int)Mp;
+    r.qs = q; r.qs_sb = tokBS; r.qs_sh = tokHS; r.qs_rows = (int)N;
+    r.y = out; r.y_sb = N * H * D; r.y_row = H * D;
+    HIPTRY(launch_route<T>(r, (int)D, true, s));
+  }
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* flarepp_last_error(void) { return g_last_error.c_str(); }
+
+const char* flarepp_version(void) { return "flarepp 0.1 (gfx950)"; }
+
+size_t flarepp_project_workspace_bytes(int dtype, int64_t C) {
+  if (check_dtype(dtype) != FLAREPP_OK || C < 1 || C > kMaxWidth) return 0;
+  return 4 * align256((size_t)dtype_bytes(dtype) * C * C);
+}
+
+int flarepp_project(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, const void* X,
+                    const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, void* K,
+                    void* V, void* Kt, void* Vt, void* ws, size_t ws_bytes, void* stream) {
+  TRY(check_mixer_shape(dtype, B, N, C, H, 1));
+  TRY(check_ptr(X, "X"));
+  const void* W[4] = {Wk, Wv, Wkt, Wvt};
+  void* Out[4] = {K, V, Kt, Vt};
+  const char* wn[4] = {"Wk", "Wv", "Wkt", "Wvt"};
+  const char* on[4] = {"K", "V", "Kt", "Vt"};
+  int n = 0;
+  for (int i = 0; i < 4; ++i) {
+    if (!W[i] != !Out[i])
+      return fail(FLAREPP_ERR_INVALID_ARG, "%s and %s must both be given or both be NULL", wn[i], on[i]);
+    if (W[i]) {
+      TRY(check_ptr(W[i], wn[i]));
+      TRY(check_ptr(Out[i], on[i]));
+      ++n;
+    }
+  }
+  if (n == 0) return fail(FLAREPP_ERR_INVALID_ARG, "no (weight, output) pair given");
+  if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
+  TRY(check_ptr(ws, "ws"));
+  const size_t need = flarepp_project_workspace_bytes(dtype, C);
+  if (ws_bytes < need)
+    return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, need);
+  using namespace flarepp;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t slot = align256((size_t)dtype_bytes(dtype) * C * C);
+  WeightFragParams wp{};
+  ProjParams pp{};
+  wp.C = (int)C;
+  pp.x = X; pp.B = (int)B; pp.N = (int)N; pp.Np = (int)round_up(N, 32); pp.C = (int)C;
+  pp.H = (int)H; pp.D = (int)(C / H);
+  for (int i = 0; i < 4; ++i) {
+    if (!W[i]) continue;
+    void* frag = static_cast<char*>(ws) + slot * wp.nw;
+    wp.w[wp.nw] = W[i]; wp.out[wp.nw] = frag; ++wp.nw;
+    pp.wf[pp.nw] = frag; pp.out[pp.nw] = Out[i]; pp.layout[pp.nw] = kHeadsTokenMajor; ++pp.nw;
+  }
+  if (dtype == FLAREPP_F32) {
+    HIPTRY(launch_weight_frags<float>(wp, s));
+    HIPTRY(launch_project<float>(pp, s));
+  } else {
+    HIPTRY(launch_weight_frags<__bf16>(wp, s));
+    HIPTRY(launch_project<__bf16>(pp, s));
+  }
+  return ok();
+}
+
+size_t flarepp_route_workspace_bytes(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M,
+                                     int64_t D) {
+  if (check_route_shape(kind, dtype, B, H, N, M, D) != FLAREPP_OK) return 0;
+  return route_ws(nullptr, kind, dtype, B, H, N, M, D, false).bytes;
+}
+
+int flarepp_route(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M, int64_t D,
+                  const void* q, int64_t route_batch_stride, const void* k, const void* v, void* out,
+                  float* lse, void* ws, size_t ws_bytes, void* stream) {
+  TRY(check_route_shape(kind, dtype, B, H, N, M, D));
+  if (route_batch_stride != 0 && route_batch_stride != H * M * D)
+    return fail(FLAREPP_ERR_INVALID_ARG, "route_batch_stride=%lld must be 0 or H*M*D=%lld",
+                (long long)route_batch_stride, (long long)(H * M * D));
+  TRY(check_ptr(q, "q"));
+  TRY(check_ptr(k, "k"));
+  TRY(check_ptr(v, "v"));
+  TRY(check_ptr(out, "out"));
+  if (kind == FLAREPP_DECODE && lse) return fail(FLAREPP_ERR_INVALID_ARG, "lse must be NULL for DECODE");
+  TRY(check_ptr(lse, "lse", true));
+  if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
+  TRY(check_ptr(ws, "ws"));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FLAREPP_F32)
+    return route_impl<float>(kind, dtype, B, H, N, M, D, q, route_batch_stride, k, v, out, lse, ws,
+                             ws_bytes, s);
+  return route_impl<__bf16>(kind, dtype, B, H, N, M, D, q, route_batch_stride, k, v, out, lse, ws,
+                            ws_bytes, s);
+}
+
+size_t flarepp_mixer_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  if (check_mixer_shape(dtype, B, N, C, H, M) != FLAREPP_OK) return 0;
+  return mixer_ws(nullptr, dtype, B, N, C, H, M).bytes;
+}
+
+int flarepp_mixer_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                          const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                          const void* Wvt, const void* Wo, const void* seeds, void* O, void* ws,
+                          size_t ws_bytes, void* stream) {
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr,
+                     nullptr, ws, ws_bytes, stream);
+}
+
+int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                                const void* Wvt, const void* Wo, const void* seeds, void* O,
+                                float* Q_out, float* Z_out, void* Y_out, void* ws, size_t ws_bytes,
+                                void* stream) {
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out, Y_out,
+                     ws, ws_bytes, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,134 @@
+// Device-side building blocks for the FLARE++ mixer kernels (gfx950, wave64).
+//
+// All contractions use the 32x32 MFMA tile.  With 64 lanes, lane l belongs to
+// half g = l / 32 and column c = l % 32.  For an A operand (32 rows x 16 k)
+// lane l holds row c, k = 8g .. 8g+7; for a B operand (16 k x 32 cols) lane l
+// holds col c, k = 8g .. 8g+7; the 32x32 fp32 result leaves register r of
+// lane l at row 8*(r/4) + 4g + (r%4), column c.  bf16 operands use one
+// v_mfma_f32_32x32x16_bf16 per 16-wide k step; fp32 operands use eight
+// v_mfma_f32_32x32x2_f32, the j-th taking element j of the same 8-element
+// fragment (so both types share one data layout).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace flarepp {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(8))) float f32x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+template <typename T> struct Frag;
+template <> struct Frag<__bf16> { typedef bf16x8 type; typedef bf16x4 half; };
+template <> struct Frag<float> { typedef f32x8 type; typedef f32x4 half; };
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int acc_row(int lane, int r) {
+  return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+
+__device__ __forceinline__ void mma(f32x16& c, const bf16x8& a, const bf16x8& b) {
+  c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x16& c, const f32x8& a, const f32x8& b) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[k], b[k], c, 0, 0, 0);
+}
+
+// ---- conversions -----------------------------------------------------------
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ __bf16 from_f32<__bf16>(float x) { return (__bf16)x; }
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
+
+// ---- fragment loads (pointers are aligned to the fragment size) ------------
+__device__ __forceinline__ bf16x8 load_frag(const __bf16* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+__device__ __forceinline__ f32x8 load_frag(const float* p) {
+  f32x4 a = *reinterpret_cast<const f32x4*>(p);
+  f32x4 b = *reinterpret_cast<const f32x4*>(p + 4);
+  f32x8 r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+  r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
+  return r;
+}
+__device__ __forceinline__ bf16x4 load_half(const __bf16* p) {
+  return *reinterpret_cast<const bf16x4*>(p);
+}
+__device__ __forceinline__ f32x4 load_half(const float* p) {
+  return *reinterpret_cast<const f32x4*>(p);
+}
+template <typename T> __device__ __forceinline__ typename Frag<T>::type zero_frag() {
+  typename Frag<T>::type z;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) z[i] = from_f32<T>(0.f);
+  return z;
+}
+template <typename T> __device__ __forceinline__ typename Frag<T>::type fill_frag(float v) {
+  typename Frag<T>::type z;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) z[i] = from_f32<T>(v);
+  return z;
+}
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type join(typename Frag<T>::half a,
+                                                       typename Frag<T>::half b) {
+  typename Frag<T>::type r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { r[i] = a[i]; r[4 + i] = b[i]; }
+  return r;
+}
+// Sum of squares of one fragment's elements, in fp32.
+__device__ __forceinline__ float sumsq(const bf16x8& f) {
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) { float x = (float)f[i]; s = __builtin_fmaf(x, x, s); }
+  return s;
+}
+__device__ __forceinline__ float sumsq(const f32x8& f) {
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s = __builtin_fmaf(f[i], f[i], s);
+  return s;
+}
+
+// ---- stores of 4 consecutive values ----------------------------------------
+__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
+  f32x4 v; v[0] = a; v[1] = b; v[2] = c; v[3] = d;
+  *reinterpret_cast<f32x4*>(p) = v;
+}
+__device__ __forceinline__ void store4(__bf16* p, float a, float b, float c, float d) {
+  bf16x4 v; v[0] = (__bf16)a; v[1] = (__bf16)b; v[2] = (__bf16)c; v[3] = (__bf16)d;
+  *reinterpret_cast<bf16x4*>(p) = v;
+}
+
+// ---- cross-lane helpers ------------------------------------------------------
+// Value held by lane l ^ 32 (the other half of the wave).
+__device__ __forceinline__ float other_half(float x) { return __shfl_xor(x, 32, 64); }
+
+// Maximum of a non-negative float over each 32-lane half of the wave, summed
+// over the two halves (an upper bound on max_c (x[c] + x[c+32])).  The result
+// is wave-uniform.  Non-negative floats order like their bit patterns, so the
+// reduction runs on integers through DPP row operations and lane reads.
+__device__ __forceinline__ float halfmax_sum_nonneg(float x) {
+  int v = __float_as_int(x);
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false)); // row_half_mirror
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false)); // row_mirror
+  int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+  int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+  return __int_as_float(max(r0, r1)) + __int_as_float(max(r2, r3));
+}
+
+// True in every lane when pred holds in every active lane.
+__device__ __forceinline__ bool wave_all(bool pred) {
+  return __builtin_amdgcn_ballot_w64(!pred) == 0;
+}
+
+}  // namespace flarepp

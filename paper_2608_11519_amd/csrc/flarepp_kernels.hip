@@ -1,0 +1,441 @@
+// HIP kernels of the FLARE++ mixer forward for gfx950.
+//
+// The mixer (Fig. 1; Sec. 2.2, Eqs. (7)-(11)) is: project K,V,K~,V~ = X W;
+// Q = SDPA(Q~, K~, V~) and Z = SDPA(Q, K, V) with the softmax over the N
+// tokens; Y = SDPA(K, Q, Z) with the softmax over the M routes; O = merge(Y) W_O.
+//
+// All three routing calls run through one kernel, k_route.  A "unit" (one
+// wave) holds NQ blocks of 32 queries in registers and streams 32-key tiles:
+//   S^T   = K_tile . Q^T             (MFMA, rows = keys, cols = queries)
+//   P     = 2^(S^T - m)              (softmax numerators, log2 units)
+//   out^T += [V^T ; 1 ; 0] . P        (MFMA; for D = 16 the row of ones
+//                                     yields the softmax denominators)
+// For the two encode calls the queries are the M routes and the keys are a
+// chunk of the N tokens; each unit writes a partial (m, l, acc) that
+// k_combine merges exactly in a fixed chunk order (App. A.2-A.3, Eqs. (19)-(28),
+// with (m, l) carrying the log-normaliser L_r = m + log l).  For the decode the
+// queries are 32-token blocks and the keys are all M routes; each unit writes
+// normalised head outputs straight into Y[B][N][C].  The N x M scores never
+// leave registers.
+//
+// Scores are pre-scaled by log2(e)/sqrt(D) on the query operand (the route
+// side), so the exponentials are bare v_exp_f32.  While the Cauchy-Schwarz
+// bound |q.k| <= max|q| max|k| keeps every score within 64 (log2 units) of zero,
+// no running maximum is needed (softmax is shift invariant); otherwise the
+// tile falls back to the usual online-maximum update.
+#include "flarepp_device.hpp"
+#include "flarepp_internal.hpp"
+
+namespace flarepp {
+
+// ---------------------------------------------------------------------------
+// Weight fragments: W [C][C] row-major (out = X W) -> per (column block cb,
+// k step ks) one 64-lane fragment; lane l holds W[16ks + 8g + j][32cb + c].
+// The same fragment is the A operand of O^T = W^T X^T and the B operand of
+// O = X W.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void k_weight_frags(WeightFragParams p) {
+  const int C = p.C, KS = C / 16;
+  const int64_t per_w = (int64_t)(C / 32) * KS * 64;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= per_w * p.nw) return;
+  const int w = (int)(idx / per_w);
+  const int64_t f = idx % per_w;
+  const int lane = (int)(f & 63), ks = (int)((f >> 6) % KS), cb = (int)((f >> 6) / KS);
+  const T* W = (const T*)p.w[w];
+  T* out = (T*)p.out[w] + f * 8;
+  const int col = 32 * cb + (lane & 31), k0 = 16 * ks + 8 * (lane >> 5);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) out[j] = W[(int64_t)(k0 + j) * C + col];
+}
+
+// ---------------------------------------------------------------------------
+// Route-side operands from an fp32 (or storage-type) [B?][H][M][D] tensor:
+//   q_op [B][H][Mp][D]  = src * qscale  (query operand of the encode calls and
+//                                        key operand of the decode call)
+//   z_op [B][H][D][Mp]  = src           (value operand of the decode call)
+// Rows M..Mp-1 are zero.
+// ---------------------------------------------------------------------------
+template <typename Ts, typename T>
+__global__ void k_route_prep(RoutePrepParams p) {
+  const int64_t total = (int64_t)p.B * p.H * p.Mp * p.D;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int d = (int)(idx % p.D);
+  const int m = (int)((idx / p.D) % p.Mp);
+  const int64_t bh = idx / ((int64_t)p.D * p.Mp);
+  const int b = (int)(bh / p.H), h = (int)(bh % p.H);
+  float v = 0.f;
+  if (m < p.M) v = to_f32(((const Ts*)p.src)[b * p.src_bstride + ((int64_t)h * p.M + m) * p.D + d]);
+  if (p.q_op) ((T*)p.q_op)[(bh * p.Mp + m) * p.D + d] = from_f32<T>(v * p.qscale);
+  if (p.z_op) ((T*)p.z_op)[(bh * p.D + d) * p.Mp + m] = from_f32<T>(v);
+}
+
+// ---------------------------------------------------------------------------
+// Token-side values [B][H][N][D] -> d-major [B][H][D][Np], zero padded.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void k_dmajor(DmajorParams p) {
+  const int64_t total = (int64_t)p.BH * p.D * p.Np;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int n = (int)(idx % p.Np);
+  const int64_t bhd = idx / p.Np;
+  const int d = (int)(bhd % p.D);
+  const int64_t bh = bhd / p.D;
+  T v = from_f32<T>(0.f);
+  if (n < p.N) v = ((const T*)p.src)[(bh * p.N + n) * p.D + d];
+  ((T*)p.dst)[idx] = v;
+}
+
+// ---------------------------------------------------------------------------
+// Projection GEMM: out = X W for up to five weights.  One wave computes one
+// 32-token x 32-column block.  Output layouts:
+//   kHeadsTokenMajor [B][H][N][D]   (heads are contiguous D-column blocks)
+//   kHeadsDMajor     [B][H][D][Np]  (zero padded to Np tokens)
+//   kPlain           [B][N][C]
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_project(ProjParams p) {
+  using F = typename Frag<T>::type;
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31;
+  const int CB = p.C / 32, KS = p.C / 16, NB = p.Np / 32;
+  const int64_t u = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t total = (int64_t)p.B * NB * CB * p.nw;
+  if (u >= total) return;
+  const int cb = (int)(u % CB);
+  const int w = (int)((u / CB) % p.nw);
+  const int64_t bn = u / ((int64_t)CB * p.nw);
+  const int b = (int)(bn / NB), n0 = (int)(bn % NB) * 32;
+  const int layout = p.layout[w];
+  const T* X = (const T*)p.x + ((int64_t)b * p.N) * p.C;
+  const T* wf = (const T*)p.wf[w] + (int64_t)cb * KS * 512;
+  const int xrow = n0 + c;
+  const bool xok = xrow < p.N;
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  for (int ks = 0; ks < KS; ++ks) {
+    F xf = xok ? load_frag(X + (int64_t)xrow * p.C + 16 * ks + 8 * g) : zero_frag<T>();
+    F wv = load_frag(wf + ((int64_t)ks * 64 + lane) * 8);
+    if (layout == kHeadsDMajor) mma(acc, xf, wv);   // rows = tokens, cols = channels
+    else mma(acc, wv, xf);                          // rows = channels, cols = tokens
+  }
+  T* out = (T*)p.out[w];
+  const int D = p.D;
+  if (layout == kHeadsDMajor) {
+    const int col = 32 * cb + c, h = col / D, d = col % D;
+    T* o = out + (((int64_t)b * p.H + h) * D + d) * p.Np + n0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      store4(o + 8 * q + 4 * g, acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+  } else if (xok) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int col = 32 * cb + 8 * q + 4 * g;
+      T* o;
+      if (layout == kPlain) {
+        o = out + ((int64_t)b * p.N + xrow) * p.C + col;
+      } else {
+        const int h = col / D, d = col % D;
+        o = out + (((int64_t)b * p.H + h) * p.N + xrow) * D + d;
+      }
+      store4(o, acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Routing attention (see the file comment).  Template parameters: storage
+// type T, head width D, query blocks per unit NQ, and whether the call is the
+// decode (softmax over routes, normalised output) or an encode (softmax over
+// a chunk of tokens, partial output).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int NQ, bool DECODE>
+__global__ __launch_bounds__(256) void k_route(RouteParams p) {
+  using F = typename Frag<T>::type;
+  constexpr int KS = D / 16;            // 16-wide k steps of the score product
+  constexpr int RB = (D + 31) / 32;     // 32-row blocks of the value product
+  constexpr bool ONES_ROW = (D == 16);  // value row 16 is all ones -> row sums
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31;
+  const int64_t u = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t total = (int64_t)p.B * p.H * p.nchunks * p.qgroups;
+  if (u >= total) return;
+  const int qg = (int)(u % p.qgroups);
+  const int r = (int)((u / p.qgroups) % p.nchunks);
+  const int64_t bh = u / ((int64_t)p.qgroups * p.nchunks);
+  const int b = (int)(bh / p.H), h = (int)(bh % p.H);
+  const int k0 = r * p.key_chunk;
+  const int k1 = min(p.key_len, k0 + p.key_chunk);
+  const int qb0 = qg * NQ;
+
+  const T* ka = (const T*)p.ka + b * p.ka_sb + h * p.ka_sh;
+  const T* va = (const T*)p.va + b * p.va_sb + h * p.va_sh;
+  const T* qs = (const T*)p.qs + b * p.qs_sb + h * p.qs_sh;
+
+  // ---- query operands, resident for the whole unit ----
+  F qf[NQ][KS];
+  float qn = 0.f;
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const int row = (qb0 + i) * 32 + c;
+    const bool ok = (qb0 + i) < p.nqb && row < p.qs_rows;
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      qf[i][j] = ok ? load_frag(qs + (int64_t)row * D + 16 * j + 8 * g) : zero_frag<T>();
+      s += sumsq(qf[i][j]);
+    }
+    qn = fmaxf(qn, s);
+  }
+  const float qmax2 = halfmax_sum_nonneg(qn);
+
+  // ---- softmax state ----
+  f32x16 acc[NQ][RB];
+  float m[NQ], ls[NQ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    m[i] = -INFINITY;
+    ls[i] = 0.f;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][rb][e] = 0.f;
+  }
+  bool fastok = true;  // every m is -inf or 0: the shift-free path is exact
+  const float fast_lim = p.fast_lim;
+
+  for (int t0 = k0; t0 < k1; t0 += 32) {
+    const int nvalid = min(32, k1 - t0);
+    // key operands: A[key][d] for the scores, A[d][key] for the values
+    F kf[KS];
+    const int krow = t0 + c;
+    float kn = 0.f;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      kf[j] = krow < p.ka_rows ? load_frag(ka + (int64_t)krow * D + 16 * j + 8 * g) : zero_frag<T>();
+      kn += sumsq(kf[j]);
+    }
+    F vf[2][RB];
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int d = rb * 32 + c;
+        if (d < D) {
+          const T* vp = va + (int64_t)d * p.va_ld + t0 + 16 * hf + 4 * g;
+          vf[hf][rb] = join<T>(load_half(vp), load_half(vp + 8));
+        } else {
+          vf[hf][rb] = (ONES_ROW && c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
+        }
+      }
+    const float kmax2 = halfmax_sum_nonneg(kn);
+    const bool fast = fastok && (qmax2 * kmax2 <= fast_lim);
+
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) {
+      if (qb0 + i >= p.nqb) continue;
+      f32x16 s;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[e] = 0.f;
+#pragma unroll
+      for (int j = 0; j < KS; ++j) mma(s, kf[j], qf[i][j]);
+      if (nvalid < 32) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (acc_row(lane, e) >= nvalid) s[e] = -INFINITY;
+      }
+      if (fast) {
+        m[i] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e]);
+      } else {
+        float mx = s[0];
+#pragma unroll
+        for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[e]);
+        mx = fmaxf(mx, other_half(mx));
+        const float mn = fmaxf(m[i], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m[i] - mn);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[i][rb][e] *= alpha;
+        ls[i] *= alpha;
+        m[i] = mn;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e] - mn);
+      }
+      if (!ONES_ROW) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) ls[i] += s[e];
+      }
+      F p0, p1;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p0[e] = from_f32<T>(s[e]);
+        p1[e] = from_f32<T>(s[8 + e]);
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        mma(acc[i][rb], vf[0][rb], p0);
+        mma(acc[i][rb], vf[1][rb], p1);
+      }
+    }
+    if (!fast) {
+      bool ok = true;
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) ok = ok && (m[i] == 0.f || m[i] == -INFINITY);
+      fastok = wave_all(ok);
+    }
+  }
+
+  // ---- epilogue ----
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    if (qb0 + i >= p.nqb) continue;
+    float l;
+    if (ONES_ROW) {
+      const float a8 = acc[i][0][8];
+      const float o = other_half(a8);
+      l = g == 0 ? a8 : o;
+    } else {
+      l = ls[i] + other_half(ls[i]);
+    }
+    const int qrow = (qb0 + i) * 32 + c;
+    constexpr int NQ4 = ONES_ROW ? 2 : 4;  // groups of 4 output rows per row block
+    if (!DECODE) {
+      const int64_t pidx = (bh * p.nchunks + r) * p.Mp + qrow;
+      float* pa = p.part_acc + pidx * D;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int q = 0; q < NQ4; ++q)
+          store4(pa + rb * 32 + 8 * q + 4 * g, acc[i][rb][4 * q], acc[i][rb][4 * q + 1],
+                 acc[i][rb][4 * q + 2], acc[i][rb][4 * q + 3]);
+      if (g == 0) {
+        p.part_ml[pidx * 2] = m[i];
+        p.part_ml[pidx * 2 + 1] = l;
+      }
+    } else if (qrow < p.qs_rows) {
+      const float inv = 1.f / l;
+      T* yp = (T*)p.y + (int64_t)b * p.y_sb + (int64_t)qrow * p.y_row + h * D;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int q = 0; q < NQ4; ++q)
+          store4(yp + rb * 32 + 8 * q + 4 * g, acc[i][rb][4 * q] * inv, acc[i][rb][4 * q + 1] * inv,
+                 acc[i][rb][4 * q + 2] * inv, acc[i][rb][4 * q + 3] * inv);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exact merge of the per-chunk partials, in fixed chunk order (App. A.3,
+// Eqs. (24)-(28)): m* = max_r m_r; a = sum_r l_r 2^(m_r - m*);
+// out = sum_r acc_r 2^(m_r - m*) / a; L = ln 2 (m* + log2 a).  Empty chunks
+// (m_r = -inf, l_r = 0, acc_r = 0) contribute nothing.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void k_combine(CombineParams p) {
+  const int64_t total = (int64_t)p.BH * p.Mp * p.D;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int d = (int)(idx % p.D);
+  const int qrow = (int)((idx / p.D) % p.Mp);
+  const int64_t bh = idx / ((int64_t)p.D * p.Mp);
+  float mmax = -INFINITY;
+  for (int r = 0; r < p.R; ++r) mmax = fmaxf(mmax, p.part_ml[((bh * p.R + r) * p.Mp + qrow) * 2]);
+  float a = 0.f, num = 0.f;
+  if (mmax > -INFINITY) {
+    for (int r = 0; r < p.R; ++r) {
+      const int64_t pidx = (bh * p.R + r) * p.Mp + qrow;
+      const float mr = p.part_ml[pidx * 2];
+      if (mr == -INFINITY) continue;
+      const float w = __builtin_amdgcn_exp2f(mr - mmax);
+      a = __builtin_fmaf(w, p.part_ml[pidx * 2 + 1], a);
+      num = __builtin_fmaf(w, p.part_acc[pidx * p.D + d], num);
+    }
+  }
+  const bool valid = qrow < p.M;
+  const float out = (valid && a > 0.f) ? num / a : 0.f;
+  if (valid && p.out32) p.out32[(bh * p.M + qrow) * p.D + d] = out;
+  if (valid && p.lse && d == 0) p.lse[bh * p.M + qrow] = 0.6931471805599453f * (mmax + __log2f(a));
+  if (p.q_op) ((T*)p.q_op)[(bh * p.Mp + qrow) * p.D + d] = from_f32<T>(out * p.qscale);
+  if (p.z_op) ((T*)p.z_op)[(bh * p.D + d) * p.Mp + qrow] = from_f32<T>(out);
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+static inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+template <typename T>
+hipError_t launch_weight_frags(const WeightFragParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)(p.C / 32) * (p.C / 16) * 64 * p.nw;
+  k_weight_frags<T><<<blocks_for(n, 256), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename Ts, typename T>
+hipError_t launch_route_prep(const RoutePrepParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.B * p.H * p.Mp * p.D;
+  k_route_prep<Ts, T><<<blocks_for(n, 256), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_dmajor(const DmajorParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.BH * p.D * p.Np;
+  k_dmajor<T><<<blocks_for(n, 256), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_project(const ProjParams& p, hipStream_t s) {
+  const int64_t units = (int64_t)p.B * (p.Np / 32) * (p.C / 32) * p.nw;
+  k_project<T><<<blocks_for(units, 4), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_combine(const CombineParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.BH * p.Mp * p.D;
+  k_combine<T><<<blocks_for(n, 256), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T, int D, bool DEC>
+static hipError_t launch_route_d(const RouteParams& p, hipStream_t s) {
+  const int64_t units = (int64_t)p.B * p.H * p.nchunks * p.qgroups;
+  const unsigned nb = blocks_for(units, 4);
+  constexpr int NQ = route_nq(D, DEC);
+  k_route<T, D, NQ, DEC><<<nb, 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_route(const RouteParams& p, int D, bool decode, hipStream_t s) {
+  switch (D) {
+    case 16: return decode ? launch_route_d<T, 16, true>(p, s) : launch_route_d<T, 16, false>(p, s);
+    case 32: return decode ? launch_route_d<T, 32, true>(p, s) : launch_route_d<T, 32, false>(p, s);
+    case 64: return decode ? launch_route_d<T, 64, true>(p, s) : launch_route_d<T, 64, false>(p, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template hipError_t launch_weight_frags<float>(const WeightFragParams&, hipStream_t);
+template hipError_t launch_weight_frags<__bf16>(const WeightFragParams&, hipStream_t);
+template hipError_t launch_route_prep<float, float>(const RoutePrepParams&, hipStream_t);
+template hipError_t launch_route_prep<float, __bf16>(const RoutePrepParams&, hipStream_t);
+template hipError_t launch_route_prep<__bf16, __bf16>(const RoutePrepParams&, hipStream_t);
+template hipError_t launch_dmajor<float>(const DmajorParams&, hipStream_t);
+template hipError_t launch_dmajor<__bf16>(const DmajorParams&, hipStream_t);
+template hipError_t launch_project<float>(const ProjParams&, hipStream_t);
+template hipError_t launch_project<__bf16>(const ProjParams&, hipStream_t);
+template hipError_t launch_combine<float>(const CombineParams&, hipStream_t);
+template hipError_t launch_combine<__bf16>(const CombineParams&, hipStream_t);
+template hipError_t launch_route<float>(const RouteParams&, int, bool, hipStream_t);
+template hipError_t launch_route<__bf16>(const RouteParams&, int, bool, hipStream_t);
+
+}  // namespace flarepp

@@ -1,0 +1,233 @@
+"""Thin ctypes binding over libflarepp.so (the C ABI in include/flarepp.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of the library.  PyTorch provides device memory and the current
+stream.  If the library is missing this module raises; there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libflarepp.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_UNSUPPORTED = -2
+ERR_WORKSPACE = -3
+ERR_HIP = -4
+F32 = 0
+BF16 = 1
+ENCODE = 0
+DECODE = 1
+
+EXPORTS = (
+    "flarepp_last_error", "flarepp_version",
+    "flarepp_project_workspace_bytes", "flarepp_project",
+    "flarepp_route_workspace_bytes", "flarepp_route",
+    "flarepp_mixer_workspace_bytes", "flarepp_mixer_forward", "flarepp_mixer_forward_debug",
+)
+
+_lib = None
+
+
+class FlareppError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"flarepp error {code}: {msg}")
+        self.code = code
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libflarepp.so once and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2608_11519_amd.build`")
+    lib = ctypes.CDLL(path)
+    i64, vp, sz, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    fp = ctypes.c_void_p
+    lib.flarepp_last_error.restype = ctypes.c_char_p
+    lib.flarepp_last_error.argtypes = []
+    lib.flarepp_version.restype = ctypes.c_char_p
+    lib.flarepp_version.argtypes = []
+    lib.flarepp_project_workspace_bytes.restype = sz
+    lib.flarepp_project_workspace_bytes.argtypes = [i32, i64]
+    lib.flarepp_project.restype = i32
+    lib.flarepp_project.argtypes = [i32, i64, i64, i64, i64] + [vp] * 9 + [vp, sz, vp]
+    lib.flarepp_route_workspace_bytes.restype = sz
+    lib.flarepp_route_workspace_bytes.argtypes = [i32, i32, i64, i64, i64, i64, i64]
+    lib.flarepp_route.restype = i32
+    lib.flarepp_route.argtypes = [i32, i32, i64, i64, i64, i64, i64, vp, i64, vp, vp, vp, fp,
+                                  vp, sz, vp]
+    lib.flarepp_mixer_workspace_bytes.restype = sz
+    lib.flarepp_mixer_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
+    lib.flarepp_mixer_forward.restype = i32
+    lib.flarepp_mixer_forward.argtypes = [i32, i64, i64, i64, i64, i64] + [vp] * 8 + [vp, sz, vp]
+    lib.flarepp_mixer_forward_debug.restype = i32
+    lib.flarepp_mixer_forward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8
+                                                + [fp, fp, vp] + [vp, sz, vp])
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load().flarepp_last_error().decode()
+
+
+def version() -> str:
+    return load().flarepp_version().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != OK:
+        raise FlareppError(rc, last_error())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _workspace(nbytes: int, device, ws: Optional[torch.Tensor]) -> torch.Tensor:
+    if ws is not None and ws.numel() * ws.element_size() >= nbytes:
+        return ws
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# workspace sizes
+# ---------------------------------------------------------------------------
+
+def flarepp_project_workspace_bytes(dtype: int, C: int) -> int:
+    return int(load().flarepp_project_workspace_bytes(dtype, C))
+
+
+def flarepp_route_workspace_bytes(kind: int, dtype: int, B: int, H: int, N: int, M: int, D: int) -> int:
+    return int(load().flarepp_route_workspace_bytes(kind, dtype, B, H, N, M, D))
+
+
+def flarepp_mixer_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
+    return int(load().flarepp_mixer_workspace_bytes(dtype, B, N, C, H, M))
+
+
+# ---------------------------------------------------------------------------
+# entry points on torch tensors
+# ---------------------------------------------------------------------------
+
+def flarepp_project(X: torch.Tensor, Wk=None, Wv=None, Wkt=None, Wvt=None, *, H: int,
+                    ws: Optional[torch.Tensor] = None) -> Tuple[Optional[torch.Tensor], ...]:
+    """K, V, K~, V~ = X W (heads split, [B, H, N, D]) for each weight given."""
+    lib = load()
+    B, N, C = X.shape
+    D = C // H
+    dt = _dtype_code(X)
+    outs = [None if W is None else torch.empty((B, H, N, D), dtype=X.dtype, device=X.device)
+            for W in (Wk, Wv, Wkt, Wvt)]
+    w = _workspace(flarepp_project_workspace_bytes(dt, C), X.device, ws)
+    rc = lib.flarepp_project(dt, B, N, C, H, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt), _ptr(Wvt),
+                             *[_ptr(o) for o in outs], _ptr(w), w.numel(), _stream(X.device))
+    _check(rc)
+    return tuple(outs)
+
+
+def flarepp_route(kind: int, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, *,
+                  shared_routes: bool = False, want_lse: bool = False,
+                  ws: Optional[torch.Tensor] = None):
+    """One routing SDPA call.
+
+    ENCODE: q float32 [B|1, H, M, D] routes; k, v [B, H, N, D] tokens ->
+    (out float32 [B, H, M, D], lse [B, H, M] or None).
+    DECODE: q [B, H, N, D] tokens; k, v float32 [B|1, H, M, D] routes ->
+    out [B, N, H*D] in the tokens' dtype.
+    """
+    lib = load()
+    if kind == ENCODE:
+        B, H, N, D = k.shape
+        M = q.shape[-2]
+        dt = _dtype_code(k)
+        if q.dtype != torch.float32:
+            raise TypeError("route-side tensors are float32")
+        out = torch.empty((B, H, M, D), dtype=torch.float32, device=k.device)
+        lse = torch.empty((B, H, M), dtype=torch.float32, device=k.device) if want_lse else None
+    else:
+        B, H, N, D = q.shape
+        M = k.shape[-2]
+        dt = _dtype_code(q)
+        if k.dtype != torch.float32 or v.dtype != torch.float32:
+            raise TypeError("route-side tensors are float32")
+        out = torch.empty((B, N, H * D), dtype=q.dtype, device=q.device)
+        lse = None
+    stride = 0 if shared_routes else H * M * D
+    dev = out.device
+    w = _workspace(flarepp_route_workspace_bytes(kind, dt, B, H, N, M, D), dev, ws)
+    rc = lib.flarepp_route(kind, dt, B, H, N, M, D, _ptr(q), stride, _ptr(k), _ptr(v), _ptr(out),
+                           _ptr(lse), _ptr(w), w.numel(), _stream(dev))
+    _check(rc)
+    return (out, lse) if kind == ENCODE else out
+
+
+def flarepp_mixer_forward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int,
+                          out: Optional[torch.Tensor] = None,
+                          ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The FLARE++ mixer forward: O [B, N, C] in X's dtype."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    dt = _dtype_code(X)
+    O = out if out is not None else torch.empty_like(X)
+    w = _workspace(flarepp_mixer_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_mixer_forward(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt),
+                                   _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(O), _ptr(w), w.numel(),
+                                   _stream(X.device))
+    _check(rc)
+    return O
+
+
+def flarepp_mixer_forward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int,
+                                ws: Optional[torch.Tensor] = None):
+    """Mixer forward that also returns the stage results: (O, Q, Z, Y)."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    D = C // H
+    dt = _dtype_code(X)
+    O = torch.empty_like(X)
+    Q = torch.empty((B, H, M, D), dtype=torch.float32, device=X.device)
+    Z = torch.empty_like(Q)
+    Y = torch.empty_like(X)
+    w = _workspace(flarepp_mixer_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_mixer_forward_debug(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt),
+                                         _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(O), _ptr(Q), _ptr(Z),
+                                         _ptr(Y), _ptr(w), w.numel(), _stream(X.device))
+    _check(rc)
+    return O, Q, Z, Y
+
+
+# short aliases
+project = flarepp_project
+route = flarepp_route
+mixer_forward = flarepp_mixer_forward
+mixer_forward_debug = flarepp_mixer_forward_debug

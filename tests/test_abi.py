@@ -1,0 +1,126 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/flarepp.h declares, sizes workspaces, and rejects invalid arguments
+before enqueuing anything (these calls never reach a HIP call)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_11519_amd import flarepp as fp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flarepp.h")
+
+
+def _lib():
+    if not os.path.exists(fp.LIB_PATH):
+        pytest.fail("libflarepp.so is not built (run __graft_entry__.build())")
+    return fp.load()
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"FLAREPP_API\s+[\w\s\*]*?\b(flarepp_\w+)\s*\(", txt)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("flarepp_project", "flarepp_route", "flarepp_mixer_forward"):
+        assert n in names
+    assert set(names) == set(fp.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib()
+    for n in _declared():
+        assert hasattr(lib, n), n
+    assert "gfx950" in fp.version()
+
+
+def test_workspace_sizes():
+    for dt in (fp.F32, fp.BF16):
+        assert fp.flarepp_project_workspace_bytes(dt, 128) >= 4 * 128 * 128 * (4 if dt == fp.F32 else 2)
+        n = fp.flarepp_mixer_workspace_bytes(dt, 4, 16384, 128, 8, 128)
+        bs = 4 if dt == fp.F32 else 2
+        assert n >= 5 * 4 * 16384 * 128 * bs  # K, K~, V, V~, Y at least
+        assert fp.flarepp_route_workspace_bytes(fp.ENCODE, dt, 2, 8, 1000, 64, 16) > 0
+        assert fp.flarepp_route_workspace_bytes(fp.DECODE, dt, 2, 8, 1000, 64, 16) > 0
+    # invalid shapes size to zero
+    assert fp.flarepp_mixer_workspace_bytes(fp.BF16, 1, 10, 100, 3, 4) == 0
+    assert fp.flarepp_mixer_workspace_bytes(7, 1, 10, 64, 4, 4) == 0
+    assert fp.flarepp_route_workspace_bytes(5, fp.BF16, 1, 1, 10, 4, 16) == 0
+
+
+def test_forced_chunk_count_changes_encode_workspace(monkeypatch):
+    base = fp.flarepp_route_workspace_bytes(fp.ENCODE, fp.BF16, 1, 1, 4096, 64, 16)
+    monkeypatch.setenv("FLAREPP_FORCE_CHUNKS", "200")
+    forced = fp.flarepp_route_workspace_bytes(fp.ENCODE, fp.BF16, 1, 1, 4096, 64, 16)
+    assert forced > base
+
+
+_P = ctypes.c_void_p(4096)  # aligned, never dereferenced: validation fails first
+
+
+def _mixer(dtype=fp.BF16, B=1, N=64, C=64, H=4, M=32, ptrs=None, ws=_P, ws_bytes=1 << 30):
+    lib = _lib()
+    p = ptrs or [_P] * 8
+    return lib.flarepp_mixer_forward(dtype, B, N, C, H, M, *p, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), fp.ERR_INVALID_ARG),
+    (dict(N=0), fp.ERR_INVALID_ARG),
+    (dict(M=0), fp.ERR_INVALID_ARG),
+    (dict(H=0), fp.ERR_INVALID_ARG),
+    (dict(C=100, H=3), fp.ERR_INVALID_ARG),
+    (dict(C=96, H=2), fp.ERR_UNSUPPORTED),     # D = 48
+    (dict(C=32, H=4), fp.ERR_UNSUPPORTED),     # D = 8
+    (dict(C=48, H=3), fp.ERR_UNSUPPORTED),     # C not a multiple of 32
+    (dict(dtype=3), fp.ERR_UNSUPPORTED),
+    (dict(ws=None), fp.ERR_WORKSPACE),
+    (dict(ws_bytes=100), fp.ERR_WORKSPACE),
+])
+def test_mixer_rejects_invalid_arguments(kw, code):
+    assert _mixer(**kw) == code
+    assert fp.last_error() != ""
+
+
+def test_mixer_rejects_null_and_misaligned_pointers():
+    for i in range(8):
+        ptrs = [_P] * 8
+        ptrs[i] = None
+        assert _mixer(ptrs=ptrs) == fp.ERR_INVALID_ARG
+        ptrs[i] = ctypes.c_void_p(4096 + 8)
+        assert _mixer(ptrs=ptrs) == fp.ERR_INVALID_ARG
+        assert "aligned" in fp.last_error()
+
+
+def test_route_rejects_invalid_arguments():
+    lib = _lib()
+
+    def call(kind=fp.ENCODE, dtype=fp.BF16, B=1, H=2, N=64, M=32, D=16, stride=0, lse=None,
+             ws=_P, wsb=1 << 30):
+        return lib.flarepp_route(kind, dtype, B, H, N, M, D, _P, stride, _P, _P, _P, lse, ws, wsb, None)
+
+    assert call(kind=2) == fp.ERR_UNSUPPORTED
+    assert call(D=24) == fp.ERR_UNSUPPORTED
+    assert call(N=0) == fp.ERR_INVALID_ARG
+    assert call(M=-1) == fp.ERR_INVALID_ARG
+    assert call(stride=5) == fp.ERR_INVALID_ARG
+    assert call(kind=fp.DECODE, lse=_P) == fp.ERR_INVALID_ARG
+    assert call(ws=None) == fp.ERR_WORKSPACE
+    assert call(wsb=16) == fp.ERR_WORKSPACE
+
+
+def test_project_rejects_unpaired_weights():
+    lib = _lib()
+    p = [_P, _P, None, None, _P, None, None, None]  # Wk, Wv given; outputs K only
+    rc = lib.flarepp_project(fp.BF16, 1, 64, 64, 4, _P, *p, _P, 1 << 20, None)
+    assert rc == fp.ERR_INVALID_ARG
+    rc = lib.flarepp_project(fp.BF16, 1, 64, 64, 4, _P, *([None] * 8), _P, 1 << 20, None)
+    assert rc == fp.ERR_INVALID_ARG
+    rc = lib.flarepp_project(fp.BF16, 1, 64, 64, 4, _P, _P, None, None, None, _P, None, None, None,
+                             _P, 16, None)
+    assert rc == fp.ERR_WORKSPACE

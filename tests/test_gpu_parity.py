@@ -1,0 +1,263 @@
+"""GPU parity of the HIP path (through the C ABI) against the float64 oracle.
+
+Gates (per tensor, relative to the reference's own max |.|): fp32 path
+1e-4, bf16 path 2e-2.  Applied to the output O and to every stage: the
+synthesised queries Q(X), the latents Z and the decoded tokens Y.  The fp32
+path also gets a centred gate on Y and O (token mean removed on both sides,
+tolerance derived in gpu_util), which a decode that ignored its scores
+would fail.
+"""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import flarepp_oracle as orc
+from paper_2608_11519_amd import flarepp as fp
+from paper_2608_11519_amd import inputs as inp
+
+from gpu_util import CENTRED_TOL, TOL, assert_close, centred, run_mixer, upload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fp.load()
+    yield
+
+
+def _check_mixer(w, d, label, centred_gate=False, stages=True):
+    print(f"[case] {label} {inp.describe(w)}", flush=True)
+    got = run_mixer(d, w, debug=stages)
+    ref = orc.mixer_forward(d["X"], d["Wk"], d["Wv"], d["Wkt"], d["Wvt"], d["Wo"], d["seeds"], w.H)
+    tol = TOL[w.dtype]
+    errs = {}
+    for k in (("O", "Q", "Z", "Y") if stages else ("O",)):
+        errs[k] = assert_close(k, got[k], ref[k], tol, label)
+    if centred_gate:
+        for k in ("Y", "O"):
+            assert_close(k + "-centred", centred(got[k]), centred(ref[k]), CENTRED_TOL, label)
+    return got, ref, errs
+
+
+# ---------------------------------------------------------------------------
+# the five workloads
+# ---------------------------------------------------------------------------
+
+def test_tiny_fp32_all_stages_and_centred():
+    w = inp.workload("tiny")
+    _check_mixer(w, inp.make_inputs(w, 0), "tiny", centred_gate=True)
+
+
+@pytest.mark.parametrize("name", ["grid2d", "lra"])
+def test_bf16_workload_full_size(name):
+    w = inp.workload(name)
+    _check_mixer(w, inp.make_inputs(w, 0), name)
+
+
+def test_mesh_workload_full_size():
+    w = inp.workload("mesh")
+    _check_mixer(w, inp.make_inputs(w, 0), "mesh")
+
+
+def test_mesh3d_full_size_sampled_tokens():
+    """The 2^20-token workload: Q and Z checked in full; Y and O on a sample
+    of tokens (the oracle's decode and merge are per token)."""
+    w = inp.workload("mesh3d")
+    d = inp.make_inputs(w, 0)
+    print(f"[case] mesh3d {inp.describe(w)}", flush=True)
+    got = run_mixer(d, w, debug=True)
+    X = d["X"].astype(np.float64)
+    H, D = w.H, w.D
+    Kt = orc.project(X, d["Wkt"], H)
+    Vt = orc.project(X, d["Wvt"], H)
+    Q, _ = orc.sdpa(d["seeds"][None], Kt, Vt)
+    del Kt, Vt
+    K = orc.project(X, d["Wk"], H)
+    V = orc.project(X, d["Wv"], H)
+    Z, _ = orc.sdpa(Q, K, V)
+    del V
+    tol = TOL[w.dtype]
+    assert_close("Q", got["Q"], Q, tol, "mesh3d")
+    assert_close("Z", got["Z"], Z, tol, "mesh3d")
+    idx = np.sort(np.random.Generator(np.random.PCG64(1)).choice(w.N, 512, replace=False))
+    idx = np.unique(np.concatenate([idx, [0, w.N - 1]]))
+    Yh, _ = orc.sdpa(K[:, :, idx], Q, Z)
+    Y = orc.merge_heads(Yh)
+    O = Y @ d["Wo"].astype(np.float64)
+    assert_close("Y[sample]", got["Y"][:, idx], Y, tol, "mesh3d")
+    assert_close("O[sample]", got["O"][:, idx], O, tol, "mesh3d")
+
+
+# ---------------------------------------------------------------------------
+# stress variants and edges
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sharp_seeds(dtype):
+    # seeds x8: routing weights far from uniform, so score bugs show
+    w = inp.Workload("sharp", 2, 2048, 128, 8, 64, dtype, "normal")
+    _check_mixer(w, inp.make_inputs(w, 1, seed_scale=8.0), "sharp", centred_gate=(dtype == "f32"))
+
+
+# "Hot" tokens (X scaled up) push the call-2 and call-3 scores beyond the
+# shift-free range, so tiles switch to the online-maximum update.  The scale is
+# bounded by the precision of the scores themselves: at X x30 the call-2 scores
+# reach ~900 (natural-log units), where fp32 rounding alone moves the
+# exponents by ~1e-4 and bf16 rounding by units, for any implementation.
+def test_hot_tokens_take_the_online_max_path_fp32():
+    w = inp.Workload("hot", 2, 1000, 64, 4, 32, "f32", "normal")
+    _check_mixer(w, inp.make_inputs(w, 2, x_scale=6.0), "hot", centred_gate=True)
+
+
+def test_hot_tokens_bf16():
+    w = inp.Workload("hot", 1, 1500, 64, 4, 32, "bf16", "normal")
+    _check_mixer(w, inp.make_inputs(w, 2, x_scale=4.0), "hot-bf16")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_online_max_path_everywhere(monkeypatch, dtype):
+    # the same mixer with the shift-free path switched off on the host
+    monkeypatch.setenv("FLAREPP_NO_FAST_PATH", "1")
+    w = inp.Workload("nofast", 2, 3000, 128, 8, 96, dtype, "normal")
+    _check_mixer(w, inp.make_inputs(w, 12, seed_scale=4.0), "nofast", centred_gate=(dtype == "f32"))
+
+
+@pytest.mark.parametrize("N", [1, 7, 31, 33, 63, 65, 1000])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_token_tails(N, dtype):
+    w = inp.Workload("tail", 2, N, 64, 4, 32, dtype, "normal")
+    _check_mixer(w, inp.make_inputs(w, 3, seed_scale=4.0), f"tail-N{N}")
+
+
+@pytest.mark.parametrize("M", [1, 16, 100, 300])
+def test_route_counts_including_m_above_n(M):
+    w = inp.Workload("routes", 2, 200, 64, 4, M, "f32", "normal")
+    got, ref, _ = _check_mixer(w, inp.make_inputs(w, 4, seed_scale=4.0), f"M{M}")
+    if M == 1:  # one route: every token receives Z
+        for h in range(w.H):
+            ys = got["Y"][:, :, h * w.D:(h + 1) * w.D]
+            np.testing.assert_allclose(ys, np.broadcast_to(got["Z"][:, h, 0][:, None], ys.shape),
+                                       rtol=1e-5, atol=1e-6)
+
+
+@pytest.mark.parametrize("D", [32, 64])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_head_widths(D, dtype):
+    w = inp.Workload("width", 2, 777, 2 * D, 2, 48, dtype, "normal")
+    _check_mixer(w, inp.make_inputs(w, 5, seed_scale=4.0), f"D{D}")
+
+
+@pytest.mark.parametrize("chunks", [1, 3, 40])
+def test_forced_chunk_counts_and_empty_chunks(monkeypatch, chunks):
+    # 40 chunks of 32 tokens over N=600 leaves the last chunks empty
+    monkeypatch.setenv("FLAREPP_FORCE_CHUNKS", str(chunks))
+    w = inp.Workload("chunks", 2, 600, 64, 4, 64, "f32", "normal")
+    _check_mixer(w, inp.make_inputs(w, 6, seed_scale=4.0), f"R{chunks}")
+
+
+def test_deterministic_bitwise():
+    w = inp.Workload("det", 2, 5000, 128, 8, 128, "bf16", "normal")
+    d = inp.make_inputs(w, 7)
+    t = upload(d, w)
+    args = (t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"], t["seeds"])
+    a = fp.flarepp_mixer_forward(*args, H=w.H)
+    b = fp.flarepp_mixer_forward(*args, H=w.H)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_permutation_equivariance_on_gpu():
+    w = inp.Workload("perm", 1, 3000, 64, 4, 32, "f32", "normal")
+    d = inp.make_inputs(w, 8, seed_scale=6.0)
+    perm = np.random.Generator(np.random.PCG64(9)).permutation(w.N)
+    a = run_mixer(d, w)
+    d2 = dict(d)
+    d2["X"] = np.ascontiguousarray(d["X"][:, perm])
+    b = run_mixer(d2, w)
+    np.testing.assert_allclose(b["O"], a["O"][:, perm], rtol=0, atol=1e-5 * np.abs(a["O"]).max())
+    np.testing.assert_allclose(b["Q"], a["Q"], rtol=0, atol=1e-5 * np.abs(a["Q"]).max())
+
+
+# ---------------------------------------------------------------------------
+# the other two entry points
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_project_entry_point(dtype):
+    w = inp.Workload("proj", 2, 333, 128, 8, 8, dtype, "normal")
+    d = inp.make_inputs(w, 10)
+    t = upload(d, w)
+    K, V, Kt, Vt = fp.flarepp_project(t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], H=w.H)
+    torch.cuda.synchronize()
+    for name, W, got in (("K", "Wk", K), ("V", "Wv", V), ("Kt", "Wkt", Kt), ("Vt", "Wvt", Vt)):
+        ref = orc.project(d["X"], d[W], w.H)
+        assert_close(name, got.float().cpu().numpy(), ref, TOL[dtype] / 2, "project")
+    # a single pair
+    K2, V2, Kt2, Vt2 = fp.flarepp_project(t["X"], Wv=t["Wv"], H=w.H)
+    torch.cuda.synchronize()
+    assert K2 is None and Kt2 is None and Vt2 is None
+    assert torch.equal(V2, V)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shared", [True, False])
+def test_route_encode_entry_point(dtype, shared):
+    B, H, N, M, D = 2, 3, 1111, 40, 32
+    Bq = 1 if shared else B
+    q = inp.make_tensor((Bq, H, M, D), 11, "f32", scale=0.8)
+    k = inp.make_tensor((B, H, N, D), 12, dtype)
+    v = inp.make_tensor((B, H, N, D), 13, dtype)
+    td = torch.float32 if dtype == "f32" else torch.bfloat16
+    tq = torch.from_numpy(q).cuda()
+    tk = torch.from_numpy(k).cuda().to(td)
+    tv = torch.from_numpy(v).cuda().to(td)
+    out, lse = fp.flarepp_route(fp.ENCODE, tq, tk, tv, shared_routes=shared, want_lse=True)
+    torch.cuda.synchronize()
+    ref, Lref = orc.sdpa(q, k, v)
+    assert_close("encode", out.cpu().numpy(), ref, TOL[dtype], "route")
+    np.testing.assert_allclose(lse.cpu().numpy(), Lref, rtol=0, atol=(1e-4 if dtype == "f32" else 2e-2))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_route_decode_entry_point(dtype):
+    B, H, N, M, D = 2, 2, 999, 70, 16
+    q = inp.make_tensor((B, H, N, D), 14, dtype)
+    k = inp.make_tensor((B, H, M, D), 15, "f32", scale=1.5)
+    v = inp.make_tensor((B, H, M, D), 16, "f32")
+    td = torch.float32 if dtype == "f32" else torch.bfloat16
+    out = fp.flarepp_route(fp.DECODE, torch.from_numpy(q).cuda().to(td),
+                           torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda())
+    torch.cuda.synchronize()
+    ref, _ = orc.sdpa(q, k, v)  # [B, H, N, D]
+    assert_close("decode", out.float().cpu().numpy(), orc.merge_heads(ref), TOL[dtype], "route")
+
+
+def test_route_encode_shift_invariance_large_logits():
+    # a large constant shift of the keys along each route leaves the output
+    # unchanged; on the GPU it drives the online-maximum path
+    B, H, N, M, D = 1, 2, 3000, 32, 16
+    q = inp.make_tensor((B, H, M, D), 17, "f32", scale=2.0)
+    k = inp.make_tensor((B, H, N, D), 18, "f32")
+    v = inp.make_tensor((B, H, N, D), 19, "f32")
+    u = inp.make_tensor((1, H, 1, D), 20, "f32", scale=30.0)
+    tq = torch.from_numpy(q).cuda()
+    a, _ = fp.flarepp_route(fp.ENCODE, tq, torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda())
+    b, _ = fp.flarepp_route(fp.ENCODE, tq, torch.from_numpy(k + u).cuda(), torch.from_numpy(v).cuda())
+    torch.cuda.synchronize()
+    ref, _ = orc.sdpa(q, k, v)
+    assert_close("shifted", b.cpu().numpy(), ref, 1e-4, "route")
+    assert_close("unshifted", a.cpu().numpy(), ref, 1e-4, "route")
+
+
+def test_errors_surface_as_exceptions():
+    w = inp.Workload("err", 1, 64, 64, 4, 8, "bf16", "normal")
+    t = upload(inp.make_inputs(w, 0), w)
+    with pytest.raises(fp.FlareppError) as ei:
+        fp.flarepp_mixer_forward(t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"], t["seeds"], H=3)
+    assert ei.value.code in (fp.ERR_INVALID_ARG, fp.ERR_UNSUPPORTED)
