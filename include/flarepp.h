@@ -142,6 +142,27 @@ FLAREPP_API int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int
                                 const void* seeds, void* O, float* Q_out, float* Z_out,
                                 void* Y_out, void* ws, size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Profiling variant of flarepp_mixer_forward for timing each stage on the
+ * device.  `events` holds FLAREPP_PROFILE_EVENTS caller-created hipEvent_t
+ * handles (created with timing enabled); events[0] is recorded on `stream`
+ * before the first launch and events[i] after stage i:
+ *   1 weight fragments and seed operands   5 call 2 (encode) partials
+ *   2 project K, V, K~, V~                 6 call 2 combine -> Z
+ *   3 call 1 (query synthesis) partials    7 call 3 (decode) -> Y
+ *   4 call 1 combine -> Q(X)               8 merge O = Y W_O
+ * The library only records the events; reading them (hipEventElapsedTime
+ * after a synchronisation) is the caller's.  n_events must be
+ * FLAREPP_PROFILE_EVENTS, or 0 (then this is flarepp_mixer_forward).
+ * ------------------------------------------------------------------------- */
+#define FLAREPP_PROFILE_EVENTS 9
+FLAREPP_API int flarepp_mixer_forward_profiled(int dtype, int64_t B, int64_t N, int64_t C,
+                                   int64_t H, int64_t M, const void* X, const void* Wk,
+                                   const void* Wv, const void* Wkt, const void* Wvt,
+                                   const void* Wo, const void* seeds, void* O, void* ws,
+                                   size_t ws_bytes, void* stream, void* const* events,
+                                   int n_events);
+
 #ifdef __cplusplus
 }
 #endif

@@ -202,13 +202,15 @@ template <typename T>
 int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
                const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
-               size_t ws_bytes, hipStream_t s) {
+               size_t ws_bytes, hipStream_t s, hipEvent_t const* ev) {
   using namespace flarepp;
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
   const MixerWs w = mixer_ws(ws, dtype, B, N, C, H, M);
   if (ws_bytes < w.bytes)
     return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
   const float qscale = route_qscale(D);
+#define STAGE(i) do { if (ev) HIPTRY(hipEventRecord(ev[i], s)); } while (0)
+  STAGE(0);
 
   // 1. weights as MFMA fragments
   WeightFragParams wp{};
@@ -223,6 +225,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   sp.src = seeds; sp.src_bstride = 0; sp.B = 1; sp.H = (int)H; sp.M = (int)M; sp.Mp = (int)Mp;
   sp.D = (int)D; sp.qscale = qscale; sp.q_op = w.seeds_op; sp.z_op = nullptr;
   HIPTRY((launch_route_prep<T, T>(sp, s)));
+  STAGE(1);
 
   // 3. project: K, K~ token-major; V, V~ d-major (value operands)
   ProjParams pp{};
@@ -233,6 +236,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   pp.wf[2] = w.wf[2]; pp.out[2] = w.Kt;   pp.layout[2] = kHeadsTokenMajor;
   pp.wf[3] = w.wf[3]; pp.out[3] = w.Vtdm; pp.layout[3] = kHeadsDMajor;
   HIPTRY(launch_project<T>(pp, s));
+  STAGE(2);
 
   const EncPlan e = encode_plan(B, H, N, Mp, D);
   const int64_t tokHS = N * D, tokBS = H * N * D;          // token-major strides
@@ -246,20 +250,24 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   r1.qs = w.seeds_op; r1.qs_sb = 0; r1.qs_sh = rtHS; r1.qs_rows = (int)Mp;
   r1.part_ml = w.part_ml; r1.part_acc = w.part_acc;
   HIPTRY(launch_route<T>(r1, (int)D, false, s));
+  STAGE(3);
   CombineParams c1{};
   c1.part_ml = w.part_ml; c1.part_acc = w.part_acc; c1.BH = B * H; c1.R = e.nchunks;
   c1.M = (int)M; c1.Mp = (int)Mp; c1.D = (int)D; c1.qscale = qscale;
   c1.out32 = Q_out; c1.lse = nullptr; c1.q_op = w.q_op; c1.z_op = nullptr;
   HIPTRY(launch_combine<T>(c1, s));
+  STAGE(4);
 
   // 5. call 2: Z = SDPA(Q, K, V), softmax over tokens
   RouteParams r2 = r1;
   r2.ka = w.K; r2.va = w.Vdm;
   r2.qs = w.q_op; r2.qs_sb = rtBS; r2.qs_sh = rtHS; r2.qs_rows = (int)Mp;
   HIPTRY(launch_route<T>(r2, (int)D, false, s));
+  STAGE(5);
   CombineParams c2 = c1;
   c2.out32 = Z_out; c2.q_op = nullptr; c2.z_op = w.z_op;
   HIPTRY(launch_combine<T>(c2, s));
+  STAGE(6);
 
   // 6. call 3: Y = SDPA(K, Q, Z), softmax over routes, heads merged
   void* Y = Y_out ? Y_out : w.Y;
@@ -269,20 +277,31 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
   r3.y = Y; r3.y_sb = N * C; r3.y_row = C;
   HIPTRY(launch_route<T>(r3, (int)D, true, s));
+  STAGE(7);
 
   // 7. merge: O = Y W_O
   ProjParams mp{};
   mp.x = Y; mp.B = (int)B; mp.N = (int)N; mp.Np = (int)Np; mp.C = (int)C; mp.H = (int)H; mp.D = (int)D;
   mp.nw = 1; mp.wf[0] = w.wf[4]; mp.out[0] = O; mp.layout[0] = kPlain;
   HIPTRY(launch_project<T>(mp, s));
+  STAGE(8);
+#undef STAGE
   return ok();
 }
 
 int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
                 const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                 const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
-                size_t ws_bytes, void* stream) {
+                size_t ws_bytes, void* stream, void* const* events, int n_events) {
   TRY(check_mixer_shape(dtype, B, N, C, H, M));
+  if (n_events != 0 && n_events != FLAREPP_PROFILE_EVENTS)
+    return fail(FLAREPP_ERR_INVALID_ARG, "n_events=%d must be 0 or %d", n_events, FLAREPP_PROFILE_EVENTS);
+  if (n_events) {
+    if (!events) return fail(FLAREPP_ERR_INVALID_ARG, "events is NULL");
+    for (int i = 0; i < n_events; ++i)
+      if (!events[i]) return fail(FLAREPP_ERR_INVALID_ARG, "events[%d] is NULL", i);
+  }
+  hipEvent_t const* ev = n_events ? reinterpret_cast<hipEvent_t const*>(events) : nullptr;
   TRY(check_ptr(X, "X"));
   TRY(check_ptr(Wk, "Wk"));
   TRY(check_ptr(Wv, "Wv"));
@@ -299,9 +318,9 @@ int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == FLAREPP_F32)
     return mixer_impl<float>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
-                             Y_out, ws, ws_bytes, s);
+                             Y_out, ws, ws_bytes, s, ev);
   return mixer_impl<__bf16>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
-                            Y_out, ws, ws_bytes, s);
+                            Y_out, ws, ws_bytes, s, ev);
 }
 
 // ---- route ------------------------------------------------------------------
@@ -496,7 +515,16 @@ int flarepp_mixer_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
                           const void* Wvt, const void* Wo, const void* seeds, void* O, void* ws,
                           size_t ws_bytes, void* stream) {
   return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr,
-                     nullptr, ws, ws_bytes, stream);
+                     nullptr, ws, ws_bytes, stream, nullptr, 0);
+}
+
+int flarepp_mixer_forward_profiled(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                   const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                                   const void* Wvt, const void* Wo, const void* seeds, void* O,
+                                   void* ws, size_t ws_bytes, void* stream, void* const* events,
+                                   int n_events) {
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr,
+                     nullptr, ws, ws_bytes, stream, events, n_events);
 }
 
 int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
@@ -505,7 +533,7 @@ int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int6
                                 float* Q_out, float* Z_out, void* Y_out, void* ws, size_t ws_bytes,
                                 void* stream) {
   return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out, Y_out,
-                     ws, ws_bytes, stream);
+                     ws, ws_bytes, stream, nullptr, 0);
 }
 
 }  // extern "C"

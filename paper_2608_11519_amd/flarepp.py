@@ -31,7 +31,11 @@ EXPORTS = (
     "flarepp_project_workspace_bytes", "flarepp_project",
     "flarepp_route_workspace_bytes", "flarepp_route",
     "flarepp_mixer_workspace_bytes", "flarepp_mixer_forward", "flarepp_mixer_forward_debug",
+    "flarepp_mixer_forward_profiled",
 )
+PROFILE_EVENTS = 9
+PROFILE_STAGES = ("prep", "project", "call1_encode", "call1_combine", "call2_encode",
+                  "call2_combine", "call3_decode", "merge")
 
 _lib = None
 
@@ -72,6 +76,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_mixer_forward_debug.restype = i32
     lib.flarepp_mixer_forward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8
                                                 + [fp, fp, vp] + [vp, sz, vp])
+    lib.flarepp_mixer_forward_profiled.restype = i32
+    lib.flarepp_mixer_forward_profiled.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8
+                                                   + [vp, sz, vp, ctypes.POINTER(vp), i32])
     _lib = lib
     return lib
 
@@ -224,6 +231,32 @@ def flarepp_mixer_forward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int,
                                          _ptr(Y), _ptr(w), w.numel(), _stream(X.device))
     _check(rc)
     return O, Q, Z, Y
+
+
+def flarepp_mixer_forward_profiled(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, events,
+                                   out: Optional[torch.Tensor] = None,
+                                   ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Mixer forward that records ``events`` (PROFILE_EVENTS torch.cuda.Event
+    objects with timing enabled) around its stages on the current stream."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    dt = _dtype_code(X)
+    if len(events) != PROFILE_EVENTS:
+        raise ValueError(f"need {PROFILE_EVENTS} events")
+    stream = torch.cuda.current_stream(X.device)
+    for e in events:  # torch creates the underlying hipEvent_t on first record
+        if e.cuda_event == 0:
+            e.record(stream)
+    handles = (ctypes.c_void_p * PROFILE_EVENTS)(*[e.cuda_event for e in events])
+    O = out if out is not None else torch.empty_like(X)
+    w = _workspace(flarepp_mixer_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_mixer_forward_profiled(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv),
+                                            _ptr(Wkt), _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(O),
+                                            _ptr(w), w.numel(), ctypes.c_void_p(stream.cuda_stream),
+                                            handles, PROFILE_EVENTS)
+    _check(rc)
+    return O
 
 
 # short aliases
