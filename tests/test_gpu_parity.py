@@ -65,33 +65,26 @@ def test_mesh_workload_full_size():
     _check_mixer(w, inp.make_inputs(w, 0), "mesh")
 
 
-def test_mesh3d_full_size_sampled_tokens():
-    """The 2^20-token workload: Q and Z checked in full; Y and O on a sample
-    of tokens (the oracle's decode and merge are per token)."""
+def test_mesh3d_full_size_sampled():
+    """The 2^20-token workload at full size.  The float64 oracle needs minutes
+    here, so its values come from tests/golden/make_mesh3d_expected.py (which
+    calls only the oracle): every 8th route of Q(X) and Z for every head, and
+    Y and O at 258 sampled tokens.  Gates are relative to the max over the
+    full reference tensors (Q, Z) or over the sampled rows (Y, O)."""
+    path = os.path.join(os.path.dirname(__file__), "golden", "mesh3d_expected.npz")
+    ref = np.load(path, allow_pickle=False)
     w = inp.workload("mesh3d")
     d = inp.make_inputs(w, 0)
     print(f"[case] mesh3d {inp.describe(w)}", flush=True)
     got = run_mixer(d, w, debug=True)
-    X = d["X"].astype(np.float64)
-    H, D = w.H, w.D
-    Kt = orc.project(X, d["Wkt"], H)
-    Vt = orc.project(X, d["Wvt"], H)
-    Q, _ = orc.sdpa(d["seeds"][None], Kt, Vt)
-    del Kt, Vt
-    K = orc.project(X, d["Wk"], H)
-    V = orc.project(X, d["Wv"], H)
-    Z, _ = orc.sdpa(Q, K, V)
-    del V
     tol = TOL[w.dtype]
-    assert_close("Q", got["Q"], Q, tol, "mesh3d")
-    assert_close("Z", got["Z"], Z, tol, "mesh3d")
-    idx = np.sort(np.random.Generator(np.random.PCG64(1)).choice(w.N, 512, replace=False))
-    idx = np.unique(np.concatenate([idx, [0, w.N - 1]]))
-    Yh, _ = orc.sdpa(K[:, :, idx], Q, Z)
-    Y = orc.merge_heads(Yh)
-    O = Y @ d["Wo"].astype(np.float64)
-    assert_close("Y[sample]", got["Y"][:, idx], Y, tol, "mesh3d")
-    assert_close("O[sample]", got["O"][:, idx], O, tol, "mesh3d")
+    routes, tok = ref["routes"], ref["tokens"]
+    for k in ("Q", "Z"):
+        e = np.abs(got[k][:, :, routes] - ref[k]).max() / float(ref[k + "_absmax"])
+        print(f"  mesh3d {k}[routes]: max|err|/max|ref| = {e:.3e} (gate {tol:g})", flush=True)
+        assert e <= tol
+    assert_close("Y[tokens]", got["Y"][:, tok], ref["Y"], tol, "mesh3d")
+    assert_close("O[tokens]", got["O"][:, tok], ref["O"], tol, "mesh3d")
 
 
 # ---------------------------------------------------------------------------
