@@ -132,6 +132,17 @@ FLAREPP_API int flarepp_mixer_forward(int dtype, int64_t B, int64_t N, int64_t C
                           const void* seeds, void* O, void* ws, size_t ws_bytes,
                           void* stream);
 
+/* Which kernel sequence flarepp_mixer_forward runs for this shape:
+ * FLAREPP_PATH_FUSED (projections inside the routing kernels, decode fused
+ * with the merge; used when C is 64, 128 or 256 and the per-wave register
+ * and LDS budgets allow) or FLAREPP_PATH_UNFUSED (projection GEMM, three
+ * routing calls over materialised K, V, K~, V~, merge GEMM).  Both compute
+ * the same function.  Negative FLAREPP_ERR_* for an invalid shape. */
+#define FLAREPP_PATH_UNFUSED 0
+#define FLAREPP_PATH_FUSED 1
+FLAREPP_API int flarepp_mixer_path(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                   int64_t M);
+
 /* As flarepp_mixer_forward, and also copies the stage results for checking:
  * Q_out, Z_out float32 [B][H][M][D] (the synthesised queries Q(X) and the
  * latents Z), Y_out dtype [B][N][C] (decoded tokens, heads merged, before
@@ -151,6 +162,8 @@ FLAREPP_API int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int
  *   2 project K, V, K~, V~                 6 call 2 combine -> Z
  *   3 call 1 (query synthesis) partials    7 call 3 (decode) -> Y
  *   4 call 1 combine -> Q(X)               8 merge O = Y W_O
+ * On the fused path stages 2 and 8 are empty: the projections run inside
+ * stages 3, 5 and 7, and the merge inside stage 7.
  * The library only records the events; reading them (hipEventElapsedTime
  * after a synchronisation) is the caller's.  n_events must be
  * FLAREPP_PROFILE_EVENTS, or 0 (then this is flarepp_mixer_forward).

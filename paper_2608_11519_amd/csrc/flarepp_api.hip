@@ -36,6 +36,7 @@ constexpr int64_t kMaxRoutes = 1 << 16;
 constexpr int64_t kMaxWidth = 4096;
 constexpr int64_t kTargetUnits = 2048;  // waves per encode launch (8 per CU)
 constexpr int kMinChunk = 128;          // tokens per encode unit
+constexpr int64_t kFusedEncWaves = 1024;  // waves per fused encode launch (4 per CU)
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -169,29 +170,78 @@ struct Carver {
   }
 };
 
+// ---- mixer plan ------------------------------------------------------------
+struct MixerPlan {
+  bool fused;
+  EncPlan enc;   // unfused split (k_route)
+  // fused split (k_encode_fused)
+  int nqw, qgroups, nchunks, chunk;
+};
+
+int64_t next_pow2(int64_t x) {
+  int64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+MixerPlan mixer_plan(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  MixerPlan pl{};
+  const int64_t D = C / H, Mp = round_up(M, 32), bs = dtype_bytes(dtype);
+  const int ksc = (int)(C / 16);
+  const int cap = flarepp::fused_width_ok((int)C) ? flarepp::enc_nqw_cap((int)bs, (int)D, ksc) : 0;
+  const char* off = std::getenv("FLAREPP_UNFUSED");
+  pl.fused = cap > 0 && flarepp::dec_fused_ok((int)bs, (int)D, ksc) &&
+             flarepp::decode_fused_fits((int)C, (int)D, (int)Mp, (int)bs) && !(off && std::atoi(off) != 0);
+  pl.enc = encode_plan(B, H, N, Mp, D);
+  if (pl.fused) {
+    const int64_t hpg = D == 16 ? 2 : 1, qb = Mp / 32, slots = hpg * qb;
+    pl.nqw = (int)std::min<int64_t>(cap, next_pow2(slots));
+    pl.qgroups = (int)cdiv(slots, pl.nqw);
+    const int64_t per = B * (H / hpg) * pl.qgroups;
+    const char* force = std::getenv("FLAREPP_FORCE_CHUNKS");
+    const int64_t forced = force ? std::atoll(force) : 0;
+    int64_t R;
+    if (forced > 0) {
+      R = std::min<int64_t>(forced, 65536);
+      pl.chunk = (int)round_up(cdiv(N, R), 32);
+    } else {
+      const char* tw = std::getenv("FLAREPP_ENC_WAVES");
+      const int64_t target = tw && std::atoll(tw) > 0 ? std::atoll(tw) : kFusedEncWaves;
+      R = std::max<int64_t>(1, std::min<int64_t>(cdiv(target, per), cdiv(N, 64)));
+      pl.chunk = (int)round_up(cdiv(N, R), 32);
+      R = cdiv(N, pl.chunk);
+    }
+    pl.nchunks = (int)R;
+  }
+  return pl;
+}
+
 struct MixerWs {
   void *wf[5], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *q_op, *z_op, *Y;
   float *part_ml, *part_acc;
   size_t bytes;
 };
 
-MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                 const MixerPlan& pl) {
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
   const size_t bs = dtype_bytes(dtype);
-  const EncPlan e = encode_plan(B, H, N, Mp, D);
+  const int64_t R = pl.fused ? pl.nchunks : pl.enc.nchunks;
   Carver cv(base);
-  MixerWs w;
+  MixerWs w{};
   for (int i = 0; i < 5; ++i) w.wf[i] = cv.take(bs * C * C);
   w.seeds_op = cv.take(bs * H * Mp * D);
-  w.K = cv.take(bs * B * H * N * D);
-  w.Kt = cv.take(bs * B * H * N * D);
-  w.Vdm = cv.take(bs * B * H * D * Np);
-  w.Vtdm = cv.take(bs * B * H * D * Np);
-  w.part_ml = (float*)cv.take(sizeof(float) * e.nchunks * B * H * Mp * 2);
-  w.part_acc = (float*)cv.take(sizeof(float) * e.nchunks * B * H * Mp * D);
+  if (!pl.fused) {
+    w.K = cv.take(bs * B * H * N * D);
+    w.Kt = cv.take(bs * B * H * N * D);
+    w.Vdm = cv.take(bs * B * H * D * Np);
+    w.Vtdm = cv.take(bs * B * H * D * Np);
+    w.Y = cv.take(bs * B * N * C);
+  }
+  w.part_ml = (float*)cv.take(sizeof(float) * R * B * H * Mp * 2);
+  w.part_acc = (float*)cv.take(sizeof(float) * R * B * H * Mp * D);
   w.q_op = cv.take(bs * B * H * Mp * D);
   w.z_op = cv.take(bs * B * H * D * Mp);
-  w.Y = cv.take(bs * B * N * C);
   w.bytes = cv.off;
   return w;
 }
@@ -205,12 +255,54 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
                size_t ws_bytes, hipStream_t s, hipEvent_t const* ev) {
   using namespace flarepp;
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
-  const MixerWs w = mixer_ws(ws, dtype, B, N, C, H, M);
+  const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
+  const MixerWs w = mixer_ws(ws, dtype, B, N, C, H, M, pl);
   if (ws_bytes < w.bytes)
     return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
   const float qscale = route_qscale(D);
 #define STAGE(i) do { if (ev) HIPTRY(hipEventRecord(ev[i], s)); } while (0)
   STAGE(0);
+  if (pl.fused) {
+    // weights as fused-path fragments and the seed operand
+    PrepFusedParams pp{};
+    pp.C = (int)C;
+    const void* win[5] = {Wk, Wv, Wkt, Wvt, Wo};
+    const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain, kFragMerge};
+    for (int i = 0; i < 5; ++i) { pp.w[i] = win[i]; pp.wf[i] = w.wf[i]; pp.mode[i] = mode[i]; }
+    pp.seeds = seeds; pp.H = (int)H; pp.M = (int)M; pp.Mp = (int)Mp; pp.D = (int)D;
+    pp.qscale = qscale; pp.seeds_op = w.seeds_op;
+    HIPTRY(launch_prep_fused<T>(pp, s));
+    STAGE(1);
+    STAGE(2);  // the projections run inside the routing kernels
+    EncFusedParams ep{};
+    ep.x = X; ep.wkf = w.wf[2]; ep.wvf = w.wf[3]; ep.q_op = w.seeds_op; ep.q_sb = 0;
+    ep.B = (int)B; ep.N = (int)N; ep.C = (int)C; ep.H = (int)H; ep.Mp = (int)Mp; ep.QB = (int)(Mp / 32);
+    ep.qgroups = pl.qgroups; ep.chunk = pl.chunk; ep.nchunks = pl.nchunks; ep.fast_lim = fast_limit();
+    ep.part_ml = w.part_ml; ep.part_acc = w.part_acc;
+    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.nqw, s));  // call 1
+    STAGE(3);
+    CombineParams cp{};
+    cp.part_ml = w.part_ml; cp.part_acc = w.part_acc; cp.BH = B * H; cp.R = pl.nchunks;
+    cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale;
+    cp.out32 = Q_out; cp.q_op = w.q_op;
+    HIPTRY(launch_combine_par<T>(cp, s));
+    STAGE(4);
+    ep.wkf = w.wf[0]; ep.wvf = w.wf[1]; ep.q_op = w.q_op; ep.q_sb = H * Mp * D;
+    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.nqw, s));  // call 2
+    STAGE(5);
+    cp.out32 = Z_out; cp.q_op = nullptr; cp.z_op = w.z_op;
+    HIPTRY(launch_combine_par<T>(cp, s));
+    STAGE(6);
+    DecFusedParams dp{};
+    dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = w.q_op; dp.z_op = w.z_op;
+    dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
+    dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O;
+    dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);
+    HIPTRY(launch_decode_fused<T>(dp, (int)D, s));  // call 3 + merge
+    STAGE(7);
+    STAGE(8);
+    return ok();
+  }
 
   // 1. weights as MFMA fragments
   WeightFragParams wp{};
@@ -238,7 +330,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   HIPTRY(launch_project<T>(pp, s));
   STAGE(2);
 
-  const EncPlan e = encode_plan(B, H, N, Mp, D);
+  const EncPlan e = pl.enc;
   const int64_t tokHS = N * D, tokBS = H * N * D;          // token-major strides
   const int64_t dmHS = D * Np, dmBS = H * D * Np;          // d-major token strides
   const int64_t rtHS = Mp * D, rtBS = H * Mp * D;          // route operand strides
@@ -255,7 +347,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   c1.part_ml = w.part_ml; c1.part_acc = w.part_acc; c1.BH = B * H; c1.R = e.nchunks;
   c1.M = (int)M; c1.Mp = (int)Mp; c1.D = (int)D; c1.qscale = qscale;
   c1.out32 = Q_out; c1.lse = nullptr; c1.q_op = w.q_op; c1.z_op = nullptr;
-  HIPTRY(launch_combine<T>(c1, s));
+  HIPTRY(launch_combine_par<T>(c1, s));
   STAGE(4);
 
   // 5. call 2: Z = SDPA(Q, K, V), softmax over tokens
@@ -266,7 +358,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   STAGE(5);
   CombineParams c2 = c1;
   c2.out32 = Z_out; c2.q_op = nullptr; c2.z_op = w.z_op;
-  HIPTRY(launch_combine<T>(c2, s));
+  HIPTRY(launch_combine_par<T>(c2, s));
   STAGE(6);
 
   // 6. call 3: Y = SDPA(K, Q, Z), softmax over routes, heads merged
@@ -398,7 +490,7 @@ int route_impl(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M, 
     CombineParams c{};
     c.part_ml = w.part_ml; c.part_acc = w.part_acc; c.BH = B * H; c.R = e.nchunks; c.M = (int)M;
     c.Mp = (int)Mp; c.D = (int)D; c.qscale = qscale; c.out32 = (float*)out; c.lse = lse;
-    HIPTRY(launch_combine<T>(c, s));
+    HIPTRY(launch_combine_par<T>(c, s));
   } else {
     rp.src = k; rp.q_op = w.q_op; rp.z_op = nullptr;
     HIPTRY((launch_route_prep<float, T>(rp, s)));
@@ -507,7 +599,12 @@ int flarepp_route(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t 
 
 size_t flarepp_mixer_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
   if (check_mixer_shape(dtype, B, N, C, H, M) != FLAREPP_OK) return 0;
-  return mixer_ws(nullptr, dtype, B, N, C, H, M).bytes;
+  return mixer_ws(nullptr, dtype, B, N, C, H, M, mixer_plan(dtype, B, N, C, H, M)).bytes;
+}
+
+int flarepp_mixer_path(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  TRY(check_mixer_shape(dtype, B, N, C, H, M));
+  return mixer_plan(dtype, B, N, C, H, M).fused ? FLAREPP_PATH_FUSED : FLAREPP_PATH_UNFUSED;
 }
 
 int flarepp_mixer_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,

@@ -131,4 +131,80 @@ __device__ __forceinline__ bool wave_all(bool pred) {
   return __builtin_amdgcn_ballot_w64(!pred) == 0;
 }
 
+// ---- one 32-key tile of the routing softmax --------------------------------
+// s holds S^T for 32 keys (rows) x 32 queries (cols) in log2 units.  Keys at
+// rows >= nvalid are masked.  Updates the query block's state: acc (out^T,
+// rows = value channels, plus the denominators in row 16 when ONES_ROW), m
+// (running shift, per query) and ls (denominator partial sums when not
+// ONES_ROW).  fast: every score of the tile lies within the shift-free range
+// and every m of the wave is -inf or 0, so the shift stays 0.
+template <typename T, int RB, bool ONES_ROW>
+__device__ __forceinline__ void softmax_pv_tile(f32x16 (&acc)[RB], float& m, float& ls, f32x16 s,
+                                                const typename Frag<T>::type (&vf)[2][RB],
+                                                int nvalid, bool fast, int lane) {
+  using F = typename Frag<T>::type;
+  if (nvalid < 32) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (acc_row(lane, e) >= nvalid) s[e] = -INFINITY;
+  }
+  if (fast) {
+    m = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e]);
+  } else {
+    float mx = s[0];
+#pragma unroll
+    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[e]);
+    mx = fmaxf(mx, other_half(mx));
+    const float mn = fmaxf(m, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m - mn);  // m = -inf -> 0
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[rb][e] *= alpha;
+    ls *= alpha;
+    m = mn;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e] - mn);
+  }
+  if (!ONES_ROW) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) ls += s[e];
+  }
+  F p0, p1;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    p0[e] = from_f32<T>(s[e]);
+    p1[e] = from_f32<T>(s[8 + e]);
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    mma(acc[rb], vf[0][rb], p0);
+    mma(acc[rb], vf[1][rb], p1);
+  }
+}
+
+// Softmax denominator of query column c after the last tile: row 16 of the
+// value product (ONES_ROW), else the two halves' partial sums.
+template <int RB, bool ONES_ROW>
+__device__ __forceinline__ float softmax_denominator(const f32x16 (&acc)[RB], float ls, int lane) {
+  if (ONES_ROW) {
+    const float a8 = acc[0][8];
+    const float o = other_half(a8);
+    return (lane >> 5) == 0 ? a8 : o;
+  }
+  return ls + other_half(ls);
+}
+
+// Upper bound on the squared norm of the rows a fragment set holds (rows are
+// split over the two wave halves), wave-uniform.
+template <typename T, int NF>
+__device__ __forceinline__ float frag_rows_max_sq(const typename Frag<T>::type (&f)[NF]) {
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NF; ++j) s += sumsq(f[j]);
+  return halfmax_sum_nonneg(s);
+}
+
 }  // namespace flarepp

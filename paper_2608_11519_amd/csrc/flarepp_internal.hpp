@@ -68,6 +68,72 @@ struct CombineParams {
   void* z_op;    // [BH][D][Mp], or null
 };
 
+// ---- fused path -------------------------------------------------------------
+enum FragMode { kFragPlain = 0, kFragKeyPerm = 1, kFragMerge = 2 };
+
+struct PrepFusedParams {
+  int C;
+  const void* w[5];  // W_K, W_V, W~_K, W~_V, W_O  [C][C]
+  void* wf[5];       // fragments [C/32][C/16][64][8]
+  int mode[5];       // FragMode per weight
+  const void* seeds;  // [H][M][D]
+  int H, M, Mp, D;
+  float qscale;
+  void* seeds_op;     // [H][Mp][D] scaled
+};
+
+struct EncFusedParams {
+  const void* x;                     // [B][N][C]
+  const void* wkf;                   // key fragments (key-permuted)
+  const void* wvf;                   // value fragments (plain)
+  const void* q_op; int64_t q_sb;    // [.][H][Mp][D] scaled queries, batch stride
+  int B, N, C, H, Mp, QB;
+  int qgroups, chunk, nchunks;
+  float fast_lim;
+  float* part_ml; float* part_acc;   // [B][H][nchunks][Mp] x {2 | D}
+};
+
+struct DecFusedParams {
+  const void* x;      // [B][N][C]
+  const void* wkf;    // key fragments (key-permuted)
+  const void* wof;    // merge fragments of W_O
+  const void* q_op;   // [B][H][Mp][D] scaled synthesised queries
+  const void* z_op;   // [B][H][D][Mp] latents
+  int B, N, C, H, M, Mp;
+  float fast_lim;
+  void* y;            // [B][N][C] decoded tokens, or null
+  void* o;            // [B][N][C]
+  int stage_elems;    // elements per LDS stage buffer
+};
+
+// Largest number of 32-query blocks one wave of the fused encode holds
+// without spilling registers (a power of two; 0: the fused encode is not
+// used for this storage size, head width and C = 16 * ksc).
+constexpr int enc_nqw_cap(int elem_bytes, int D, int ksc) {
+  if (elem_bytes == 2) {
+    if (D == 16) return ksc <= 8 ? 8 : 4;
+    if (D == 32) return 4;
+    return ksc <= 8 ? 2 : 0;
+  }
+  if (D == 16) return ksc <= 8 ? 4 : 0;
+  if (D == 32) return ksc <= 4 ? 4 : (ksc <= 8 ? 2 : 0);
+  return ksc <= 4 ? 1 : 0;
+}
+// The fused decode is used unless it would spill (fp32 with D = 64, C >= 128).
+constexpr bool dec_fused_ok(int elem_bytes, int D, int ksc) { return !(elem_bytes == 4 && D == 64 && ksc >= 8); }
+// The fused kernels are instantiated for these widths.
+constexpr bool fused_width_ok(int C) { return C == 64 || C == 128 || C == 256; }
+constexpr size_t enc_fused_lds(int C, int D, int elem_bytes) {
+  return 2ull * (D == 64 ? 2 : 1) * (C / 16) * 512 * elem_bytes;
+}
+int decode_stage_elems(int C, int D, int Mp);
+bool decode_fused_fits(int C, int D, int Mp, int elem_bytes);
+
+template <typename T> hipError_t launch_prep_fused(const PrepFusedParams&, hipStream_t);
+template <typename T> hipError_t launch_encode_fused(const EncFusedParams&, int D, int nqw, hipStream_t);
+template <typename T> hipError_t launch_combine_par(const CombineParams&, hipStream_t);
+template <typename T> hipError_t launch_decode_fused(const DecFusedParams&, int D, hipStream_t);
+
 // Exponent range (log2 units) inside which the softmax runs without a running
 // maximum: with |t| <= 64 every 2^t, every row sum over 2^20+ keys and every
 // weighted sum of values stays a normal fp32 number.
@@ -82,7 +148,6 @@ template <typename T> hipError_t launch_weight_frags(const WeightFragParams&, hi
 template <typename Ts, typename T> hipError_t launch_route_prep(const RoutePrepParams&, hipStream_t);
 template <typename T> hipError_t launch_dmajor(const DmajorParams&, hipStream_t);
 template <typename T> hipError_t launch_project(const ProjParams&, hipStream_t);
-template <typename T> hipError_t launch_combine(const CombineParams&, hipStream_t);
 template <typename T> hipError_t launch_route(const RouteParams&, int D, bool decode, hipStream_t);
 
 }  // namespace flarepp

@@ -12,11 +12,11 @@
 //                                     yields the softmax denominators)
 // For the two encode calls the queries are the M routes and the keys are a
 // chunk of the N tokens; each unit writes a partial (m, l, acc) that
-// k_combine merges exactly in a fixed chunk order (App. A.2-A.3, Eqs. (19)-(28),
+// k_combine_par merges exactly in a fixed chunk order (App. A.2-A.3, Eqs. (19)-(28),
 // with (m, l) carrying the log-normaliser L_r = m + log l).  For the decode the
 // queries are 32-token blocks and the keys are all M routes; each unit writes
 // normalised head outputs straight into Y[B][N][C].  The N x M scores never
-// leave registers.
+// leave registers.  k_combine_par (flarepp_fused.hip) merges the partials.
 //
 // Scores are pre-scaled by log2(e)/sqrt(D) on the query operand (the route
 // side), so the exponentials are bare v_exp_f32.  While the Cauchy-Schwarz
@@ -241,46 +241,7 @@ __global__ __launch_bounds__(256) void k_route(RouteParams p) {
       for (int e = 0; e < 16; ++e) s[e] = 0.f;
 #pragma unroll
       for (int j = 0; j < KS; ++j) mma(s, kf[j], qf[i][j]);
-      if (nvalid < 32) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (acc_row(lane, e) >= nvalid) s[e] = -INFINITY;
-      }
-      if (fast) {
-        m[i] = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e]);
-      } else {
-        float mx = s[0];
-#pragma unroll
-        for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[e]);
-        mx = fmaxf(mx, other_half(mx));
-        const float mn = fmaxf(m[i], mx);
-        const float alpha = __builtin_amdgcn_exp2f(m[i] - mn);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[i][rb][e] *= alpha;
-        ls[i] *= alpha;
-        m[i] = mn;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e] - mn);
-      }
-      if (!ONES_ROW) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) ls[i] += s[e];
-      }
-      F p0, p1;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p0[e] = from_f32<T>(s[e]);
-        p1[e] = from_f32<T>(s[8 + e]);
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        mma(acc[i][rb], vf[0][rb], p0);
-        mma(acc[i][rb], vf[1][rb], p1);
-      }
+      softmax_pv_tile<T, RB, ONES_ROW>(acc[i], m[i], ls[i], s, vf, nvalid, fast, lane);
     }
     if (!fast) {
       bool ok = true;
@@ -294,14 +255,7 @@ __global__ __launch_bounds__(256) void k_route(RouteParams p) {
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
     if (qb0 + i >= p.nqb) continue;
-    float l;
-    if (ONES_ROW) {
-      const float a8 = acc[i][0][8];
-      const float o = other_half(a8);
-      l = g == 0 ? a8 : o;
-    } else {
-      l = ls[i] + other_half(ls[i]);
-    }
+    const float l = softmax_denominator<RB, ONES_ROW>(acc[i], ls[i], lane);
     const int qrow = (qb0 + i) * 32 + c;
     constexpr int NQ4 = ONES_ROW ? 2 : 4;  // groups of 4 output rows per row block
     if (!DECODE) {
@@ -328,41 +282,6 @@ __global__ __launch_bounds__(256) void k_route(RouteParams p) {
                  acc[i][rb][4 * q + 2] * inv, acc[i][rb][4 * q + 3] * inv);
     }
   }
-}
-
-// ---------------------------------------------------------------------------
-// Exact merge of the per-chunk partials, in fixed chunk order (App. A.3,
-// Eqs. (24)-(28)): m* = max_r m_r; a = sum_r l_r 2^(m_r - m*);
-// out = sum_r acc_r 2^(m_r - m*) / a; L = ln 2 (m* + log2 a).  Empty chunks
-// (m_r = -inf, l_r = 0, acc_r = 0) contribute nothing.
-// ---------------------------------------------------------------------------
-template <typename T>
-__global__ void k_combine(CombineParams p) {
-  const int64_t total = (int64_t)p.BH * p.Mp * p.D;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= total) return;
-  const int d = (int)(idx % p.D);
-  const int qrow = (int)((idx / p.D) % p.Mp);
-  const int64_t bh = idx / ((int64_t)p.D * p.Mp);
-  float mmax = -INFINITY;
-  for (int r = 0; r < p.R; ++r) mmax = fmaxf(mmax, p.part_ml[((bh * p.R + r) * p.Mp + qrow) * 2]);
-  float a = 0.f, num = 0.f;
-  if (mmax > -INFINITY) {
-    for (int r = 0; r < p.R; ++r) {
-      const int64_t pidx = (bh * p.R + r) * p.Mp + qrow;
-      const float mr = p.part_ml[pidx * 2];
-      if (mr == -INFINITY) continue;
-      const float w = __builtin_amdgcn_exp2f(mr - mmax);
-      a = __builtin_fmaf(w, p.part_ml[pidx * 2 + 1], a);
-      num = __builtin_fmaf(w, p.part_acc[pidx * p.D + d], num);
-    }
-  }
-  const bool valid = qrow < p.M;
-  const float out = (valid && a > 0.f) ? num / a : 0.f;
-  if (valid && p.out32) p.out32[(bh * p.M + qrow) * p.D + d] = out;
-  if (valid && p.lse && d == 0) p.lse[bh * p.M + qrow] = 0.6931471805599453f * (mmax + __log2f(a));
-  if (p.q_op) ((T*)p.q_op)[(bh * p.Mp + qrow) * p.D + d] = from_f32<T>(out * p.qscale);
-  if (p.z_op) ((T*)p.z_op)[(bh * p.D + d) * p.Mp + qrow] = from_f32<T>(out);
 }
 
 // ---------------------------------------------------------------------------
@@ -398,13 +317,6 @@ hipError_t launch_project(const ProjParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t launch_combine(const CombineParams& p, hipStream_t s) {
-  const int64_t n = (int64_t)p.BH * p.Mp * p.D;
-  k_combine<T><<<blocks_for(n, 256), 256, 0, s>>>(p);
-  return hipGetLastError();
-}
-
 template <typename T, int D, bool DEC>
 static hipError_t launch_route_d(const RouteParams& p, hipStream_t s) {
   const int64_t units = (int64_t)p.B * p.H * p.nchunks * p.qgroups;
@@ -433,8 +345,6 @@ template hipError_t launch_dmajor<float>(const DmajorParams&, hipStream_t);
 template hipError_t launch_dmajor<__bf16>(const DmajorParams&, hipStream_t);
 template hipError_t launch_project<float>(const ProjParams&, hipStream_t);
 template hipError_t launch_project<__bf16>(const ProjParams&, hipStream_t);
-template hipError_t launch_combine<float>(const CombineParams&, hipStream_t);
-template hipError_t launch_combine<__bf16>(const CombineParams&, hipStream_t);
 template hipError_t launch_route<float>(const RouteParams&, int, bool, hipStream_t);
 template hipError_t launch_route<__bf16>(const RouteParams&, int, bool, hipStream_t);
 

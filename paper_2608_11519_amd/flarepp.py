@@ -31,8 +31,10 @@ EXPORTS = (
     "flarepp_project_workspace_bytes", "flarepp_project",
     "flarepp_route_workspace_bytes", "flarepp_route",
     "flarepp_mixer_workspace_bytes", "flarepp_mixer_forward", "flarepp_mixer_forward_debug",
-    "flarepp_mixer_forward_profiled",
+    "flarepp_mixer_forward_profiled", "flarepp_mixer_path",
 )
+PATH_UNFUSED = 0
+PATH_FUSED = 1
 PROFILE_EVENTS = 9
 PROFILE_STAGES = ("prep", "project", "call1_encode", "call1_combine", "call2_encode",
                   "call2_combine", "call3_decode", "merge")
@@ -76,6 +78,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_mixer_forward_debug.restype = i32
     lib.flarepp_mixer_forward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8
                                                 + [fp, fp, vp] + [vp, sz, vp])
+    lib.flarepp_mixer_path.restype = i32
+    lib.flarepp_mixer_path.argtypes = [i32, i64, i64, i64, i64, i64]
     lib.flarepp_mixer_forward_profiled.restype = i32
     lib.flarepp_mixer_forward_profiled.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8
                                                    + [vp, sz, vp, ctypes.POINTER(vp), i32])
@@ -138,6 +142,13 @@ def flarepp_route_workspace_bytes(kind: int, dtype: int, B: int, H: int, N: int,
 
 def flarepp_mixer_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
     return int(load().flarepp_mixer_workspace_bytes(dtype, B, N, C, H, M))
+
+
+def flarepp_mixer_path(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
+    """PATH_FUSED or PATH_UNFUSED (the kernel sequence the mixer runs)."""
+    rc = int(load().flarepp_mixer_path(dtype, B, N, C, H, M))
+    _check(rc if rc < 0 else OK)
+    return rc
 
 
 # ---------------------------------------------------------------------------

@@ -39,18 +39,42 @@ def test_library_exports_every_declared_symbol():
     assert "gfx950" in fp.version()
 
 
-def test_workspace_sizes():
+def test_workspace_sizes(monkeypatch):
     for dt in (fp.F32, fp.BF16):
-        assert fp.flarepp_project_workspace_bytes(dt, 128) >= 4 * 128 * 128 * (4 if dt == fp.F32 else 2)
-        n = fp.flarepp_mixer_workspace_bytes(dt, 4, 16384, 128, 8, 128)
         bs = 4 if dt == fp.F32 else 2
-        assert n >= 5 * 4 * 16384 * 128 * bs  # K, K~, V, V~, Y at least
+        assert fp.flarepp_project_workspace_bytes(dt, 128) >= 4 * 128 * 128 * bs
+        n = fp.flarepp_mixer_workspace_bytes(dt, 4, 16384, 128, 8, 128)
+        assert n >= 5 * 128 * 128 * bs + 2 * 4 * 8 * 128 * 16 * bs  # weights, Q and Z operands
+        monkeypatch.setenv("FLAREPP_UNFUSED", "1")
+        nu = fp.flarepp_mixer_workspace_bytes(dt, 4, 16384, 128, 8, 128)
+        monkeypatch.delenv("FLAREPP_UNFUSED")
+        assert nu >= 5 * 4 * 16384 * 128 * bs  # K, K~, V, V~, Y
+        # the fused path never materialises K, V, K~, V~ or Y
+        assert n < nu - 4 * 4 * 16384 * 128 * bs
         assert fp.flarepp_route_workspace_bytes(fp.ENCODE, dt, 2, 8, 1000, 64, 16) > 0
         assert fp.flarepp_route_workspace_bytes(fp.DECODE, dt, 2, 8, 1000, 64, 16) > 0
     # invalid shapes size to zero
     assert fp.flarepp_mixer_workspace_bytes(fp.BF16, 1, 10, 100, 3, 4) == 0
     assert fp.flarepp_mixer_workspace_bytes(7, 1, 10, 64, 4, 4) == 0
     assert fp.flarepp_route_workspace_bytes(5, fp.BF16, 1, 1, 10, 4, 16) == 0
+
+
+@pytest.mark.parametrize("name", ["tiny", "grid2d", "mesh", "lra", "mesh3d"])
+def test_workloads_take_the_fused_path(name):
+    from paper_2608_11519_amd import inputs as inp
+    w = inp.workload(name)
+    dt = fp.F32 if w.dtype == "f32" else fp.BF16
+    assert fp.flarepp_mixer_path(dt, w.B, w.N, w.C, w.H, w.M) == fp.PATH_FUSED
+
+
+def test_unfused_path_for_other_widths(monkeypatch):
+    assert fp.flarepp_mixer_path(fp.BF16, 1, 100, 32, 2, 16) == fp.PATH_UNFUSED   # C = 32
+    assert fp.flarepp_mixer_path(fp.BF16, 1, 100, 512, 8, 16) == fp.PATH_UNFUSED  # C = 512
+    assert fp.flarepp_mixer_path(fp.F32, 1, 100, 128, 2, 16) == fp.PATH_UNFUSED   # fp32, D = 64
+    monkeypatch.setenv("FLAREPP_UNFUSED", "1")
+    assert fp.flarepp_mixer_path(fp.BF16, 4, 16384, 128, 8, 128) == fp.PATH_UNFUSED
+    with pytest.raises(fp.FlareppError):
+        fp.flarepp_mixer_path(fp.BF16, 1, 100, 100, 3, 16)
 
 
 def test_forced_chunk_count_changes_encode_workspace(monkeypatch):

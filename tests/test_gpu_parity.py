@@ -154,6 +154,29 @@ def test_forced_chunk_counts_and_empty_chunks(monkeypatch, chunks):
     _check_mixer(w, inp.make_inputs(w, 6, seed_scale=4.0), f"R{chunks}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", ["sharp", "tail"])
+def test_unfused_path(monkeypatch, dtype, name):
+    # the projection GEMM + routing kernels over materialised K, V, K~, V~
+    monkeypatch.setenv("FLAREPP_UNFUSED", "1")
+    if name == "sharp":
+        w = inp.Workload("unfused", 2, 2048, 128, 8, 64, dtype, "normal")
+        d = inp.make_inputs(w, 1, seed_scale=8.0)
+    else:
+        w = inp.Workload("unfused", 2, 77, 64, 4, 40, dtype, "normal")
+        d = inp.make_inputs(w, 3, seed_scale=4.0)
+    dt = fp.F32 if dtype == "f32" else fp.BF16
+    assert fp.flarepp_mixer_path(dt, w.B, w.N, w.C, w.H, w.M) == fp.PATH_UNFUSED
+    _check_mixer(w, d, f"unfused-{name}", centred_gate=(dtype == "f32"))
+
+
+@pytest.mark.parametrize("C,H", [(32, 2), (512, 8)])
+def test_widths_outside_the_fused_kernels(C, H):
+    w = inp.Workload("wide", 1, 300, C, H, 32, "bf16", "normal")
+    assert fp.flarepp_mixer_path(fp.BF16, w.B, w.N, w.C, w.H, w.M) == fp.PATH_UNFUSED
+    _check_mixer(w, inp.make_inputs(w, 13, seed_scale=4.0), f"C{C}")
+
+
 def test_deterministic_bitwise():
     w = inp.Workload("det", 2, 5000, 128, 8, 128, "bf16", "normal")
     d = inp.make_inputs(w, 7)
