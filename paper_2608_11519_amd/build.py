@@ -30,6 +30,9 @@ def command(out: str = LIB):
         hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
         # packed fp32 ops are kept out of the generated code on purpose
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # MFMA accumulators in VGPRs: the softmax reads and rescales them with
+        # VALU, and the AGPR form would copy them around every MFMA
+        "-mllvm", "-amdgpu-mfma-vgpr-form=1",
         "-fvisibility=hidden", "-Wall", "-Wno-unused-result",
         "-o", out,
     ] + [os.path.join(CSRC, s) for s in SOURCES]

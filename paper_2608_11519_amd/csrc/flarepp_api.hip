@@ -36,7 +36,7 @@ constexpr int64_t kMaxRoutes = 1 << 16;
 constexpr int64_t kMaxWidth = 4096;
 constexpr int64_t kTargetUnits = 2048;  // waves per encode launch (8 per CU)
 constexpr int kMinChunk = 128;          // tokens per encode unit
-constexpr int64_t kFusedEncWaves = 1024;  // waves per fused encode launch (4 per CU)
+constexpr int64_t kFusedEncWaves = 2048;  // waves per fused encode launch (8 per CU)
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -175,7 +175,7 @@ struct MixerPlan {
   bool fused;
   EncPlan enc;   // unfused split (k_route)
   // fused split (k_encode_fused)
-  int nqw, qgroups, nchunks, chunk;
+  int waves, nqw, qgroups, nchunks, chunk;
 };
 
 int64_t next_pow2(int64_t x) {
@@ -188,27 +188,30 @@ MixerPlan mixer_plan(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int6
   MixerPlan pl{};
   const int64_t D = C / H, Mp = round_up(M, 32), bs = dtype_bytes(dtype);
   const int ksc = (int)(C / 16);
-  const int cap = flarepp::fused_width_ok((int)C) ? flarepp::enc_nqw_cap((int)bs, (int)D, ksc) : 0;
+  const int64_t hpg = D == 16 ? 2 : 1, slots = hpg * (Mp / 32);
+  pl.waves = flarepp::enc_waves((int)D, (int)C, (int)slots);
   const char* off = std::getenv("FLAREPP_UNFUSED");
-  pl.fused = cap > 0 && flarepp::dec_fused_ok((int)bs, (int)D, ksc) &&
-             flarepp::decode_fused_fits((int)C, (int)D, (int)Mp, (int)bs) && !(off && std::atoi(off) != 0);
+  pl.fused = flarepp::fused_width_ok((int)C, (int)bs) && flarepp::dec_fused_ok((int)bs, (int)D, ksc) &&
+             flarepp::decode_fused_fits((int)C, (int)D, (int)Mp, (int)bs) &&
+             flarepp::enc_fused_lds_bytes((int)C, (int)D, pl.waves, (int)bs) <= 160 * 1024 &&
+             !(off && std::atoi(off) != 0);
   pl.enc = encode_plan(B, H, N, Mp, D);
   if (pl.fused) {
-    const int64_t hpg = D == 16 ? 2 : 1, qb = Mp / 32, slots = hpg * qb;
-    pl.nqw = (int)std::min<int64_t>(cap, next_pow2(slots));
-    pl.qgroups = (int)cdiv(slots, pl.nqw);
-    const int64_t per = B * (H / hpg) * pl.qgroups;
+    pl.nqw = (int)std::min<int64_t>(flarepp::enc_nqw_cap((int)D, pl.waves), next_pow2(cdiv(slots, pl.waves)));
+    pl.qgroups = (int)cdiv(slots, (int64_t)pl.waves * pl.nqw);
+    const int64_t per = B * (H / hpg) * pl.qgroups;  // workgroups per token chunk
+    const int64_t step = 32 * pl.waves;                // tokens per workgroup step
     const char* force = std::getenv("FLAREPP_FORCE_CHUNKS");
     const int64_t forced = force ? std::atoll(force) : 0;
     int64_t R;
     if (forced > 0) {
       R = std::min<int64_t>(forced, 65536);
-      pl.chunk = (int)round_up(cdiv(N, R), 32);
+      pl.chunk = (int)round_up(cdiv(N, R), step);
     } else {
       const char* tw = std::getenv("FLAREPP_ENC_WAVES");
       const int64_t target = tw && std::atoll(tw) > 0 ? std::atoll(tw) : kFusedEncWaves;
-      R = std::max<int64_t>(1, std::min<int64_t>(cdiv(target, per), cdiv(N, 64)));
-      pl.chunk = (int)round_up(cdiv(N, R), 32);
+      R = std::max<int64_t>(1, std::min<int64_t>(cdiv(target / pl.waves, per), cdiv(N, step)));
+      pl.chunk = (int)round_up(cdiv(N, R), step);
       R = cdiv(N, pl.chunk);
     }
     pl.nchunks = (int)R;
@@ -219,6 +222,7 @@ MixerPlan mixer_plan(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int6
 struct MixerWs {
   void *wf[5], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *q_op, *z_op, *Y;
   float *part_ml, *part_acc;
+  unsigned* rnorm2;
   size_t bytes;
 };
 
@@ -241,7 +245,8 @@ MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t
   w.part_ml = (float*)cv.take(sizeof(float) * R * B * H * Mp * 2);
   w.part_acc = (float*)cv.take(sizeof(float) * R * B * H * Mp * D);
   w.q_op = cv.take(bs * B * H * Mp * D);
-  w.z_op = cv.take(bs * B * H * D * Mp);
+  w.z_op = cv.take(bs * B * H * (pl.fused ? flarepp::z_frag_elems_per_head((int)Mp, (int)D) : D * Mp));
+  w.rnorm2 = (unsigned*)cv.take(sizeof(unsigned) * B * H);
   w.bytes = cv.off;
   return w;
 }
@@ -270,31 +275,31 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain, kFragMerge};
     for (int i = 0; i < 5; ++i) { pp.w[i] = win[i]; pp.wf[i] = w.wf[i]; pp.mode[i] = mode[i]; }
     pp.seeds = seeds; pp.H = (int)H; pp.M = (int)M; pp.Mp = (int)Mp; pp.D = (int)D;
-    pp.qscale = qscale; pp.seeds_op = w.seeds_op;
+    pp.qscale = qscale; pp.seeds_op = w.seeds_op; pp.zero = w.rnorm2; pp.n_zero = (int)(B * H);
     HIPTRY(launch_prep_fused<T>(pp, s));
     STAGE(1);
     STAGE(2);  // the projections run inside the routing kernels
     EncFusedParams ep{};
     ep.x = X; ep.wkf = w.wf[2]; ep.wvf = w.wf[3]; ep.q_op = w.seeds_op; ep.q_sb = 0;
     ep.B = (int)B; ep.N = (int)N; ep.C = (int)C; ep.H = (int)H; ep.Mp = (int)Mp; ep.QB = (int)(Mp / 32);
-    ep.qgroups = pl.qgroups; ep.chunk = pl.chunk; ep.nchunks = pl.nchunks; ep.fast_lim = fast_limit();
-    ep.part_ml = w.part_ml; ep.part_acc = w.part_acc;
-    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.nqw, s));  // call 1
+    ep.nqw = pl.nqw; ep.qgroups = pl.qgroups; ep.chunk = pl.chunk; ep.nchunks = pl.nchunks;
+    ep.fast_lim = fast_limit(); ep.part_ml = w.part_ml; ep.part_acc = w.part_acc;
+    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 1
     STAGE(3);
     CombineParams cp{};
     cp.part_ml = w.part_ml; cp.part_acc = w.part_acc; cp.BH = B * H; cp.R = pl.nchunks;
-    cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale;
-    cp.out32 = Q_out; cp.q_op = w.q_op;
+    cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale; cp.frag = 1;
+    cp.out32 = Q_out; cp.q_op = w.q_op; cp.rnorm2 = w.rnorm2;
     HIPTRY(launch_combine_par<T>(cp, s));
     STAGE(4);
     ep.wkf = w.wf[0]; ep.wvf = w.wf[1]; ep.q_op = w.q_op; ep.q_sb = H * Mp * D;
-    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.nqw, s));  // call 2
+    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 2
     STAGE(5);
-    cp.out32 = Z_out; cp.q_op = nullptr; cp.z_op = w.z_op;
+    cp.out32 = Z_out; cp.q_op = nullptr; cp.rnorm2 = nullptr; cp.z_op = w.z_op;
     HIPTRY(launch_combine_par<T>(cp, s));
     STAGE(6);
     DecFusedParams dp{};
-    dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = w.q_op; dp.z_op = w.z_op;
+    dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = w.q_op; dp.z_op = w.z_op; dp.rnorm2 = w.rnorm2;
     dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
     dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O;
     dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);

@@ -26,6 +26,11 @@ template <> struct Frag<__bf16> { typedef bf16x8 type; typedef bf16x4 half; };
 template <> struct Frag<float> { typedef f32x8 type; typedef f32x4 half; };
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+// Wave index in the block, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+// A predicate every lane agrees on, made visibly wave-uniform so that the
+// compiler emits a scalar branch instead of running both paths under exec.
+__device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfirstlane((int)p) != 0; }
 __device__ __forceinline__ int acc_row(int lane, int r) {
   return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 }
@@ -123,7 +128,8 @@ __device__ __forceinline__ float halfmax_sum_nonneg(float x) {
   v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false)); // row_mirror
   int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
   int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
-  return __int_as_float(max(r0, r1)) + __int_as_float(max(r2, r3));
+  const float s = __int_as_float(max(r0, r1)) + __int_as_float(max(r2, r3));
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s)));
 }
 
 // True in every lane when pred holds in every active lane.
@@ -132,42 +138,28 @@ __device__ __forceinline__ bool wave_all(bool pred) {
 }
 
 // ---- one 32-key tile of the routing softmax --------------------------------
-// s holds S^T for 32 keys (rows) x 32 queries (cols) in log2 units.  Keys at
-// rows >= nvalid are masked.  Updates the query block's state: acc (out^T,
-// rows = value channels, plus the denominators in row 16 when ONES_ROW), m
-// (running shift, per query) and ls (denominator partial sums when not
-// ONES_ROW).  fast: every score of the tile lies within the shift-free range
-// and every m of the wave is -inf or 0, so the shift stays 0.
-template <typename T, int RB, bool ONES_ROW>
-__device__ __forceinline__ void softmax_pv_tile(f32x16 (&acc)[RB], float& m, float& ls, f32x16 s,
-                                                const typename Frag<T>::type (&vf)[2][RB],
-                                                int nvalid, bool fast, int lane) {
-  using F = typename Frag<T>::type;
-  if (nvalid < 32) {
+// s holds S^T for 32 keys (rows) x 32 queries (cols) in log2 units.  With
+// MASK, keys at rows >= nvalid are excluded.  acc is out^T (rows = value
+// channels, plus the denominators in row 16 when ONES_ROW); m is the running
+// shift per query and ls the denominator partial sums when not ONES_ROW.
+//
+// tile_shift_free: every score of the tile lies within the shift-free range
+// and the shift is 0, so the numerators are bare 2^s.  tile_online: the
+// usual online-maximum update.  Kernels run whole loops of one kind (no
+// per-tile branch between them), so the accumulators stay in place.
+template <bool MASK>
+__device__ __forceinline__ void mask_keys(f32x16& s, int nvalid, int lane) {
+  if (MASK) {
 #pragma unroll
     for (int e = 0; e < 16; ++e)
       if (acc_row(lane, e) >= nvalid) s[e] = -INFINITY;
   }
-  if (fast) {
-    m = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e]);
-  } else {
-    float mx = s[0];
-#pragma unroll
-    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[e]);
-    mx = fmaxf(mx, other_half(mx));
-    const float mn = fmaxf(m, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m - mn);  // m = -inf -> 0
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[rb][e] *= alpha;
-    ls *= alpha;
-    m = mn;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e] - mn);
-  }
+}
+
+template <typename T, int RB, bool ONES_ROW>
+__device__ __forceinline__ void pv_product(f32x16 (&acc)[RB], float& ls, const f32x16& s,
+                                           const typename Frag<T>::type (&vf)[2][RB]) {
+  using F = typename Frag<T>::type;
   if (!ONES_ROW) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) ls += s[e];
@@ -182,6 +174,57 @@ __device__ __forceinline__ void softmax_pv_tile(f32x16 (&acc)[RB], float& m, flo
   for (int rb = 0; rb < RB; ++rb) {
     mma(acc[rb], vf[0][rb], p0);
     mma(acc[rb], vf[1][rb], p1);
+  }
+}
+
+template <typename T, int RB, bool ONES_ROW, bool MASK>
+__device__ __forceinline__ void tile_shift_free(f32x16 (&acc)[RB], float& ls, f32x16 s,
+                                                const typename Frag<T>::type (&vf)[2][RB], int nvalid,
+                                                int lane) {
+  mask_keys<MASK>(s, nvalid, lane);
+#pragma unroll
+  for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e]);
+  pv_product<T, RB, ONES_ROW>(acc, ls, s, vf);
+}
+
+template <typename T, int RB, bool ONES_ROW, bool MASK>
+__device__ __forceinline__ void tile_online(f32x16 (&acc)[RB], float& m, float& ls, f32x16 s,
+                                            const typename Frag<T>::type (&vf)[2][RB], int nvalid, int lane) {
+  mask_keys<MASK>(s, nvalid, lane);
+  float mx = s[0];
+#pragma unroll
+  for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[e]);
+  mx = fmaxf(mx, other_half(mx));
+  const float mn = fmaxf(m, mx);
+  const float alpha = __builtin_amdgcn_exp2f(m - mn);  // m = -inf -> 0
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[rb][e] *= alpha;
+  ls *= alpha;
+  m = mn;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) s[e] = __builtin_amdgcn_exp2f(s[e] - mn);
+  pv_product<T, RB, ONES_ROW>(acc, ls, s, vf);
+}
+
+// Per-tile choice between the two (used where a loop mixes both kinds).
+template <typename T, int RB, bool ONES_ROW>
+__device__ __forceinline__ void softmax_pv_tile(f32x16 (&acc)[RB], float& m, float& ls, f32x16 s,
+                                                const typename Frag<T>::type (&vf)[2][RB],
+                                                int nvalid, bool fast, int lane) {
+  if (nvalid < 32) {
+    if (fast) {
+      m = 0.f;
+      tile_shift_free<T, RB, ONES_ROW, true>(acc, ls, s, vf, nvalid, lane);
+    } else {
+      tile_online<T, RB, ONES_ROW, true>(acc, m, ls, s, vf, nvalid, lane);
+    }
+  } else if (fast) {
+    m = 0.f;
+    tile_shift_free<T, RB, ONES_ROW, false>(acc, ls, s, vf, nvalid, lane);
+  } else {
+    tile_online<T, RB, ONES_ROW, false>(acc, m, ls, s, vf, nvalid, lane);
   }
 }
 

@@ -3,8 +3,8 @@
 // The mixer reads X three times (the two encode calls and the decode each
 // need a global reduction over all tokens before the next can start) and
 // writes O once; the projections K, V, K~, V~ and the decoded tokens Y never
-// reach HBM.  Each kernel recomputes the projection it needs from a 32-token
-// tile of X with MFMA, directly in the operand layout of the routing MFMAs:
+// reach HBM.  Each kernel recomputes the projection it needs from 32-token
+// tiles of X with MFMA, directly in the operand layout of the routing MFMAs:
 //
 //  * key projection, out^T = W^T X^T (rows = channels, cols = tokens): lane
 //    (c, g) receives token c and the channels of its accumulator rows.  The
@@ -14,20 +14,30 @@
 //    (d x tokens) of the decode scores.
 //  * value projection, out = X W (rows = tokens, cols = channels): lane (c, g)
 //    receives channel c for the tokens of its accumulator rows, which is the
-//    key order the score tile hands to the value product.  No data movement.
+//    key order the score tile hands to the value product.
 //  * decode output: the normalised head outputs stay in registers as the B
 //    operand of the merge O^T = W_O^T Y^T; the merge fragments read W_O rows
-//    in the accumulator's row order (merge_row) instead of moving data.
+//    in the accumulator's row order (acc_row16) instead of moving data.
 //
-// k_encode_fused  calls 1 and 2 (Sec. 2.2, Eqs. (8) and (10)): per (batch,
-//                 32-channel head group, query group, token chunk) one wave;
-//                 writes split-key partials (m, l, acc) per route.
+// Route operands (the seeds, Q(X) and Z) live in "fragment order" (see
+// flarepp_internal.hpp): every lane reads 16 contiguous bytes, so operand
+// loads from LDS or memory are free of bank conflicts.
+//
+// k_prep_fused    weight fragments, seed operand, cleared norm bounds.
+// k_encode_fused  calls 1 and 2 (Sec. 2.2, Eqs. (8) and (10)).  A workgroup
+//                 of W waves owns (batch, 32-channel head group, token chunk);
+//                 per step each wave projects one 32-token sub-tile into LDS,
+//                 then every wave runs its query blocks over all W sub-tiles.
+//                 Writes split-key partials (m, l, acc) per route.
 // k_combine_par   exact merge of the partials (App. A.3, Eqs. (24)-(28)) in a
-//                 fixed order, parallel over chunk slices.
+//                 fixed order, parallel over chunk slices; writes the next
+//                 call's route operands.
 // k_decode_fused  call 3 (Eq. (11)) and the merge with W_O (Fig. 1): per
-//                 (batch, 256 tokens) one workgroup of 8 waves; the route
-//                 operands of each head group and the W_O blocks are staged
-//                 through LDS, double buffered.
+//                 (batch, 32 * waves tokens) one workgroup; the route operands
+//                 of each head group and the W_O blocks are staged through LDS
+//                 (direct global -> LDS copies), double buffered.
+#include <type_traits>
+
 #include "flarepp_device.hpp"
 #include "flarepp_internal.hpp"
 
@@ -41,18 +51,37 @@ constexpr int kFrag = 512;  // elements of one 64-lane x 8 fragment
 __device__ __forceinline__ int key_perm(int rho) {
   return 16 * (rho >> 4) + 8 * ((rho >> 2) & 1) + 4 * ((rho & 15) >> 3) + (rho & 3);
 }
-// Input channel (within a 16-channel k step) of element j of a merge
-// fragment in half g: the accumulator row order of the decode output.
-__device__ __forceinline__ int merge_row(int g, int j) { return 8 * (j >> 2) + 4 * g + (j & 3); }
+// Row (within a 16-row group) of element j of half g: the accumulator row
+// order of a 32x32 MFMA result, 8 (j / 4) + 4 g + j % 4.
+__device__ __forceinline__ int acc_row16(int g, int j) { return 8 * (j >> 2) + 4 * g + (j & 3); }
+
+__device__ __forceinline__ void lds_wait_barrier() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+}
+
+// Copy n16 16-byte chunks src -> LDS dst with direct global -> LDS loads by
+// all nt threads of the block (each wave fills 1 KiB per step).
+__device__ __forceinline__ void copy_to_lds(const void* src, char* dst, int n16, int nt) {
+  const int wave = wave_id();
+  for (int k = 0; k * nt < n16; ++k) {
+    const int i = k * nt + threadIdx.x;
+    if (i < n16)
+      __builtin_amdgcn_global_load_lds(static_cast<const char*>(src) + (size_t)i * 16,
+                                       (__attribute__((address_space(3))) void*)(dst + (size_t)(k * nt + wave * 64) * 16),
+                                       16, 0, 0);
+  }
+}
 
 // ---------------------------------------------------------------------------
-// Weight fragments of the fused path and the seed operand, one launch.
+// Weight fragments of the fused path, seed operand, cleared norm bounds.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void k_prep_fused(PrepFusedParams p) {
   const int C = p.C, KS = C / 16;
   const int64_t per_w = (int64_t)C * C / 8;  // fragment lanes per weight
-  const int64_t nseed = (int64_t)p.H * p.Mp * p.D;
+  const int QB = p.Mp / 32, DS = p.D / 16;
+  const int64_t nseed = (int64_t)p.H * QB * DS * 64;
   int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx < 5 * per_w) {
     const int w = (int)(idx / per_w);
@@ -64,19 +93,26 @@ __global__ void k_prep_fused(PrepFusedParams p) {
     T* out = (T*)p.wf[w] + f * 8;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int row = 16 * ks + (mode == kFragMerge ? merge_row(g, j) : 8 * g + j);
+      const int row = 16 * ks + (mode == kFragMerge ? acc_row16(g, j) : 8 * g + j);
       out[j] = W[(int64_t)row * C + col];
     }
     return;
   }
   idx -= 5 * per_w;
-  if (idx < nseed) {
-    const int d = (int)(idx % p.D);
-    const int m = (int)((idx / p.D) % p.Mp);
-    const int h = (int)(idx / ((int64_t)p.D * p.Mp));
-    const float v = m < p.M ? to_f32(((const T*)p.seeds)[((int64_t)h * p.M + m) * p.D + d]) : 0.f;
-    ((T*)p.seeds_op)[idx] = from_f32<T>(v * p.qscale);
+  if (idx < nseed) {  // seeds -> q fragment order, scaled
+    const int lane = (int)(idx & 63), js = (int)((idx >> 6) % DS);
+    const int qb = (int)((idx >> 6) / DS % QB), h = (int)((idx >> 6) / DS / QB);
+    const int g = lane >> 5, m = 32 * qb + (lane & 31);
+    T* out = (T*)p.seeds_op + idx * 8;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float v = m < p.M ? to_f32(((const T*)p.seeds)[((int64_t)h * p.M + m) * p.D + 16 * js + 8 * g + j]) : 0.f;
+      out[j] = from_f32<T>(v * p.qscale);
+    }
+    return;
   }
+  idx -= nseed;
+  if (idx < p.n_zero) p.zero[idx] = 0u;
 }
 
 // ---- small helpers -----------------------------------------------------------
@@ -87,84 +123,73 @@ __device__ __forceinline__ typename Frag<T>::type cvt8(const f32x16& a, int off,
   for (int e = 0; e < 8; ++e) r[e] = from_f32<T>(a[off + e] * scale);
   return r;
 }
-// The fragment of lane l ^ 16 (moves the upper 16 columns of each half down).
-__device__ __forceinline__ bf16x8 xor16(const bf16x8& v) {
-  typedef __attribute__((ext_vector_type(4))) int i32x4;
-  i32x4 w = __builtin_bit_cast(i32x4, v);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = __shfl_xor(w[i], 16, 64);
-  return __builtin_bit_cast(bf16x8, w);
-}
-__device__ __forceinline__ f32x8 xor16(const f32x8& v) {
-  f32x8 r;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = __shfl_xor(v[i], 16, 64);
-  return r;
-}
 template <typename T>
-__device__ __forceinline__ typename Frag<T>::type pick(bool a, const typename Frag<T>::type& x,
-                                                       const typename Frag<T>::type& y) {
-  typename Frag<T>::type r;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = a ? x[e] : y[e];
-  return r;
+__device__ __forceinline__ void store_frag(T* p, const typename Frag<T>::type& v) {
+  *reinterpret_cast<typename Frag<T>::type*>(p) = v;
 }
 
 // ---------------------------------------------------------------------------
 // Encode with the projection fused (calls 1 and 2).
 // ---------------------------------------------------------------------------
-template <typename T, int D, int KSC, int NQW>
-__global__ __launch_bounds__(256) void k_encode_fused(EncFusedParams p) {
+template <int D> struct EncShape {
+  static constexpr int HPG = (D == 16) ? 2 : 1;  // heads per 32-channel group
+  static constexpr int GB = (D == 64) ? 2 : 1;   // 32-channel blocks per group
+  static constexpr int KS = D / 16, RB = (D + 31) / 32;
+  static constexpr int KFR = HPG * KS;           // key fragments per sub-tile
+  static constexpr int VFR = 2 * GB;             // value fragments per sub-tile
+  static constexpr int TILE = (KFR + VFR) * kFrag;
+};
+
+size_t enc_fused_lds_bytes(int C, int D, int waves, int elem_bytes) {
+  const int gb = D == 64 ? 2 : 1, hpg = D == 16 ? 2 : 1;
+  const size_t welems = (size_t)gb * (C / 16) * kFrag;
+  const size_t tile = (size_t)(hpg * (D / 16) + 2 * gb) * kFrag;
+  return (2 * welems + 2 * waves * tile) * elem_bytes + 2 * waves * hpg * sizeof(float);
+}
+
+template <typename T, int D, int KSC, int NQW, int W>
+__global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   using F = typename Frag<T>::type;
-  constexpr int HPG = (D == 16) ? 2 : 1;  // heads per 32-channel group
-  constexpr int GB = (D == 64) ? 2 : 1;   // 32-channel blocks per group
-  constexpr int KS = D / 16, RB = (D + 31) / 32;
+  using S = EncShape<D>;
+  constexpr int HPG = S::HPG, GB = S::GB, KS = S::KS, RB = S::RB, KFR = S::KFR, TILE = S::TILE;
   constexpr bool ONES_ROW = (D == 16);
-  constexpr int WELEMS = GB * KSC * kFrag;  // fragments of one weight slice
-  __shared__ __attribute__((aligned(16))) T wlds[2 * WELEMS];
+  constexpr int WELEMS = GB * KSC * kFrag;  // one weight slice of the head group
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  T* wk_l = reinterpret_cast<T*>(smem);
+  T* wv_l = wk_l + WELEMS;
+  T* tiles = wv_l + WELEMS;  // [2][W][TILE]
+  float* kmx = reinterpret_cast<float*>(tiles + 2 * W * TILE);  // [2][W][HPG]
 
-  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = threadIdx.x >> 6;
-  const int HG = p.H / HPG;
-  const int ncg = (p.nchunks + 3) >> 2;
-  int bid = blockIdx.x;
-  const int cg = bid % ncg;
-  bid /= ncg;
-  const int qg = bid % p.qgroups;
-  bid /= p.qgroups;
-  const int hg = bid % HG;
-  const int b = bid / HG;
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
+  const int HG = p.H / HPG, G = HG * p.qgroups;
+  // blocks of one token chunk (all head and query groups) share an XCD
+  const int bid = blockIdx.x;
+  const int64_t chunk_id = (int64_t)(bid >> 3) / G * 8 + (bid & 7);
+  if (chunk_id >= (int64_t)p.B * p.nchunks) return;  // whole block, before any barrier
+  const int hgq = (bid >> 3) % G;
+  const int hg = hgq / p.qgroups, qg = hgq % p.qgroups;
+  const int b = (int)(chunk_id / p.nchunks), r = (int)(chunk_id % p.nchunks);
 
-  {  // the head group's key and value weight slices -> LDS
-    constexpr int n16 = WELEMS * (int)sizeof(T) / 16;
-    const uint4* sk = reinterpret_cast<const uint4*>((const T*)p.wkf + (int64_t)hg * WELEMS);
-    const uint4* sv = reinterpret_cast<const uint4*>((const T*)p.wvf + (int64_t)hg * WELEMS);
-    uint4* dst = reinterpret_cast<uint4*>(wlds);
-    for (int i = threadIdx.x; i < n16; i += 256) {
-      dst[i] = sk[i];
-      dst[n16 + i] = sv[i];
-    }
-  }
-  __syncthreads();
-  const int r = cg * 4 + wave;
-  if (r >= p.nchunks) return;  // no barrier below
-  const T* wk_l = wlds;
-  const T* wv_l = wlds + WELEMS;
+  copy_to_lds((const T*)p.wkf + (int64_t)hg * WELEMS, smem, WELEMS * (int)sizeof(T) / 16, 64 * W);
+  copy_to_lds((const T*)p.wvf + (int64_t)hg * WELEMS, smem + WELEMS * sizeof(T), WELEMS * (int)sizeof(T) / 16,
+              64 * W);
 
-  // ---- query operands of the wave's slots (slot = head-in-group x block) ----
+  // ---- this wave's query slots (slot = head-in-group x 32-query block) ----
   const int nslots = HPG * p.QB;
+  const int slot0 = (qg * W + wave) * NQW;
   F qf[NQW][KS];
   float qn = 0.f;
 #pragma unroll
   for (int i = 0; i < NQW; ++i) {
-    const int s = qg * NQW + i;
+    const int s = slot0 + i;
     const bool ok = s < nslots;
     const int h = hg * HPG + (ok ? s / p.QB : 0), qb = ok ? s % p.QB : 0;
-    const T* qp = (const T*)p.q_op + (int64_t)b * p.q_sb + ((int64_t)h * p.Mp + qb * 32 + c) * D;
+    const T* qp = (const T*)p.q_op + (int64_t)b * p.q_sb + (int64_t)h * p.Mp * D;
     float sq = 0.f;
 #pragma unroll
-    for (int j = 0; j < KS; ++j) {
-      qf[i][j] = ok ? load_frag(qp + 16 * j + 8 * g) : zero_frag<T>();
-      sq += sumsq(qf[i][j]);
+    for (int js = 0; js < KS; ++js) {
+      qf[i][js] = ok ? load_frag(qp + ((int64_t)(qb * KS + js) * 64 + lane) * 8) : zero_frag<T>();
+      sq += sumsq(qf[i][js]);
     }
     qn = fmaxf(qn, sq);
   }
@@ -174,116 +199,147 @@ __global__ __launch_bounds__(256) void k_encode_fused(EncFusedParams p) {
   float m[NQW], ls[NQW];
 #pragma unroll
   for (int i = 0; i < NQW; ++i) {
-    m[i] = -INFINITY;
+    m[i] = 0.f;  // the shift of the shift-free phase
     ls[i] = 0.f;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][rb][e] = 0.f;
   }
-  bool fastok = true;
 
   const int k0 = r * p.chunk, k1 = min(p.N, k0 + p.chunk);
   const T* xb = (const T*)p.x + (int64_t)b * p.N * p.C;
   F xf[KSC];
   {
-    const bool ok = k0 + c < k1;
+    const int row = k0 + 32 * wave + c;
+    const bool ok = row < k1;
 #pragma unroll
     for (int ks = 0; ks < KSC; ++ks)
-      xf[ks] = ok ? load_frag(xb + (int64_t)(k0 + c) * p.C + 16 * ks + 8 * g) : zero_frag<T>();
+      xf[ks] = ok ? load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g) : zero_frag<T>();
   }
+  lds_wait_barrier();  // weight slices in LDS
 
-  for (int t0 = k0; t0 < k1; t0 += 32) {
-    const int nvalid = min(32, k1 - t0);
-    // prefetch the next tile of X
-    F xn[KSC];
-    {
-      const bool ok = t0 + 32 + c < k1;
-#pragma unroll
-      for (int ks = 0; ks < KSC; ++ks)
-        xn[ks] = ok ? load_frag(xb + (int64_t)(t0 + 32 + c) * p.C + 16 * ks + 8 * g) : zero_frag<T>();
-    }
-    // key projection -> score A operands
-    f32x16 ka[GB];
+  // Project sub-tile `wave` of the super-tile at t0 into LDS buffer it & 1.
+  auto produce = [&](int it, int t0) {
+    const int buf = it & 1;
+    f32x16 ka[GB], va[GB];
 #pragma unroll
     for (int cb = 0; cb < GB; ++cb) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) ka[cb][e] = 0.f;
+      for (int e = 0; e < 16; ++e) { ka[cb][e] = 0.f; va[cb][e] = 0.f; }
 #pragma unroll
-      for (int ks = 0; ks < KSC; ++ks)
-        mma(ka[cb], load_frag(wk_l + ((cb * KSC + ks) * 64 + lane) * 8), xf[ks]);
-    }
-    F kf[HPG][KS];
-#pragma unroll
-    for (int hh = 0; hh < HPG; ++hh)
-#pragma unroll
-      for (int j = 0; j < KS; ++j) {
-        const int fi = hh * KS + j;
-        kf[hh][j] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
-      }
-    // value projection -> value A operands (rows = channels)
-    f32x16 va[GB];
-#pragma unroll
-    for (int cb = 0; cb < GB; ++cb) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) va[cb][e] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KSC; ++ks)
-        mma(va[cb], xf[ks], load_frag(wv_l + ((cb * KSC + ks) * 64 + lane) * 8));
-    }
-    F vf[HPG][2][RB];
-    if (ONES_ROW) {
-      const F v0 = cvt8<T>(va[0], 0), v1 = cvt8<T>(va[0], 8);
-      const F w0 = xor16(v0), w1 = xor16(v1);
-      const F fill = (c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
-      vf[0][0][0] = pick<T>(c < 16, v0, fill);
-      vf[0][1][0] = pick<T>(c < 16, v1, fill);
-      vf[HPG - 1][0][0] = pick<T>(c < 16, w0, fill);
-      vf[HPG - 1][1][0] = pick<T>(c < 16, w1, fill);
-    } else {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        vf[0][0][rb] = cvt8<T>(va[rb], 0);
-        vf[0][1][rb] = cvt8<T>(va[rb], 8);
+      for (int ks = 0; ks < KSC; ++ks) {
+        const int fo = ((cb * KSC + ks) * 64 + lane) * 8;
+        mma(ka[cb], load_frag(wk_l + fo), xf[ks]);
+        mma(va[cb], xf[ks], load_frag(wv_l + fo));
       }
     }
-    float kmax2 = 0.f;
+    {  // prefetch this wave's rows of the next super-tile
+      const int row = t0 + 32 * W + 32 * wave + c;
+      const bool ok = row < k1;
 #pragma unroll
-    for (int hh = 0; hh < HPG; ++hh) kmax2 = fmaxf(kmax2, frag_rows_max_sq<T, KS>(kf[hh]));
-    const bool fast = fastok && (qmax2 * kmax2 <= p.fast_lim);
+      for (int ks = 0; ks < KSC; ++ks)
+        xf[ks] = ok ? load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g) : zero_frag<T>();
+    }
+    T* tl = tiles + (buf * W + wave) * TILE;
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      F kf[KS];
+#pragma unroll
+      for (int js = 0; js < KS; ++js) {
+        const int fi = hh * KS + js;
+        kf[js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
+        store_frag<T>(tl + fi * kFrag + lane * 8, kf[js]);
+      }
+      const float kb = frag_rows_max_sq<T, KS>(kf);
+      if (lane == 0) kmx[(buf * W + wave) * HPG + hh] = kb;
+    }
+#pragma unroll
+    for (int cb = 0; cb < GB; ++cb)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+        store_frag<T>(tl + (KFR + 2 * cb + hf) * kFrag + lane * 8, cvt8<T>(va[cb], 8 * hf));
+    __syncthreads();
+  };
 
+  // Run the wave's query slots over every sub-tile of the super-tile at t0,
+  // all shift-free (sf = true) or all with the online maximum.
+  auto consume = [&](auto sf, int it, int t0) {
+    constexpr bool SF = decltype(sf)::value;
+    const int buf = it & 1;
+#pragma unroll 1
+    for (int j = 0; j < W; ++j) {
+      const int nvalid = min(32, k1 - (t0 + 32 * j));
+      if (nvalid <= 0) break;
+      const T* tl = tiles + (buf * W + j) * TILE;
 #pragma unroll
-    for (int i = 0; i < NQW; ++i) {
-      const int s = qg * NQW + i;
-      if (s >= nslots) continue;
-      f32x16 sc;
+      for (int i = 0; i < NQW; ++i) {
+        const int s = slot0 + i;
+        if (s >= nslots) continue;
+        const int hh = HPG == 1 ? 0 : s / p.QB;
+        F kf[KS];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sc[e] = 0.f;
-      if (HPG == 1 || s < p.QB) {
+        for (int js = 0; js < KS; ++js) kf[js] = load_frag(tl + (hh * KS + js) * kFrag + lane * 8);
+        F vf[2][RB];
+        if (ONES_ROW) {
+          const F fill = (c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
 #pragma unroll
-        for (int j = 0; j < KS; ++j) mma(sc, kf[0][j], qf[i][j]);
-        softmax_pv_tile<T, RB, ONES_ROW>(acc[i], m[i], ls[i], sc, vf[0], nvalid, fast, lane);
-      } else {
+          for (int hf = 0; hf < 2; ++hf)
+            vf[hf][0] = c < 16 ? load_frag(tl + (KFR + hf) * kFrag + (16 * hh + c + 32 * g) * 8) : fill;
+        } else {
 #pragma unroll
-        for (int j = 0; j < KS; ++j) mma(sc, kf[HPG - 1][j], qf[i][j]);
-        softmax_pv_tile<T, RB, ONES_ROW>(acc[i], m[i], ls[i], sc, vf[HPG - 1], nvalid, fast, lane);
+          for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) vf[hf][rb] = load_frag(tl + (KFR + 2 * rb + hf) * kFrag + lane * 8);
+        }
+        f32x16 sc;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+        for (int js = 0; js < KS; ++js) mma(sc, kf[js], qf[i][js]);
+        if (nvalid == 32) {
+          if (SF) tile_shift_free<T, RB, ONES_ROW, false>(acc[i], ls[i], sc, vf, 32, lane);
+          else tile_online<T, RB, ONES_ROW, false>(acc[i], m[i], ls[i], sc, vf, 32, lane);
+        } else {
+          if (SF) tile_shift_free<T, RB, ONES_ROW, true>(acc[i], ls[i], sc, vf, nvalid, lane);
+          else tile_online<T, RB, ONES_ROW, true>(acc[i], m[i], ls[i], sc, vf, nvalid, lane);
+        }
       }
     }
-    if (!fast) {
-      bool ok = true;
+  };
+
+  // Shift-free phase: while every score of a super-tile is provably within
+  // the shift-free range (|q.k| <= max|q| max|k|); then the online phase.
+  int it = 0, t0 = k0;
+  bool used = false;
+  for (; t0 < k1; t0 += 32 * W, ++it) {
+    produce(it, t0);
+    float kb = 0.f;
+    for (int j = 0; j < W * HPG; ++j) kb = fmaxf(kb, kmx[(it & 1) * W * HPG + j]);
+    if (!uniform(qmax2 * kb <= p.fast_lim)) break;
+    consume(std::true_type{}, it, t0);
+    used = true;
+  }
+  if (t0 < k1) {
+    if (!used) {
 #pragma unroll
-      for (int i = 0; i < NQW; ++i) ok = ok && (m[i] == 0.f || m[i] == -INFINITY);
-      fastok = wave_all(ok);
+      for (int i = 0; i < NQW; ++i) m[i] = -INFINITY;
     }
+    consume(std::false_type{}, it, t0);
+    for (t0 += 32 * W, ++it; t0 < k1; t0 += 32 * W, ++it) {
+      produce(it, t0);
+      consume(std::false_type{}, it, t0);
+    }
+  } else if (!used) {
 #pragma unroll
-    for (int ks = 0; ks < KSC; ++ks) xf[ks] = xn[ks];
+    for (int i = 0; i < NQW; ++i) m[i] = -INFINITY;  // empty chunk
   }
 
   // ---- partials ----
   constexpr int NQ4 = ONES_ROW ? 2 : 4;
 #pragma unroll
   for (int i = 0; i < NQW; ++i) {
-    const int s = qg * NQW + i;
+    const int s = slot0 + i;
     if (s >= nslots) continue;
     const int h = hg * HPG + s / p.QB, qb = s % p.QB;
     const float l = softmax_denominator<RB, ONES_ROW>(acc[i], ls[i], lane);
@@ -310,6 +366,7 @@ __global__ __launch_bounds__(256) void k_encode_fused(EncFusedParams p) {
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
+  constexpr int KS = D / 16;
   const int t = threadIdx.x, rs = t & 15;
   const int rows_per_bh = p.Mp / 16;
   const int64_t bh = blockIdx.x / rows_per_bh;
@@ -352,6 +409,16 @@ __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
   }
   const bool valid = qrow < p.M;
   const float inv = (valid && l > 0.f) ? 1.f / l : 0.f;
+  const int qb = qrow >> 5, qc = qrow & 31;
+  if (p.frag && p.q_op && p.rnorm2 && rs == 0 && valid) {
+    float n2 = 0.f;
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const float q = to_f32(from_f32<T>(a[d] * inv * p.qscale));
+      n2 = __builtin_fmaf(q, q, n2);
+    }
+    atomicMax(p.rnorm2 + bh, __float_as_uint(n2));
+  }
 #pragma unroll
   for (int d0 = 0; d0 < D; d0 += 16) {
     const int d = d0 + rs;
@@ -361,8 +428,21 @@ __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
       if (k == d) v = a[k];
     const float out = v * inv;
     if (valid && p.out32) p.out32[(bh * p.M + qrow) * D + d] = out;
-    if (p.q_op) ((T*)p.q_op)[(bh * p.Mp + qrow) * D + d] = from_f32<T>(out * p.qscale);
-    if (p.z_op) ((T*)p.z_op)[(bh * D + d) * p.Mp + qrow] = from_f32<T>(out);
+    if (!p.frag) {
+      if (p.q_op) ((T*)p.q_op)[(bh * p.Mp + qrow) * D + d] = from_f32<T>(out * p.qscale);
+      if (p.z_op) ((T*)p.z_op)[(bh * D + d) * p.Mp + qrow] = from_f32<T>(out);
+    } else {
+      if (p.q_op) {  // q fragment order
+        const int js = d >> 4, gq = (d >> 3) & 1, jj = d & 7;
+        const int64_t off = (int64_t)bh * p.Mp * D + ((int64_t)(qb * KS + js) * 64 + gq * 32 + qc) * 8 + jj;
+        ((T*)p.q_op)[off] = from_f32<T>(out * p.qscale);
+      }
+      if (p.z_op) {  // z fragment order; row qc of route tile qb
+        const int hf = qc >> 4, rr = qc & 15, gz = (rr >> 2) & 1, jj = 4 * (rr >> 3) + (rr & 3);
+        T* z = (T*)p.z_op + bh * z_frag_elems_per_head(p.Mp, D);
+        z[z_frag_index(qb, hf, d >> 5, gz, d & 31, jj, D)] = from_f32<T>(out);
+      }
+    }
   }
   if (valid && p.lse && rs == 0) p.lse[bh * p.M + qrow] = 0.6931471805599453f * (m + __log2f(l));
 }
@@ -374,31 +454,38 @@ __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
 // resident X and Y fragments need more than 256 registers.
 constexpr int dec_waves(int C) { return C >= 256 ? 4 : 8; }
 
-// Issue the global -> LDS copy of decode stage s (see k_decode_fused) into
-// buffer s & 1; completion is awaited with vmcnt before the next barrier.
+int decode_stage_elems(int C, int D, int Mp) {
+  const int hpg = D == 16 ? 2 : 1, gb = D == 64 ? 2 : 1;
+  const int head_stage = gb * (C / 16) * kFrag + hpg * (Mp * D + (int)z_frag_elems_per_head(Mp, D));
+  const int wo_stage = (C / 16) * kFrag;
+  return head_stage > wo_stage ? head_stage : wo_stage;
+}
+
+bool decode_fused_fits(int C, int D, int Mp, int elem_bytes) {
+  const size_t se = (size_t)decode_stage_elems(C, D, Mp) * elem_bytes;
+  return 2 * se <= 160 * 1024;
+}
+
+// Issue the global -> LDS copy of decode stage s into buffer s & 1: for
+// s < HG [key weight slice][q fragments of the group's heads][z fragments of
+// them]; for s = HG + cb the W_O fragments of output block cb.
 template <typename T, int D, int KSC>
-__device__ __forceinline__ void decode_stage_issue(const DecFusedParams& p, char* smem, int SE, int b,
-                                                   int s) {
+__device__ __forceinline__ void decode_stage_issue(const DecFusedParams& p, char* smem, int SE, int b, int s) {
   constexpr int HPG = (D == 16) ? 2 : 1, GB = (D == 64) ? 2 : 1;
   constexpr int C = KSC * 16, HG = C / 32 / GB, WELEMS = GB * KSC * kFrag;
   constexpr int NT = 64 * dec_waves(C), per16 = 16 / (int)sizeof(T);
-  const int Mp = p.Mp, nq = HPG * Mp * D;
-  const int n16 = (s < HG ? WELEMS + 2 * nq : KSC * kFrag) / per16;
-  const int wave = threadIdx.x >> 6;
-  const int64_t h0 = (int64_t)b * p.H + (int64_t)s * HPG;
   char* dst = smem + (size_t)(s & 1) * SE * sizeof(T);
-  for (int k = 0; k * NT < n16; ++k) {
-    const int i = k * NT + threadIdx.x;
-    if (i >= n16) continue;
-    const int e = i * per16;
-    const T* src;
-    if (s >= HG) src = (const T*)p.wof + (int64_t)(s - HG) * KSC * kFrag + e;
-    else if (e < WELEMS) src = (const T*)p.wkf + (int64_t)s * WELEMS + e;
-    else if (e - WELEMS < nq) src = (const T*)p.q_op + h0 * Mp * D + (e - WELEMS);
-    else src = (const T*)p.z_op + h0 * D * Mp + (e - WELEMS - nq);
-    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(dst + (size_t)(k * NT + wave * 64) * 16),
-                                     16, 0, 0);
+  if (s >= HG) {
+    copy_to_lds((const T*)p.wof + (int64_t)(s - HG) * KSC * kFrag, dst, KSC * kFrag / per16, NT);
+    return;
   }
+  const int64_t h0 = (int64_t)b * p.H + (int64_t)s * HPG;
+  const int nq = HPG * p.Mp * D;
+  const int64_t nz = (int64_t)HPG * z_frag_elems_per_head(p.Mp, D);
+  copy_to_lds((const T*)p.wkf + (int64_t)s * WELEMS, dst, WELEMS / per16, NT);
+  copy_to_lds((const T*)p.q_op + h0 * p.Mp * D, dst + (size_t)WELEMS * sizeof(T), nq / per16, NT);
+  copy_to_lds((const T*)p.z_op + h0 * z_frag_elems_per_head(p.Mp, D), dst + (size_t)(WELEMS + nq) * sizeof(T),
+              (int)(nz / per16), NT);
 }
 
 template <typename T, int D, int KSC>
@@ -409,40 +496,30 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
   constexpr bool ONES_ROW = (D == 16);
   constexpr int C = KSC * 16, CB = C / 32, HG = CB / GB;
   constexpr int WELEMS = GB * KSC * kFrag;  // key weight slice of one head group
-  constexpr int NW = dec_waves(C), NT = 64 * NW, TOK = 32 * NW;
+  constexpr int NW = dec_waves(C), TOK = 32 * NW;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T* bufs = reinterpret_cast<T*>(smem);
   const int SE = p.stage_elems;
 
-  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = threadIdx.x >> 6;
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
   const int nblk = (p.N + TOK - 1) / TOK;
   const int b = blockIdx.x / nblk;
   const int xrow = (blockIdx.x % nblk) * TOK + wave * 32 + c;
   const bool xok = xrow < p.N;
-  const int Mp = p.Mp;
-  const int RT = Mp / 32;
+  const int Mp = p.Mp, RT = Mp / 32;
+  const int ZH = (int)z_frag_elems_per_head(Mp, D);
 
-  // stage s < HG: [key weight slice][q_op of the group's heads][z_op of them];
-  // stage HG + cb: the W_O fragments of output block cb.  Stage s lives in
-  // buffer s & 1 and is copied global -> LDS directly (16 bytes per lane).
-  auto stage_issue = [&](int s) { decode_stage_issue<T, D, KSC>(p, smem, SE, b, s); };
-  auto stage_wait = [&]() {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-  };
-
-  stage_issue(0);
+  decode_stage_issue<T, D, KSC>(p, smem, SE, b, 0);
   F xf[KSC];
 #pragma unroll
   for (int ks = 0; ks < KSC; ++ks)
-    xf[ks] = xok ? load_frag((const T*)p.x + ((int64_t)b * p.N + xrow) * C + 16 * ks + 8 * g)
-                 : zero_frag<T>();
-  stage_wait();
+    xf[ks] = xok ? load_frag((const T*)p.x + ((int64_t)b * p.N + xrow) * C + 16 * ks + 8 * g) : zero_frag<T>();
+  lds_wait_barrier();
 
   F yf[KSC];  // decoded tokens, merge B operands (16 channels per k step)
 #pragma unroll
   for (int hg = 0; hg < HG; ++hg) {
-    stage_issue(hg + 1);
+    decode_stage_issue<T, D, KSC>(p, smem, SE, b, hg + 1);
     const T* sb = bufs + (hg & 1) * SE;
     f32x16 ka[GB];
 #pragma unroll
@@ -457,47 +534,52 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
       const int h = hg * HPG + hh;
       F kf[KS];
 #pragma unroll
-      for (int j = 0; j < KS; ++j) {
-        const int fi = hh * KS + j;
-        kf[j] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
+      for (int js = 0; js < KS; ++js) {
+        const int fi = hh * KS + js;
+        kf[js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
       }
-      const float qmax2 = frag_rows_max_sq<T, KS>(kf);
+      // |score| bound: token-key norms x the route-query norm bound
+      const float bound = frag_rows_max_sq<T, KS>(kf) * __uint_as_float(p.rnorm2[(int64_t)b * p.H + h]);
+      const bool fast = uniform(bound <= p.fast_lim);
       const T* ql = sb + WELEMS + hh * Mp * D;
-      const T* zl = sb + WELEMS + HPG * Mp * D + hh * D * Mp;
+      const T* zl = sb + WELEMS + HPG * Mp * D + hh * ZH;
       f32x16 acc[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[rb][e] = 0.f;
       float m = -INFINITY, ls = 0.f;
-      bool fastok = true;
-      for (int rt = 0; rt < RT; ++rt) {
-        F qa[KS];
+      const F zfill = (c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
+      // all route tiles of the head shift-free (sf = true) or online
+      auto routes = [&](auto sf) {
+        constexpr bool SF = decltype(sf)::value;
+        for (int rt = 0; rt < RT; ++rt) {
+          F qa[KS];
 #pragma unroll
-        for (int j = 0; j < KS; ++j) qa[j] = load_frag(ql + (rt * 32 + c) * D + 16 * j + 8 * g);
-        F zv[2][RB];
+          for (int js = 0; js < KS; ++js) qa[js] = load_frag(ql + ((rt * KS + js) * 64 + lane) * 8);
+          F zv[2][RB];
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
+          for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-          for (int rb = 0; rb < RB; ++rb) {
-            const int d = rb * 32 + c;
-            if (d < D) {
-              const T* zp = zl + d * Mp + rt * 32 + 16 * hf + 4 * g;
-              zv[hf][rb] = join<T>(load_half(zp), load_half(zp + 8));
-            } else {
-              zv[hf][rb] = (ONES_ROW && c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
-            }
+            for (int rb = 0; rb < RB; ++rb)
+              zv[hf][rb] = (ONES_ROW && c >= 16) ? zfill : load_frag(zl + z_frag_index(rt, hf, rb, g, c, 0, D));
+          f32x16 sc;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+          for (int js = 0; js < KS; ++js) mma(sc, qa[js], kf[js]);
+          const int nvalid = min(32, p.M - rt * 32);
+          if (nvalid == 32) {
+            if (SF) tile_shift_free<T, RB, ONES_ROW, false>(acc, ls, sc, zv, 32, lane);
+            else tile_online<T, RB, ONES_ROW, false>(acc, m, ls, sc, zv, 32, lane);
+          } else {
+            if (SF) tile_shift_free<T, RB, ONES_ROW, true>(acc, ls, sc, zv, nvalid, lane);
+            else tile_online<T, RB, ONES_ROW, true>(acc, m, ls, sc, zv, nvalid, lane);
           }
-        const float kmax2 = frag_rows_max_sq<T, KS>(qa);
-        const bool fast = fastok && (qmax2 * kmax2 <= p.fast_lim);
-        f32x16 sc;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sc[e] = 0.f;
-#pragma unroll
-        for (int j = 0; j < KS; ++j) mma(sc, qa[j], kf[j]);
-        softmax_pv_tile<T, RB, ONES_ROW>(acc, m, ls, sc, zv, min(32, p.M - rt * 32), fast, lane);
-        if (!fast) fastok = wave_all(m == 0.f || m == -INFINITY);
-      }
+        }
+      };
+      if (fast) routes(std::true_type{});
+      else routes(std::false_type{});
       const float inv = 1.f / softmax_denominator<RB, ONES_ROW>(acc, ls, lane);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
@@ -515,14 +597,14 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
                    acc[rb][4 * q + 2] * inv, acc[rb][4 * q + 3] * inv);
       }
     }
-    stage_wait();
+    lds_wait_barrier();
   }
 
   // ---- merge: O^T = W_O^T Y^T, one 32-channel output block per stage ----
 #pragma unroll
   for (int cbo = 0; cbo < CB; ++cbo) {
     const int s = HG + cbo;
-    if (cbo + 1 < CB) stage_issue(s + 1);
+    if (cbo + 1 < CB) decode_stage_issue<T, D, KSC>(p, smem, SE, b, s + 1);
     const T* sb = bufs + (s & 1) * SE;
     f32x16 o;
 #pragma unroll
@@ -534,7 +616,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 #pragma unroll
       for (int q = 0; q < 4; ++q) store4(op + 8 * q + 4 * g, o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
     }
-    if (cbo + 1 < CB) stage_wait();
+    if (cbo + 1 < CB) lds_wait_barrier();
   }
 }
 
@@ -543,50 +625,59 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 // ---------------------------------------------------------------------------
 template <typename T>
 hipError_t launch_prep_fused(const PrepFusedParams& p, hipStream_t s) {
-  const int64_t n = 5 * (int64_t)p.C * p.C / 8 + (int64_t)p.H * p.Mp * p.D;
+  const int64_t n = 5 * (int64_t)p.C * p.C / 8 + (int64_t)p.H * (p.Mp / 32) * (p.D / 16) * 64 + p.n_zero;
   k_prep_fused<T><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
   return hipGetLastError();
 }
 
-template <typename T, int D, int KSC, int NQW>
-static hipError_t enc_one(const EncFusedParams& p, unsigned grid, hipStream_t s) {
-  if constexpr (NQW > enc_nqw_cap(sizeof(T), D, KSC) || enc_fused_lds(KSC * 16, D, sizeof(T)) > 65536) {
+template <typename T, int D, int KSC, int NQW, int W>
+static hipError_t enc_one(const EncFusedParams& p, hipStream_t s) {
+  if constexpr (NQW > enc_nqw_cap(D, W) || (W == 8 && (D != 16 || KSC > 8)) ||
+                !fused_width_ok(16 * KSC, sizeof(T))) {
     return hipErrorInvalidValue;
   } else {
-    k_encode_fused<T, D, KSC, NQW><<<grid, 256, 0, s>>>(p);
+    const int HG = p.H / EncShape<D>::HPG;
+    const int64_t nck = (int64_t)p.B * p.nchunks;
+    const unsigned grid = (unsigned)(((nck + 7) / 8) * 8 * HG * p.qgroups);
+    const size_t lds = enc_fused_lds_bytes(16 * KSC, D, W, sizeof(T));
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_encode_fused<T, D, KSC, NQW, W>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    k_encode_fused<T, D, KSC, NQW, W><<<grid, 64 * W, lds, s>>>(p);
     return hipGetLastError();
   }
 }
 
-template <typename T, int D, int KSC>
-static hipError_t enc_nqw(const EncFusedParams& p, int nqw, unsigned grid, hipStream_t s) {
-  switch (nqw) {
-    case 1: return enc_one<T, D, KSC, 1>(p, grid, s);
-    case 2: return enc_one<T, D, KSC, 2>(p, grid, s);
-    case 4: return enc_one<T, D, KSC, 4>(p, grid, s);
-    case 8: return enc_one<T, D, KSC, 8>(p, grid, s);
+template <typename T, int D, int KSC, int W>
+static hipError_t enc_nqw(const EncFusedParams& p, hipStream_t s) {
+  switch (p.nqw) {
+    case 1: return enc_one<T, D, KSC, 1, W>(p, s);
+    case 2: return enc_one<T, D, KSC, 2, W>(p, s);
+    case 4: return enc_one<T, D, KSC, 4, W>(p, s);
   }
   return hipErrorInvalidValue;
 }
 
-template <typename T, int D>
-static hipError_t enc_ksc(const EncFusedParams& p, int nqw, unsigned grid, hipStream_t s) {
+template <typename T, int D, int W>
+static hipError_t enc_ksc(const EncFusedParams& p, hipStream_t s) {
   switch (p.C) {
-    case 64: return enc_nqw<T, D, 4>(p, nqw, grid, s);
-    case 128: return enc_nqw<T, D, 8>(p, nqw, grid, s);
-    case 256: return enc_nqw<T, D, 16>(p, nqw, grid, s);
+    case 64: return enc_nqw<T, D, 4, W>(p, s);
+    case 128: return enc_nqw<T, D, 8, W>(p, s);
+    case 256: return enc_nqw<T, D, 16, W>(p, s);
   }
   return hipErrorInvalidValue;
 }
 
 template <typename T>
-hipError_t launch_encode_fused(const EncFusedParams& p, int D, int nqw, hipStream_t s) {
-  const int hpg = D == 16 ? 2 : 1;
-  const int64_t grid = (int64_t)p.B * (p.H / hpg) * p.qgroups * ((p.nchunks + 3) / 4);
+hipError_t launch_encode_fused(const EncFusedParams& p, int D, int waves, hipStream_t s) {
+  if (waves == 8) {
+    if (D == 16) return enc_ksc<T, 16, 8>(p, s);
+    return hipErrorInvalidValue;
+  }
   switch (D) {
-    case 16: return enc_ksc<T, 16>(p, nqw, (unsigned)grid, s);
-    case 32: return enc_ksc<T, 32>(p, nqw, (unsigned)grid, s);
-    case 64: return enc_ksc<T, 64>(p, nqw, (unsigned)grid, s);
+    case 16: return enc_ksc<T, 16, 4>(p, s);
+    case 32: return enc_ksc<T, 32, 4>(p, s);
+    case 64: return enc_ksc<T, 64, 4>(p, s);
   }
   return hipErrorInvalidValue;
 }
@@ -603,31 +694,19 @@ hipError_t launch_combine_par(const CombineParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-int decode_stage_elems(int C, int D, int Mp) {
-  const int hpg = D == 16 ? 2 : 1, gb = D == 64 ? 2 : 1;
-  const int head_stage = gb * (C / 16) * kFrag + 2 * hpg * Mp * D;
-  const int wo_stage = (C / 16) * kFrag;
-  return head_stage > wo_stage ? head_stage : wo_stage;
-}
-
-bool decode_fused_fits(int C, int D, int Mp, int elem_bytes) {
-  const size_t se = (size_t)decode_stage_elems(C, D, Mp) * elem_bytes;
-  return 2 * se <= 160 * 1024;
-}
-
 template <typename T, int D, int KSC>
 static hipError_t dec_launch(const DecFusedParams& p, hipStream_t s) {
-  if constexpr (!dec_fused_ok(sizeof(T), D, KSC)) {
+  if constexpr (!dec_fused_ok(sizeof(T), D, KSC) || !fused_width_ok(16 * KSC, sizeof(T))) {
     return hipErrorInvalidValue;
   } else {
-  constexpr int NW = dec_waves(16 * KSC);
-  const unsigned grid = (unsigned)((int64_t)p.B * ((p.N + 32 * NW - 1) / (32 * NW)));
-  const size_t lds = 2 * (size_t)p.stage_elems * sizeof(T);
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_fused<T, D, KSC>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  k_decode_fused<T, D, KSC><<<grid, 64 * NW, lds, s>>>(p);
-  return hipGetLastError();
+    constexpr int NW = dec_waves(16 * KSC);
+    const unsigned grid = (unsigned)((int64_t)p.B * ((p.N + 32 * NW - 1) / (32 * NW)));
+    const size_t lds = 2 * (size_t)p.stage_elems * sizeof(T);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_fused<T, D, KSC>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    k_decode_fused<T, D, KSC><<<grid, 64 * NW, lds, s>>>(p);
+    return hipGetLastError();
   }
 }
 

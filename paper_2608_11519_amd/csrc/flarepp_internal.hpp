@@ -64,9 +64,27 @@ struct CombineParams {
   float qscale;
   float* out32;  // [BH][M][D] or null
   float* lse;    // [BH][M] or null (natural log)
-  void* q_op;    // [BH][Mp][D] scaled, or null
-  void* z_op;    // [BH][D][Mp], or null
+  // Route operands for the next call, in one of two layouts:
+  //  frag == 0: q_op [BH][Mp][D] (scaled), z_op [BH][D][Mp]       (k_route)
+  //  frag == 1: fragment order, see q_frag_index / z_frag_index   (fused)
+  int frag;
+  void* q_op;
+  void* z_op;
+  unsigned* rnorm2;  // frag == 1 with q_op: per (b, h) max over routes of
+                     // |scaled q|^2 as float bits (atomic max; zeroed before)
 };
+
+// Fragment order of the route operands of the fused kernels (per (b, h)):
+//  q: [Mp/32][D/16][64 lanes][8]; lane (c, g) element j = q[32 qb + c][16 js + 8 g + j]
+//     (the B operand of the encode scores and the A operand of the decode scores)
+//  z: [Mp/32][2 halves][RB][2 g][ZC][8] with ZC = min(D, 32) value channels c:
+//     element j = z[32 rt + 16 hf + 8 (j / 4) + 4 g + j % 4][32 rb + c]
+//     (the A operand of the decode value product for lanes (c, g), c < ZC; for
+//     D = 16 the kernel supplies rows 16 (ones: the softmax denominators) to 31)
+__host__ __device__ constexpr int64_t z_frag_elems_per_head(int Mp, int D) { return (int64_t)Mp * D; }
+__host__ __device__ constexpr int64_t z_frag_index(int rt, int hf, int rb, int g, int c, int j, int D) {
+  return (((((int64_t)rt * 2 + hf) * ((D + 31) / 32) + rb) * 2 + g) * (D < 32 ? D : 32) + c) * 8 + j;
+}
 
 // ---- fused path -------------------------------------------------------------
 enum FragMode { kFragPlain = 0, kFragKeyPerm = 1, kFragMerge = 2 };
@@ -79,16 +97,19 @@ struct PrepFusedParams {
   const void* seeds;  // [H][M][D]
   int H, M, Mp, D;
   float qscale;
-  void* seeds_op;     // [H][Mp][D] scaled
+  void* seeds_op;     // [H] x q fragment order, scaled
+  unsigned* zero;     // n_zero words cleared to 0 (route norm bounds)
+  int n_zero;
 };
 
 struct EncFusedParams {
   const void* x;                     // [B][N][C]
   const void* wkf;                   // key fragments (key-permuted)
   const void* wvf;                   // value fragments (plain)
-  const void* q_op; int64_t q_sb;    // [.][H][Mp][D] scaled queries, batch stride
+  const void* q_op; int64_t q_sb;    // [.][H] x q fragment order, scaled; batch stride
   int B, N, C, H, Mp, QB;
-  int qgroups, chunk, nchunks;
+  int nqw, qgroups, chunk, nchunks;  // query blocks per wave, query groups, tokens
+                                     // per chunk (multiple of 32 * waves), chunks
   float fast_lim;
   float* part_ml; float* part_acc;   // [B][H][nchunks][Mp] x {2 | D}
 };
@@ -97,8 +118,9 @@ struct DecFusedParams {
   const void* x;      // [B][N][C]
   const void* wkf;    // key fragments (key-permuted)
   const void* wof;    // merge fragments of W_O
-  const void* q_op;   // [B][H][Mp][D] scaled synthesised queries
-  const void* z_op;   // [B][H][D][Mp] latents
+  const void* q_op;   // [B][H] x q fragment order: scaled synthesised queries
+  const void* z_op;   // [B][H] x z fragment order: latents
+  const unsigned* rnorm2;  // [B][H] max |scaled q|^2 over the routes (float bits)
   int B, N, C, H, M, Mp;
   float fast_lim;
   void* y;            // [B][N][C] decoded tokens, or null
@@ -106,31 +128,21 @@ struct DecFusedParams {
   int stage_elems;    // elements per LDS stage buffer
 };
 
-// Largest number of 32-query blocks one wave of the fused encode holds
-// without spilling registers (a power of two; 0: the fused encode is not
-// used for this storage size, head width and C = 16 * ksc).
-constexpr int enc_nqw_cap(int elem_bytes, int D, int ksc) {
-  if (elem_bytes == 2) {
-    if (D == 16) return ksc <= 8 ? 8 : 4;
-    if (D == 32) return 4;
-    return ksc <= 8 ? 2 : 0;
-  }
-  if (D == 16) return ksc <= 8 ? 4 : 0;
-  if (D == 32) return ksc <= 4 ? 4 : (ksc <= 8 ? 2 : 0);
-  return ksc <= 4 ? 1 : 0;
+// Fused path coverage.  bf16: C in {64, 128, 256}; fp32 (a correctness path):
+// C = 64.  Query blocks per wave of the fused encode: a power of two up to
+// enc_nqw_cap; waves per encode workgroup: enc_waves.
+constexpr bool fused_width_ok(int C, int elem_bytes) {
+  return elem_bytes == 2 ? (C == 64 || C == 128 || C == 256) : C == 64;
 }
-// The fused decode is used unless it would spill (fp32 with D = 64, C >= 128).
+constexpr int enc_nqw_cap(int D, int waves) { return D == 16 ? (waves == 8 ? 2 : 4) : (D == 32 ? 2 : 1); }
+constexpr int enc_waves(int D, int C, int slots) { return (D == 16 && C <= 128 && slots >= 16) ? 8 : 4; }
 constexpr bool dec_fused_ok(int elem_bytes, int D, int ksc) { return !(elem_bytes == 4 && D == 64 && ksc >= 8); }
-// The fused kernels are instantiated for these widths.
-constexpr bool fused_width_ok(int C) { return C == 64 || C == 128 || C == 256; }
-constexpr size_t enc_fused_lds(int C, int D, int elem_bytes) {
-  return 2ull * (D == 64 ? 2 : 1) * (C / 16) * 512 * elem_bytes;
-}
+size_t enc_fused_lds_bytes(int C, int D, int waves, int elem_bytes);
 int decode_stage_elems(int C, int D, int Mp);
 bool decode_fused_fits(int C, int D, int Mp, int elem_bytes);
 
 template <typename T> hipError_t launch_prep_fused(const PrepFusedParams&, hipStream_t);
-template <typename T> hipError_t launch_encode_fused(const EncFusedParams&, int D, int nqw, hipStream_t);
+template <typename T> hipError_t launch_encode_fused(const EncFusedParams&, int D, int waves, hipStream_t);
 template <typename T> hipError_t launch_combine_par(const CombineParams&, hipStream_t);
 template <typename T> hipError_t launch_decode_fused(const DecFusedParams&, int D, hipStream_t);
 

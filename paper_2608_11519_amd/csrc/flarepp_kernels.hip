@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
   using F = typename Frag<T>::type;
   const int lane = lane_id(), g = lane >> 5, c = lane & 31;
   const int CB = p.C / 32, KS = p.C / 16, NB = p.Np / 32;
-  const int64_t u = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t u = (int64_t)blockIdx.x * 4 + wave_id();
   const int64_t total = (int64_t)p.B * NB * CB * p.nw;
   if (u >= total) return;
   const int cb = (int)(u % CB);
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(256) void k_route(RouteParams p) {
   constexpr int RB = (D + 31) / 32;     // 32-row blocks of the value product
   constexpr bool ONES_ROW = (D == 16);  // value row 16 is all ones -> row sums
   const int lane = lane_id(), g = lane >> 5, c = lane & 31;
-  const int64_t u = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t u = (int64_t)blockIdx.x * 4 + wave_id();
   const int64_t total = (int64_t)p.B * p.H * p.nchunks * p.qgroups;
   if (u >= total) return;
   const int qg = (int)(u % p.qgroups);
@@ -231,7 +231,7 @@ __global__ __launch_bounds__(256) void k_route(RouteParams p) {
         }
       }
     const float kmax2 = halfmax_sum_nonneg(kn);
-    const bool fast = fastok && (qmax2 * kmax2 <= fast_lim);
+    const bool fast = fastok && uniform(qmax2 * kmax2 <= fast_lim);
 
 #pragma unroll
     for (int i = 0; i < NQ; ++i) {
