@@ -47,28 +47,54 @@ def parse_args(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host seconds spent timing the oracle")
+    ap.add_argument("--stage-reps", type=int, default=20,
+                    help="back-to-back launches per stage when timing stages alone")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for counter scaling)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
+                         "script into profiles/traffic_<workload>.json and exit")
+    ap.add_argument("--pmc-command", default="", help="the profiled command, recorded in the summary")
     return ap.parse_args(argv)
 
 
-def stage_work(w):
+def stage_work(w, fused):
     """Algorithmic flops, HBM bytes and exponentials per launch of each stage.
 
-    Bytes count only what the method must move at this stage boundary
-    (inputs read once, outputs written once), not re-reads."""
-    T, C, M, H = w.B * w.N, w.C, w.M, w.H
+    Flops: 4*T*M*C per routing call (scores and values over all heads) plus
+    2*T*C*C for each C x C projection the stage owns (the fused decode's
+    recompute of K is not counted).  Bytes: what the stage must move at its
+    boundary (X read once, O written once, the route operands it produces);
+    the split-key partials are not counted, they exist only because of the
+    split."""
+    T, C, M, H, D = w.B * w.N, w.C, w.M, w.H, w.D
     bs = 2 if w.dtype == "bf16" else 4
-    enc_flops = 4.0 * T * M * C
+    route = 4.0 * T * M * C
+    gemm = 2.0 * T * C * C
+    exps = 1.0 * T * H * M
+    prep = 10.0 * C * C * bs + 2.0 * H * M * D * bs
+    comb = w.B * H * M * D * (4.0 + bs)
+    zero = dict(flops=0.0, bytes=0.0, exps=0.0)
+    if fused:
+        return {
+            "prep": dict(flops=0.0, bytes=prep, exps=0.0),
+            "project": zero,
+            "call1_encode": dict(flops=route + 2 * gemm, bytes=T * C * bs, exps=exps),
+            "call1_combine": dict(flops=0.0, bytes=comb, exps=0.0),
+            "call2_encode": dict(flops=route + 2 * gemm, bytes=T * C * bs, exps=exps),
+            "call2_combine": dict(flops=0.0, bytes=comb, exps=0.0),
+            "call3_decode": dict(flops=route + gemm, bytes=2.0 * T * C * bs, exps=exps),
+            "merge": zero,
+        }
     return {
-        "prep": dict(flops=0.0, bytes=5.0 * C * C * bs, exps=0.0),
-        "project": dict(flops=8.0 * T * C * C, bytes=5.0 * T * C * bs, exps=0.0),
-        "call1_encode": dict(flops=enc_flops, bytes=2.0 * T * C * bs, exps=1.0 * T * H * M),
-        "call1_combine": dict(flops=0.0, bytes=4.0 * w.B * H * M * w.D, exps=0.0),
-        "call2_encode": dict(flops=enc_flops, bytes=2.0 * T * C * bs, exps=1.0 * T * H * M),
-        "call2_combine": dict(flops=0.0, bytes=4.0 * w.B * H * M * w.D, exps=0.0),
-        "call3_decode": dict(flops=enc_flops, bytes=2.0 * T * C * bs, exps=1.0 * T * H * M),
-        "merge": dict(flops=2.0 * T * C * C, bytes=2.0 * T * C * bs, exps=0.0),
+        "prep": dict(flops=0.0, bytes=prep, exps=0.0),
+        "project": dict(flops=4 * gemm, bytes=5.0 * T * C * bs, exps=0.0),
+        "call1_encode": dict(flops=route, bytes=2.0 * T * C * bs, exps=exps),
+        "call1_combine": dict(flops=0.0, bytes=comb, exps=0.0),
+        "call2_encode": dict(flops=route, bytes=2.0 * T * C * bs, exps=exps),
+        "call2_combine": dict(flops=0.0, bytes=comb, exps=0.0),
+        "call3_decode": dict(flops=route, bytes=2.0 * T * C * bs, exps=exps),
+        "merge": dict(flops=gemm, bytes=2.0 * T * C * bs, exps=0.0),
     }
 
 
@@ -91,6 +117,88 @@ def roofline(work, ms, dtype):
         a, p, unit = work["exps"] / s / 1e12, PEAK_EXP_TPS, "Texp/s"
     return {"bound": bound, "achieved": round(a, 3), "peak": p, "unit": unit,
             "frac": round(a / p, 4), "traffic": None}
+
+
+# Kernel (symbol substring) that carries each stage, for the counter tables.
+STAGE_KERNELS_FUSED = {"prep": "k_prep_fused", "call1_encode": "k_encode_fused",
+                       "call1_combine": "k_combine_par", "call2_encode": "k_encode_fused",
+                       "call2_combine": "k_combine_par", "call3_decode": "k_decode_fused"}
+
+
+def sources_digest():
+    """SHA-256 over the kernel sources and the build flags: counters taken
+    for other sources are not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    pkg = os.path.join(ROOT, "paper_2608_11519_amd")
+    files = sorted(os.path.join(pkg, "csrc", f) for f in os.listdir(os.path.join(pkg, "csrc")))
+    for f in files + [os.path.join(pkg, "build.py"), os.path.join(ROOT, "include", "flarepp.h")]:
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+
+
+def measured_traffic(w, stage):
+    """HBM bytes per launch of the stage's kernel from the committed counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by the plain-copy calibration),
+    or None when there is none for the current kernel sources."""
+    path = traffic_file(w.name)
+    kern = STAGE_KERNELS_FUSED.get(stage)
+    if not kern or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("sources_sha256") != sources_digest() or kern not in t.get("kernels", {}):
+        return None
+    return t["kernels"][kern]["bytes_per_dispatch"]
+
+
+def pmc_summary(fetch_dir, write_dir, workload, copy_mib, command):
+    """Average FETCH_SIZE / WRITE_SIZE per dispatch of every flarepp kernel
+    in two rocprofv3 --pmc runs, scaled by the counters of the plain device
+    copy of copy_mib MiB that bench.py ran in the same process."""
+    import csv
+    import glob
+
+    def read(d, counter):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                rows += [r for r in csv.DictReader(fh) if r["Counter_Name"] == counter]
+        if not rows:
+            raise SystemExit(f"no {counter} rows under {d}")
+        return rows
+
+    fetch, write = read(fetch_dir, "FETCH_SIZE"), read(write_dir, "WRITE_SIZE")
+    copy_kib = copy_mib * 1024.0
+    # the copy: the non-flarepp dispatch that fetched the most / wrote the most
+    cf = max((r for r in fetch if "flarepp" not in r["Kernel_Name"]), key=lambda r: float(r["Counter_Value"]))
+    copy_name = cf["Kernel_Name"]
+    cw = max((r for r in write if r["Kernel_Name"] == copy_name), key=lambda r: float(r["Counter_Value"]))
+    f_fac = copy_kib / float(cf["Counter_Value"])
+    w_fac = copy_kib / float(cw["Counter_Value"])
+    kernels = {}
+    for kern in sorted(set(STAGE_KERNELS_FUSED.values())):
+        fv = [float(r["Counter_Value"]) for r in fetch if kern in r["Kernel_Name"]]
+        wv = [float(r["Counter_Value"]) for r in write if kern in r["Kernel_Name"]]
+        if not fv or not wv:
+            continue
+        fk, wk = sum(fv) / len(fv), sum(wv) / len(wv)
+        kernels[kern] = {"dispatches": len(fv), "fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
+                         "bytes_per_dispatch": round((fk * f_fac + wk * w_fac) * 1024.0)}
+    out = {"workload": workload, "sources_sha256": sources_digest(), "command": command,
+           "copy": {"mib": copy_mib, "kernel": copy_name[:80], "fetch_kib": float(cf["Counter_Value"]),
+                    "write_kib": float(cw["Counter_Value"]), "fetch_factor": round(f_fac, 4),
+                    "write_factor": round(w_fac, 4)},
+           "kernels": kernels}
+    with open(traffic_file(workload), "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out, indent=1))
 
 
 def cpu_baseline(w, d, min_seconds):
@@ -118,6 +226,10 @@ def cpu_baseline(w, d, min_seconds):
 
 def main(argv=None):
     args = parse_args(argv)
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.workload,
+                    args.copy_calibration_mib or 256, args.pmc_command)
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the mixer forward is benchmarked on a single MI355X)", file=sys.stderr)
@@ -178,21 +290,47 @@ def main(argv=None):
     value = tokens / (ms_per_step * 1e-3)
     print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
 
-    # ---- per-stage device times (HIP events around each stage) ----
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(fp.PROFILE_EVENTS)]
-           for _ in range(args.steps)]
-    for k in range(args.steps):
-        fp.flarepp_mixer_forward_profiled(*margs, H=w.H, events=evs[k], out=O, ws=ws)
-    torch.cuda.synchronize()
+    # ---- per-stage device times: each stage launched alone, back to back ----
+    fused = fp.flarepp_mixer_path(dcode, w.B, w.N, w.C, w.H, w.M) == fp.PATH_FUSED
+    empty = {"project", "merge"} if fused else set()
+    reps = max(args.stage_reps, 1)
     stage_ms = {}
-    for i, name in enumerate(fp.PROFILE_STAGES):
-        stage_ms[name] = float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
-    work = stage_work(w)
+    for k, name in enumerate(fp.PROFILE_STAGES, start=1):
+        if name in empty:
+            stage_ms[name] = 0.0
+            continue
+
+        def run_stage(k=k):
+            for _ in range(reps):
+                fp.flarepp_mixer_stage(k, *margs, H=w.H, out=O, ws=ws)
+
+        sg = None
+        if graph is not None:
+            sg = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(sg):
+                run_stage()
+            sg.replay()
+        else:
+            run_stage()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        if sg is not None:
+            sg.replay()
+        else:
+            run_stage()
+        e1.record()
+        torch.cuda.synchronize()
+        stage_ms[name] = e0.elapsed_time(e1) / reps
+    step()  # leave the workspace and O as one complete step wrote them
+    torch.cuda.synchronize()
+    work = stage_work(w, fused)
     stages = {n: {"ms": round(stage_ms[n], 5), **roofline(work[n], stage_ms[n], w.dtype)}
-              for n in fp.PROFILE_STAGES}
+              for n in fp.PROFILE_STAGES if n not in empty}
     dominant = max(stage_ms, key=stage_ms.get)
     roof = dict(roofline(work[dominant], stage_ms[dominant], w.dtype))
     roof["kernel"] = dominant
+    roof["traffic"] = measured_traffic(w, dominant)
     route_names = ("call1_encode", "call1_combine", "call2_encode", "call2_combine", "call3_decode")
     route_ms = sum(stage_ms[n] for n in route_names)
     route_flops = 3 * 4.0 * tokens * w.M * w.C

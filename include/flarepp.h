@@ -176,6 +176,20 @@ FLAREPP_API int flarepp_mixer_forward_profiled(int dtype, int64_t B, int64_t N, 
                                    size_t ws_bytes, void* stream, void* const* events,
                                    int n_events);
 
+/* Runs stage `stage` (1 .. FLAREPP_PROFILE_EVENTS - 1, numbered as for
+ * flarepp_mixer_forward_profiled) of flarepp_mixer_forward alone, for timing
+ * one kernel in isolation.  The workspace must hold what a complete
+ * flarepp_mixer_forward with the same arguments left in it; the stage then
+ * recomputes and rewrites exactly the values it wrote there (its inputs are
+ * unchanged), so it may be launched any number of times or captured into a
+ * graph.  An empty stage launches nothing.  Errors as flarepp_mixer_forward,
+ * and FLAREPP_ERR_INVALID_ARG for a stage outside that range. */
+FLAREPP_API int flarepp_mixer_stage(int stage, int dtype, int64_t B, int64_t N, int64_t C,
+                                    int64_t H, int64_t M, const void* X, const void* Wk,
+                                    const void* Wv, const void* Wkt, const void* Wvt,
+                                    const void* Wo, const void* seeds, void* O, void* ws,
+                                    size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -198,6 +198,8 @@ MixerPlan mixer_plan(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int6
   pl.enc = encode_plan(B, H, N, Mp, D);
   if (pl.fused) {
     pl.nqw = (int)std::min<int64_t>(flarepp::enc_nqw_cap((int)D, pl.waves), next_pow2(cdiv(slots, pl.waves)));
+    // every wave's query slots must belong to one head of the group
+    while (hpg > 1 && (Mp / 32) % pl.nqw != 0) pl.nqw /= 2;
     pl.qgroups = (int)cdiv(slots, (int64_t)pl.waves * pl.nqw);
     const int64_t per = B * (H / hpg) * pl.qgroups;  // workgroups per token chunk
     const int64_t step = 32 * pl.waves;                // tokens per workgroup step
@@ -222,7 +224,7 @@ MixerPlan mixer_plan(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int6
 struct MixerWs {
   void *wf[5], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *q_op, *z_op, *Y;
   float *part_ml, *part_acc;
-  unsigned* rnorm2;
+  float* qnorm2;
   size_t bytes;
 };
 
@@ -246,7 +248,7 @@ MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t
   w.part_acc = (float*)cv.take(sizeof(float) * R * B * H * Mp * D);
   w.q_op = cv.take(bs * B * H * Mp * D);
   w.z_op = cv.take(bs * B * H * (pl.fused ? flarepp::z_frag_elems_per_head((int)Mp, (int)D) : D * Mp));
-  w.rnorm2 = (unsigned*)cv.take(sizeof(unsigned) * B * H);
+  w.qnorm2 = (float*)cv.take(sizeof(float) * B * H * (Mp / 4));
   w.bytes = cv.off;
   return w;
 }
@@ -257,7 +259,7 @@ template <typename T>
 int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
                const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
-               size_t ws_bytes, hipStream_t s, hipEvent_t const* ev) {
+               size_t ws_bytes, hipStream_t s, hipEvent_t const* ev, int only) {
   using namespace flarepp;
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
   const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
@@ -266,6 +268,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
   const float qscale = route_qscale(D);
 #define STAGE(i) do { if (ev) HIPTRY(hipEventRecord(ev[i], s)); } while (0)
+#define RUN(i) (only == 0 || only == (i))
   STAGE(0);
   if (pl.fused) {
     // weights as fused-path fragments and the seed operand
@@ -275,8 +278,8 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain, kFragMerge};
     for (int i = 0; i < 5; ++i) { pp.w[i] = win[i]; pp.wf[i] = w.wf[i]; pp.mode[i] = mode[i]; }
     pp.seeds = seeds; pp.H = (int)H; pp.M = (int)M; pp.Mp = (int)Mp; pp.D = (int)D;
-    pp.qscale = qscale; pp.seeds_op = w.seeds_op; pp.zero = w.rnorm2; pp.n_zero = (int)(B * H);
-    HIPTRY(launch_prep_fused<T>(pp, s));
+    pp.qscale = qscale; pp.seeds_op = w.seeds_op;
+    if (RUN(1)) HIPTRY(launch_prep_fused<T>(pp, s));
     STAGE(1);
     STAGE(2);  // the projections run inside the routing kernels
     EncFusedParams ep{};
@@ -284,26 +287,26 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     ep.B = (int)B; ep.N = (int)N; ep.C = (int)C; ep.H = (int)H; ep.Mp = (int)Mp; ep.QB = (int)(Mp / 32);
     ep.nqw = pl.nqw; ep.qgroups = pl.qgroups; ep.chunk = pl.chunk; ep.nchunks = pl.nchunks;
     ep.fast_lim = fast_limit(); ep.part_ml = w.part_ml; ep.part_acc = w.part_acc;
-    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 1
+    if (RUN(3)) HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 1
     STAGE(3);
     CombineParams cp{};
     cp.part_ml = w.part_ml; cp.part_acc = w.part_acc; cp.BH = B * H; cp.R = pl.nchunks;
     cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale; cp.frag = 1;
-    cp.out32 = Q_out; cp.q_op = w.q_op; cp.rnorm2 = w.rnorm2;
-    HIPTRY(launch_combine_par<T>(cp, s));
+    cp.out32 = Q_out; cp.q_op = w.q_op; cp.qnorm2 = w.qnorm2;
+    if (RUN(4)) HIPTRY(launch_combine_par<T>(cp, s));
     STAGE(4);
     ep.wkf = w.wf[0]; ep.wvf = w.wf[1]; ep.q_op = w.q_op; ep.q_sb = H * Mp * D;
-    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 2
+    if (RUN(5)) HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 2
     STAGE(5);
-    cp.out32 = Z_out; cp.q_op = nullptr; cp.rnorm2 = nullptr; cp.z_op = w.z_op;
-    HIPTRY(launch_combine_par<T>(cp, s));
+    cp.out32 = Z_out; cp.q_op = nullptr; cp.qnorm2 = nullptr; cp.z_op = w.z_op;
+    if (RUN(6)) HIPTRY(launch_combine_par<T>(cp, s));
     STAGE(6);
     DecFusedParams dp{};
-    dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = w.q_op; dp.z_op = w.z_op; dp.rnorm2 = w.rnorm2;
+    dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = w.q_op; dp.z_op = w.z_op; dp.qnorm2 = w.qnorm2;
     dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
     dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O;
     dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);
-    HIPTRY(launch_decode_fused<T>(dp, (int)D, s));  // call 3 + merge
+    if (RUN(7)) HIPTRY(launch_decode_fused<T>(dp, (int)D, s));  // call 3 + merge
     STAGE(7);
     STAGE(8);
     return ok();
@@ -315,13 +318,13 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   wp.nw = 5;
   const void* ws_in[5] = {Wk, Wv, Wkt, Wvt, Wo};
   for (int i = 0; i < 5; ++i) { wp.w[i] = ws_in[i]; wp.out[i] = w.wf[i]; }
-  HIPTRY(launch_weight_frags<T>(wp, s));
+  if (RUN(1)) HIPTRY(launch_weight_frags<T>(wp, s));
 
   // 2. seeds -> scaled route operand (shared by the batch)
   RoutePrepParams sp{};
   sp.src = seeds; sp.src_bstride = 0; sp.B = 1; sp.H = (int)H; sp.M = (int)M; sp.Mp = (int)Mp;
   sp.D = (int)D; sp.qscale = qscale; sp.q_op = w.seeds_op; sp.z_op = nullptr;
-  HIPTRY((launch_route_prep<T, T>(sp, s)));
+  if (RUN(1)) HIPTRY((launch_route_prep<T, T>(sp, s)));
   STAGE(1);
 
   // 3. project: K, K~ token-major; V, V~ d-major (value operands)
@@ -332,7 +335,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   pp.wf[1] = w.wf[1]; pp.out[1] = w.Vdm;  pp.layout[1] = kHeadsDMajor;
   pp.wf[2] = w.wf[2]; pp.out[2] = w.Kt;   pp.layout[2] = kHeadsTokenMajor;
   pp.wf[3] = w.wf[3]; pp.out[3] = w.Vtdm; pp.layout[3] = kHeadsDMajor;
-  HIPTRY(launch_project<T>(pp, s));
+  if (RUN(2)) HIPTRY(launch_project<T>(pp, s));
   STAGE(2);
 
   const EncPlan e = pl.enc;
@@ -346,24 +349,24 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   r1.va = w.Vtdm; r1.va_sb = dmBS; r1.va_sh = dmHS; r1.va_ld = (int)Np;
   r1.qs = w.seeds_op; r1.qs_sb = 0; r1.qs_sh = rtHS; r1.qs_rows = (int)Mp;
   r1.part_ml = w.part_ml; r1.part_acc = w.part_acc;
-  HIPTRY(launch_route<T>(r1, (int)D, false, s));
+  if (RUN(3)) HIPTRY(launch_route<T>(r1, (int)D, false, s));
   STAGE(3);
   CombineParams c1{};
   c1.part_ml = w.part_ml; c1.part_acc = w.part_acc; c1.BH = B * H; c1.R = e.nchunks;
   c1.M = (int)M; c1.Mp = (int)Mp; c1.D = (int)D; c1.qscale = qscale;
   c1.out32 = Q_out; c1.lse = nullptr; c1.q_op = w.q_op; c1.z_op = nullptr;
-  HIPTRY(launch_combine_par<T>(c1, s));
+  if (RUN(4)) HIPTRY(launch_combine_par<T>(c1, s));
   STAGE(4);
 
   // 5. call 2: Z = SDPA(Q, K, V), softmax over tokens
   RouteParams r2 = r1;
   r2.ka = w.K; r2.va = w.Vdm;
   r2.qs = w.q_op; r2.qs_sb = rtBS; r2.qs_sh = rtHS; r2.qs_rows = (int)Mp;
-  HIPTRY(launch_route<T>(r2, (int)D, false, s));
+  if (RUN(5)) HIPTRY(launch_route<T>(r2, (int)D, false, s));
   STAGE(5);
   CombineParams c2 = c1;
   c2.out32 = Z_out; c2.q_op = nullptr; c2.z_op = w.z_op;
-  HIPTRY(launch_combine_par<T>(c2, s));
+  if (RUN(6)) HIPTRY(launch_combine_par<T>(c2, s));
   STAGE(6);
 
   // 6. call 3: Y = SDPA(K, Q, Z), softmax over routes, heads merged
@@ -373,15 +376,16 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;
   r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
   r3.y = Y; r3.y_sb = N * C; r3.y_row = C;
-  HIPTRY(launch_route<T>(r3, (int)D, true, s));
+  if (RUN(7)) HIPTRY(launch_route<T>(r3, (int)D, true, s));
   STAGE(7);
 
   // 7. merge: O = Y W_O
   ProjParams mp{};
   mp.x = Y; mp.B = (int)B; mp.N = (int)N; mp.Np = (int)Np; mp.C = (int)C; mp.H = (int)H; mp.D = (int)D;
   mp.nw = 1; mp.wf[0] = w.wf[4]; mp.out[0] = O; mp.layout[0] = kPlain;
-  HIPTRY(launch_project<T>(mp, s));
+  if (RUN(8)) HIPTRY(launch_project<T>(mp, s));
   STAGE(8);
+#undef RUN
 #undef STAGE
   return ok();
 }
@@ -389,8 +393,10 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
 int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
                 const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                 const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
-                size_t ws_bytes, void* stream, void* const* events, int n_events) {
+                size_t ws_bytes, void* stream, void* const* events, int n_events, int only = 0) {
   TRY(check_mixer_shape(dtype, B, N, C, H, M));
+  if (only < 0 || only > FLAREPP_PROFILE_EVENTS - 1)
+    return fail(FLAREPP_ERR_INVALID_ARG, "stage=%d must be in [1, %d]", only, FLAREPP_PROFILE_EVENTS - 1);
   if (n_events != 0 && n_events != FLAREPP_PROFILE_EVENTS)
     return fail(FLAREPP_ERR_INVALID_ARG, "n_events=%d must be 0 or %d", n_events, FLAREPP_PROFILE_EVENTS);
   if (n_events) {
@@ -415,9 +421,9 @@ int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == FLAREPP_F32)
     return mixer_impl<float>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
-                             Y_out, ws, ws_bytes, s, ev);
+                             Y_out, ws, ws_bytes, s, ev, only);
   return mixer_impl<__bf16>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
-                            Y_out, ws, ws_bytes, s, ev);
+                            Y_out, ws, ws_bytes, s, ev, only);
 }
 
 // ---- route ------------------------------------------------------------------
@@ -627,6 +633,15 @@ int flarepp_mixer_forward_profiled(int dtype, int64_t B, int64_t N, int64_t C, i
                                    int n_events) {
   return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr,
                      nullptr, ws, ws_bytes, stream, events, n_events);
+}
+
+int flarepp_mixer_stage(int stage, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                        const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                        const void* Wvt, const void* Wo, const void* seeds, void* O, void* ws,
+                        size_t ws_bytes, void* stream) {
+  if (stage < 1) return fail(FLAREPP_ERR_INVALID_ARG, "stage=%d must be in [1, %d]", stage, FLAREPP_PROFILE_EVENTS - 1);
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr,
+                     nullptr, ws, ws_bytes, stream, nullptr, 0, stage);
 }
 
 int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,

@@ -20,6 +20,7 @@ typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(8))) float f32x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(2))) float f32x2;
 
 template <typename T> struct Frag;
 template <> struct Frag<__bf16> { typedef bf16x8 type; typedef bf16x4 half; };
@@ -130,6 +131,18 @@ __device__ __forceinline__ float halfmax_sum_nonneg(float x) {
   int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
   const float s = __int_as_float(max(r0, r1)) + __int_as_float(max(r2, r3));
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s)));
+}
+
+// Maximum of a non-negative float over the whole wave, wave-uniform.
+__device__ __forceinline__ float wave_max_nonneg(float x) {
+  int v = __float_as_int(x);
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false)); // row_half_mirror
+  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false)); // row_mirror
+  const int r = max(max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+                    max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+  return __int_as_float(__builtin_amdgcn_readfirstlane(r));
 }
 
 // True in every lane when pred holds in every active lane.

@@ -111,8 +111,6 @@ __global__ void k_prep_fused(PrepFusedParams p) {
     }
     return;
   }
-  idx -= nseed;
-  if (idx < p.n_zero) p.zero[idx] = 0u;
 }
 
 // ---- small helpers -----------------------------------------------------------
@@ -136,17 +134,27 @@ template <int D> struct EncShape {
   static constexpr int GB = (D == 64) ? 2 : 1;   // 32-channel blocks per group
   static constexpr int KS = D / 16, RB = (D + 31) / 32;
   static constexpr int KFR = HPG * KS;           // key fragments per sub-tile
-  static constexpr int VFR = 2 * GB;             // value fragments per sub-tile
+  static constexpr int VFR = HPG * 2 * RB;       // value-operand fragments per sub-tile
   static constexpr int TILE = (KFR + VFR) * kFrag;
 };
 
 size_t enc_fused_lds_bytes(int C, int D, int waves, int elem_bytes) {
-  const int gb = D == 64 ? 2 : 1, hpg = D == 16 ? 2 : 1;
+  const int gb = D == 64 ? 2 : 1, hpg = D == 16 ? 2 : 1, rb = (D + 31) / 32;
   const size_t welems = (size_t)gb * (C / 16) * kFrag;
-  const size_t tile = (size_t)(hpg * (D / 16) + 2 * gb) * kFrag;
+  const size_t tile = (size_t)(hpg * (D / 16) + hpg * 2 * rb) * kFrag;
   return (2 * welems + 2 * waves * tile) * elem_bytes + 2 * waves * hpg * sizeof(float);
 }
 
+// LDS layout of one projected 32-token sub-tile:
+//   key fragments (hh, js)          [KFR][64 lanes][8]: lane (c, g) = token c,
+//                                    dims 16 js + 8 g .. + 7 of head hh
+//   value operands (hh, rb, hf)     [VFR][64 lanes][8]: the A operand of the
+//                                    value product for keys 16 hf .. 16 hf + 15
+//                                    (in the score tile's row order); lane
+//                                    (c, g) = channel 32 rb + c of head hh.
+//                                    For D = 16 rows 16 .. 31 are constant
+//                                    (row 16 ones: the denominators, the rest
+//                                    zeros) and are written once.
 template <typename T, int D, int KSC, int NQW, int W>
 __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   using F = typename Frag<T>::type;
@@ -154,6 +162,7 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   constexpr int HPG = S::HPG, GB = S::GB, KS = S::KS, RB = S::RB, KFR = S::KFR, TILE = S::TILE;
   constexpr bool ONES_ROW = (D == 16);
   constexpr int WELEMS = GB * KSC * kFrag;  // one weight slice of the head group
+  constexpr int STEP = 32 * W;              // tokens per super-tile
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T* wk_l = reinterpret_cast<T*>(smem);
   T* wv_l = wk_l + WELEMS;
@@ -173,18 +182,28 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   copy_to_lds((const T*)p.wkf + (int64_t)hg * WELEMS, smem, WELEMS * (int)sizeof(T) / 16, 64 * W);
   copy_to_lds((const T*)p.wvf + (int64_t)hg * WELEMS, smem + WELEMS * sizeof(T), WELEMS * (int)sizeof(T) / 16,
               64 * W);
+  if constexpr (ONES_ROW) {  // constant rows 16 .. 31 of every value operand
+    constexpr int NCONST = 2 * W * S::VFR * 32;
+    for (int i = threadIdx.x; i < NCONST; i += 64 * W) {
+      const int rr = i & 15, gg = (i >> 4) & 1, f = i >> 5;  // f = (buf * W + j) * VFR + vf
+      T* dst = tiles + (f / S::VFR) * TILE + (KFR + f % S::VFR) * kFrag + (16 + rr + 32 * gg) * 8;
+      store_frag<T>(dst, rr == 0 ? fill_frag<T>(1.f) : zero_frag<T>());
+    }
+  }
 
-  // ---- this wave's query slots (slot = head-in-group x 32-query block) ----
+  // ---- this wave's query slots (slot = head-in-group x 32-query block); the
+  // host makes every wave's slots belong to one head ----
   const int nslots = HPG * p.QB;
   const int slot0 = (qg * W + wave) * NQW;
+  const int hh = HPG == 1 ? 0 : __builtin_amdgcn_readfirstlane(min(slot0, nslots - 1) / p.QB);
   F qf[NQW][KS];
   float qn = 0.f;
 #pragma unroll
   for (int i = 0; i < NQW; ++i) {
     const int s = slot0 + i;
     const bool ok = s < nslots;
-    const int h = hg * HPG + (ok ? s / p.QB : 0), qb = ok ? s % p.QB : 0;
-    const T* qp = (const T*)p.q_op + (int64_t)b * p.q_sb + (int64_t)h * p.Mp * D;
+    const int qb = ok ? s % p.QB : 0;
+    const T* qp = (const T*)p.q_op + (int64_t)b * p.q_sb + (int64_t)(hg * HPG + hh) * p.Mp * D;
     float sq = 0.f;
 #pragma unroll
     for (int js = 0; js < KS; ++js) {
@@ -217,10 +236,11 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
     for (int ks = 0; ks < KSC; ++ks)
       xf[ks] = ok ? load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g) : zero_frag<T>();
   }
-  lds_wait_barrier();  // weight slices in LDS
+  lds_wait_barrier();  // weight slices and constant rows in LDS
 
-  // Project sub-tile `wave` of the super-tile at t0 into LDS buffer it & 1.
-  auto produce = [&](int it, int t0) {
+  // Project sub-tile `wave` of the super-tile at t0 into LDS buffer it & 1
+  // and prefetch this wave's X rows of the next super-tile.
+  auto produce = [&](int it, int t0) __attribute__((always_inline)) {
     const int buf = it & 1;
     f32x16 ka[GB], va[GB];
 #pragma unroll
@@ -234,8 +254,8 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
         mma(va[cb], xf[ks], load_frag(wv_l + fo));
       }
     }
-    {  // prefetch this wave's rows of the next super-tile
-      const int row = t0 + 32 * W + 32 * wave + c;
+    {
+      const int row = t0 + STEP + 32 * wave + c;
       const bool ok = row < k1;
 #pragma unroll
       for (int ks = 0; ks < KSC; ++ks)
@@ -243,96 +263,104 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
     }
     T* tl = tiles + (buf * W + wave) * TILE;
 #pragma unroll
-    for (int hh = 0; hh < HPG; ++hh) {
+    for (int h2 = 0; h2 < HPG; ++h2) {
       F kf[KS];
 #pragma unroll
       for (int js = 0; js < KS; ++js) {
-        const int fi = hh * KS + js;
+        const int fi = h2 * KS + js;
         kf[js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
         store_frag<T>(tl + fi * kFrag + lane * 8, kf[js]);
       }
       const float kb = frag_rows_max_sq<T, KS>(kf);
-      if (lane == 0) kmx[(buf * W + wave) * HPG + hh] = kb;
+      if (lane == 0) kmx[(buf * W + wave) * HPG + h2] = kb;
     }
-#pragma unroll
-    for (int cb = 0; cb < GB; ++cb)
+    if constexpr (ONES_ROW) {  // channel c -> row c % 16 of head c / 16's operand
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf)
-        store_frag<T>(tl + (KFR + 2 * cb + hf) * kFrag + lane * 8, cvt8<T>(va[cb], 8 * hf));
+        store_frag<T>(tl + (KFR + (c >> 4) * 2 + hf) * kFrag + ((c & 15) + 32 * g) * 8, cvt8<T>(va[0], 8 * hf));
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < GB; ++cb)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+          store_frag<T>(tl + (KFR + 2 * cb + hf) * kFrag + lane * 8, cvt8<T>(va[cb], 8 * hf));
+    }
     __syncthreads();
   };
 
-  // Run the wave's query slots over every sub-tile of the super-tile at t0,
-  // all shift-free (sf = true) or all with the online maximum.
-  auto consume = [&](auto sf, int it, int t0) {
-    constexpr bool SF = decltype(sf)::value;
+  // Run the wave's query slots over every sub-tile of the super-tile at t0:
+  // shift-free (SF) or with the online maximum; MASK only for the last,
+  // partial super-tile of a chunk; ALL when every slot of the wave is a real
+  // one (no per-slot branch inside the tile sequence).
+  const bool all_slots = slot0 + NQW <= nslots;
+  auto consume_v = [&](auto sf, auto mask, auto all, int it, int t0) __attribute__((always_inline)) {
+    constexpr bool SF = decltype(sf)::value, MASK = decltype(mask)::value, ALL = decltype(all)::value;
     const int buf = it & 1;
-#pragma unroll 1
+#pragma unroll
     for (int j = 0; j < W; ++j) {
-      const int nvalid = min(32, k1 - (t0 + 32 * j));
-      if (nvalid <= 0) break;
+      int nvalid = 32;
+      if (MASK) {
+        nvalid = min(32, k1 - (t0 + 32 * j));
+        if (nvalid <= 0) break;
+      }
       const T* tl = tiles + (buf * W + j) * TILE;
+      F kf[KS];
+#pragma unroll
+      for (int js = 0; js < KS; ++js) kf[js] = load_frag(tl + (hh * KS + js) * kFrag + lane * 8);
+      F vf[2][RB];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          vf[hf][rb] = load_frag(tl + (KFR + (hh * RB + rb) * 2 + hf) * kFrag + lane * 8);
 #pragma unroll
       for (int i = 0; i < NQW; ++i) {
-        const int s = slot0 + i;
-        if (s >= nslots) continue;
-        const int hh = HPG == 1 ? 0 : s / p.QB;
-        F kf[KS];
+        if (ALL || slot0 + i < nslots) {
+          f32x16 sc;
 #pragma unroll
-        for (int js = 0; js < KS; ++js) kf[js] = load_frag(tl + (hh * KS + js) * kFrag + lane * 8);
-        F vf[2][RB];
-        if (ONES_ROW) {
-          const F fill = (c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
+          for (int e = 0; e < 16; ++e) sc[e] = 0.f;
 #pragma unroll
-          for (int hf = 0; hf < 2; ++hf)
-            vf[hf][0] = c < 16 ? load_frag(tl + (KFR + hf) * kFrag + (16 * hh + c + 32 * g) * 8) : fill;
-        } else {
-#pragma unroll
-          for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) vf[hf][rb] = load_frag(tl + (KFR + 2 * rb + hf) * kFrag + lane * 8);
-        }
-        f32x16 sc;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sc[e] = 0.f;
-#pragma unroll
-        for (int js = 0; js < KS; ++js) mma(sc, kf[js], qf[i][js]);
-        if (nvalid == 32) {
-          if (SF) tile_shift_free<T, RB, ONES_ROW, false>(acc[i], ls[i], sc, vf, 32, lane);
-          else tile_online<T, RB, ONES_ROW, false>(acc[i], m[i], ls[i], sc, vf, 32, lane);
-        } else {
-          if (SF) tile_shift_free<T, RB, ONES_ROW, true>(acc[i], ls[i], sc, vf, nvalid, lane);
-          else tile_online<T, RB, ONES_ROW, true>(acc[i], m[i], ls[i], sc, vf, nvalid, lane);
+          for (int js = 0; js < KS; ++js) mma(sc, kf[js], qf[i][js]);
+          if (SF) tile_shift_free<T, RB, ONES_ROW, MASK>(acc[i], ls[i], sc, vf, nvalid, lane);
+          else tile_online<T, RB, ONES_ROW, MASK>(acc[i], m[i], ls[i], sc, vf, nvalid, lane);
         }
       }
     }
   };
+  auto consume = [&](auto sf, auto mask, int it, int t0) __attribute__((always_inline)) {
+    if (all_slots) consume_v(sf, mask, std::true_type{}, it, t0);
+    else consume_v(sf, mask, std::false_type{}, it, t0);
+  };
 
-  // Shift-free phase: while every score of a super-tile is provably within
-  // the shift-free range (|q.k| <= max|q| max|k|); then the online phase.
+  // Full super-tiles: shift-free while every score of the super-tile is
+  // provably within the shift-free range (|q.k| <= max|q| max|k|), then
+  // online; a partial last super-tile runs online with masked keys.
+  const int nfull = (k1 - k0) / STEP;
+  const bool tail = (k1 - k0) % STEP != 0;
   int it = 0, t0 = k0;
   bool used = false;
-  for (; t0 < k1; t0 += 32 * W, ++it) {
+  for (; it < nfull; ++it, t0 += STEP) {
     produce(it, t0);
     float kb = 0.f;
     for (int j = 0; j < W * HPG; ++j) kb = fmaxf(kb, kmx[(it & 1) * W * HPG + j]);
     if (!uniform(qmax2 * kb <= p.fast_lim)) break;
-    consume(std::true_type{}, it, t0);
+    consume(std::true_type{}, std::false_type{}, it, t0);
     used = true;
   }
-  if (t0 < k1) {
-    if (!used) {
+  if (!used) {
 #pragma unroll
-      for (int i = 0; i < NQW; ++i) m[i] = -INFINITY;
-    }
-    consume(std::false_type{}, it, t0);
-    for (t0 += 32 * W, ++it; t0 < k1; t0 += 32 * W, ++it) {
+    for (int i = 0; i < NQW; ++i) m[i] = -INFINITY;
+  }
+  if (it < nfull) {  // super-tile `it` is produced, not yet consumed
+    consume(std::false_type{}, std::false_type{}, it, t0);
+    for (++it, t0 += STEP; it < nfull; ++it, t0 += STEP) {
       produce(it, t0);
-      consume(std::false_type{}, it, t0);
+      consume(std::false_type{}, std::false_type{}, it, t0);
     }
-  } else if (!used) {
-#pragma unroll
-    for (int i = 0; i < NQW; ++i) m[i] = -INFINITY;  // empty chunk
+  }
+  if (tail) {
+    produce(it, t0);
+    consume(std::false_type{}, std::true_type{}, it, t0);
   }
 
   // ---- partials ----
@@ -341,7 +369,7 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   for (int i = 0; i < NQW; ++i) {
     const int s = slot0 + i;
     if (s >= nslots) continue;
-    const int h = hg * HPG + s / p.QB, qb = s % p.QB;
+    const int h = hg * HPG + hh, qb = s % p.QB;
     const float l = softmax_denominator<RB, ONES_ROW>(acc[i], ls[i], lane);
     const int64_t pidx = (((int64_t)b * p.H + h) * p.nchunks + r) * p.Mp + qb * 32 + c;
     float* pa = p.part_acc + pidx * D;
@@ -361,9 +389,25 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
 // ---------------------------------------------------------------------------
 // Exact merge of split-key partials, parallel over chunk slices.  A block of
 // 256 threads owns 16 rows; thread (row, rs) folds chunks rs, rs+16, ... in
-// order, then the 16 slices of a row are folded pairwise (xor 1, 2, 4, 8).
-// The pairwise fold is symmetric, so every slice ends with the same bits.
+// order, then the 16 slices of a row are folded pairwise (xor 1, 2, 4, 8);
+// every slice then holds the whole row (equal up to the rounding order of its
+// folds), and output element d is taken from slice d % 16.  Each thread issues the loads of kCombineBatch partials before folding any
+// of them, so a batch costs one memory round trip.
 // ---------------------------------------------------------------------------
+constexpr int kCombineBatch = 4;
+
+template <int D>
+__device__ __forceinline__ void fold_partial(float& m, float& l, float (&a)[D], float mr, float lr,
+                                             const float (&ar)[D]) {
+  if (mr == -INFINITY) return;  // empty chunk: (-inf, 0, 0)
+  const float mn = fmaxf(m, mr);
+  const float wa = __builtin_amdgcn_exp2f(m - mn), wb = __builtin_amdgcn_exp2f(mr - mn);
+  l = l * wa + lr * wb;
+#pragma unroll
+  for (int d = 0; d < D; ++d) a[d] = a[d] * wa + ar[d] * wb;
+  m = mn;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
   constexpr int KS = D / 16;
@@ -374,50 +418,55 @@ __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
   float m = -INFINITY, l = 0.f, a[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) a[d] = 0.f;
-  for (int r = rs; r < p.R; r += 16) {
-    const int64_t pidx = (bh * p.R + r) * p.Mp + qrow;
-    const float mr = p.part_ml[pidx * 2];
-    if (mr == -INFINITY) continue;
-    const float lr = p.part_ml[pidx * 2 + 1];
-    float ar[D];
+  for (int r0 = rs; r0 < p.R; r0 += 16 * kCombineBatch) {
+    float mr[kCombineBatch], lr[kCombineBatch], ar[kCombineBatch][D];
 #pragma unroll
-    for (int d = 0; d < D; d += 4) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(p.part_acc + pidx * D + d);
-      ar[d] = v[0]; ar[d + 1] = v[1]; ar[d + 2] = v[2]; ar[d + 3] = v[3];
+    for (int u = 0; u < kCombineBatch; ++u) {
+      const int r = r0 + 16 * u;
+      mr[u] = -INFINITY;
+      lr[u] = 0.f;
+#pragma unroll
+      for (int d = 0; d < D; ++d) ar[u][d] = 0.f;
+      if (r < p.R) {
+        const int64_t pidx = (bh * p.R + r) * p.Mp + qrow;
+        const f32x2 ml = *reinterpret_cast<const f32x2*>(p.part_ml + pidx * 2);
+        mr[u] = ml[0];
+        lr[u] = ml[1];
+#pragma unroll
+        for (int d = 0; d < D; d += 4) {
+          const f32x4 v = *reinterpret_cast<const f32x4*>(p.part_acc + pidx * D + d);
+          ar[u][d] = v[0]; ar[u][d + 1] = v[1]; ar[u][d + 2] = v[2]; ar[u][d + 3] = v[3];
+        }
+      }
     }
-    const float mn = fmaxf(m, mr);
-    const float wa = __builtin_amdgcn_exp2f(m - mn), wb = __builtin_amdgcn_exp2f(mr - mn);
-    l = l * wa + lr * wb;
 #pragma unroll
-    for (int d = 0; d < D; ++d) a[d] = a[d] * wa + ar[d] * wb;
-    m = mn;
+    for (int u = 0; u < kCombineBatch; ++u) fold_partial<D>(m, l, a, mr[u], lr[u], ar[u]);
   }
 #pragma unroll
   for (int k = 1; k < 16; k <<= 1) {
-    const float mo = __shfl_xor(m, k, 64), lo = __shfl_xor(l, k, 64);
     float ao[D];
 #pragma unroll
     for (int d = 0; d < D; ++d) ao[d] = __shfl_xor(a[d], k, 64);
-    const float mn = fmaxf(m, mo);
-    if (mn != -INFINITY) {
-      const float wa = __builtin_amdgcn_exp2f(m - mn), wb = __builtin_amdgcn_exp2f(mo - mn);
-      l = l * wa + lo * wb;
-#pragma unroll
-      for (int d = 0; d < D; ++d) a[d] = a[d] * wa + ao[d] * wb;
-      m = mn;
-    }
+    const float mo = __shfl_xor(m, k, 64), lo = __shfl_xor(l, k, 64);
+    fold_partial<D>(m, l, a, mo, lo, ao);
   }
   const bool valid = qrow < p.M;
   const float inv = (valid && l > 0.f) ? 1.f / l : 0.f;
   const int qb = qrow >> 5, qc = qrow & 31;
-  if (p.frag && p.q_op && p.rnorm2 && rs == 0 && valid) {
+  if (p.frag && p.q_op && p.qnorm2) {
+    // max over the wave's 4 rows of |scaled q|^2 (of the rounded operand),
+    // one entry per wave
     float n2 = 0.f;
+    if (valid) {
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const float q = to_f32(from_f32<T>(a[d] * inv * p.qscale));
-      n2 = __builtin_fmaf(q, q, n2);
+      for (int d = 0; d < D; ++d) {
+        const float q = to_f32(from_f32<T>(a[d] * inv * p.qscale));
+        n2 = __builtin_fmaf(q, q, n2);
+      }
     }
-    atomicMax(p.rnorm2 + bh, __float_as_uint(n2));
+    n2 = fmaxf(n2, __shfl_xor(n2, 16, 64));
+    n2 = fmaxf(n2, __shfl_xor(n2, 32, 64));
+    if ((t & 63) == 0) p.qnorm2[bh * (p.Mp / 4) + (blockIdx.x % rows_per_bh) * 4 + (t >> 6)] = n2;
   }
 #pragma unroll
   for (int d0 = 0; d0 < D; d0 += 16) {
@@ -520,6 +569,16 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 #pragma unroll
   for (int hg = 0; hg < HG; ++hg) {
     decode_stage_issue<T, D, KSC>(p, smem, SE, b, hg + 1);
+    // route-query norm bound of each head of the group (max over the
+    // combine's per-wave entries)
+    float qn2[HPG];
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      const float* qp = p.qnorm2 + ((int64_t)b * p.H + hg * HPG + hh) * (Mp / 4);
+      float v = 0.f;
+      for (int i = lane; i < Mp / 4; i += 64) v = fmaxf(v, qp[i]);
+      qn2[hh] = v;
+    }
     const T* sb = bufs + (hg & 1) * SE;
     f32x16 ka[GB];
 #pragma unroll
@@ -539,7 +598,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
         kf[js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
       }
       // |score| bound: token-key norms x the route-query norm bound
-      const float bound = frag_rows_max_sq<T, KS>(kf) * __uint_as_float(p.rnorm2[(int64_t)b * p.H + h]);
+      const float bound = frag_rows_max_sq<T, KS>(kf) * wave_max_nonneg(qn2[hh]);
       const bool fast = uniform(bound <= p.fast_lim);
       const T* ql = sb + WELEMS + hh * Mp * D;
       const T* zl = sb + WELEMS + HPG * Mp * D + hh * ZH;
@@ -550,10 +609,13 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
         for (int e = 0; e < 16; ++e) acc[rb][e] = 0.f;
       float m = -INFINITY, ls = 0.f;
       const F zfill = (c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
-      // all route tiles of the head shift-free (sf = true) or online
-      auto routes = [&](auto sf) {
+      // all route tiles of the head shift-free (sf = true) or online; only the
+      // last route tile can be partial (M % 32 != 0) and it alone is masked
+      const int rt_full = p.M / 32;
+      auto routes = [&](auto sf) __attribute__((always_inline)) {
         constexpr bool SF = decltype(sf)::value;
-        for (int rt = 0; rt < RT; ++rt) {
+        auto tile = [&](int rt, auto mask) __attribute__((always_inline)) {
+          constexpr bool MASK = decltype(mask)::value;
           F qa[KS];
 #pragma unroll
           for (int js = 0; js < KS; ++js) qa[js] = load_frag(ql + ((rt * KS + js) * 64 + lane) * 8);
@@ -568,15 +630,12 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
           for (int e = 0; e < 16; ++e) sc[e] = 0.f;
 #pragma unroll
           for (int js = 0; js < KS; ++js) mma(sc, qa[js], kf[js]);
-          const int nvalid = min(32, p.M - rt * 32);
-          if (nvalid == 32) {
-            if (SF) tile_shift_free<T, RB, ONES_ROW, false>(acc, ls, sc, zv, 32, lane);
-            else tile_online<T, RB, ONES_ROW, false>(acc, m, ls, sc, zv, 32, lane);
-          } else {
-            if (SF) tile_shift_free<T, RB, ONES_ROW, true>(acc, ls, sc, zv, nvalid, lane);
-            else tile_online<T, RB, ONES_ROW, true>(acc, m, ls, sc, zv, nvalid, lane);
-          }
-        }
+          const int nvalid = MASK ? p.M - rt * 32 : 32;
+          if (SF) tile_shift_free<T, RB, ONES_ROW, MASK>(acc, ls, sc, zv, nvalid, lane);
+          else tile_online<T, RB, ONES_ROW, MASK>(acc, m, ls, sc, zv, nvalid, lane);
+        };
+        for (int rt = 0; rt < rt_full; ++rt) tile(rt, std::false_type{});
+        if (rt_full < RT) tile(rt_full, std::true_type{});
       };
       if (fast) routes(std::true_type{});
       else routes(std::false_type{});
@@ -625,7 +684,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 // ---------------------------------------------------------------------------
 template <typename T>
 hipError_t launch_prep_fused(const PrepFusedParams& p, hipStream_t s) {
-  const int64_t n = 5 * (int64_t)p.C * p.C / 8 + (int64_t)p.H * (p.Mp / 32) * (p.D / 16) * 64 + p.n_zero;
+  const int64_t n = 5 * (int64_t)p.C * p.C / 8 + (int64_t)p.H * (p.Mp / 32) * (p.D / 16) * 64;
   k_prep_fused<T><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
   return hipGetLastError();
 }
@@ -636,6 +695,7 @@ static hipError_t enc_one(const EncFusedParams& p, hipStream_t s) {
                 !fused_width_ok(16 * KSC, sizeof(T))) {
     return hipErrorInvalidValue;
   } else {
+    if (EncShape<D>::HPG > 1 && p.QB % NQW != 0) return hipErrorInvalidValue;  // one head per wave
     const int HG = p.H / EncShape<D>::HPG;
     const int64_t nck = (int64_t)p.B * p.nchunks;
     const unsigned grid = (unsigned)(((nck + 7) / 8) * 8 * HG * p.qgroups);

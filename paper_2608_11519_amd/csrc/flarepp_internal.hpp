@@ -70,8 +70,8 @@ struct CombineParams {
   int frag;
   void* q_op;
   void* z_op;
-  unsigned* rnorm2;  // frag == 1 with q_op: per (b, h) max over routes of
-                     // |scaled q|^2 as float bits (atomic max; zeroed before)
+  float* qnorm2;  // frag == 1 with q_op: [BH][Mp / 4] max of |scaled q|^2 over
+                  // each group of 4 routes (one entry per wave), or null
 };
 
 // Fragment order of the route operands of the fused kernels (per (b, h)):
@@ -98,8 +98,6 @@ struct PrepFusedParams {
   int H, M, Mp, D;
   float qscale;
   void* seeds_op;     // [H] x q fragment order, scaled
-  unsigned* zero;     // n_zero words cleared to 0 (route norm bounds)
-  int n_zero;
 };
 
 struct EncFusedParams {
@@ -120,7 +118,7 @@ struct DecFusedParams {
   const void* wof;    // merge fragments of W_O
   const void* q_op;   // [B][H] x q fragment order: scaled synthesised queries
   const void* z_op;   // [B][H] x z fragment order: latents
-  const unsigned* rnorm2;  // [B][H] max |scaled q|^2 over the routes (float bits)
+  const float* qnorm2;  // [B][H][Mp / 4] max |scaled q|^2 per group of 4 routes
   int B, N, C, H, M, Mp;
   float fast_lim;
   void* y;            // [B][N][C] decoded tokens, or null

@@ -31,7 +31,7 @@ EXPORTS = (
     "flarepp_project_workspace_bytes", "flarepp_project",
     "flarepp_route_workspace_bytes", "flarepp_route",
     "flarepp_mixer_workspace_bytes", "flarepp_mixer_forward", "flarepp_mixer_forward_debug",
-    "flarepp_mixer_forward_profiled", "flarepp_mixer_path",
+    "flarepp_mixer_forward_profiled", "flarepp_mixer_path", "flarepp_mixer_stage",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -83,6 +83,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_mixer_forward_profiled.restype = i32
     lib.flarepp_mixer_forward_profiled.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8
                                                    + [vp, sz, vp, ctypes.POINTER(vp), i32])
+    lib.flarepp_mixer_stage.restype = i32
+    lib.flarepp_mixer_stage.argtypes = [i32, i32, i64, i64, i64, i64, i64] + [vp] * 8 + [vp, sz, vp]
     _lib = lib
     return lib
 
@@ -268,6 +270,21 @@ def flarepp_mixer_forward_profiled(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, ev
                                             handles, PROFILE_EVENTS)
     _check(rc)
     return O
+
+
+def flarepp_mixer_stage(stage: int, X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, out: torch.Tensor,
+                        ws: torch.Tensor) -> None:
+    """Run stage ``stage`` (1-based, as PROFILE_STAGES) of the mixer alone.
+    ``ws`` and ``out`` must be those of a complete mixer forward with the same
+    arguments."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    dt = _dtype_code(X)
+    rc = lib.flarepp_mixer_stage(stage, dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt),
+                                 _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(out), _ptr(ws), ws.numel(),
+                                 _stream(X.device))
+    _check(rc)
 
 
 # short aliases

@@ -113,6 +113,14 @@ def test_hot_tokens_bf16():
     _check_mixer(w, inp.make_inputs(w, 2, x_scale=4.0), "hot-bf16")
 
 
+@pytest.mark.parametrize("M", [96, 160])
+def test_odd_route_block_counts_bf16(M):
+    # M / 32 odd at D = 16: the two heads of a channel group each own an odd
+    # number of 32-route blocks, so query slots must not straddle heads
+    w = inp.Workload("oddblocks", 2, 1500, 128, 8, M, "bf16", "normal")
+    _check_mixer(w, inp.make_inputs(w, 13, seed_scale=4.0), f"oddblocks-M{M}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_online_max_path_everywhere(monkeypatch, dtype):
     # the same mixer with the shift-free path switched off on the host
