@@ -120,6 +120,18 @@ EncPlan encode_plan(int64_t B, int64_t H, int64_t N, int64_t Mp, int64_t D) {
   return e;
 }
 
+// Decode kernel for a shape; FLAREPP_DECODE_KIND (0, 1, 2) may force a
+// smaller-footprint kernel than the one chosen (for testing every kernel).
+int decode_kind_for(int C, int D, int Mp, int elem_bytes) {
+  int k = flarepp::decode_kind(C, D, Mp, elem_bytes);
+  const char* f = std::getenv("FLAREPP_DECODE_KIND");
+  if (f) {
+    const int want = std::atoi(f);
+    if (want >= 0 && want < k) k = want;
+  }
+  return k;
+}
+
 // Squared score bound of the shift-free softmax path (2% below kFastRange^2
 // for the rounding of the norms); FLAREPP_NO_FAST_PATH=1 disables the path.
 float fast_limit() {
@@ -275,7 +287,9 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     PrepFusedParams pp{};
     pp.C = (int)C;
     const void* win[5] = {Wk, Wv, Wkt, Wvt, Wo};
-    const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain, kFragMerge};
+    const int dkind = decode_kind_for((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype));
+    const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain,
+                         dkind == kDecodeStaged ? kFragMerge : kFragMergeHg};
     for (int i = 0; i < 5; ++i) { pp.w[i] = win[i]; pp.wf[i] = w.wf[i]; pp.mode[i] = mode[i]; }
     pp.seeds = seeds; pp.H = (int)H; pp.M = (int)M; pp.Mp = (int)Mp; pp.D = (int)D;
     pp.qscale = qscale; pp.seeds_op = w.seeds_op;
@@ -306,6 +320,8 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
     dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O;
     dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);
+    dp.stage_bytes = (int)dec2_stage_bytes((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype));
+    dp.kind = dkind;
     if (RUN(7)) HIPTRY(launch_decode_fused<T>(dp, (int)D, s));  // call 3 + merge
     STAGE(7);
     STAGE(8);

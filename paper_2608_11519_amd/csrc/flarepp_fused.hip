@@ -90,10 +90,15 @@ __global__ void k_prep_fused(PrepFusedParams p) {
     const int g = lane >> 5, c = lane & 31, mode = p.mode[w];
     const int col = 32 * cb + (mode == kFragKeyPerm ? key_perm(c) : c);
     const T* W = (const T*)p.w[w];
-    T* out = (T*)p.wf[w] + f * 8;
+    int64_t fo = f;
+    if (mode == kFragMergeHg) {  // [head group][output block][k step in group][64][8]
+      const int kpg = p.D == 64 ? 4 : 2, CB = C / 32;
+      fo = ((int64_t)((ks / kpg) * CB + cb) * kpg + ks % kpg) * 64 + lane;
+    }
+    T* out = (T*)p.wf[w] + fo * 8;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int row = 16 * ks + (mode == kFragMerge ? acc_row16(g, j) : 8 * g + j);
+      const int row = 16 * ks + (mode == kFragMerge || mode == kFragMergeHg ? acc_row16(g, j) : 8 * g + j);
       out[j] = W[(int64_t)row * C + col];
     }
     return;
@@ -228,13 +233,15 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
 
   const int k0 = r * p.chunk, k1 = min(p.N, k0 + p.chunk);
   const T* xb = (const T*)p.x + (int64_t)b * p.N * p.C;
+  // X rows past the chunk are clamped to its last row: their keys and values
+  // duplicate a real token's (masked out of the softmax, and never above the
+  // key norm bound), and every load is unconditional, so the compiler can
+  // count the loads in flight and wait for the previous super-tile's only
   F xf[KSC];
   {
-    const int row = k0 + 32 * wave + c;
-    const bool ok = row < k1;
+    const int row = min(k0 + 32 * wave + c, k1 - 1);
 #pragma unroll
-    for (int ks = 0; ks < KSC; ++ks)
-      xf[ks] = ok ? load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g) : zero_frag<T>();
+    for (int ks = 0; ks < KSC; ++ks) xf[ks] = load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g);
   }
   lds_wait_barrier();  // weight slices and constant rows in LDS
 
@@ -255,11 +262,9 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
       }
     }
     {
-      const int row = t0 + STEP + 32 * wave + c;
-      const bool ok = row < k1;
+      const int row = min(t0 + STEP + 32 * wave + c, k1 - 1);
 #pragma unroll
-      for (int ks = 0; ks < KSC; ++ks)
-        xf[ks] = ok ? load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g) : zero_frag<T>();
+      for (int ks = 0; ks < KSC; ++ks) xf[ks] = load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g);
     }
     T* tl = tiles + (buf * W + wave) * TILE;
 #pragma unroll
@@ -496,6 +501,47 @@ __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
   if (valid && p.lse && rs == 0) p.lse[bh * p.M + qrow] = 0.6931471805599453f * (m + __log2f(l));
 }
 
+// Route tiles of the HPG heads of a group, software pipelined over the
+// sequence (rt, hh): the score tile of the next pair is issued (its MFMA runs
+// in the matrix pipe) before the softmax and value product of the current
+// one.  score(rt, hh) returns a score tile, finish(rt, hh, s, mask) consumes
+// it.  Route tiles below rt_full are whole; tile rt_full (when rt_full < RT)
+// is the partial, masked one.
+template <int HPG, class Score, class Finish>
+__device__ __forceinline__ void pipelined_routes2(int RT, int rt_full, Score&& score, Finish&& finish) {
+  f32x16 a = score(0, 0), bb;
+  if constexpr (HPG == 2) {
+    int rt = 0;
+    for (; rt < rt_full; ++rt) {
+      bb = score(rt, 1);
+      finish(rt, 0, a, std::false_type{});
+      if (rt + 1 < RT) a = score(rt + 1, 0);
+      finish(rt, 1, bb, std::false_type{});
+    }
+    if (rt < RT) {
+      bb = score(rt, 1);
+      finish(rt, 0, a, std::true_type{});
+      finish(rt, 1, bb, std::true_type{});
+    }
+  } else {
+    int rt = 0;
+    for (; rt + 2 <= rt_full; rt += 2) {
+      bb = score(rt + 1, 0);
+      finish(rt, 0, a, std::false_type{});
+      if (rt + 2 < RT) a = score(rt + 2, 0);
+      finish(rt + 1, 0, bb, std::false_type{});
+    }
+    if (rt < rt_full) {  // one whole tile left (scores in a), maybe a partial one after it
+      const bool part = rt + 1 < RT;
+      if (part) bb = score(rt + 1, 0);
+      finish(rt, 0, a, std::false_type{});
+      if (part) finish(rt + 1, 0, bb, std::true_type{});
+    } else if (rt < RT) {  // only the partial tile left (scores in a)
+      finish(rt, 0, a, std::true_type{});
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Decode with the key projection and the merge fused (call 3 + W_O).
 // ---------------------------------------------------------------------------
@@ -512,7 +558,7 @@ int decode_stage_elems(int C, int D, int Mp) {
 
 bool decode_fused_fits(int C, int D, int Mp, int elem_bytes) {
   const size_t se = (size_t)decode_stage_elems(C, D, Mp) * elem_bytes;
-  return 2 * se <= 160 * 1024;
+  return decode_kind(C, D, Mp, elem_bytes) != kDecodeStaged || 2 * se + 16 * elem_bytes <= 160 * 1024;
 }
 
 // Issue the global -> LDS copy of decode stage s into buffer s & 1: for
@@ -557,28 +603,42 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
   const bool xok = xrow < p.N;
   const int Mp = p.Mp, RT = Mp / 32;
   const int ZH = (int)z_frag_elems_per_head(Mp, D);
+  constexpr int ZC = D < 32 ? D : 32;  // value rows per z fragment
+  // constant value-operand rows for D = 16 (after the two stage buffers):
+  // 8 ones (row 16, the denominators), then 8 zeros (rows 17 .. 31)
+  const int zconst_off = 2 * SE * (int)sizeof(T);
+  if (ONES_ROW && threadIdx.x < 2)
+    store_frag<T>(reinterpret_cast<T*>(smem + zconst_off) + 8 * threadIdx.x,
+                  threadIdx.x == 0 ? fill_frag<T>(1.f) : zero_frag<T>());
 
   decode_stage_issue<T, D, KSC>(p, smem, SE, b, 0);
   F xf[KSC];
 #pragma unroll
   for (int ks = 0; ks < KSC; ++ks)
-    xf[ks] = xok ? load_frag((const T*)p.x + ((int64_t)b * p.N + xrow) * C + 16 * ks + 8 * g) : zero_frag<T>();
+    xf[ks] = load_frag((const T*)p.x + ((int64_t)b * p.N + min(xrow, p.N - 1)) * C + 16 * ks + 8 * g);
   lds_wait_barrier();
+
+  // route-query norm bound of each head of a group (this lane's share of the
+  // max over the combine's per-wave entries), loaded one group ahead
+  auto load_qn2 = [&](int hg, float (&v)[HPG]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      const float* qp = p.qnorm2 + ((int64_t)b * p.H + hg * HPG + hh) * (Mp / 4);
+      v[hh] = 0.f;
+      for (int i = lane; i < Mp / 4; i += 64) v[hh] = fmaxf(v[hh], qp[i]);
+    }
+  };
+  float qn2_next[HPG];
+  load_qn2(0, qn2_next);
 
   F yf[KSC];  // decoded tokens, merge B operands (16 channels per k step)
 #pragma unroll
   for (int hg = 0; hg < HG; ++hg) {
     decode_stage_issue<T, D, KSC>(p, smem, SE, b, hg + 1);
-    // route-query norm bound of each head of the group (max over the
-    // combine's per-wave entries)
     float qn2[HPG];
 #pragma unroll
-    for (int hh = 0; hh < HPG; ++hh) {
-      const float* qp = p.qnorm2 + ((int64_t)b * p.H + hg * HPG + hh) * (Mp / 4);
-      float v = 0.f;
-      for (int i = lane; i < Mp / 4; i += 64) v = fmaxf(v, qp[i]);
-      qn2[hh] = v;
-    }
+    for (int hh = 0; hh < HPG; ++hh) qn2[hh] = qn2_next[hh];
+    if (hg + 1 < HG) load_qn2(hg + 1, qn2_next);
     const T* sb = bufs + (hg & 1) * SE;
     f32x16 ka[GB];
 #pragma unroll
@@ -588,63 +648,84 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 #pragma unroll
       for (int ks = 0; ks < KSC; ++ks) mma(ka[cb], load_frag(sb + ((cb * KSC + ks) * 64 + lane) * 8), xf[ks]);
     }
+    // token keys of the group's heads, and the |score| bound (token-key
+    // norms x the route-query norm bound); the heads of a group go through
+    // one route loop together, shift-free only if both bounds allow it
+    F kf[HPG][KS];
+    float bnd = 0.f;
 #pragma unroll
     for (int hh = 0; hh < HPG; ++hh) {
-      const int h = hg * HPG + hh;
-      F kf[KS];
 #pragma unroll
       for (int js = 0; js < KS; ++js) {
         const int fi = hh * KS + js;
-        kf[js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
+        kf[hh][js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
       }
-      // |score| bound: token-key norms x the route-query norm bound
-      const float bound = frag_rows_max_sq<T, KS>(kf) * wave_max_nonneg(qn2[hh]);
-      const bool fast = uniform(bound <= p.fast_lim);
-      const T* ql = sb + WELEMS + hh * Mp * D;
-      const T* zl = sb + WELEMS + HPG * Mp * D + hh * ZH;
-      f32x16 acc[RB];
+      bnd = fmaxf(bnd, frag_rows_max_sq<T, KS>(kf[hh]) * wave_max_nonneg(qn2[hh]));
+    }
+    const bool fast = uniform(bnd <= p.fast_lim);
+    // z operand addresses (bytes into LDS): lanes of value rows walk the
+    // head's z fragments; on D = 16 the lanes of rows 16 .. 31 read the
+    // constant ones / zeros block instead
+    const char* sbc = reinterpret_cast<const char*>(sb);
+    uint32_t zbase[HPG], zstep;
+    {
+      const bool konst = ONES_ROW && c >= 16;
+      zstep = konst ? 0u : (uint32_t)(2 * ZC * 8 * sizeof(T));
+#pragma unroll
+      for (int hh = 0; hh < HPG; ++hh)
+        zbase[hh] = konst ? (uint32_t)(zconst_off + (c == 16 ? 0 : 8 * (int)sizeof(T)))
+                          : (uint32_t)((sbc - smem) + (WELEMS + HPG * Mp * D + hh * ZH + (g * ZC + c) * 8) * sizeof(T));
+    }
+    f32x16 acc[HPG][RB];
+    float m[HPG], ls[HPG];
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      m[hh] = -INFINITY;
+      ls[hh] = 0.f;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[rb][e] = 0.f;
-      float m = -INFINITY, ls = 0.f;
-      const F zfill = (c == 16) ? fill_frag<T>(1.f) : zero_frag<T>();
-      // all route tiles of the head shift-free (sf = true) or online; only the
-      // last route tile can be partial (M % 32 != 0) and it alone is masked
-      const int rt_full = p.M / 32;
-      auto routes = [&](auto sf) __attribute__((always_inline)) {
-        constexpr bool SF = decltype(sf)::value;
-        auto tile = [&](int rt, auto mask) __attribute__((always_inline)) {
-          constexpr bool MASK = decltype(mask)::value;
-          F qa[KS];
+        for (int e = 0; e < 16; ++e) acc[hh][rb][e] = 0.f;
+    }
+    // all route tiles shift-free (sf = true) or online; only the last route
+    // tile can be partial (M % 32 != 0) and it alone is masked
+    const int rt_full = p.M / 32;
+    auto score = [&](int rt, int hh) __attribute__((always_inline)) {
+      f32x16 sc;
 #pragma unroll
-          for (int js = 0; js < KS; ++js) qa[js] = load_frag(ql + ((rt * KS + js) * 64 + lane) * 8);
-          F zv[2][RB];
+      for (int e = 0; e < 16; ++e) sc[e] = 0.f;
 #pragma unroll
-          for (int hf = 0; hf < 2; ++hf)
+      for (int js = 0; js < KS; ++js)
+        mma(sc, load_frag(sb + WELEMS + hh * Mp * D + ((rt * KS + js) * 64 + lane) * 8), kf[hh][js]);
+      return sc;
+    };
+    auto routes = [&](auto sf) __attribute__((always_inline)) {
+      constexpr bool SF = decltype(sf)::value;
+      auto finish = [&](int rt, int hh, const f32x16& sc, auto mask) __attribute__((always_inline)) {
+        constexpr bool MASK = decltype(mask)::value;
+        const int nvalid = MASK ? p.M - rt * 32 : 32;
+        F zv[2][RB];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-              zv[hf][rb] = (ONES_ROW && c >= 16) ? zfill : load_frag(zl + z_frag_index(rt, hf, rb, g, c, 0, D));
-          f32x16 sc;
+        for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) sc[e] = 0.f;
-#pragma unroll
-          for (int js = 0; js < KS; ++js) mma(sc, qa[js], kf[js]);
-          const int nvalid = MASK ? p.M - rt * 32 : 32;
-          if (SF) tile_shift_free<T, RB, ONES_ROW, MASK>(acc, ls, sc, zv, nvalid, lane);
-          else tile_online<T, RB, ONES_ROW, MASK>(acc, m, ls, sc, zv, nvalid, lane);
-        };
-        for (int rt = 0; rt < rt_full; ++rt) tile(rt, std::false_type{});
-        if (rt_full < RT) tile(rt_full, std::true_type{});
+          for (int rb = 0; rb < RB; ++rb)
+            zv[hf][rb] = *reinterpret_cast<const F*>(smem + zbase[hh] + zstep * ((rt * 2 + hf) * RB + rb));
+        if (SF) tile_shift_free<T, RB, ONES_ROW, MASK>(acc[hh], ls[hh], sc, zv, nvalid, lane);
+        else tile_online<T, RB, ONES_ROW, MASK>(acc[hh], m[hh], ls[hh], sc, zv, nvalid, lane);
       };
-      if (fast) routes(std::true_type{});
-      else routes(std::false_type{});
-      const float inv = 1.f / softmax_denominator<RB, ONES_ROW>(acc, ls, lane);
+      pipelined_routes2<HPG>(RT, rt_full, score, finish);
+    };
+    if (fast) routes(std::true_type{});
+    else routes(std::false_type{});
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      const int h = hg * HPG + hh;
+      const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane));
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
-          if (rb * 32 + 16 * hf < D) yf[h * KS + 2 * rb + hf] = cvt8<T>(acc[rb], 8 * hf, inv);
+          if (rb * 32 + 16 * hf < D) yf[h * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
       if (p.y && xok) {
         T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + h * D;
         constexpr int NQ4 = ONES_ROW ? 2 : 4;
@@ -652,8 +733,8 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
           for (int q = 0; q < NQ4; ++q)
-            store4(yp + rb * 32 + 8 * q + 4 * g, acc[rb][4 * q] * inv, acc[rb][4 * q + 1] * inv,
-                   acc[rb][4 * q + 2] * inv, acc[rb][4 * q + 3] * inv);
+            store4(yp + rb * 32 + 8 * q + 4 * g, acc[hh][rb][4 * q] * inv, acc[hh][rb][4 * q + 1] * inv,
+                   acc[hh][rb][4 * q + 2] * inv, acc[hh][rb][4 * q + 3] * inv);
       }
     }
     lds_wait_barrier();
@@ -676,6 +757,252 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
       for (int q = 0; q < 4; ++q) store4(op + 8 * q + 4 * g, o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
     }
     if (cbo + 1 < CB) lds_wait_barrier();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Decode for C <= 128, one stage per head group.  A stage holds everything
+// the group needs: [key weight slice][W_O rows of the group's channels (all
+// output blocks)][q of its heads][z of its heads][route norm bounds].  With
+// RES every stage is copied into LDS once at the start (when all fit) and the
+// waves never synchronise again; otherwise two stage buffers alternate.  The
+// merge accumulates O^T += W_O^T Y^T over the head groups, so the decoded
+// tokens of a group are used as soon as they exist.
+// ---------------------------------------------------------------------------
+size_t dec2_stage_bytes(int C, int D, int Mp, int elem_bytes) {
+  const int hpg = D == 16 ? 2 : 1, gb = D == 64 ? 2 : 1;
+  const size_t el = (size_t)gb * (C / 16) * kFrag + (size_t)(C / 32) * 2 * gb * kFrag +
+                    (size_t)hpg * ((size_t)Mp * D + z_frag_elems_per_head(Mp, D));
+  return el * elem_bytes + (size_t)hpg * Mp;  // + hpg * Mp / 4 float bounds
+}
+
+size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res) {
+  const int hg = C / 32 / (D == 64 ? 2 : 1);
+  return (res ? hg : 2) * dec2_stage_bytes(C, D, Mp, elem_bytes) + 16 * elem_bytes;
+}
+
+int decode_kind(int C, int D, int Mp, int elem_bytes) {
+  if (C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, true) <= 160 * 1024) return kDecodeGroupsResident;
+  if (C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, false) <= 160 * 1024) return kDecodeGroupsStaged;
+  return kDecodeStaged;
+}
+
+template <typename T, int D, int KSC>
+__device__ __forceinline__ void dec2_stage_issue(const DecFusedParams& p, char* dst, int b, int hg) {
+  constexpr int HPG = (D == 16) ? 2 : 1, GB = (D == 64) ? 2 : 1;
+  constexpr int C = KSC * 16, CB = C / 32, H = C / D, NT = 64 * dec_waves(C), PER16 = 16 / (int)sizeof(T);
+  constexpr int WELEMS = GB * KSC * kFrag, WOE = CB * 2 * GB * kFrag;
+  const int Mp = p.Mp, QE = HPG * Mp * D;
+  const int ZE = HPG * (int)z_frag_elems_per_head(Mp, D);
+  const int64_t h0 = (int64_t)b * H + hg * HPG;
+  copy_to_lds((const T*)p.wkf + (int64_t)hg * WELEMS, dst, WELEMS / PER16, NT);
+  dst += WELEMS * sizeof(T);
+  copy_to_lds((const T*)p.wof + (int64_t)hg * WOE, dst, WOE / PER16, NT);
+  dst += WOE * sizeof(T);
+  copy_to_lds((const T*)p.q_op + h0 * Mp * D, dst, QE / PER16, NT);
+  dst += QE * sizeof(T);
+  copy_to_lds((const T*)p.z_op + h0 * z_frag_elems_per_head(Mp, D), dst, ZE / PER16, NT);
+  dst += ZE * sizeof(T);
+  copy_to_lds(p.qnorm2 + h0 * (Mp / 4), dst, HPG * Mp / 16, NT);
+}
+
+template <typename T, int D, int KSC, bool RES>
+__global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode2(DecFusedParams p) {
+  using F = typename Frag<T>::type;
+  constexpr int HPG = (D == 16) ? 2 : 1, GB = (D == 64) ? 2 : 1;
+  constexpr int KS = D / 16, RB = (D + 31) / 32, KPG = 2 * GB;  // k steps (16 channels) per group
+  constexpr bool ONES_ROW = (D == 16);
+  constexpr int C = KSC * 16, CB = C / 32, HG = CB / GB;
+  constexpr int WELEMS = GB * KSC * kFrag, WOE = CB * KPG * kFrag;
+  constexpr int NW = dec_waves(C), TOK = 32 * NW;
+  constexpr int ZC = D < 32 ? D : 32;  // value rows per z fragment
+  static_assert(C <= 128, "per-group merge accumulators are sized for C <= 128");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int Mp = p.Mp, RT = Mp / 32, QH = Mp * D;
+  const int ZH = (int)z_frag_elems_per_head(Mp, D);
+  const int SB = p.stage_bytes;
+  T* cst = reinterpret_cast<T*>(smem + (RES ? HG : 2) * SB);  // 8 ones (row 16), 8 zeros
+
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
+  const int nblk = (p.N + TOK - 1) / TOK;
+  const int b = blockIdx.x / nblk;
+  const int xrow = (blockIdx.x % nblk) * TOK + wave * 32 + c;
+  const bool xok = xrow < p.N;
+
+  if (RES) {
+    for (int hg = 0; hg < HG; ++hg) dec2_stage_issue<T, D, KSC>(p, smem + hg * SB, b, hg);
+  } else {
+    dec2_stage_issue<T, D, KSC>(p, smem, b, 0);
+  }
+  if (ONES_ROW && threadIdx.x < 2) store_frag<T>(cst + 8 * threadIdx.x, threadIdx.x == 0 ? fill_frag<T>(1.f) : zero_frag<T>());
+  F xf[KSC];
+#pragma unroll
+  for (int ks = 0; ks < KSC; ++ks)
+    xf[ks] = load_frag((const T*)p.x + ((int64_t)b * p.N + min(xrow, p.N - 1)) * C + 16 * ks + 8 * g);
+  lds_wait_barrier();
+
+  // z operand lanes: value-row lanes walk the head's z fragments; on D = 16
+  // the lanes of rows 16 .. 31 read the constant block
+  const bool konst = ONES_ROW && c >= 16;
+  const uint32_t zstep = konst ? 0u : (uint32_t)(2 * ZC * 8 * sizeof(T));
+  const uint32_t zhead = konst ? 0u : (uint32_t)(ZH * sizeof(T));
+  const uint32_t zlane = konst ? (uint32_t)((reinterpret_cast<char*>(cst) - smem) + (c == 16 ? 0 : 8 * sizeof(T)))
+                               : (uint32_t)((WELEMS + WOE + HPG * QH + (g * ZC + c) * 8) * sizeof(T));
+
+  f32x16 o[CB];  // O^T blocks of this wave's 32 tokens
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[cb][e] = 0.f;
+
+  // key projection of head group hg from the stage at byte offset so
+  auto project = [&](int so, f32x16 (&ka)[GB]) __attribute__((always_inline)) {
+    const T* wk = reinterpret_cast<const T*>(smem + so);
+#pragma unroll
+    for (int cb = 0; cb < GB; ++cb) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) ka[cb][e] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KSC; ++ks) mma(ka[cb], load_frag(wk + ((cb * KSC + ks) * 64 + lane) * 8), xf[ks]);
+    }
+  };
+  // max over a head's routes of |scaled q|^2 (wave-uniform), from its stage
+  auto route_norm = [&](int so, int hh) __attribute__((always_inline)) {
+    const float* qn = reinterpret_cast<const float*>(smem + so + (WELEMS + WOE + HPG * (QH + ZH)) * sizeof(T));
+    float v = 0.f;
+    for (int i = lane; i < Mp / 4; i += 64) v = fmaxf(v, qn[hh * (Mp / 4) + i]);
+    return wave_max_nonneg(v);
+  };
+  // With every stage resident the next group's projection is issued before
+  // this group's routes (the MFMAs run beside the softmax), and all route
+  // norms are reduced up front.
+  f32x16 ka[GB];
+  float qn_all[RES ? HG * HPG : 1];
+  if constexpr (RES) {
+    project(0, ka);
+#pragma unroll
+    for (int i = 0; i < HG * HPG; ++i) qn_all[i] = route_norm((i / HPG) * SB, i % HPG);
+  }
+
+  for (int hg = 0; hg < HG; ++hg) {
+    if (!RES && hg + 1 < HG) dec2_stage_issue<T, D, KSC>(p, smem + ((hg + 1) & 1) * SB, b, hg + 1);
+    const int so = (RES ? hg : (hg & 1)) * SB;  // this group's stage (bytes)
+    const T* st = reinterpret_cast<const T*>(smem + so);
+    if constexpr (!RES) project(so, ka);
+    // token keys of the group's heads
+    F kf[HPG][KS];
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh)
+#pragma unroll
+      for (int js = 0; js < KS; ++js) {
+        const int fi = hh * KS + js;
+        kf[hh][js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
+      }
+    // |score| bound: token-key norms x route-query norms; both heads of the
+    // group go shift-free only if both bounds allow it
+    float bnd = 0.f;
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      float qmax;
+      if constexpr (RES) {
+        qmax = 0.f;
+#pragma unroll
+        for (int i = 0; i < HG * HPG; ++i)
+          if (i == hg * HPG + hh) qmax = qn_all[i];
+      } else {
+        qmax = route_norm(so, hh);
+      }
+      bnd = fmaxf(bnd, frag_rows_max_sq<T, KS>(kf[hh]) * qmax);
+    }
+    const bool fast = uniform(bnd <= p.fast_lim);
+    if constexpr (RES) {
+      if (hg + 1 < HG) project((hg + 1) * SB, ka);
+    }
+
+    f32x16 acc[HPG][RB];
+    float m[HPG], ls[HPG];
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      m[hh] = -INFINITY;
+      ls[hh] = 0.f;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[hh][rb][e] = 0.f;
+    }
+    const int rt_full = p.M / 32;
+    auto score = [&](int rt, int hh) __attribute__((always_inline)) {
+      f32x16 sc;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+      for (int js = 0; js < KS; ++js)
+        mma(sc, load_frag(st + WELEMS + WOE + hh * QH + ((rt * KS + js) * 64 + lane) * 8), kf[hh][js]);
+      return sc;
+    };
+    auto zfrags = [&](int rt, int hh, F (&zv)[2][RB]) __attribute__((always_inline)) {
+      const uint32_t base = zlane + (konst ? 0u : (uint32_t)so) + zhead * hh;
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          zv[hf][rb] = *reinterpret_cast<const F*>(smem + base + zstep * ((rt * 2 + hf) * RB + rb));
+    };
+    if (fast) {
+      auto finish = [&](int rt, int hh, const f32x16& sc, auto mask) __attribute__((always_inline)) {
+        constexpr bool MASK = decltype(mask)::value;
+        F zv[2][RB];
+        zfrags(rt, hh, zv);
+        tile_shift_free<T, RB, ONES_ROW, MASK>(acc[hh], ls[hh], sc, zv, MASK ? p.M - rt * 32 : 32, lane);
+      };
+      pipelined_routes2<HPG>(RT, rt_full, score, finish);
+    } else {  // online maximum (rare): plain loop, every tile masked
+      for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int hh = 0; hh < HPG; ++hh) {
+          F zv[2][RB];
+          zfrags(rt, hh, zv);
+          tile_online<T, RB, ONES_ROW, true>(acc[hh], m[hh], ls[hh], score(rt, hh), zv, min(32, p.M - rt * 32), lane);
+        }
+      }
+    }
+
+    // decoded tokens of the group -> merge operands, and the partial merge
+    F yg[KPG];
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane));
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+          if (rb * 32 + 16 * hf < D) yg[hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
+      if (p.y && xok) {
+        T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + (hg * HPG + hh) * D;
+        constexpr int NQ4 = ONES_ROW ? 2 : 4;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int q = 0; q < NQ4; ++q)
+            store4(yp + rb * 32 + 8 * q + 4 * g, acc[hh][rb][4 * q] * inv, acc[hh][rb][4 * q + 1] * inv,
+                   acc[hh][rb][4 * q + 2] * inv, acc[hh][rb][4 * q + 3] * inv);
+      }
+    }
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int j = 0; j < KPG; ++j) mma(o[cb], load_frag(st + WELEMS + ((cb * KPG + j) * 64 + lane) * 8), yg[j]);
+    if (!RES && hg + 1 < HG) lds_wait_barrier();  // next stage in; this one free
+  }
+
+  if (xok) {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      T* op = (T*)p.o + ((int64_t)b * p.N + xrow) * C + 32 * cb;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        store4(op + 8 * q + 4 * g, o[cb][4 * q], o[cb][4 * q + 1], o[cb][4 * q + 2], o[cb][4 * q + 3]);
+    }
   }
 }
 
@@ -761,12 +1088,28 @@ static hipError_t dec_launch(const DecFusedParams& p, hipStream_t s) {
   } else {
     constexpr int NW = dec_waves(16 * KSC);
     const unsigned grid = (unsigned)((int64_t)p.B * ((p.N + 32 * NW - 1) / (32 * NW)));
-    const size_t lds = 2 * (size_t)p.stage_elems * sizeof(T);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_fused<T, D, KSC>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    k_decode_fused<T, D, KSC><<<grid, 64 * NW, lds, s>>>(p);
-    return hipGetLastError();
+    if constexpr (16 * KSC <= 128) {  // per-group stages (k_decode2)
+      if (p.kind != kDecodeStaged) {
+        const bool res = p.kind == kDecodeGroupsResident;
+        const size_t lds = dec2_lds_bytes(16 * KSC, D, p.Mp, sizeof(T), res);
+        const void* fn = res ? reinterpret_cast<const void*>(&k_decode2<T, D, KSC, true>)
+                             : reinterpret_cast<const void*>(&k_decode2<T, D, KSC, false>);
+        hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        if (res) k_decode2<T, D, KSC, true><<<grid, 64 * NW, lds, s>>>(p);
+        else k_decode2<T, D, KSC, false><<<grid, 64 * NW, lds, s>>>(p);
+        return hipGetLastError();
+      }
+    }
+    if (p.kind != kDecodeStaged) return hipErrorInvalidValue;
+    {
+      const size_t lds = (2 * (size_t)p.stage_elems + 16) * sizeof(T);  // + the constant rows
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_fused<T, D, KSC>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      k_decode_fused<T, D, KSC><<<grid, 64 * NW, lds, s>>>(p);
+      return hipGetLastError();
+    }
   }
 }
 

@@ -87,7 +87,9 @@ __host__ __device__ constexpr int64_t z_frag_index(int rt, int hf, int rb, int g
 }
 
 // ---- fused path -------------------------------------------------------------
-enum FragMode { kFragPlain = 0, kFragKeyPerm = 1, kFragMerge = 2 };
+// kFragMergeHg: the kFragMerge fragments stored head-group major,
+// [C/32 / (D == 64 ? 2 : 1) groups][C/32 output blocks][k steps of the group][64][8]
+enum FragMode { kFragPlain = 0, kFragKeyPerm = 1, kFragMerge = 2, kFragMergeHg = 3 };
 
 struct PrepFusedParams {
   int C;
@@ -123,7 +125,9 @@ struct DecFusedParams {
   float fast_lim;
   void* y;            // [B][N][C] decoded tokens, or null
   void* o;            // [B][N][C]
-  int stage_elems;    // elements per LDS stage buffer
+  int stage_elems;    // elements per LDS stage buffer (k_decode_fused)
+  int stage_bytes;    // bytes per head-group stage (k_decode2)
+  int kind;           // DecodeKind
 };
 
 // Fused path coverage.  bf16: C in {64, 128, 256}; fp32 (a correctness path):
@@ -138,6 +142,13 @@ constexpr bool dec_fused_ok(int elem_bytes, int D, int ksc) { return !(elem_byte
 size_t enc_fused_lds_bytes(int C, int D, int waves, int elem_bytes);
 int decode_stage_elems(int C, int D, int Mp);
 bool decode_fused_fits(int C, int D, int Mp, int elem_bytes);
+// Decode kernels: k_decode_fused (per-group stages of keys and routes, W_O
+// staged by output block at the end), k_decode2 with per-group stages that
+// also carry the group's W_O rows (two alternating buffers, or all resident).
+enum DecodeKind { kDecodeStaged = 0, kDecodeGroupsStaged = 1, kDecodeGroupsResident = 2 };
+int decode_kind(int C, int D, int Mp, int elem_bytes);
+size_t dec2_stage_bytes(int C, int D, int Mp, int elem_bytes);
+size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res);
 
 template <typename T> hipError_t launch_prep_fused(const PrepFusedParams&, hipStream_t);
 template <typename T> hipError_t launch_encode_fused(const EncFusedParams&, int D, int waves, hipStream_t);

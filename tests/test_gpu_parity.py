@@ -121,6 +121,16 @@ def test_odd_route_block_counts_bf16(M):
     _check_mixer(w, inp.make_inputs(w, 13, seed_scale=4.0), f"oddblocks-M{M}")
 
 
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("M", [64, 80])
+def test_every_decode_kernel(monkeypatch, kind, M):
+    # the decode kernels with smaller LDS footprints than the one the shape
+    # would get (per-group stages, then output-block staging of W_O)
+    monkeypatch.setenv("FLAREPP_DECODE_KIND", str(kind))
+    w = inp.Workload("deckind", 2, 1500, 128, 8, M, "bf16", "normal")
+    _check_mixer(w, inp.make_inputs(w, 14, seed_scale=4.0), f"decode-kind{kind}-M{M}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_online_max_path_everywhere(monkeypatch, dtype):
     # the same mixer with the shift-free path switched off on the host
