@@ -119,22 +119,30 @@ def roofline(work, ms, dtype):
             "frac": round(a / p, 4), "traffic": None}
 
 
-# Kernel (symbol substring) that carries each stage, for the counter tables.
-STAGE_KERNELS_FUSED = {"prep": "k_prep_fused", "call1_encode": "k_encode_fused",
-                       "call1_combine": "k_combine_par", "call2_encode": "k_encode_fused",
-                       "call2_combine": "k_combine_par", "call3_decode": "k_decode_fused"}
+# Kernels (symbol substrings) that can carry each stage on the fused path, for
+# the counter tables; the decode is k_decode2 for C <= 128 when its stages fit.
+STAGE_KERNELS_FUSED = {"prep": ("k_prep_fused",), "call1_encode": ("k_encode_fused",),
+                       "call1_combine": ("k_combine_par",), "call2_encode": ("k_encode_fused",),
+                       "call2_combine": ("k_combine_par",),
+                       "call3_decode": ("k_decode2", "k_decode_fused")}
 
 
 def sources_digest():
-    """SHA-256 over the kernel sources and the build flags: counters taken
-    for other sources are not reported."""
+    """SHA-256 over the kernel sources (comments and layout removed) and the
+    build command: counters taken for other kernels are not reported."""
     import hashlib
+    import re
+    from paper_2608_11519_amd import build
+
     h = hashlib.sha256()
-    pkg = os.path.join(ROOT, "paper_2608_11519_amd")
-    files = sorted(os.path.join(pkg, "csrc", f) for f in os.listdir(os.path.join(pkg, "csrc")))
-    for f in files + [os.path.join(pkg, "build.py"), os.path.join(ROOT, "include", "flarepp.h")]:
-        with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    csrc = os.path.join(ROOT, "paper_2608_11519_amd", "csrc")
+    for name in sorted(os.listdir(csrc)) + ["../../include/flarepp.h"]:
+        with open(os.path.join(csrc, name)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(os.path.basename(name).encode() + b"\0" + " ".join(text.split()).encode())
+    h.update(" ".join(os.path.basename(a) for a in build.command("lib")).encode())
     return h.hexdigest()
 
 
@@ -147,14 +155,16 @@ def measured_traffic(w, stage):
     summary (FETCH_SIZE + WRITE_SIZE, scaled by the plain-copy calibration),
     or None when there is none for the current kernel sources."""
     path = traffic_file(w.name)
-    kern = STAGE_KERNELS_FUSED.get(stage)
-    if not kern or not os.path.exists(path):
+    if stage not in STAGE_KERNELS_FUSED or not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("sources_sha256") != sources_digest() or kern not in t.get("kernels", {}):
+    if t.get("sources_sha256") != sources_digest():
         return None
-    return t["kernels"][kern]["bytes_per_dispatch"]
+    for kern in STAGE_KERNELS_FUSED[stage]:
+        if kern in t.get("kernels", {}):
+            return t["kernels"][kern]["bytes_per_dispatch"]
+    return None
 
 
 def pmc_summary(fetch_dir, write_dir, workload, copy_mib, command):
@@ -182,7 +192,7 @@ def pmc_summary(fetch_dir, write_dir, workload, copy_mib, command):
     f_fac = copy_kib / float(cf["Counter_Value"])
     w_fac = copy_kib / float(cw["Counter_Value"])
     kernels = {}
-    for kern in sorted(set(STAGE_KERNELS_FUSED.values())):
+    for kern in sorted({k for ks in STAGE_KERNELS_FUSED.values() for k in ks}):
         fv = [float(r["Counter_Value"]) for r in fetch if kern in r["Kernel_Name"]]
         wv = [float(r["Counter_Value"]) for r in write if kern in r["Kernel_Name"]]
         if not fv or not wv:

@@ -6,14 +6,14 @@
  * routing" (arXiv 2608.11519):
  *
  *   project   K = X W_K, V = X W_V, K~ = X W~_K, V~ = X W~_V, each split into
- *             H heads of width D = C / H                (Sec. 2.1 Eq. (4);
- *                                                         Sec. 2.2 Eqs. (7), (9))
+ *             H heads of width D = C / H                (Sec. 3.1 Eq. (4);
+ *                                                         Sec. 3.2 Eqs. (7), (9))
  *   route     rectangular SDPA, softmax(Q K^T / sqrt(D)) V, with the softmax
- *             over the keys (Sec. 2.1 Eq. (3)).  ENCODE: M route queries over
+ *             over the keys (Sec. 3.1 Eq. (3)).  ENCODE: M route queries over
  *             N token keys (Eqs. (8), (10)); DECODE: N token queries over the
  *             M routes (Eq. (11)).
  *   mixer     project; Q = SDPA(Q~, K~, V~); Z = SDPA(Q, K, V);
- *             Y = SDPA(K, Q, Z); O = [Y_1 .. Y_H] W_O  (Fig. 1; Sec. 2.2)
+ *             Y = SDPA(K, Q, Z); O = [Y_1 .. Y_H] W_O  (Fig. 1; Sec. 3.2)
  *
  * Conventions shared by every entry point:
  *   - All tensors are dense, row-major, in device memory (hipMalloc or any
@@ -75,7 +75,7 @@ FLAREPP_API const char* flarepp_last_error(void);
 FLAREPP_API const char* flarepp_version(void);
 
 /* ---------------------------------------------------------------------------
- * Project (Sec. 2.1 Eq. (4); Sec. 2.2 Eqs. (7), (9)).
+ * Project (Sec. 3.1 Eq. (4); Sec. 3.2 Eqs. (7), (9)).
  *
  * X [B][N][C] and W* [C][C] in dtype.  For each non-null (W, out) pair,
  * out [B][H][N][D] = X W split into heads.  At least one pair must be given;
@@ -90,7 +90,7 @@ FLAREPP_API int flarepp_project(int dtype, int64_t B, int64_t N, int64_t C, int6
 
 /* ---------------------------------------------------------------------------
  * Route: one rectangular SDPA call with M routes and N tokens per (b, h)
- * (Sec. 2.1 Eq. (3)).
+ * (Sec. 3.1 Eq. (3)).
  *
  * FLAREPP_ENCODE (Eqs. (8), (10)):
  *   q    route queries, float32 [B][H][M][D]; route_batch_stride is the
@@ -105,7 +105,7 @@ FLAREPP_API int flarepp_project(int dtype, int64_t B, int64_t N, int64_t C, int6
  *   k, v route keys and values, float32 [B][H][M][D] (Q(X) and Z);
  *        route_batch_stride as above applies to both.
  *   out  dtype [B][N][H*D]: token n, head h at channels [h*D, (h+1)*D) =
- *        softmax_M(q_n k^T / sqrt(D)) v (heads merged, Sec. 2.1).
+ *        softmax_M(q_n k^T / sqrt(D)) v (heads merged, Sec. 3.1).
  *   lse  must be NULL.
  * Route-side inputs are rounded to the MFMA operand type inside the call.
  * ------------------------------------------------------------------------- */
@@ -117,7 +117,7 @@ FLAREPP_API int flarepp_route(int kind, int dtype, int64_t B, int64_t H, int64_t
                   void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
- * Whole mixer forward (Fig. 1; Sec. 2.2 Eqs. (7)-(11)).
+ * Whole mixer forward (Fig. 1; Sec. 3.2 Eqs. (7)-(11)).
  *
  * X [B][N][C]; Wk, Wv, Wkt (W~_K), Wvt (W~_V), Wo [C][C]; seeds (the learned
  * Q~, shared by the batch) [H][M][D]; O [B][N][C] -- all in dtype.

@@ -8,20 +8,20 @@ calls it and shares no code with it.
 It computes the plain definitions, in float64, in the paper's order:
 
 * ``project``     K = X W per weight, heads are contiguous D-wide column
-                  blocks (Sec. 2.1, Eq. (4); Sec. 2.2, Eqs. (7), (9)).
+                  blocks (Sec. 3.1, Eq. (4); Sec. 3.2, Eqs. (7), (9)).
 * ``sdpa``        rectangular scaled dot-product attention, softmax over the
-                  keys, scale 1/sqrt(D) (Sec. 2.1, Eq. (3)).  Also returns the
+                  keys, scale 1/sqrt(D) (Sec. 3.1, Eq. (3)).  Also returns the
                   row log-normaliser L = logsumexp of the scaled scores
                   (App. A.2, Eq. (20)).
 * ``mixer_forward`` project; Q = SDPA(Q~, K~, V~) (Eq. (8));
                   Z = SDPA(Q, K, V) (Eq. (10)); Y = SDPA(K, Q, Z) (Eq. (11));
-                  heads merged and multiplied by W_O (Sec. 2.1 after Eq. (2);
+                  heads merged and multiplied by W_O (Sec. 3.1 after Eq. (2);
                   Fig. 1 "merge(Y) @ Wo").
 * ``split_merge`` the exact split-key merge of partial results
                   (App. A.2, Eqs. (22)-(23); stable form App. A.3,
                   Eqs. (24)-(28), including the empty-row convention).
-* ``materialised_operator`` W_eff = W_dec W_enc per head (Sec. 2.1, Eq. (6);
-                  Sec. 2.2, Eq. (12)), for small N only.
+* ``materialised_operator`` W_eff = W_dec W_enc per head (Sec. 3.1, Eq. (6);
+                  Sec. 3.2, Eq. (12)), for small N only.
 
 Readings of points the paper leaves open (all fixed here, in the same way as
 in the input generator):
@@ -72,7 +72,7 @@ def _f64(a) -> np.ndarray:
 
 
 def project(X: np.ndarray, W: np.ndarray, H: int) -> np.ndarray:
-    """Head-split projection ``X W`` (Sec. 2.1, Eq. (4); Sec. 2.2, Eq. (7)).
+    """Head-split projection ``X W`` (Sec. 3.1, Eq. (4); Sec. 3.2, Eq. (7)).
 
     X: [B, N, C]; W: [C, C] (out = X @ W).  Returns [B, H, N, D] where head h
     holds output channels [h D, (h+1) D).
@@ -88,14 +88,14 @@ def project(X: np.ndarray, W: np.ndarray, H: int) -> np.ndarray:
 
 
 def merge_heads(Yh: np.ndarray) -> np.ndarray:
-    """Concatenate heads: [B, H, N, D] -> [B, N, H*D] (Sec. 2.1, after Eq. (2))."""
+    """Concatenate heads: [B, H, N, D] -> [B, N, H*D] (Sec. 3.1, after Eq. (2))."""
     B, H, N, D = Yh.shape
     return Yh.transpose(0, 2, 1, 3).reshape(B, N, H * D).copy()
 
 
 def sdpa(Q: np.ndarray, K: np.ndarray, V: np.ndarray,
          scale: float | None = None) -> Tuple[np.ndarray, np.ndarray]:
-    """Rectangular SDPA, softmax over the keys (Sec. 2.1, Eq. (3)).
+    """Rectangular SDPA, softmax over the keys (Sec. 3.1, Eq. (3)).
 
     Q: [..., Nq, D]; K: [..., Nk, D]; V: [..., Nk, Dv]; leading dimensions
     broadcast.  Returns ``(out [..., Nq, Dv], L [..., Nq])`` where
@@ -133,7 +133,7 @@ def sdpa(Q: np.ndarray, K: np.ndarray, V: np.ndarray,
 
 
 def mixer_forward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int) -> Dict[str, np.ndarray]:
-    """The FLARE++ mixer forward (Fig. 1; Sec. 2.2, Eqs. (7)-(11)).
+    """The FLARE++ mixer forward (Fig. 1; Sec. 3.2, Eqs. (7)-(11)).
 
     X: [B, N, C]; W*: [C, C]; seeds: [H, M, D].  Returns a dict with
     ``O [B,N,C]`` and the intermediates ``Q, Z [B,H,M,D]``, ``Y [B,N,C]``
@@ -166,7 +166,7 @@ def mixer_forward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int) -> Dict[str, np.ndarra
 
 
 def flare_forward(X, Wk, Wv, Wo, Qlat, H: int) -> Dict[str, np.ndarray]:
-    """Fixed-query FLARE mixer (Sec. 2.1, Eqs. (4)-(5)): Z = SDPA(Q, K, V),
+    """Fixed-query FLARE mixer (Sec. 3.1, Eqs. (4)-(5)): Z = SDPA(Q, K, V),
     Y = SDPA(K, Q, Z) with learned per-head queries Q [H, M, D]."""
     X = _f64(X)
     K = project(X, Wk, H)
@@ -215,7 +215,7 @@ def materialised_operator(X, Wk, Wv, Wkt, Wvt, seeds, H: int) -> Dict[str, np.nd
 
     W_enc = softmax over N of S = s Q K^T (rows are routes), W_dec = softmax
     over M of S^T (rows are tokens), W_eff = W_dec W_enc in R^{N x N}
-    (Sec. 2.1, Eq. (6); Sec. 2.2, Eq. (12)).  Q is the synthesised query set
+    (Sec. 3.1, Eq. (6); Sec. 3.2, Eq. (12)).  Q is the synthesised query set
     Q(X) (Eq. (8)).  Returns ``W_enc [B,H,M,N]``, ``W_dec [B,H,N,M]``,
     ``W_eff [B,H,N,N]`` and ``V [B,H,N,D]``; the mixer's per-head output
     before merging is ``W_eff @ V``.

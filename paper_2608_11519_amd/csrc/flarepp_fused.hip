@@ -24,7 +24,7 @@
 // loads from LDS or memory are free of bank conflicts.
 //
 // k_prep_fused    weight fragments, seed operand, cleared norm bounds.
-// k_encode_fused  calls 1 and 2 (Sec. 2.2, Eqs. (8) and (10)).  A workgroup
+// k_encode_fused  calls 1 and 2 (Sec. 3.2, Eqs. (8) and (10)).  A workgroup
 //                 of W waves owns (batch, 32-channel head group, token chunk);
 //                 per step each wave projects one 32-token sub-tile into LDS,
 //                 then every wave runs its query blocks over all W sub-tiles.

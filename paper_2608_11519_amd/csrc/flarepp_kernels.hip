@@ -1,6 +1,6 @@
 // HIP kernels of the FLARE++ mixer forward for gfx950.
 //
-// The mixer (Fig. 1; Sec. 2.2, Eqs. (7)-(11)) is: project K,V,K~,V~ = X W;
+// The mixer (Fig. 1; Sec. 3.2, Eqs. (7)-(11)) is: project K,V,K~,V~ = X W;
 // Q = SDPA(Q~, K~, V~) and Z = SDPA(Q, K, V) with the softmax over the N
 // tokens; Y = SDPA(K, Q, Z) with the softmax over the M routes; O = merge(Y) W_O.
 //

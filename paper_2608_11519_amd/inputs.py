@@ -4,10 +4,10 @@ This module generates data only: it holds none of the mixer's arithmetic, so
 both the float64 oracle (``oracle/``) and the HIP path may draw their inputs
 from it without sharing any computation.
 
-Problem statement (Sec. 2.1 and App. A.1 of the paper): tokens
+Problem statement (Sec. 3.1 and App. A.1 of the paper): tokens
 ``X in R^{B x N x C}``, five ``C x C`` weights (``W_K, W_V, W~_K, W~_V, W_O``;
-Sec. 2.2, Eqs. (7), (9)-(11) and Fig. 1) and the learned seeds
-``Q~ in R^{H x M x D}`` with ``D = C / H`` (Sec. 2.2, Eq. (8); App. A.1).
+Sec. 3.2, Eqs. (7), (9)-(11) and Fig. 1) and the learned seeds
+``Q~ in R^{H x M x D}`` with ``D = C / H`` (Sec. 3.2, Eq. (8); App. A.1).
 
 Workload recipes (the paper's benchmarks are not available; these synthetic
 inputs stand in for them, with the paper's token counts and widths):

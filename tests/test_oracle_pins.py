@@ -3,7 +3,7 @@
 Each test checks the oracle against something other than itself: a
 hand-derived worked example with exact rational answers, brute-force loops
 with ``math.fsum``, PyTorch's own scaled_dot_product_attention (the paper
-states that the whole mixer is three standard SDPA calls, Sec. 2.2 and
+states that the whole mixer is three standard SDPA calls, Sec. 3.2 and
 Fig. 1), closed forms, and the structural facts the paper states (rank <= M,
 row-stochastic routing factors, token-order independence, the exact
 split-key merge of App. A.2-A.3).
@@ -312,7 +312,7 @@ def test_materialised_operator_rank_and_rows():
     np.testing.assert_allclose(mo["W_eff"].sum(-1), 1.0, atol=1e-13)
     assert mo["W_enc"].shape[-2:] == (w.M, w.N)
     assert mo["W_dec"].shape[-2:] == (w.N, w.M)
-    # rank <= M (Sec. 2.2, Eq. (12))
+    # rank <= M (Sec. 3.2, Eq. (12))
     for h in range(w.H):
         sv = np.linalg.svd(mo["W_eff"][0, h], compute_uv=False)
         assert sv[w.M] / sv[0] < 1e-10
@@ -383,7 +383,7 @@ def test_batch_independence_and_head_locality():
 
 
 def test_flare_special_case_matches_flarepp_with_synthesised_queries():
-    # FLARE++ equals FLARE run with Q(X) as its learned query set (Sec. 2.2)
+    # FLARE++ equals FLARE run with Q(X) as its learned query set (Sec. 3.2)
     w, d = _small(seed=10, B=1, seed_scale=6.0)
     r = orc.mixer_forward(*_args(d), w.H)
     f = orc.flare_forward(d["X"], d["Wk"], d["Wv"], d["Wo"], r["Q"][0], w.H)
