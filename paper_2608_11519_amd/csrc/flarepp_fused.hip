@@ -248,6 +248,8 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   // Project sub-tile `wave` of the super-tile at t0 into LDS buffer it & 1
   // and prefetch this wave's X rows of the next super-tile.
   auto produce = [&](int it, int t0) __attribute__((always_inline)) {
+    // the projection MFMAs yield the matrix pipe to waves in their softmax
+    __builtin_amdgcn_s_setprio(0);
     const int buf = it & 1;
     f32x16 ka[GB], va[GB];
 #pragma unroll
@@ -300,7 +302,46 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   const bool all_slots = slot0 + NQW <= nslots;
   auto consume_v = [&](auto sf, auto mask, auto all, int it, int t0) __attribute__((always_inline)) {
     constexpr bool SF = decltype(sf)::value, MASK = decltype(mask)::value, ALL = decltype(all)::value;
+    __builtin_amdgcn_s_setprio(2);
     const int buf = it & 1;
+    if constexpr (ALL && !MASK) {
+      // Tiles n = j * NQW + i (sub-tile j, slot i); the score MFMA of tile
+      // n + 1 is issued before the softmax of tile n, so its latency (and any
+      // wait for the matrix pipe) is hidden behind the exponentials.
+      F kfj[W][KS];
+      auto score = [&](int n) __attribute__((always_inline)) {
+        const int j = n / NQW, i = n % NQW;
+        if (i == 0) {
+          const T* tl = tiles + (buf * W + j) * TILE;
+#pragma unroll
+          for (int js = 0; js < KS; ++js) kfj[j][js] = load_frag(tl + (hh * KS + js) * kFrag + lane * 8);
+        }
+        f32x16 sc;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+        for (int js = 0; js < KS; ++js) mma(sc, kfj[j][js], qf[i][js]);
+        return sc;
+      };
+      f32x16 cur = score(0);
+#pragma unroll
+      for (int n = 0; n < W * NQW; ++n) {
+        const int j = n / NQW, i = n % NQW;
+        f32x16 nxt;
+        if (n + 1 < W * NQW) nxt = score(n + 1);
+        const T* tl = tiles + (buf * W + j) * TILE;
+        F vf[2][RB];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            vf[hf][rb] = load_frag(tl + (KFR + (hh * RB + rb) * 2 + hf) * kFrag + lane * 8);
+        if (SF) tile_shift_free<T, RB, ONES_ROW, false>(acc[i], ls[i], cur, vf, 32, lane);
+        else tile_online<T, RB, ONES_ROW, false>(acc[i], m[i], ls[i], cur, vf, 32, lane);
+        if (n + 1 < W * NQW) cur = nxt;
+      }
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < W; ++j) {
       int nvalid = 32;
