@@ -329,6 +329,8 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
         const int j = n / NQW, i = n % NQW;
         f32x16 nxt;
         if (n + 1 < W * NQW) nxt = score(n + 1);
+        // keep the next score MFMA ahead of this tile's softmax
+        __builtin_amdgcn_sched_barrier(0);
         const T* tl = tiles + (buf * W + j) * TILE;
         F vf[2][RB];
 #pragma unroll
@@ -1048,6 +1050,222 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode2(DecFusedPa
 }
 
 // ---------------------------------------------------------------------------
+// Decode with every stage resident and a compile-time route-tile count RT:
+// the route tiles of a group are unrolled, and the key projection of the next
+// group and the merge of the previous group are spread over them (one or two
+// MFMAs after each tile), so the matrix work runs beside the softmax instead
+// of stalling the wave in dependent MFMA chains.  Same LDS layout, stages and
+// results as k_decode2<..., RES = true>.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int KSC, int RT>
+__global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedParams p) {
+  using F = typename Frag<T>::type;
+  constexpr int HPG = (D == 16) ? 2 : 1, GB = (D == 64) ? 2 : 1;
+  constexpr int KS = D / 16, RB = (D + 31) / 32, KPG = 2 * GB;
+  constexpr bool ONES_ROW = (D == 16);
+  constexpr int C = KSC * 16, CB = C / 32, HG = CB / GB;
+  constexpr int WELEMS = GB * KSC * kFrag, WOE = CB * KPG * kFrag;
+  constexpr int NW = dec_waves(C), TOK = 32 * NW;
+  constexpr int ZC = D < 32 ? D : 32;
+  constexpr int NT = RT * HPG;      // route tiles per group
+  constexpr int NP = GB * KSC;      // projection MFMAs per group
+  constexpr int NM = CB * KPG;      // merge MFMAs per group
+  static_assert(C <= 128, "per-group merge accumulators are sized for C <= 128");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int Mp = p.Mp, QH = Mp * D;
+  const int ZH = (int)z_frag_elems_per_head(Mp, D);
+  const int SB = p.stage_bytes;
+  T* cst = reinterpret_cast<T*>(smem + HG * SB);
+
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
+  const int nblk = (p.N + TOK - 1) / TOK;
+  const int b = blockIdx.x / nblk;
+  const int xrow = (blockIdx.x % nblk) * TOK + wave * 32 + c;
+  const bool xok = xrow < p.N;
+
+  // X and the first group's stage first; the other stages are issued after
+  // the first barrier and land while the first group computes
+  F xf[KSC];
+#pragma unroll
+  for (int ks = 0; ks < KSC; ++ks)
+    xf[ks] = load_frag((const T*)p.x + ((int64_t)b * p.N + min(xrow, p.N - 1)) * C + 16 * ks + 8 * g);
+  dec2_stage_issue<T, D, KSC>(p, smem, b, 0);
+  if (ONES_ROW && threadIdx.x < 2) store_frag<T>(cst + 8 * threadIdx.x, threadIdx.x == 0 ? fill_frag<T>(1.f) : zero_frag<T>());
+  lds_wait_barrier();
+  for (int hg = 1; hg < HG; ++hg) dec2_stage_issue<T, D, KSC>(p, smem + hg * SB, b, hg);
+
+  const bool konst = ONES_ROW && c >= 16;
+  const uint32_t zstep = konst ? 0u : (uint32_t)(2 * ZC * 8 * sizeof(T));
+  const uint32_t zhead = konst ? 0u : (uint32_t)(ZH * sizeof(T));
+  const uint32_t zlane = konst ? (uint32_t)((reinterpret_cast<char*>(cst) - smem) + (c == 16 ? 0 : 8 * sizeof(T)))
+                               : (uint32_t)((WELEMS + WOE + HPG * QH + (g * ZC + c) * 8) * sizeof(T));
+
+  f32x16 o[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[cb][e] = 0.f;
+  f32x16 ka[GB];
+  F yprev[KPG];
+#pragma unroll
+  for (int j = 0; j < KPG; ++j) yprev[j] = zero_frag<T>();
+  // k-th projection MFMA of the group whose stage starts at byte `so`
+  auto proj_mfma = [&](int so, int k) __attribute__((always_inline)) {
+    const int cb = k / KSC, ks = k % KSC;
+    const T* wk = reinterpret_cast<const T*>(smem + so);
+    if (ks == 0) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) ka[cb][e] = 0.f;
+    }
+    mma(ka[cb], load_frag(wk + ((cb * KSC + ks) * 64 + lane) * 8), xf[ks]);
+  };
+  // k-th merge MFMA of the group whose stage starts at byte `so` (operands yprev)
+  auto merge_mfma = [&](int so, int k) __attribute__((always_inline)) {
+    const int cb = k / KPG, j = k % KPG;
+    const T* wo = reinterpret_cast<const T*>(smem + so) + WELEMS;
+    mma(o[cb], load_frag(wo + ((cb * KPG + j) * 64 + lane) * 8), yprev[j]);
+  };
+  auto route_norm = [&](int so, int hh) __attribute__((always_inline)) {
+    const float* qn = reinterpret_cast<const float*>(smem + so + (WELEMS + WOE + HPG * (QH + ZH)) * sizeof(T));
+    float v = 0.f;
+    for (int i = lane; i < Mp / 4; i += 64) v = fmaxf(v, qn[hh * (Mp / 4) + i]);
+    return wave_max_nonneg(v);
+  };
+#pragma unroll
+  for (int k = 0; k < NP; ++k) proj_mfma(0, k);
+
+  const bool partial = p.M < 32 * RT;  // the last route tile is partial
+  for (int hg = 0; hg < HG; ++hg) {
+    if (hg == 1) lds_wait_barrier();  // the remaining stages are in
+    const int so = hg * SB;
+    const T* st = reinterpret_cast<const T*>(smem + so);
+    F kf[HPG][KS];
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh)
+#pragma unroll
+      for (int js = 0; js < KS; ++js) {
+        const int fi = hh * KS + js;
+        kf[hh][js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
+      }
+    // |score| bound for both heads of the group at once: max |k|^2 over the
+    // group's heads times max |q|^2 over its routes
+    float ksq = 0.f, qsq = 0.f;
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      float sq = 0.f;
+#pragma unroll
+      for (int js = 0; js < KS; ++js) sq += sumsq(kf[hh][js]);
+      ksq = fmaxf(ksq, sq);
+      qsq = fmaxf(qsq, route_norm(so, hh));
+    }
+    const bool fast = uniform(halfmax_sum_nonneg(ksq) * qsq <= p.fast_lim);
+    // the next group's stage (the last group projects its own again: unused)
+    const int so_next = min(hg + 1, HG - 1) * SB, so_prev = max(hg - 1, 0) * SB;
+
+    f32x16 acc[HPG][RB];
+    float m[HPG], ls[HPG];
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      m[hh] = -INFINITY;
+      ls[hh] = 0.f;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[hh][rb][e] = 0.f;
+    }
+    auto score = [&](int n) __attribute__((always_inline)) {
+      const int rt = n / HPG, hh = n % HPG;
+      f32x16 sc;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+      for (int js = 0; js < KS; ++js)
+        mma(sc, load_frag(st + WELEMS + WOE + hh * QH + ((rt * KS + js) * 64 + lane) * 8), kf[hh][js]);
+      return sc;
+    };
+    auto zfrags = [&](int n, F (&zv)[2][RB]) __attribute__((always_inline)) {
+      const int rt = n / HPG, hh = n % HPG;
+      const uint32_t base = zlane + (konst ? 0u : (uint32_t)so) + zhead * hh;
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          zv[hf][rb] = *reinterpret_cast<const F*>(smem + base + zstep * ((rt * 2 + hf) * RB + rb));
+    };
+    // the matrix work spread after tile n (no branches: before the first
+    // group's routes yprev is zero, so its merge adds nothing)
+    auto hooks = [&](int n) __attribute__((always_inline)) {
+#pragma unroll
+      for (int k = n * NP / NT; k < (n + 1) * NP / NT; ++k) proj_mfma(so_next, k);
+#pragma unroll
+      for (int k = n * NM / NT; k < (n + 1) * NM / NT; ++k) merge_mfma(so_prev, k);
+    };
+    if (fast) {
+      f32x16 cur = score(0);
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        f32x16 nxt;
+        if (n + 1 < NT) nxt = score(n + 1);
+        // keep the next score MFMA ahead of this tile's softmax
+        __builtin_amdgcn_sched_barrier(0);
+        F zv[2][RB];
+        zfrags(n, zv);
+        const int rt = n / HPG, hh = n % HPG;
+        if (rt == RT - 1 && partial)
+          tile_shift_free<T, RB, ONES_ROW, true>(acc[hh], ls[hh], cur, zv, p.M - rt * 32, lane);
+        else
+          tile_shift_free<T, RB, ONES_ROW, false>(acc[hh], ls[hh], cur, zv, 32, lane);
+        hooks(n);
+        if (n + 1 < NT) cur = nxt;
+      }
+    } else {  // online maximum (rare): every tile masked, matrix work afterwards
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int rt = n / HPG, hh = n % HPG;
+        F zv[2][RB];
+        zfrags(n, zv);
+        tile_online<T, RB, ONES_ROW, true>(acc[hh], m[hh], ls[hh], score(n), zv, min(32, p.M - rt * 32), lane);
+      }
+#pragma unroll
+      for (int n = 0; n < NT; ++n) hooks(n);
+    }
+    // this group's decoded tokens become the merge operands of the next step
+#pragma unroll
+    for (int hh = 0; hh < HPG; ++hh) {
+      const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane));
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+          if (rb * 32 + 16 * hf < D) yprev[hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
+      if (p.y && xok) {
+        T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + (hg * HPG + hh) * D;
+        constexpr int NQ4 = ONES_ROW ? 2 : 4;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int q = 0; q < NQ4; ++q)
+            store4(yp + rb * 32 + 8 * q + 4 * g, acc[hh][rb][4 * q] * inv, acc[hh][rb][4 * q + 1] * inv,
+                   acc[hh][rb][4 * q + 2] * inv, acc[hh][rb][4 * q + 3] * inv);
+      }
+    }
+  }
+  // the last group's merge
+#pragma unroll
+  for (int k = 0; k < NM; ++k) merge_mfma((HG - 1) * SB, k);
+
+  if (xok) {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      T* op = (T*)p.o + ((int64_t)b * p.N + xrow) * C + 32 * cb;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        store4(op + 8 * q + 4 * g, o[cb][4 * q], o[cb][4 * q + 1], o[cb][4 * q + 2], o[cb][4 * q + 3]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 template <typename T>
@@ -1130,6 +1348,25 @@ static hipError_t dec_launch(const DecFusedParams& p, hipStream_t s) {
     constexpr int NW = dec_waves(16 * KSC);
     const unsigned grid = (unsigned)((int64_t)p.B * ((p.N + 32 * NW - 1) / (32 * NW)));
     if constexpr (16 * KSC <= 128) {  // per-group stages (k_decode2)
+      if constexpr (sizeof(T) == 2 && (D == 16 || (D == 32 && KSC <= 4))) {
+        const int rt = p.Mp / 32;
+        if (p.kind == kDecodeGroupsResident && rt <= 4) {
+          const size_t lds = dec2_lds_bytes(16 * KSC, D, p.Mp, sizeof(T), true);
+          const void* fn = rt == 1   ? reinterpret_cast<const void*>(&k_decode3<T, D, KSC, 1>)
+                           : rt == 2 ? reinterpret_cast<const void*>(&k_decode3<T, D, KSC, 2>)
+                           : rt == 3 ? reinterpret_cast<const void*>(&k_decode3<T, D, KSC, 3>)
+                                     : reinterpret_cast<const void*>(&k_decode3<T, D, KSC, 4>);
+          hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+          if (e != hipSuccess) return e;
+          switch (rt) {
+            case 1: k_decode3<T, D, KSC, 1><<<grid, 64 * NW, lds, s>>>(p); break;
+            case 2: k_decode3<T, D, KSC, 2><<<grid, 64 * NW, lds, s>>>(p); break;
+            case 3: k_decode3<T, D, KSC, 3><<<grid, 64 * NW, lds, s>>>(p); break;
+            default: k_decode3<T, D, KSC, 4><<<grid, 64 * NW, lds, s>>>(p); break;
+          }
+          return hipGetLastError();
+        }
+      }
       if (p.kind != kDecodeStaged) {
         const bool res = p.kind == kDecodeGroupsResident;
         const size_t lds = dec2_lds_bytes(16 * KSC, D, p.Mp, sizeof(T), res);
