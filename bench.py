@@ -120,11 +120,12 @@ def roofline(work, ms, dtype):
 
 
 # Kernels (symbol substrings) that can carry each stage on the fused path, for
-# the counter tables; the decode is k_decode2 for C <= 128 when its stages fit.
+# the counter tables; for C <= 128 the decode is k_decode3 or k_decode2 when
+# the head-group stages fit, otherwise k_decode_fused.
 STAGE_KERNELS_FUSED = {"prep": ("k_prep_fused",), "call1_encode": ("k_encode_fused",),
                        "call1_combine": ("k_combine_par",), "call2_encode": ("k_encode_fused",),
                        "call2_combine": ("k_combine_par",),
-                       "call3_decode": ("k_decode2", "k_decode_fused")}
+                       "call3_decode": ("k_decode3", "k_decode2", "k_decode_fused")}
 
 
 def sources_digest():
