@@ -60,6 +60,15 @@ __device__ __forceinline__ void lds_wait_barrier() {
   __syncthreads();
 }
 
+// Workgroup barrier over LDS traffic only.  __syncthreads() also waits for
+// every global load the wave has in flight (vmcnt counts loads too), which
+// would drain a prefetch issued before it; here only this wave's LDS
+// operations are waited for.  Use it where the barrier orders LDS accesses
+// and nothing written to global memory by another wave is read afterwards.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Copy n16 16-byte chunks src -> LDS dst with direct global -> LDS loads by
 // all nt threads of the block (each wave fills 1 KiB per step).
 __device__ __forceinline__ void copy_to_lds(const void* src, char* dst, int n16, int nt) {
@@ -202,22 +211,16 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   const int slot0 = (qg * W + wave) * NQW;
   const int hh = HPG == 1 ? 0 : __builtin_amdgcn_readfirstlane(min(slot0, nslots - 1) / p.QB);
   F qf[NQW][KS];
-  float qn = 0.f;
 #pragma unroll
   for (int i = 0; i < NQW; ++i) {
     const int s = slot0 + i;
     const bool ok = s < nslots;
     const int qb = ok ? s % p.QB : 0;
     const T* qp = (const T*)p.q_op + (int64_t)b * p.q_sb + (int64_t)(hg * HPG + hh) * p.Mp * D;
-    float sq = 0.f;
 #pragma unroll
-    for (int js = 0; js < KS; ++js) {
+    for (int js = 0; js < KS; ++js)
       qf[i][js] = ok ? load_frag(qp + ((int64_t)(qb * KS + js) * 64 + lane) * 8) : zero_frag<T>();
-      sq += sumsq(qf[i][js]);
-    }
-    qn = fmaxf(qn, sq);
   }
-  const float qmax2 = halfmax_sum_nonneg(qn);
 
   f32x16 acc[NQW][RB];
   float m[NQW], ls[NQW];
@@ -236,38 +239,55 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   // X rows past the chunk are clamped to its last row: their keys and values
   // duplicate a real token's (masked out of the softmax, and never above the
   // key norm bound), and every load is unconditional, so the compiler can
-  // count the loads in flight and wait for the previous super-tile's only
+  // count the loads in flight.  Each super-tile's rows are requested one
+  // super-tile ahead and stay in flight across the LDS barriers.
   F xf[KSC];
-  {
-    const int row = min(k0 + 32 * wave + c, k1 - 1);
+  auto load_x = [&](int t) __attribute__((always_inline)) {
+    const int row = min(t + 32 * wave + c, k1 - 1);
 #pragma unroll
     for (int ks = 0; ks < KSC; ++ks) xf[ks] = load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g);
-  }
-  lds_wait_barrier();  // weight slices and constant rows in LDS
-
-  // Project sub-tile `wave` of the super-tile at t0 into LDS buffer it & 1
-  // and prefetch this wave's X rows of the next super-tile.
-  auto produce = [&](int it, int t0) __attribute__((always_inline)) {
-    // the projection MFMAs yield the matrix pipe to waves in their softmax
-    __builtin_amdgcn_s_setprio(0);
-    const int buf = it & 1;
-    f32x16 ka[GB], va[GB];
+  };
+  asm volatile("" ::: "memory");  // the weight copies and route loads are issued first
+  load_x(k0);
+  // weight slices and constant rows in LDS (every load but the X rows)
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KSC) : "memory");
+  lds_barrier();
+  __builtin_amdgcn_sched_barrier(0);  // the norms below must not wait for the X loads
+  float qn = 0.f;
 #pragma unroll
-    for (int cb = 0; cb < GB; ++cb) {
+  for (int i = 0; i < NQW; ++i) {
+    float sq = 0.f;
+#pragma unroll
+    for (int js = 0; js < KS; ++js) sq += sumsq(qf[i][js]);
+    qn = fmaxf(qn, sq);
+  }
+  const float qmax2 = halfmax_sum_nonneg(qn);
+
+  // Projection of this wave's 32-token sub-tile of a super-tile: K and V of
+  // the head group accumulate over the KSC k-steps of X (xf).  Each k-step
+  // is issued after one route tile of the previous super-tile, so the matrix
+  // work and the X traffic run beside the softmax; xf[ks] is refilled with
+  // the rows of the super-tile after that right after its last use, which
+  // gives every X load a whole super-tile to arrive.
+  f32x16 ka[GB], va[GB];
+  auto proj_zero = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int cb = 0; cb < GB; ++cb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) { ka[cb][e] = 0.f; va[cb][e] = 0.f; }
+  };
+  auto proj_step = [&](int ks, int trefill) __attribute__((always_inline)) {
 #pragma unroll
-      for (int ks = 0; ks < KSC; ++ks) {
-        const int fo = ((cb * KSC + ks) * 64 + lane) * 8;
-        mma(ka[cb], load_frag(wk_l + fo), xf[ks]);
-        mma(va[cb], xf[ks], load_frag(wv_l + fo));
-      }
+    for (int cb = 0; cb < GB; ++cb) {
+      const int fo = ((cb * KSC + ks) * 64 + lane) * 8;
+      mma(ka[cb], load_frag(wk_l + fo), xf[ks]);
+      mma(va[cb], xf[ks], load_frag(wv_l + fo));
     }
-    {
-      const int row = min(t0 + STEP + 32 * wave + c, k1 - 1);
-#pragma unroll
-      for (int ks = 0; ks < KSC; ++ks) xf[ks] = load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g);
-    }
+    const int row = min(trefill + 32 * wave + c, k1 - 1);
+    xf[ks] = load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g);
+  };
+  // the projected sub-tile into LDS buffer buf, with its key norm bound
+  auto proj_store = [&](int buf) __attribute__((always_inline)) {
     T* tl = tiles + (buf * W + wave) * TILE;
 #pragma unroll
     for (int h2 = 0; h2 < HPG; ++h2) {
@@ -292,18 +312,192 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
         for (int hf = 0; hf < 2; ++hf)
           store_frag<T>(tl + (KFR + 2 * cb + hf) * kFrag + lane * 8, cvt8<T>(va[cb], 8 * hf));
     }
-    __syncthreads();
   };
 
-  // Run the wave's query slots over every sub-tile of the super-tile at t0:
-  // shift-free (SF) or with the online maximum; MASK only for the last,
-  // partial super-tile of a chunk; ALL when every slot of the wave is a real
-  // one (no per-slot branch inside the tile sequence).
+  // the first super-tile is projected before any route tile
+  proj_zero();
+#pragma unroll
+  for (int ks = 0; ks < KSC; ++ks) proj_step(ks, k0 + STEP);
+  proj_store(0);
+  lds_barrier();
+
+  // Run the wave's query slots over every sub-tile of the super-tile at t0
+  // (LDS buffer it & 1): shift-free (SF) or with the online maximum; MASK
+  // only for the last, partial super-tile of a chunk; ALL when every slot of
+  // the wave is a real one (no per-slot branch inside the tile sequence).
+  // Unmasked runs also project the super-tile after this one (the k-steps
+  // spread over the NT route tiles); after the last full super-tile of a
+  // chunk without a tail that projection is of clamped rows and unused.
+  constexpr int NT = W * NQW;
   const bool all_slots = slot0 + NQW <= nslots;
   auto consume_v = [&](auto sf, auto mask, auto all, int it, int t0) __attribute__((always_inline)) {
     constexpr bool SF = decltype(sf)::value, MASK = decltype(mask)::value, ALL = decltype(all)::value;
-    __builtin_amdgcn_s_setprio(2);
     const int buf = it & 1;
+    if (!MASK) proj_zero();
+    auto hooks = [&](int n) __attribute__((always_inline)) {
+      if constexpr (!MASK) {
+#pragma unroll
+        for (int ks = n * KSC / NT; ks < (n + 1) * KSC / NT; ++ks) proj_step(ks, t0 + 2 * STEP);
+      }
+    };
+    if constexpr (ALL && !MASK && SF) {
+      // Shift-free tiles n = j * NQW + i (sub-tile j, slot i), software
+      // pipelined so that every MFMA is issued between groups of
+      // exponentials whose inputs are long ready (a wave issues in order: an
+      // MFMA waiting on the P it was just given, or on the busy matrix pipe,
+      // stalls the exponentials behind it).  Per tile n, five phases:
+      //   0: score MFMA of tile n + 1; LDS reads for tiles n + 1 and n + 2;
+      //      2^s of scores 0..3
+      //   1: value MFMAs of tile n - 1, keys 0..15; 2^s 4..7; pack P 0..7
+      //   2: key-projection MFMAs (hook k-steps); 2^s 8..11
+      //   3: value MFMAs of tile n - 1, keys 16..31; 2^s 12..15; pack P 8..15
+      //   4: value-projection MFMAs and the X refills
+      // The value MFMAs of the last tile follow the loop.
+      constexpr int KPT = (KSC + NT - 1) / NT;  // hook k-steps per tile (at most)
+      auto tl_of = [&](int n) __attribute__((always_inline)) { return tiles + (buf * W + n / NQW) * TILE; };
+      auto ld_k = [&](int n, F (&kf)[KS]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int js = 0; js < KS; ++js) kf[js] = load_frag(tl_of(n) + (hh * KS + js) * kFrag + lane * 8);
+      };
+      auto ld_v = [&](int n, F (&vf)[2][RB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            vf[hf][rb] = load_frag(tl_of(n) + (KFR + (hh * RB + rb) * 2 + hf) * kFrag + lane * 8);
+      };
+      auto ld_w = [&](int n, F (&wk)[KPT][GB], F (&wv)[KPT][GB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) {
+          const int ks = n * KSC / NT + q;
+          if (ks < (n + 1) * KSC / NT) {
+#pragma unroll
+            for (int cb = 0; cb < GB; ++cb) {
+              const int fo = ((cb * KSC + ks) * 64 + lane) * 8;
+              wk[q][cb] = load_frag(wk_l + fo);
+              wv[q][cb] = load_frag(wv_l + fo);
+            }
+          }
+        }
+      };
+      auto score_mma = [&](int n, const F (&kf)[KS]) __attribute__((always_inline)) {
+        f32x16 sc;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+        for (int js = 0; js < KS; ++js) mma(sc, kf[js], qf[n % NQW][js]);
+        return sc;
+      };
+      F kc[KS], kn[KS], vc[2][RB], vn[2][RB], wkc[KPT][GB], wvc[KPT][GB], wkn[KPT][GB], wvn[KPT][GB];
+      F pp[2], vp[2][RB];  // P and value operands of the previous tile
+      ld_k(0, kc);
+      ld_v(0, vc);
+      ld_w(0, wkc, wvc);
+      f32x16 cur = score_mma(0, kc);
+      if (NT > 1) ld_k(1, kn);
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int i = n % NQW, ip = (n + NQW - 1) % NQW;
+        f32x16 nxt;
+        // phase 0
+        __builtin_amdgcn_sched_barrier(0);
+        if (n + 1 < NT) {
+          nxt = score_mma(n + 1, kn);
+          ld_v(n + 1, vn);
+          ld_w(n + 1, wkn, wvn);
+          if (n + 2 < NT) {
+            if ((n + 2) % NQW == 0) ld_k(n + 2, kc);  // kc is free: sub-tile of n + 2
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        // phase 1
+        __builtin_amdgcn_sched_barrier(0);
+        if (n > 0) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) mma(acc[ip][rb], vp[0][rb], pp[0]);
+        }
+#pragma unroll
+        for (int e = 4; e < 8; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        F p0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p0[e] = from_f32<T>(cur[e]);
+        // phase 2
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) {
+          const int ks = n * KSC / NT + q;
+          if (ks < (n + 1) * KSC / NT) {
+#pragma unroll
+            for (int cb = 0; cb < GB; ++cb) mma(ka[cb], wkc[q][cb], xf[ks]);
+          }
+        }
+#pragma unroll
+        for (int e = 8; e < 12; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        if (!ONES_ROW) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) ls[i] += cur[e];
+        }
+        // phase 3
+        __builtin_amdgcn_sched_barrier(0);
+        if (n > 0) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) mma(acc[ip][rb], vp[1][rb], pp[1]);
+        }
+#pragma unroll
+        for (int e = 12; e < 16; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        F p1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p1[e] = from_f32<T>(cur[8 + e]);
+        if (!ONES_ROW) {
+#pragma unroll
+          for (int e = 8; e < 16; ++e) ls[i] += cur[e];
+        }
+        // phase 4
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) {
+          const int ks = n * KSC / NT + q;
+          if (ks < (n + 1) * KSC / NT) {
+#pragma unroll
+            for (int cb = 0; cb < GB; ++cb) mma(va[cb], xf[ks], wvc[q][cb]);
+            const int row = min(t0 + 2 * STEP + 32 * wave + c, k1 - 1);
+            xf[ks] = load_frag(xb + (int64_t)row * p.C + 16 * ks + 8 * g);
+          }
+        }
+        pp[0] = p0;
+        pp[1] = p1;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) vp[hf][rb] = vc[hf][rb];
+        if (n + 1 < NT) {
+          cur = nxt;
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) vc[hf][rb] = vn[hf][rb];
+#pragma unroll
+          for (int q = 0; q < KPT; ++q)
+#pragma unroll
+            for (int cb = 0; cb < GB; ++cb) { wkc[q][cb] = wkn[q][cb]; wvc[q][cb] = wvn[q][cb]; }
+          if ((n + 2) % NQW == 0) {
+#pragma unroll
+            for (int js = 0; js < KS; ++js) kn[js] = kc[js];
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      {
+        constexpr int il = (NT - 1) % NQW;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          mma(acc[il][rb], vp[0][rb], pp[0]);
+          mma(acc[il][rb], vp[1][rb], pp[1]);
+        }
+      }
+      return;
+    }
     if constexpr (ALL && !MASK) {
       // Tiles n = j * NQW + i (sub-tile j, slot i); the score MFMA of tile
       // n + 1 is issued before the softmax of tile n, so its latency (and any
@@ -325,10 +519,10 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
       };
       f32x16 cur = score(0);
 #pragma unroll
-      for (int n = 0; n < W * NQW; ++n) {
+      for (int n = 0; n < NT; ++n) {
         const int j = n / NQW, i = n % NQW;
         f32x16 nxt;
-        if (n + 1 < W * NQW) nxt = score(n + 1);
+        if (n + 1 < NT) nxt = score(n + 1);
         // keep the next score MFMA ahead of this tile's softmax
         __builtin_amdgcn_sched_barrier(0);
         const T* tl = tiles + (buf * W + j) * TILE;
@@ -340,7 +534,8 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
             vf[hf][rb] = load_frag(tl + (KFR + (hh * RB + rb) * 2 + hf) * kFrag + lane * 8);
         if (SF) tile_shift_free<T, RB, ONES_ROW, false>(acc[i], ls[i], cur, vf, 32, lane);
         else tile_online<T, RB, ONES_ROW, false>(acc[i], m[i], ls[i], cur, vf, 32, lane);
-        if (n + 1 < W * NQW) cur = nxt;
+        hooks(n);
+        if (n + 1 < NT) cur = nxt;
       }
       return;
     }
@@ -372,6 +567,7 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
           if (SF) tile_shift_free<T, RB, ONES_ROW, MASK>(acc[i], ls[i], sc, vf, nvalid, lane);
           else tile_online<T, RB, ONES_ROW, MASK>(acc[i], m[i], ls[i], sc, vf, nvalid, lane);
         }
+        hooks(j * NQW + i);
       }
     }
   };
@@ -382,33 +578,41 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
 
   // Full super-tiles: shift-free while every score of the super-tile is
   // provably within the shift-free range (|q.k| <= max|q| max|k|), then
-  // online; a partial last super-tile runs online with masked keys.
+  // online from the first super-tile that fails the bound on; a partial last
+  // super-tile runs online with masked keys.
   const int nfull = (k1 - k0) / STEP;
   const bool tail = (k1 - k0) % STEP != 0;
-  int it = 0, t0 = k0;
-  bool used = false;
-  for (; it < nfull; ++it, t0 += STEP) {
-    produce(it, t0);
-    float kb = 0.f;
-    for (int j = 0; j < W * HPG; ++j) kb = fmaxf(kb, kmx[(it & 1) * W * HPG + j]);
-    if (!uniform(qmax2 * kb <= p.fast_lim)) break;
-    consume(std::true_type{}, std::false_type{}, it, t0);
-    used = true;
-  }
-  if (!used) {
+  const int nst = nfull + (tail ? 1 : 0);
+  bool fast = true, used = false;
+  auto go_online = [&]() __attribute__((always_inline)) {
+    if (!used) {
 #pragma unroll
-    for (int i = 0; i < NQW; ++i) m[i] = -INFINITY;
-  }
-  if (it < nfull) {  // super-tile `it` is produced, not yet consumed
-    consume(std::false_type{}, std::false_type{}, it, t0);
-    for (++it, t0 += STEP; it < nfull; ++it, t0 += STEP) {
-      produce(it, t0);
+      for (int i = 0; i < NQW; ++i) m[i] = -INFINITY;
+      used = true;
+    }
+  };
+  int t0 = k0;
+  for (int it = 0; it < nfull; ++it, t0 += STEP) {
+    if (fast) {
+      float kb = 0.f;
+      for (int j = 0; j < W * HPG; ++j) kb = fmaxf(kb, kmx[(it & 1) * W * HPG + j]);
+      fast = uniform(qmax2 * kb <= p.fast_lim);
+    }
+    if (fast) {
+      consume(std::true_type{}, std::false_type{}, it, t0);
+      used = true;
+    } else {
+      go_online();
       consume(std::false_type{}, std::false_type{}, it, t0);
+    }
+    if (it + 1 < nst) {  // the next super-tile, projected during this one
+      proj_store((it + 1) & 1);
+      lds_barrier();
     }
   }
   if (tail) {
-    produce(it, t0);
-    consume(std::false_type{}, std::true_type{}, it, t0);
+    go_online();
+    consume(std::false_type{}, std::true_type{}, nfull, t0);
   }
 
   // ---- partials ----
