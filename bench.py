@@ -235,6 +235,46 @@ def cpu_baseline(w, d, min_seconds):
                       f"{el:.1f} s on {len(os.sched_getaffinity(0))} host cores"}
 
 
+def time_flare(args, w, t, use_graph):
+    """The fixed-query FLARE mixer (Sec. 3.1) on the same workload and
+    weights (its learned queries: the seeds), timed like the FLARE++ step:
+    the paper's cost comparison of the two mixers (Sec. 3.2 end; App. C.3)."""
+    import torch
+
+    from paper_2608_11519_amd import flarepp as fp
+
+    dcode = fp.BF16 if w.dtype == "bf16" else fp.F32
+    O = torch.empty_like(t["X"])
+    ws = torch.empty(fp.flarepp_flare_workspace_bytes(dcode, w.B, w.N, w.C, w.H, w.M),
+                     dtype=torch.uint8, device=t["X"].device)
+
+    def step():
+        fp.flarepp_flare_forward(t["X"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], H=w.H, out=O, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    graph = None
+    if use_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    return {"ms_per_step": round(ms, 5), "tokens_per_s": round(w.B * w.N / (ms * 1e-3), 1)}
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.pmc_summary:
@@ -335,6 +375,7 @@ def main(argv=None):
         stage_ms[name] = e0.elapsed_time(e1) / reps
     step()  # leave the workspace and O as one complete step wrote them
     torch.cuda.synchronize()
+    flare = time_flare(args, w, t, graph is not None)
     work = stage_work(w, fused)
     stages = {n: {"ms": round(stage_ms[n], 5), **roofline(work[n], stage_ms[n], w.dtype)}
               for n in fp.PROFILE_STAGES if n not in empty}
@@ -375,6 +416,7 @@ def main(argv=None):
         "mfma_frac_mixer": round(total_flops / (ms_per_step * 1e-3) / (peak * 1e12), 4),
         "stages": stages,
         "wall_ms_timed_region": round(wall_ms, 3),
+        "flare": {**flare, "flarepp_over_flare_time": round(ms_per_step / flare["ms_per_step"], 3)},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)

@@ -154,6 +154,36 @@ FLAREPP_API int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int
                                 void* Y_out, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Fixed-query FLARE mixer forward (Sec. 3.1, Eqs. (4)-(5)): the baseline
+ * that FLARE++ generalises.  Per head h, with learned queries Q_h:
+ *   K = X Wk, V = X Wv (head h = columns [hD, (h+1)D)),
+ *   Z_h = softmax_N(Q_h K_h^T / sqrt(D)) V_h        (encode, softmax over N),
+ *   Y_h = softmax_M(K_h Q_h^T / sqrt(D)) Z_h        (decode, softmax over M),
+ *   O = [Y_1 .. Y_H] Wo.
+ * It is FLARE++ without the query synthesis (call 1): the same kernels, with
+ * `queries` in place of Q(X).
+ *
+ * X [B][N][C]; Wk, Wv, Wo [C][C] (out = X W); queries [H][M][D], shared by
+ * the batch; O [B][N][C] -- all in dtype.  Sizes, layouts, ownership,
+ * determinism and errors as flarepp_mixer_forward; size the workspace with
+ * flarepp_flare_workspace_bytes (0 for an invalid shape).
+ * flarepp_flare_forward_debug also writes Z_out float32 [B][H][M][D] and
+ * Y_out dtype [B][N][C] (decoded tokens, heads merged, before Wo); each may
+ * be NULL.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_flare_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C,
+                                                 int64_t H, int64_t M);
+FLAREPP_API int flarepp_flare_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                      int64_t M, const void* X, const void* Wk, const void* Wv,
+                                      const void* Wo, const void* queries, void* O, void* ws,
+                                      size_t ws_bytes, void* stream);
+FLAREPP_API int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                            int64_t M, const void* X, const void* Wk,
+                                            const void* Wv, const void* Wo, const void* queries,
+                                            void* O, float* Z_out, void* Y_out, void* ws,
+                                            size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Profiling variant of flarepp_mixer_forward for timing each stage on the
  * device.  `events` holds FLAREPP_PROFILE_EVENTS caller-created hipEvent_t
  * handles (created with timing enabled); events[0] is recorded on `stream`

@@ -240,25 +240,28 @@ struct MixerWs {
   size_t bytes;
 };
 
+// flare: the fixed-query mixer (no query synthesis): no W~ fragments, no K~
+// or V~, and on the fused path the seed operand is copied per batch entry
+// (the decode reads route operands per batch entry).
 MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
-                 const MixerPlan& pl) {
+                 const MixerPlan& pl, bool flare = false) {
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
   const size_t bs = dtype_bytes(dtype);
   const int64_t R = pl.fused ? pl.nchunks : pl.enc.nchunks;
   Carver cv(base);
   MixerWs w{};
-  for (int i = 0; i < 5; ++i) w.wf[i] = cv.take(bs * C * C);
-  w.seeds_op = cv.take(bs * H * Mp * D);
+  for (int i = 0; i < 5; ++i) w.wf[i] = (flare && (i == 2 || i == 3)) ? nullptr : cv.take(bs * C * C);
+  w.seeds_op = cv.take(bs * (flare && pl.fused ? B : 1) * H * Mp * D);
   if (!pl.fused) {
     w.K = cv.take(bs * B * H * N * D);
-    w.Kt = cv.take(bs * B * H * N * D);
+    w.Kt = flare ? nullptr : cv.take(bs * B * H * N * D);
     w.Vdm = cv.take(bs * B * H * D * Np);
-    w.Vtdm = cv.take(bs * B * H * D * Np);
+    w.Vtdm = flare ? nullptr : cv.take(bs * B * H * D * Np);
     w.Y = cv.take(bs * B * N * C);
   }
   w.part_ml = (float*)cv.take(sizeof(float) * R * B * H * Mp * 2);
   w.part_acc = (float*)cv.take(sizeof(float) * R * B * H * Mp * D);
-  w.q_op = cv.take(bs * B * H * Mp * D);
+  w.q_op = flare ? nullptr : cv.take(bs * B * H * Mp * D);
   w.z_op = cv.take(bs * B * H * (pl.fused ? flarepp::z_frag_elems_per_head((int)Mp, (int)D) : D * Mp));
   w.qnorm2 = (float*)cv.take(sizeof(float) * B * H * (Mp / 4));
   w.bytes = cv.off;
@@ -267,15 +270,19 @@ MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t
 
 float route_qscale(int64_t D) { return (float)(1.4426950408889634 / std::sqrt((double)D)); }
 
+// The FLARE++ mixer (Sec. 3.2, Eqs. (7)-(11)) or, with flare, the
+// fixed-query FLARE mixer (Sec. 3.1, Eqs. (4)-(5)): the seeds are then the
+// learned queries Q_h of both routing calls, and call 1 (stages 3 and 4) and
+// the W~ projections are absent.
 template <typename T>
 int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
                const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
-               size_t ws_bytes, hipStream_t s, hipEvent_t const* ev, int only) {
+               size_t ws_bytes, hipStream_t s, hipEvent_t const* ev, int only, bool flare) {
   using namespace flarepp;
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
   const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
-  const MixerWs w = mixer_ws(ws, dtype, B, N, C, H, M, pl);
+  const MixerWs w = mixer_ws(ws, dtype, B, N, C, H, M, pl, flare);
   if (ws_bytes < w.bytes)
     return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
   const float qscale = route_qscale(D);
@@ -286,13 +293,20 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     // weights as fused-path fragments and the seed operand
     PrepFusedParams pp{};
     pp.C = (int)C;
-    const void* win[5] = {Wk, Wv, Wkt, Wvt, Wo};
     const int dkind = decode_kind_for((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype));
-    const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain,
-                         dkind == kDecodeStaged ? kFragMerge : kFragMergeHg};
-    for (int i = 0; i < 5; ++i) { pp.w[i] = win[i]; pp.wf[i] = w.wf[i]; pp.mode[i] = mode[i]; }
+    const int merge_mode = dkind == kDecodeStaged ? kFragMerge : kFragMergeHg;
+    const void* win[5] = {Wk, Wv, Wkt, Wvt, Wo};
+    const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain, merge_mode};
+    for (int i = 0; i < 5; ++i) {
+      if (flare && (i == 2 || i == 3)) continue;
+      pp.w[pp.nw] = win[i]; pp.wf[pp.nw] = w.wf[i]; pp.mode[pp.nw] = mode[i]; ++pp.nw;
+    }
     pp.seeds = seeds; pp.H = (int)H; pp.M = (int)M; pp.Mp = (int)Mp; pp.D = (int)D;
     pp.qscale = qscale; pp.seeds_op = w.seeds_op;
+    // fixed queries: they are the decode's routes too, per batch entry, with
+    // their norm bounds (on FLARE++ the combine of call 1 writes both)
+    pp.seed_copies = flare ? (int)B : 1;
+    pp.qnorm2 = flare ? w.qnorm2 : nullptr;
     if (RUN(1)) HIPTRY(launch_prep_fused<T>(pp, s));
     STAGE(1);
     STAGE(2);  // the projections run inside the routing kernels
@@ -301,22 +315,25 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     ep.B = (int)B; ep.N = (int)N; ep.C = (int)C; ep.H = (int)H; ep.Mp = (int)Mp; ep.QB = (int)(Mp / 32);
     ep.nqw = pl.nqw; ep.qgroups = pl.qgroups; ep.chunk = pl.chunk; ep.nchunks = pl.nchunks;
     ep.fast_lim = fast_limit(); ep.part_ml = w.part_ml; ep.part_acc = w.part_acc;
-    if (RUN(3)) HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 1
+    if (!flare && RUN(3)) HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 1
     STAGE(3);
     CombineParams cp{};
     cp.part_ml = w.part_ml; cp.part_acc = w.part_acc; cp.BH = B * H; cp.R = pl.nchunks;
     cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale; cp.frag = 1;
     cp.out32 = Q_out; cp.q_op = w.q_op; cp.qnorm2 = w.qnorm2;
-    if (RUN(4)) HIPTRY(launch_combine_par<T>(cp, s));
+    if (!flare && RUN(4)) HIPTRY(launch_combine_par<T>(cp, s));
     STAGE(4);
-    ep.wkf = w.wf[0]; ep.wvf = w.wf[1]; ep.q_op = w.q_op; ep.q_sb = H * Mp * D;
-    if (RUN(5)) HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 2
+    ep.wkf = w.wf[0]; ep.wvf = w.wf[1];
+    ep.q_op = flare ? w.seeds_op : w.q_op;
+    ep.q_sb = flare ? 0 : H * Mp * D;
+    if (RUN(5)) HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 2 / FLARE encode
     STAGE(5);
     cp.out32 = Z_out; cp.q_op = nullptr; cp.qnorm2 = nullptr; cp.z_op = w.z_op;
     if (RUN(6)) HIPTRY(launch_combine_par<T>(cp, s));
     STAGE(6);
     DecFusedParams dp{};
-    dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = w.q_op; dp.z_op = w.z_op; dp.qnorm2 = w.qnorm2;
+    dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = flare ? w.seeds_op : w.q_op;
+    dp.z_op = w.z_op; dp.qnorm2 = w.qnorm2;
     dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
     dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O;
     dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);
@@ -331,9 +348,11 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   // 1. weights as MFMA fragments
   WeightFragParams wp{};
   wp.C = (int)C;
-  wp.nw = 5;
   const void* ws_in[5] = {Wk, Wv, Wkt, Wvt, Wo};
-  for (int i = 0; i < 5; ++i) { wp.w[i] = ws_in[i]; wp.out[i] = w.wf[i]; }
+  for (int i = 0; i < 5; ++i) {
+    if (flare && (i == 2 || i == 3)) continue;
+    wp.w[wp.nw] = ws_in[i]; wp.out[wp.nw] = w.wf[i]; ++wp.nw;
+  }
   if (RUN(1)) HIPTRY(launch_weight_frags<T>(wp, s));
 
   // 2. seeds -> scaled route operand (shared by the batch)
@@ -346,7 +365,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   // 3. project: K, K~ token-major; V, V~ d-major (value operands)
   ProjParams pp{};
   pp.x = X; pp.B = (int)B; pp.N = (int)N; pp.Np = (int)Np; pp.C = (int)C; pp.H = (int)H; pp.D = (int)D;
-  pp.nw = 4;
+  pp.nw = flare ? 2 : 4;
   pp.wf[0] = w.wf[0]; pp.out[0] = w.K;    pp.layout[0] = kHeadsTokenMajor;
   pp.wf[1] = w.wf[1]; pp.out[1] = w.Vdm;  pp.layout[1] = kHeadsDMajor;
   pp.wf[2] = w.wf[2]; pp.out[2] = w.Kt;   pp.layout[2] = kHeadsTokenMajor;
@@ -365,19 +384,20 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   r1.va = w.Vtdm; r1.va_sb = dmBS; r1.va_sh = dmHS; r1.va_ld = (int)Np;
   r1.qs = w.seeds_op; r1.qs_sb = 0; r1.qs_sh = rtHS; r1.qs_rows = (int)Mp;
   r1.part_ml = w.part_ml; r1.part_acc = w.part_acc;
-  if (RUN(3)) HIPTRY(launch_route<T>(r1, (int)D, false, s));
+  if (!flare && RUN(3)) HIPTRY(launch_route<T>(r1, (int)D, false, s));
   STAGE(3);
   CombineParams c1{};
   c1.part_ml = w.part_ml; c1.part_acc = w.part_acc; c1.BH = B * H; c1.R = e.nchunks;
   c1.M = (int)M; c1.Mp = (int)Mp; c1.D = (int)D; c1.qscale = qscale;
   c1.out32 = Q_out; c1.lse = nullptr; c1.q_op = w.q_op; c1.z_op = nullptr;
-  if (RUN(4)) HIPTRY(launch_combine_par<T>(c1, s));
+  if (!flare && RUN(4)) HIPTRY(launch_combine_par<T>(c1, s));
   STAGE(4);
 
-  // 5. call 2: Z = SDPA(Q, K, V), softmax over tokens
+  // 5. call 2: Z = SDPA(Q, K, V), softmax over tokens (FLARE: the learned
+  // queries, shared by the batch)
   RouteParams r2 = r1;
   r2.ka = w.K; r2.va = w.Vdm;
-  r2.qs = w.q_op; r2.qs_sb = rtBS; r2.qs_sh = rtHS; r2.qs_rows = (int)Mp;
+  r2.qs = flare ? w.seeds_op : w.q_op; r2.qs_sb = flare ? 0 : rtBS; r2.qs_sh = rtHS; r2.qs_rows = (int)Mp;
   if (RUN(5)) HIPTRY(launch_route<T>(r2, (int)D, false, s));
   STAGE(5);
   CombineParams c2 = c1;
@@ -388,7 +408,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   // 6. call 3: Y = SDPA(K, Q, Z), softmax over routes, heads merged
   void* Y = Y_out ? Y_out : w.Y;
   RouteParams r3 = decode_params(B, H, N, M, D);
-  r3.ka = w.q_op; r3.ka_sb = rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
+  r3.ka = flare ? w.seeds_op : w.q_op; r3.ka_sb = flare ? 0 : rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
   r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;
   r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
   r3.y = Y; r3.y_sb = N * C; r3.y_row = C;
@@ -409,7 +429,8 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
 int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
                 const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                 const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
-                size_t ws_bytes, void* stream, void* const* events, int n_events, int only = 0) {
+                size_t ws_bytes, void* stream, void* const* events, int n_events, int only = 0,
+                bool flare = false) {
   TRY(check_mixer_shape(dtype, B, N, C, H, M));
   if (only < 0 || only > FLAREPP_PROFILE_EVENTS - 1)
     return fail(FLAREPP_ERR_INVALID_ARG, "stage=%d must be in [1, %d]", only, FLAREPP_PROFILE_EVENTS - 1);
@@ -424,10 +445,12 @@ int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M
   TRY(check_ptr(X, "X"));
   TRY(check_ptr(Wk, "Wk"));
   TRY(check_ptr(Wv, "Wv"));
-  TRY(check_ptr(Wkt, "Wkt"));
-  TRY(check_ptr(Wvt, "Wvt"));
+  if (!flare) {
+    TRY(check_ptr(Wkt, "Wkt"));
+    TRY(check_ptr(Wvt, "Wvt"));
+  }
   TRY(check_ptr(Wo, "Wo"));
-  TRY(check_ptr(seeds, "seeds"));
+  TRY(check_ptr(seeds, flare ? "queries" : "seeds"));
   TRY(check_ptr(O, "O"));
   TRY(check_ptr(Q_out, "Q_out", true));
   TRY(check_ptr(Z_out, "Z_out", true));
@@ -437,9 +460,9 @@ int mixer_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == FLAREPP_F32)
     return mixer_impl<float>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
-                             Y_out, ws, ws_bytes, s, ev, only);
+                             Y_out, ws, ws_bytes, s, ev, only, flare);
   return mixer_impl<__bf16>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out,
-                            Y_out, ws, ws_bytes, s, ev, only);
+                            Y_out, ws, ws_bytes, s, ev, only, flare);
 }
 
 // ---- route ------------------------------------------------------------------
@@ -667,6 +690,26 @@ int flarepp_mixer_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int6
                                 void* stream) {
   return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, Q_out, Z_out, Y_out,
                      ws, ws_bytes, stream, nullptr, 0);
+}
+
+size_t flarepp_flare_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  if (check_mixer_shape(dtype, B, N, C, H, M) != FLAREPP_OK) return 0;
+  return mixer_ws(nullptr, dtype, B, N, C, H, M, mixer_plan(dtype, B, N, C, H, M), true).bytes;
+}
+
+int flarepp_flare_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                          const void* X, const void* Wk, const void* Wv, const void* Wo,
+                          const void* queries, void* O, void* ws, size_t ws_bytes, void* stream) {
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, nullptr, nullptr, Wo, queries, O, nullptr, nullptr,
+                     nullptr, ws, ws_bytes, stream, nullptr, 0, 0, true);
+}
+
+int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                const void* X, const void* Wk, const void* Wv, const void* Wo,
+                                const void* queries, void* O, float* Z_out, void* Y_out, void* ws,
+                                size_t ws_bytes, void* stream) {
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, nullptr, nullptr, Wo, queries, O, nullptr, Z_out,
+                     Y_out, ws, ws_bytes, stream, nullptr, 0, 0, true);
 }
 
 }  // extern "C"

@@ -23,12 +23,14 @@
 // flarepp_internal.hpp): every lane reads 16 contiguous bytes, so operand
 // loads from LDS or memory are free of bank conflicts.
 //
-// k_prep_fused    weight fragments, seed operand, cleared norm bounds.
-// k_encode_fused  calls 1 and 2 (Sec. 3.2, Eqs. (8) and (10)).  A workgroup
-//                 of W waves owns (batch, 32-channel head group, token chunk);
-//                 per step each wave projects one 32-token sub-tile into LDS,
-//                 then every wave runs its query blocks over all W sub-tiles.
-//                 Writes split-key partials (m, l, acc) per route.
+// k_prep_fused    weight fragments, seed operand (and, on the fixed-query
+//                 path, its route-norm bounds).
+// k_encode_fused  calls 1 and 2 (Sec. 3.2, Eqs. (8) and (10)); the fixed-
+//                 query encode (Sec. 3.1, Eq. (5)).  A workgroup of W waves
+//                 owns (batch, 32-channel head group, token chunk); each wave
+//                 projects one 32-token sub-tile of the next super-tile into
+//                 LDS while it runs its query blocks over the W sub-tiles of
+//                 the current one.  Writes split-key partials (m, l, acc).
 // k_combine_par   exact merge of the partials (App. A.3, Eqs. (24)-(28)) in a
 //                 fixed order, parallel over chunk slices; writes the next
 //                 call's route operands.
@@ -83,7 +85,10 @@ __device__ __forceinline__ void copy_to_lds(const void* src, char* dst, int n16,
 }
 
 // ---------------------------------------------------------------------------
-// Weight fragments of the fused path, seed operand, cleared norm bounds.
+// Weight fragments of the fused path and the seed operand (scaled, in q
+// fragment order, seed_copies copies); with qnorm2, also the seed operand's
+// route-norm bounds for the decode (the fixed-query path, where the seeds are
+// the decode's routes).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void k_prep_fused(PrepFusedParams p) {
@@ -92,7 +97,7 @@ __global__ void k_prep_fused(PrepFusedParams p) {
   const int QB = p.Mp / 32, DS = p.D / 16;
   const int64_t nseed = (int64_t)p.H * QB * DS * 64;
   int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx < 5 * per_w) {
+  if (idx < p.nw * per_w) {
     const int w = (int)(idx / per_w);
     const int64_t f = idx % per_w;
     const int lane = (int)(f & 63), ks = (int)((f >> 6) % KS), cb = (int)((f >> 6) / KS);
@@ -112,18 +117,35 @@ __global__ void k_prep_fused(PrepFusedParams p) {
     }
     return;
   }
-  idx -= 5 * per_w;
-  if (idx < nseed) {  // seeds -> q fragment order, scaled
-    const int lane = (int)(idx & 63), js = (int)((idx >> 6) % DS);
-    const int qb = (int)((idx >> 6) / DS % QB), h = (int)((idx >> 6) / DS / QB);
+  idx -= p.nw * per_w;
+  if (idx < p.seed_copies * nseed) {  // seeds -> q fragment order, scaled
+    const int64_t copy = idx / nseed, si = idx % nseed;
+    const int lane = (int)(si & 63), js = (int)((si >> 6) % DS);
+    const int qb = (int)((si >> 6) / DS % QB), h = (int)((si >> 6) / DS / QB);
     const int g = lane >> 5, m = 32 * qb + (lane & 31);
-    T* out = (T*)p.seeds_op + idx * 8;
+    T* out = (T*)p.seeds_op + (copy * nseed + si) * 8;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float v = m < p.M ? to_f32(((const T*)p.seeds)[((int64_t)h * p.M + m) * p.D + 16 * js + 8 * g + j]) : 0.f;
       out[j] = from_f32<T>(v * p.qscale);
     }
     return;
+  }
+  idx -= p.seed_copies * nseed;
+  if (p.qnorm2 && idx < (int64_t)p.seed_copies * p.H * (p.Mp / 4)) {
+    // max over routes 4i .. 4i+3 of |scaled q|^2 of the rounded operand
+    const int64_t per = (int64_t)p.H * (p.Mp / 4);
+    const int h = (int)(idx % per / (p.Mp / 4)), i = (int)(idx % (p.Mp / 4));
+    float n2 = 0.f;
+    for (int m = 4 * i; m < min(4 * i + 4, p.M); ++m) {
+      float s = 0.f;
+      for (int d = 0; d < p.D; ++d) {
+        const float q = to_f32(from_f32<T>(to_f32(((const T*)p.seeds)[((int64_t)h * p.M + m) * p.D + d]) * p.qscale));
+        s = __builtin_fmaf(q, q, s);
+      }
+      n2 = fmaxf(n2, s);
+    }
+    p.qnorm2[idx] = n2;
   }
 }
 
@@ -1474,7 +1496,9 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 // ---------------------------------------------------------------------------
 template <typename T>
 hipError_t launch_prep_fused(const PrepFusedParams& p, hipStream_t s) {
-  const int64_t n = 5 * (int64_t)p.C * p.C / 8 + (int64_t)p.H * (p.Mp / 32) * (p.D / 16) * 64;
+  const int64_t n = p.nw * (int64_t)p.C * p.C / 8 +
+                    (int64_t)p.seed_copies * p.H * (p.Mp / 32) * (p.D / 16) * 64 +
+                    (p.qnorm2 ? (int64_t)p.seed_copies * p.H * (p.Mp / 4) : 0);
   k_prep_fused<T><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
   return hipGetLastError();
 }

@@ -92,14 +92,16 @@ __host__ __device__ constexpr int64_t z_frag_index(int rt, int hf, int rb, int g
 enum FragMode { kFragPlain = 0, kFragKeyPerm = 1, kFragMerge = 2, kFragMergeHg = 3 };
 
 struct PrepFusedParams {
-  int C;
-  const void* w[5];  // W_K, W_V, W~_K, W~_V, W_O  [C][C]
+  int C, nw;         // nw weights converted
+  const void* w[5];  // [C][C] each
   void* wf[5];       // fragments [C/32][C/16][64][8]
   int mode[5];       // FragMode per weight
   const void* seeds;  // [H][M][D]
   int H, M, Mp, D;
   float qscale;
-  void* seeds_op;     // [H] x q fragment order, scaled
+  int seed_copies;    // copies of the seed operand written back to back
+  void* seeds_op;     // [seed_copies][H] x q fragment order, scaled
+  float* qnorm2;      // [seed_copies][H][Mp / 4] max |scaled q|^2 per 4 routes, or null
 };
 
 struct EncFusedParams {

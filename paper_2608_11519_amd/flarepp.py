@@ -32,6 +32,7 @@ EXPORTS = (
     "flarepp_route_workspace_bytes", "flarepp_route",
     "flarepp_mixer_workspace_bytes", "flarepp_mixer_forward", "flarepp_mixer_forward_debug",
     "flarepp_mixer_forward_profiled", "flarepp_mixer_path", "flarepp_mixer_stage",
+    "flarepp_flare_workspace_bytes", "flarepp_flare_forward", "flarepp_flare_forward_debug",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -85,6 +86,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                    + [vp, sz, vp, ctypes.POINTER(vp), i32])
     lib.flarepp_mixer_stage.restype = i32
     lib.flarepp_mixer_stage.argtypes = [i32, i32, i64, i64, i64, i64, i64] + [vp] * 8 + [vp, sz, vp]
+    lib.flarepp_flare_workspace_bytes.restype = sz
+    lib.flarepp_flare_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
+    lib.flarepp_flare_forward.restype = i32
+    lib.flarepp_flare_forward.argtypes = [i32, i64, i64, i64, i64, i64] + [vp] * 6 + [vp, sz, vp]
+    lib.flarepp_flare_forward_debug.restype = i32
+    lib.flarepp_flare_forward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 6
+                                                + [fp, vp] + [vp, sz, vp])
     _lib = lib
     return lib
 
@@ -287,8 +295,50 @@ def flarepp_mixer_stage(stage: int, X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, o
     _check(rc)
 
 
+def flarepp_flare_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
+    return int(load().flarepp_flare_workspace_bytes(dtype, B, N, C, H, M))
+
+
+def flarepp_flare_forward(X, Wk, Wv, Wo, queries, *, H: int,
+                          out: Optional[torch.Tensor] = None,
+                          ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The fixed-query FLARE mixer forward: O [B, N, C] in X's dtype;
+    ``queries`` [H, M, D] are the learned routing queries."""
+    lib = load()
+    B, N, C = X.shape
+    M = queries.shape[1]
+    dt = _dtype_code(X)
+    O = out if out is not None else torch.empty_like(X)
+    w = _workspace(flarepp_flare_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_flare_forward(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wo),
+                                   _ptr(queries), _ptr(O), _ptr(w), w.numel(), _stream(X.device))
+    _check(rc)
+    return O
+
+
+def flarepp_flare_forward_debug(X, Wk, Wv, Wo, queries, *, H: int,
+                                ws: Optional[torch.Tensor] = None):
+    """Fixed-query FLARE forward that also returns the stage results: (O, Z, Y)."""
+    lib = load()
+    B, N, C = X.shape
+    M = queries.shape[1]
+    D = C // H
+    dt = _dtype_code(X)
+    O = torch.empty_like(X)
+    Z = torch.empty((B, H, M, D), dtype=torch.float32, device=X.device)
+    Y = torch.empty_like(X)
+    w = _workspace(flarepp_flare_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_flare_forward_debug(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wo),
+                                         _ptr(queries), _ptr(O), _ptr(Z), _ptr(Y), _ptr(w), w.numel(),
+                                         _stream(X.device))
+    _check(rc)
+    return O, Z, Y
+
+
 # short aliases
 project = flarepp_project
 route = flarepp_route
 mixer_forward = flarepp_mixer_forward
 mixer_forward_debug = flarepp_mixer_forward_debug
+flare_forward = flarepp_flare_forward
+flare_forward_debug = flarepp_flare_forward_debug

@@ -148,3 +148,43 @@ def test_project_rejects_unpaired_weights():
     rc = lib.flarepp_project(fp.BF16, 1, 64, 64, 4, _P, _P, None, None, None, _P, None, None, None,
                              _P, 16, None)
     assert rc == fp.ERR_WORKSPACE
+
+
+def _flare(dtype=fp.BF16, B=1, N=64, C=64, H=4, M=32, ptrs=None, ws=_P, ws_bytes=1 << 30):
+    lib = _lib()
+    p = ptrs or [_P] * 6  # X, Wk, Wv, Wo, queries, O
+    return lib.flarepp_flare_forward(dtype, B, N, C, H, M, *p, ws, ws_bytes, None)
+
+
+def test_flare_workspace_is_smaller_than_the_mixer_one(monkeypatch):
+    for dt in (fp.F32, fp.BF16):
+        for unfused in (False, True):
+            if unfused:
+                monkeypatch.setenv("FLAREPP_UNFUSED", "1")
+            f = fp.flarepp_flare_workspace_bytes(dt, 4, 16384, 128, 8, 128)
+            m = fp.flarepp_mixer_workspace_bytes(dt, 4, 16384, 128, 8, 128)
+            monkeypatch.delenv("FLAREPP_UNFUSED", raising=False)
+            assert 0 < f < m
+    assert fp.flarepp_flare_workspace_bytes(fp.BF16, 1, 10, 100, 3, 4) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), fp.ERR_INVALID_ARG),
+    (dict(M=0), fp.ERR_INVALID_ARG),
+    (dict(C=96, H=2), fp.ERR_UNSUPPORTED),
+    (dict(dtype=3), fp.ERR_UNSUPPORTED),
+    (dict(ws=None), fp.ERR_WORKSPACE),
+    (dict(ws_bytes=100), fp.ERR_WORKSPACE),
+])
+def test_flare_rejects_invalid_arguments(kw, code):
+    assert _flare(**kw) == code
+    assert fp.last_error() != ""
+
+
+def test_flare_rejects_null_and_misaligned_pointers():
+    for i in range(6):
+        ptrs = [_P] * 6
+        ptrs[i] = None
+        assert _flare(ptrs=ptrs) == fp.ERR_INVALID_ARG
+        ptrs[i] = ctypes.c_void_p(4096 + 4)
+        assert _flare(ptrs=ptrs) == fp.ERR_INVALID_ARG

@@ -391,6 +391,59 @@ def test_flare_special_case_matches_flarepp_with_synthesised_queries():
     np.testing.assert_allclose(f["Z"], r["Z"], atol=1e-12)
 
 
+def test_flare_matches_two_library_sdpa_calls():
+    # FLARE (Sec. 3.1, Eq. (5)): Z = SDPA(Q, K, V), Y = SDPA(K, Q, Z), merge with W_O;
+    # checked against torch's own SDPA in float64
+    w, d = _small(seed=12, B=2, seed_scale=4.0)
+    H = w.H
+    Qlat = d["seeds"].astype(np.float64)
+    f = orc.flare_forward(d["X"], d["Wk"], d["Wv"], d["Wo"], Qlat, H)
+    X = torch.from_numpy(d["X"].astype(np.float64))
+    B, N, C = X.shape
+    D = C // H
+    K = (X @ torch.from_numpy(d["Wk"].astype(np.float64))).reshape(B, N, H, D).transpose(1, 2)
+    V = (X @ torch.from_numpy(d["Wv"].astype(np.float64))).reshape(B, N, H, D).transpose(1, 2)
+    Q = torch.from_numpy(Qlat)[None].expand(B, -1, -1, -1)
+    Z = torch.nn.functional.scaled_dot_product_attention(Q, K, V)
+    Y = torch.nn.functional.scaled_dot_product_attention(K, Q, Z)
+    Ym = Y.transpose(1, 2).reshape(B, N, C)
+    O = Ym @ torch.from_numpy(d["Wo"].astype(np.float64))
+    np.testing.assert_allclose(f["Z"], Z.numpy(), atol=1e-12)
+    np.testing.assert_allclose(f["Y"], Ym.numpy(), atol=1e-12)
+    np.testing.assert_allclose(f["O"], O.numpy(), atol=1e-12)
+
+
+def test_flare_operator_has_rank_at_most_m_and_stochastic_rows():
+    # W_eff = W_dec W_enc (Sec. 3.1, Eq. (6)) with fixed queries: Y_h = W_eff V_h,
+    # rank <= M, rows sum to one
+    w, d = _small(seed=13, B=1, N=24, C=16, H=2, M=3, seed_scale=3.0)
+    H, D, M = w.H, w.D, w.M
+    f = orc.flare_forward(d["X"], d["Wk"], d["Wv"], d["Wo"], d["seeds"], H)
+    K = orc.project(d["X"], d["Wk"], H)[0]
+    V = orc.project(d["X"], d["Wv"], H)[0]
+    for h in range(H):
+        S = d["seeds"][h].astype(np.float64) @ K[h].T / math.sqrt(D)  # M x N
+        enc = np.exp(S - S.max(axis=1, keepdims=True))
+        enc /= enc.sum(axis=1, keepdims=True)
+        dec = np.exp(S.T - S.T.max(axis=1, keepdims=True))
+        dec /= dec.sum(axis=1, keepdims=True)
+        Weff = dec @ enc
+        np.testing.assert_allclose(Weff.sum(axis=1), 1.0, atol=1e-13)
+        sv = np.linalg.svd(Weff, compute_uv=False)
+        assert sv[M] / sv[0] < 1e-10
+        np.testing.assert_allclose(f["Y"][0, :, h * D:(h + 1) * D], Weff @ V[h], atol=1e-12)
+
+
+def test_flare_single_route_broadcasts_the_latent():
+    # with M = 1 the decode softmax has one entry: every token receives Z
+    w, d = _small(seed=14, B=2, M=1, seed_scale=2.0)
+    f = orc.flare_forward(d["X"], d["Wk"], d["Wv"], d["Wo"], d["seeds"], w.H)
+    D = w.D
+    for h in range(w.H):
+        np.testing.assert_allclose(f["Y"][:, :, h * D:(h + 1) * D], np.broadcast_to(
+            f["Z"][:, h, 0][:, None, :], f["Y"][:, :, h * D:(h + 1) * D].shape), atol=1e-13)
+
+
 def test_lse_outputs_match_bruteforce():
     w, d = _small(seed=11, B=1, N=9, C=8, H=2, M=3, seed_scale=5.0)
     r = orc.mixer_forward(*_args(d), w.H)
