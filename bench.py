@@ -75,9 +75,9 @@ def stage_work(w, fused):
     prep = 10.0 * C * C * bs + 2.0 * H * M * D * bs
     comb = w.B * H * M * D * (4.0 + bs)
     zero = dict(flops=0.0, bytes=0.0, exps=0.0)
-    if fused:
+    if fused:  # the first encode call converts the weights (stage 1 is empty)
         return {
-            "prep": dict(flops=0.0, bytes=prep, exps=0.0),
+            "prep": zero,
             "project": zero,
             "call1_encode": dict(flops=route + 2 * gemm, bytes=T * C * bs, exps=exps),
             "call1_combine": dict(flops=0.0, bytes=comb, exps=0.0),
@@ -122,7 +122,7 @@ def roofline(work, ms, dtype):
 # Kernels (symbol substrings) that can carry each stage on the fused path, for
 # the counter tables; for C <= 128 the decode is k_decode3 or k_decode2 when
 # the head-group stages fit, otherwise k_decode_fused.
-STAGE_KERNELS_FUSED = {"prep": ("k_prep_fused",), "call1_encode": ("k_encode_fused",),
+STAGE_KERNELS_FUSED = {"call1_encode": ("k_encode_fused",),
                        "call1_combine": ("k_combine_par",), "call2_encode": ("k_encode_fused",),
                        "call2_combine": ("k_combine_par",),
                        "call3_decode": ("k_decode3", "k_decode2", "k_decode_fused")}
@@ -343,7 +343,7 @@ def main(argv=None):
 
     # ---- per-stage device times: each stage launched alone, back to back ----
     fused = fp.flarepp_mixer_path(dcode, w.B, w.N, w.C, w.H, w.M) == fp.PATH_FUSED
-    empty = {"project", "merge"} if fused else set()
+    empty = {"prep", "project", "merge"} if fused else set()
     reps = max(args.stage_reps, 1)
     stage_ms = {}
     for k, name in enumerate(fp.PROFILE_STAGES, start=1):

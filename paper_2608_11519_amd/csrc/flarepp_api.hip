@@ -251,7 +251,9 @@ MixerWs mixer_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t
   Carver cv(base);
   MixerWs w{};
   for (int i = 0; i < 5; ++i) w.wf[i] = (flare && (i == 2 || i == 3)) ? nullptr : cv.take(bs * C * C);
-  w.seeds_op = cv.take(bs * (flare && pl.fused ? B : 1) * H * Mp * D);
+  // seed operand: the unfused path's (shared by the batch), or on the fused
+  // fixed-query path one per batch entry (FLARE++'s first call reads the seeds)
+  w.seeds_op = pl.fused && !flare ? nullptr : cv.take(bs * (flare && pl.fused ? B : 1) * H * Mp * D);
   if (!pl.fused) {
     w.K = cv.take(bs * B * H * N * D);
     w.Kt = flare ? nullptr : cv.take(bs * B * H * N * D);
@@ -291,27 +293,32 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   STAGE(0);
   if (pl.fused) {
     // weights as fused-path fragments and the seed operand
+    // The first routing call reads the row-major weights and the seeds itself;
+    // the first combine converts what the later kernels read into fragment
+    // order: W_K and W_O for the decode, W_V for the second encode of
+    // FLARE++, and for the fixed queries of FLARE (the decode's routes too)
+    // a seed operand per batch entry with its route-norm bounds (on FLARE++
+    // the combine of call 1 writes both from Q(X)).  Stages 1 and 2 launch
+    // nothing.
     PrepFusedParams pp{};
     pp.C = (int)C;
     const int dkind = decode_kind_for((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype));
     const int merge_mode = dkind == kDecodeStaged ? kFragMerge : kFragMergeHg;
-    const void* win[5] = {Wk, Wv, Wkt, Wvt, Wo};
-    const int mode[5] = {kFragKeyPerm, kFragPlain, kFragKeyPerm, kFragPlain, merge_mode};
-    for (int i = 0; i < 5; ++i) {
-      if (flare && (i == 2 || i == 3)) continue;
-      pp.w[pp.nw] = win[i]; pp.wf[pp.nw] = w.wf[i]; pp.mode[pp.nw] = mode[i]; ++pp.nw;
-    }
+    auto add = [&](const void* wt, int slot, int mode) {
+      pp.w[pp.nw] = wt; pp.wf[pp.nw] = w.wf[slot]; pp.mode[pp.nw] = mode; ++pp.nw;
+    };
+    add(Wk, 0, kFragKeyPerm);
+    if (!flare) add(Wv, 1, kFragPlain);
+    add(Wo, 4, merge_mode);
     pp.seeds = seeds; pp.H = (int)H; pp.M = (int)M; pp.Mp = (int)Mp; pp.D = (int)D;
     pp.qscale = qscale; pp.seeds_op = w.seeds_op;
-    // fixed queries: they are the decode's routes too, per batch entry, with
-    // their norm bounds (on FLARE++ the combine of call 1 writes both)
-    pp.seed_copies = flare ? (int)B : 1;
+    pp.seed_copies = flare ? (int)B : 0;
     pp.qnorm2 = flare ? w.qnorm2 : nullptr;
-    if (RUN(1)) HIPTRY(launch_prep_fused<T>(pp, s));
     STAGE(1);
     STAGE(2);  // the projections run inside the routing kernels
     EncFusedParams ep{};
-    ep.x = X; ep.wkf = w.wf[2]; ep.wvf = w.wf[3]; ep.q_op = w.seeds_op; ep.q_sb = 0;
+    ep.x = X; ep.wk_raw = flare ? Wk : Wkt; ep.wv_raw = flare ? Wv : Wvt; ep.seeds_raw = seeds;
+    ep.q_sb = 0; ep.M = (int)M; ep.qscale = qscale;
     ep.B = (int)B; ep.N = (int)N; ep.C = (int)C; ep.H = (int)H; ep.Mp = (int)Mp; ep.QB = (int)(Mp / 32);
     ep.nqw = pl.nqw; ep.qgroups = pl.qgroups; ep.chunk = pl.chunk; ep.nchunks = pl.nchunks;
     ep.fast_lim = fast_limit(); ep.part_ml = w.part_ml; ep.part_acc = w.part_acc;
@@ -321,11 +328,14 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     cp.part_ml = w.part_ml; cp.part_acc = w.part_acc; cp.BH = B * H; cp.R = pl.nchunks;
     cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale; cp.frag = 1;
     cp.out32 = Q_out; cp.q_op = w.q_op; cp.qnorm2 = w.qnorm2;
+    cp.prep = pp; cp.prep_n = prep_fused_items(pp);
     if (!flare && RUN(4)) HIPTRY(launch_combine_par<T>(cp, s));
     STAGE(4);
-    ep.wkf = w.wf[0]; ep.wvf = w.wf[1];
-    ep.q_op = flare ? w.seeds_op : w.q_op;
-    ep.q_sb = flare ? 0 : H * Mp * D;
+    if (!flare) {  // call 2 reads the fragments the first combine wrote and Q(X)
+      ep.wk_raw = ep.wv_raw = ep.seeds_raw = nullptr;
+      ep.wkf = w.wf[0]; ep.wvf = w.wf[1]; ep.q_op = w.q_op; ep.q_sb = H * Mp * D;
+      cp.prep_n = 0;
+    }
     if (RUN(5)) HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));  // call 2 / FLARE encode
     STAGE(5);
     cp.out32 = Z_out; cp.q_op = nullptr; cp.qnorm2 = nullptr; cp.z_op = w.z_op;

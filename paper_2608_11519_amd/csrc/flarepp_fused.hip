@@ -23,14 +23,14 @@
 // flarepp_internal.hpp): every lane reads 16 contiguous bytes, so operand
 // loads from LDS or memory are free of bank conflicts.
 //
-// k_prep_fused    weight fragments, seed operand (and, on the fixed-query
-//                 path, its route-norm bounds).
 // k_encode_fused  calls 1 and 2 (Sec. 3.2, Eqs. (8) and (10)); the fixed-
 //                 query encode (Sec. 3.1, Eq. (5)).  A workgroup of W waves
 //                 owns (batch, 32-channel head group, token chunk); each wave
 //                 projects one 32-token sub-tile of the next super-tile into
 //                 LDS while it runs its query blocks over the W sub-tiles of
 //                 the current one.  Writes split-key partials (m, l, acc).
+//                 The first call of a forward also converts the weights and
+//                 seeds the later kernels read into fragment order.
 // k_combine_par   exact merge of the partials (App. A.3, Eqs. (24)-(28)) in a
 //                 fixed order, parallel over chunk slices; writes the next
 //                 call's route operands.
@@ -84,51 +84,89 @@ __device__ __forceinline__ void copy_to_lds(const void* src, char* dst, int n16,
   }
 }
 
-// ---------------------------------------------------------------------------
-// Weight fragments of the fused path and the seed operand (scaled, in q
-// fragment order, seed_copies copies); with qnorm2, also the seed operand's
-// route-norm bounds for the decode (the fixed-query path, where the seeds are
-// the decode's routes).
-// ---------------------------------------------------------------------------
+// ---- small helpers -----------------------------------------------------------
 template <typename T>
-__global__ void k_prep_fused(PrepFusedParams p) {
+__device__ __forceinline__ typename Frag<T>::type cvt8(const f32x16& a, int off, float scale = 1.f) {
+  typename Frag<T>::type r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = from_f32<T>(a[off + e] * scale);
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ void store_frag(T* p, const typename Frag<T>::type& v) {
+  *reinterpret_cast<typename Frag<T>::type*>(p) = v;
+}
+
+// ---------------------------------------------------------------------------
+// One item of the fused path's preparation: a lane of a weight fragment, a
+// lane of the seed operand (scaled, in q fragment order, seed_copies copies)
+// or, with qnorm2, one route-norm bound of the seed operand for the decode
+// (the fixed-query path, where the seeds are the decode's routes).  The first
+// combine of a forward runs them, spread over its threads: prep_load issues
+// an item's loads, prep_store writes it once the combine's own work is done.
+// ---------------------------------------------------------------------------
+int64_t prep_fused_items(const PrepFusedParams& p) {
+  return p.nw * (int64_t)p.C * p.C / 8 + (int64_t)p.seed_copies * p.H * (p.Mp / 32) * (p.D / 16) * 64 +
+         (p.qnorm2 ? (int64_t)p.seed_copies * p.H * (p.Mp / 4) : 0);
+}
+
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type prep_load(const PrepFusedParams& p, int64_t idx) {
   const int C = p.C, KS = C / 16;
   const int64_t per_w = (int64_t)C * C / 8;  // fragment lanes per weight
   const int QB = p.Mp / 32, DS = p.D / 16;
   const int64_t nseed = (int64_t)p.H * QB * DS * 64;
-  int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx < p.nw * per_w) {
+  typename Frag<T>::type v = zero_frag<T>();
+  if (idx < p.nw * per_w) {  // a weight fragment lane
     const int w = (int)(idx / per_w);
     const int64_t f = idx % per_w;
     const int lane = (int)(f & 63), ks = (int)((f >> 6) % KS), cb = (int)((f >> 6) / KS);
     const int g = lane >> 5, c = lane & 31, mode = p.mode[w];
     const int col = 32 * cb + (mode == kFragKeyPerm ? key_perm(c) : c);
     const T* W = (const T*)p.w[w];
-    int64_t fo = f;
-    if (mode == kFragMergeHg) {  // [head group][output block][k step in group][64][8]
-      const int kpg = p.D == 64 ? 4 : 2, CB = C / 32;
-      fo = ((int64_t)((ks / kpg) * CB + cb) * kpg + ks % kpg) * 64 + lane;
-    }
-    T* out = (T*)p.wf[w] + fo * 8;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int row = 16 * ks + (mode == kFragMerge || mode == kFragMergeHg ? acc_row16(g, j) : 8 * g + j);
-      out[j] = W[(int64_t)row * C + col];
+      v[j] = W[(int64_t)row * C + col];
     }
-    return;
+    return v;
   }
   idx -= p.nw * per_w;
-  if (idx < p.seed_copies * nseed) {  // seeds -> q fragment order, scaled
-    const int64_t copy = idx / nseed, si = idx % nseed;
+  if (idx < p.seed_copies * nseed) {  // a seed operand lane, scaled
+    const int64_t si = idx % nseed;
     const int lane = (int)(si & 63), js = (int)((si >> 6) % DS);
     const int qb = (int)((si >> 6) / DS % QB), h = (int)((si >> 6) / DS / QB);
     const int g = lane >> 5, m = 32 * qb + (lane & 31);
-    T* out = (T*)p.seeds_op + (copy * nseed + si) * 8;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const float v = m < p.M ? to_f32(((const T*)p.seeds)[((int64_t)h * p.M + m) * p.D + 16 * js + 8 * g + j]) : 0.f;
-      out[j] = from_f32<T>(v * p.qscale);
+      const float x = m < p.M ? to_f32(((const T*)p.seeds)[((int64_t)h * p.M + m) * p.D + 16 * js + 8 * g + j]) : 0.f;
+      v[j] = from_f32<T>(x * p.qscale);
     }
+  }
+  return v;
+}
+
+template <typename T>
+__device__ __forceinline__ void prep_store(const PrepFusedParams& p, int64_t idx, const typename Frag<T>::type& v) {
+  const int C = p.C, KS = C / 16;
+  const int64_t per_w = (int64_t)C * C / 8;
+  const int QB = p.Mp / 32, DS = p.D / 16;
+  const int64_t nseed = (int64_t)p.H * QB * DS * 64;
+  if (idx < p.nw * per_w) {
+    const int w = (int)(idx / per_w);
+    const int64_t f = idx % per_w;
+    int64_t fo = f;
+    if (p.mode[w] == kFragMergeHg) {  // [head group][output block][k step in group][64][8]
+      const int lane = (int)(f & 63), ks = (int)((f >> 6) % KS), cb = (int)((f >> 6) / KS);
+      const int kpg = p.D == 64 ? 4 : 2, CB = C / 32;
+      fo = ((int64_t)((ks / kpg) * CB + cb) * kpg + ks % kpg) * 64 + lane;
+    }
+    store_frag<T>((T*)p.wf[w] + fo * 8, v);
+    return;
+  }
+  idx -= p.nw * per_w;
+  if (idx < p.seed_copies * nseed) {
+    store_frag<T>((T*)p.seeds_op + idx * 8, v);
     return;
   }
   idx -= p.seed_copies * nseed;
@@ -147,19 +185,6 @@ __global__ void k_prep_fused(PrepFusedParams p) {
     }
     p.qnorm2[idx] = n2;
   }
-}
-
-// ---- small helpers -----------------------------------------------------------
-template <typename T>
-__device__ __forceinline__ typename Frag<T>::type cvt8(const f32x16& a, int off, float scale = 1.f) {
-  typename Frag<T>::type r;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = from_f32<T>(a[off + e] * scale);
-  return r;
-}
-template <typename T>
-__device__ __forceinline__ void store_frag(T* p, const typename Frag<T>::type& v) {
-  *reinterpret_cast<typename Frag<T>::type*>(p) = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -215,9 +240,33 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   const int hg = hgq / p.qgroups, qg = hgq % p.qgroups;
   const int b = (int)(chunk_id / p.nchunks), r = (int)(chunk_id % p.nchunks);
 
-  copy_to_lds((const T*)p.wkf + (int64_t)hg * WELEMS, smem, WELEMS * (int)sizeof(T) / 16, 64 * W);
-  copy_to_lds((const T*)p.wvf + (int64_t)hg * WELEMS, smem + WELEMS * sizeof(T), WELEMS * (int)sizeof(T) / 16,
-              64 * W);
+  // The head group's weight slices in LDS, in fragment order: copied from the
+  // fragments, or gathered from the row-major weights (key projection with
+  // its columns key-permuted); the gathered lanes are written to LDS after
+  // the route and X loads are issued.
+  constexpr int WL = GB * KSC * 64, WPT = (WL + 64 * W - 1) / (64 * W);  // lanes, per thread
+  F wkg[WPT], wvg[WPT];
+  if (p.wk_raw) {
+    const T* Wk = (const T*)p.wk_raw;
+    const T* Wv = (const T*)p.wv_raw;
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int i = u * 64 * W + threadIdx.x;
+      if (i < WL) {
+        const int cb = hg * GB + i / (KSC * 64), ks = (i / 64) % KSC, ln = i % 64, gg = ln >> 5, cc = ln & 31;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int64_t row = (int64_t)(16 * ks + 8 * gg + j) * p.C + 32 * cb;
+          wkg[u][j] = Wk[row + key_perm(cc)];
+          wvg[u][j] = Wv[row + cc];
+        }
+      }
+    }
+  } else {
+    copy_to_lds((const T*)p.wkf + (int64_t)hg * WELEMS, smem, WELEMS * (int)sizeof(T) / 16, 64 * W);
+    copy_to_lds((const T*)p.wvf + (int64_t)hg * WELEMS, smem + WELEMS * sizeof(T), WELEMS * (int)sizeof(T) / 16,
+                64 * W);
+  }
   if constexpr (ONES_ROW) {  // constant rows 16 .. 31 of every value operand
     constexpr int NCONST = 2 * W * S::VFR * 32;
     for (int i = threadIdx.x; i < NCONST; i += 64 * W) {
@@ -238,10 +287,25 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
     const int s = slot0 + i;
     const bool ok = s < nslots;
     const int qb = ok ? s % p.QB : 0;
-    const T* qp = (const T*)p.q_op + (int64_t)b * p.q_sb + (int64_t)(hg * HPG + hh) * p.Mp * D;
+    if (p.seeds_raw) {  // the learned seeds, shared by the batch, scaled here
+      const int m = 32 * qb + c;
+      const T* sp = (const T*)p.seeds_raw + ((int64_t)(hg * HPG + hh) * p.M + m) * D;
 #pragma unroll
-    for (int js = 0; js < KS; ++js)
-      qf[i][js] = ok ? load_frag(qp + ((int64_t)(qb * KS + js) * 64 + lane) * 8) : zero_frag<T>();
+      for (int js = 0; js < KS; ++js) {
+        F v = zero_frag<T>();
+        if (ok && m < p.M) {
+          const F raw = load_frag(sp + 16 * js + 8 * g);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = from_f32<T>(to_f32(raw[e]) * p.qscale);
+        }
+        qf[i][js] = v;
+      }
+    } else {
+      const T* qp = (const T*)p.q_op + (int64_t)b * p.q_sb + (int64_t)(hg * HPG + hh) * p.Mp * D;
+#pragma unroll
+      for (int js = 0; js < KS; ++js)
+        qf[i][js] = ok ? load_frag(qp + ((int64_t)(qb * KS + js) * 64 + lane) * 8) : zero_frag<T>();
+    }
   }
 
   f32x16 acc[NQW][RB];
@@ -271,6 +335,16 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   };
   asm volatile("" ::: "memory");  // the weight copies and route loads are issued first
   load_x(k0);
+  if (p.wk_raw) {
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int i = u * 64 * W + threadIdx.x;
+      if (i < WL) {
+        store_frag<T>(wk_l + i * 8, wkg[u]);
+        store_frag<T>(wv_l + i * 8, wvg[u]);
+      }
+    }
+  }
   // weight slices and constant rows in LDS (every load but the X rows)
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KSC) : "memory");
   lds_barrier();
@@ -686,6 +760,10 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
   constexpr int KS = D / 16;
   const int t = threadIdx.x, rs = t & 15;
+  // this thread's first preparation item: loads now, store at the end
+  const int64_t pi0 = (int64_t)threadIdx.x * gridDim.x + blockIdx.x;
+  typename Frag<T>::type pv;
+  if (pi0 < p.prep_n) pv = prep_load<T>(p.prep, pi0);
   const int rows_per_bh = p.Mp / 16;
   const int64_t bh = blockIdx.x / rows_per_bh;
   const int qrow = (blockIdx.x % rows_per_bh) * 16 + (t >> 4);
@@ -768,6 +846,12 @@ __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
     }
   }
   if (valid && p.lse && rs == 0) p.lse[bh * p.M + qrow] = 0.6931471805599453f * (m + __log2f(l));
+  if (pi0 < p.prep_n) prep_store<T>(p.prep, pi0, pv);
+  for (int64_t k = 1;; ++k) {  // further items (when there are more than threads)
+    const int64_t i = (k * blockDim.x + threadIdx.x) * gridDim.x + blockIdx.x;
+    if (i >= p.prep_n) break;
+    prep_store<T>(p.prep, i, prep_load<T>(p.prep, i));
+  }
 }
 
 // Route tiles of the HPG heads of a group, software pipelined over the
@@ -1494,15 +1578,6 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
-template <typename T>
-hipError_t launch_prep_fused(const PrepFusedParams& p, hipStream_t s) {
-  const int64_t n = p.nw * (int64_t)p.C * p.C / 8 +
-                    (int64_t)p.seed_copies * p.H * (p.Mp / 32) * (p.D / 16) * 64 +
-                    (p.qnorm2 ? (int64_t)p.seed_copies * p.H * (p.Mp / 4) : 0);
-  k_prep_fused<T><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
-  return hipGetLastError();
-}
-
 template <typename T, int D, int KSC, int NQW, int W>
 static hipError_t enc_one(const EncFusedParams& p, hipStream_t s) {
   if constexpr (NQW > enc_nqw_cap(D, W) || (W == 8 && (D != 16 || KSC > 8)) ||
@@ -1639,8 +1714,6 @@ hipError_t launch_decode_fused(const DecFusedParams& p, int D, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-template hipError_t launch_prep_fused<float>(const PrepFusedParams&, hipStream_t);
-template hipError_t launch_prep_fused<__bf16>(const PrepFusedParams&, hipStream_t);
 template hipError_t launch_encode_fused<float>(const EncFusedParams&, int, int, hipStream_t);
 template hipError_t launch_encode_fused<__bf16>(const EncFusedParams&, int, int, hipStream_t);
 template hipError_t launch_combine_par<float>(const CombineParams&, hipStream_t);

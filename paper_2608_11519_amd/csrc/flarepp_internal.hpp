@@ -57,6 +57,19 @@ struct RouteParams {
   void* y; int64_t y_sb, y_row;
 };
 
+struct PrepFusedParams {
+  int C, nw;         // nw weights converted
+  const void* w[5];  // [C][C] each
+  void* wf[5];       // fragments [C/32][C/16][64][8]
+  int mode[5];       // FragMode per weight
+  const void* seeds;  // [H][M][D]
+  int H, M, Mp, D;
+  float qscale;
+  int seed_copies;    // copies of the seed operand written back to back
+  void* seeds_op;     // [seed_copies][H] x q fragment order, scaled
+  float* qnorm2;      // [seed_copies][H][Mp / 4] max |scaled q|^2 per 4 routes, or null
+};
+
 struct CombineParams {
   const float* part_ml; const float* part_acc;
   int64_t BH;
@@ -72,6 +85,10 @@ struct CombineParams {
   void* z_op;
   float* qnorm2;  // frag == 1 with q_op: [BH][Mp / 4] max of |scaled q|^2 over
                   // each group of 4 routes (one entry per wave), or null
+  // fragment conversion for the later kernels (prep_n items), spread over the
+  // threads: each issues its item's loads first and stores it at the end
+  PrepFusedParams prep;
+  int64_t prep_n;
 };
 
 // Fragment order of the route operands of the fused kernels (per (b, h)):
@@ -91,18 +108,6 @@ __host__ __device__ constexpr int64_t z_frag_index(int rt, int hf, int rb, int g
 // [C/32 / (D == 64 ? 2 : 1) groups][C/32 output blocks][k steps of the group][64][8]
 enum FragMode { kFragPlain = 0, kFragKeyPerm = 1, kFragMerge = 2, kFragMergeHg = 3 };
 
-struct PrepFusedParams {
-  int C, nw;         // nw weights converted
-  const void* w[5];  // [C][C] each
-  void* wf[5];       // fragments [C/32][C/16][64][8]
-  int mode[5];       // FragMode per weight
-  const void* seeds;  // [H][M][D]
-  int H, M, Mp, D;
-  float qscale;
-  int seed_copies;    // copies of the seed operand written back to back
-  void* seeds_op;     // [seed_copies][H] x q fragment order, scaled
-  float* qnorm2;      // [seed_copies][H][Mp / 4] max |scaled q|^2 per 4 routes, or null
-};
 
 struct EncFusedParams {
   const void* x;                     // [B][N][C]
@@ -114,6 +119,13 @@ struct EncFusedParams {
                                      // per chunk (multiple of 32 * waves), chunks
   float fast_lim;
   float* part_ml; float* part_acc;   // [B][H][nchunks][Mp] x {2 | D}
+  // The first routing call of a forward reads the row-major weights and the
+  // learned seeds itself (wk_raw, wv_raw [C][C], seeds_raw [H][M][D]); when
+  // null the fragments wkf / wvf and q_op are read.
+  const void* wk_raw; const void* wv_raw;
+  const void* seeds_raw;
+  int M;
+  float qscale;
 };
 
 struct DecFusedParams {
@@ -152,7 +164,8 @@ int decode_kind(int C, int D, int Mp, int elem_bytes);
 size_t dec2_stage_bytes(int C, int D, int Mp, int elem_bytes);
 size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res);
 
-template <typename T> hipError_t launch_prep_fused(const PrepFusedParams&, hipStream_t);
+// Items of work (fragment lanes, seed operand lanes, norm bounds) in a prep.
+int64_t prep_fused_items(const PrepFusedParams& p);
 template <typename T> hipError_t launch_encode_fused(const EncFusedParams&, int D, int waves, hipStream_t);
 template <typename T> hipError_t launch_combine_par(const CombineParams&, hipStream_t);
 template <typename T> hipError_t launch_decode_fused(const DecFusedParams&, int D, hipStream_t);
