@@ -1360,12 +1360,14 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode2(DecFusedPa
 }
 
 // ---------------------------------------------------------------------------
-// Decode with every stage resident and a compile-time route-tile count RT:
-// the route tiles of a group are unrolled, and the key projection of the next
-// group and the merge of the previous group are spread over them (one or two
-// MFMAs after each tile), so the matrix work runs beside the softmax instead
-// of stalling the wave in dependent MFMA chains.  Same LDS layout, stages and
-// results as k_decode2<..., RES = true>.
+// Decode with every stage resident and a compile-time route-tile count RT.
+// The route tiles of a group are unrolled and software pipelined as the
+// encode's shift-free tiles, with the key projection of the next group spread
+// over them.  The decoded tokens of every group are kept (as MFMA operands)
+// and the merge O^T = W_O^T Y^T runs after the last group, one 32-channel
+// output block at a time, so the merge accumulators never share the register
+// budget with the route tiles.  Same LDS layout and stages as
+// k_decode2<..., RES = true>.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int KSC, int RT>
 __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedParams p) {
@@ -1380,7 +1382,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
   constexpr int NT = RT * HPG;      // route tiles per group
   constexpr int NP = GB * KSC;      // projection MFMAs per group
   constexpr int NM = CB * KPG;      // merge MFMAs per group
-  static_assert(C <= 128, "per-group merge accumulators are sized for C <= 128");
+  static_assert(C <= 128, "the decoded tokens of every group are kept in registers");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int Mp = p.Mp, QH = Mp * D;
   const int ZH = (int)z_frag_elems_per_head(Mp, D);
@@ -1410,15 +1412,14 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
   const uint32_t zlane = konst ? (uint32_t)((reinterpret_cast<char*>(cst) - smem) + (c == 16 ? 0 : 8 * sizeof(T)))
                                : (uint32_t)((WELEMS + WOE + HPG * QH + (g * ZC + c) * 8) * sizeof(T));
 
-  f32x16 o[CB];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[cb][e] = 0.f;
   f32x16 ka[GB];
-  F yprev[KPG];
+  // decoded tokens of the finished groups, oldest first (a shift register:
+  // after the last group entry hg holds group hg)
+  F yall[HG][KPG];
 #pragma unroll
-  for (int j = 0; j < KPG; ++j) yprev[j] = zero_frag<T>();
+  for (int u = 0; u < HG; ++u)
+#pragma unroll
+    for (int j = 0; j < KPG; ++j) yall[u][j] = zero_frag<T>();
   // k-th projection MFMA of the group whose stage starts at byte `so`
   auto proj_mfma = [&](int so, int k) __attribute__((always_inline)) {
     const int cb = k / KSC, ks = k % KSC;
@@ -1428,12 +1429,6 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
       for (int e = 0; e < 16; ++e) ka[cb][e] = 0.f;
     }
     mma(ka[cb], load_frag(wk + ((cb * KSC + ks) * 64 + lane) * 8), xf[ks]);
-  };
-  // k-th merge MFMA of the group whose stage starts at byte `so` (operands yprev)
-  auto merge_mfma = [&](int so, int k) __attribute__((always_inline)) {
-    const int cb = k / KPG, j = k % KPG;
-    const T* wo = reinterpret_cast<const T*>(smem + so) + WELEMS;
-    mma(o[cb], load_frag(wo + ((cb * KPG + j) * 64 + lane) * 8), yprev[j]);
   };
   auto route_norm = [&](int so, int hh) __attribute__((always_inline)) {
     const float* qn = reinterpret_cast<const float*>(smem + so + (WELEMS + WOE + HPG * (QH + ZH)) * sizeof(T));
@@ -1470,7 +1465,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
     }
     const bool fast = uniform(halfmax_sum_nonneg(ksq) * qsq <= p.fast_lim);
     // the next group's stage (the last group projects its own again: unused)
-    const int so_next = min(hg + 1, HG - 1) * SB, so_prev = max(hg - 1, 0) * SB;
+    const int so_next = min(hg + 1, HG - 1) * SB;
 
     f32x16 acc[HPG][RB];
     float m[HPG], ls[HPG];
@@ -1483,15 +1478,25 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[hh][rb][e] = 0.f;
     }
-    auto score = [&](int n) __attribute__((always_inline)) {
+    auto ld_q = [&](int n, F (&qv)[KS]) __attribute__((always_inline)) {
       const int rt = n / HPG, hh = n % HPG;
+#pragma unroll
+      for (int js = 0; js < KS; ++js)
+        qv[js] = load_frag(st + WELEMS + WOE + hh * QH + ((rt * KS + js) * 64 + lane) * 8);
+    };
+    auto score_q = [&](int n, const F (&qv)[KS]) __attribute__((always_inline)) {
+      const int hh = n % HPG;
       f32x16 sc;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[e] = 0.f;
 #pragma unroll
-      for (int js = 0; js < KS; ++js)
-        mma(sc, load_frag(st + WELEMS + WOE + hh * QH + ((rt * KS + js) * 64 + lane) * 8), kf[hh][js]);
+      for (int js = 0; js < KS; ++js) mma(sc, qv[js], kf[hh][js]);
       return sc;
+    };
+    auto score = [&](int n) __attribute__((always_inline)) {
+      F qv[KS];
+      ld_q(n, qv);
+      return score_q(n, qv);
     };
     auto zfrags = [&](int n, F (&zv)[2][RB]) __attribute__((always_inline)) {
       const int rt = n / HPG, hh = n % HPG;
@@ -1502,15 +1507,105 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
         for (int rb = 0; rb < RB; ++rb)
           zv[hf][rb] = *reinterpret_cast<const F*>(smem + base + zstep * ((rt * 2 + hf) * RB + rb));
     };
-    // the matrix work spread after tile n (no branches: before the first
-    // group's routes yprev is zero, so its merge adds nothing)
+    // the next group's key projection, spread after the route tiles
+    constexpr int PK = (NP + NT - 1) / NT;  // projection k-steps per tile (at most)
     auto hooks = [&](int n) __attribute__((always_inline)) {
 #pragma unroll
       for (int k = n * NP / NT; k < (n + 1) * NP / NT; ++k) proj_mfma(so_next, k);
-#pragma unroll
-      for (int k = n * NM / NT; k < (n + 1) * NM / NT; ++k) merge_mfma(so_prev, k);
     };
-    if (fast) {
+    if (fast && !partial) {
+      // Software pipelined as the encode's shift-free tiles.  Per tile n:
+      //   0: LDS reads (route keys of tile n + 2, latents of tile n - 1,
+      //      projection weights of tile n); 2^s of scores 0..3
+      //   1: value MFMAs of tile n - 1, routes 0..15; 2^s 4..7; pack P 0..7
+      //   2: projection MFMAs (next group); 2^s 8..11
+      //   3: value MFMAs of tile n - 1, routes 16..31; 2^s 12..15; pack P 8..15
+      //   4: score MFMA of tile n + 1 (into this tile's score registers)
+      F qc[KS], qn[KS], zp[2][RB], pp[2], wp[PK];
+      ld_q(0, qc);
+      f32x16 cur = score_q(0, qc);
+      if (NT > 1) ld_q(1, qn);
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int hh = n % HPG, hp = (n + HPG - 1) % HPG;
+        // phase 0
+        __builtin_amdgcn_sched_barrier(0);
+        if (n > 0) zfrags(n - 1, zp);
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+          const int k = n * NP / NT + u;
+          if (k < (n + 1) * NP / NT) wp[u] = load_frag(reinterpret_cast<const T*>(smem + so_next) + (k * 64 + lane) * 8);
+        }
+        if (n + 2 < NT) ld_q(n + 2, qc);  // qc is free
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        // phase 1
+        __builtin_amdgcn_sched_barrier(0);
+        if (n > 0) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) mma(acc[hp][rb], zp[0][rb], pp[0]);
+        }
+#pragma unroll
+        for (int e = 4; e < 8; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        F p0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p0[e] = from_f32<T>(cur[e]);
+        // phase 2
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+          const int k = n * NP / NT + u;
+          if (k < (n + 1) * NP / NT) {
+            const int cb = k / KSC, ks = k % KSC;
+            if (ks == 0) {
+#pragma unroll
+              for (int e = 0; e < 16; ++e) ka[cb][e] = 0.f;
+            }
+            mma(ka[cb], wp[u], xf[ks]);
+          }
+        }
+#pragma unroll
+        for (int e = 8; e < 12; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        if (!ONES_ROW) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) ls[hh] += cur[e];
+        }
+        // phase 3
+        __builtin_amdgcn_sched_barrier(0);
+        if (n > 0) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) mma(acc[hp][rb], zp[1][rb], pp[1]);
+        }
+#pragma unroll
+        for (int e = 12; e < 16; ++e) cur[e] = __builtin_amdgcn_exp2f(cur[e]);
+        F p1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p1[e] = from_f32<T>(cur[8 + e]);
+        if (!ONES_ROW) {
+#pragma unroll
+          for (int e = 8; e < 16; ++e) ls[hh] += cur[e];
+        }
+        // phase 4
+        __builtin_amdgcn_sched_barrier(0);
+        if (n + 1 < NT) cur = score_q(n + 1, qn);
+        pp[0] = p0;
+        pp[1] = p1;
+        if (n + 1 < NT) {
+#pragma unroll
+          for (int js = 0; js < KS; ++js) qn[js] = qc[js];
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      zfrags(NT - 1, zp);
+      {
+        constexpr int hl = (NT - 1) % HPG;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          mma(acc[hl][rb], zp[0][rb], pp[0]);
+          mma(acc[hl][rb], zp[1][rb], pp[1]);
+        }
+      }
+    } else if (fast) {
       f32x16 cur = score(0);
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
@@ -1539,7 +1634,11 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 #pragma unroll
       for (int n = 0; n < NT; ++n) hooks(n);
     }
-    // this group's decoded tokens become the merge operands of the next step
+    // this group's decoded tokens join the merge operands
+#pragma unroll
+    for (int u = 0; u + 1 < HG; ++u)
+#pragma unroll
+      for (int j = 0; j < KPG; ++j) yall[u][j] = yall[u + 1][j];
 #pragma unroll
     for (int hh = 0; hh < HPG; ++hh) {
       const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane));
@@ -1547,7 +1646,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
-          if (rb * 32 + 16 * hf < D) yprev[hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
+          if (rb * 32 + 16 * hf < D) yall[HG - 1][hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
       if (p.y && xok) {
         T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + (hg * HPG + hh) * D;
         constexpr int NQ4 = ONES_ROW ? 2 : 4;
@@ -1560,17 +1659,22 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
       }
     }
   }
-  // the last group's merge
+  // merge: output block cb of O^T = sum over the groups of W_O^T rows x Y^T
 #pragma unroll
-  for (int k = 0; k < NM; ++k) merge_mfma((HG - 1) * SB, k);
-
-  if (xok) {
+  for (int cb = 0; cb < CB; ++cb) {
+    f32x16 oc;
 #pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
+    for (int e = 0; e < 16; ++e) oc[e] = 0.f;
+#pragma unroll
+    for (int u = 0; u < HG; ++u) {
+      const T* wo = reinterpret_cast<const T*>(smem + u * SB) + WELEMS;
+#pragma unroll
+      for (int j = 0; j < KPG; ++j) mma(oc, load_frag(wo + ((cb * KPG + j) * 64 + lane) * 8), yall[u][j]);
+    }
+    if (xok) {
       T* op = (T*)p.o + ((int64_t)b * p.N + xrow) * C + 32 * cb;
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        store4(op + 8 * q + 4 * g, o[cb][4 * q], o[cb][4 * q + 1], o[cb][4 * q + 2], o[cb][4 * q + 3]);
+      for (int q = 0; q < 4; ++q) store4(op + 8 * q + 4 * g, oc[4 * q], oc[4 * q + 1], oc[4 * q + 2], oc[4 * q + 3]);
     }
   }
 }
