@@ -1381,7 +1381,6 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
   constexpr int ZC = D < 32 ? D : 32;
   constexpr int NT = RT * HPG;      // route tiles per group
   constexpr int NP = GB * KSC;      // projection MFMAs per group
-  constexpr int NM = CB * KPG;      // merge MFMAs per group
   static_assert(C <= 128, "the decoded tokens of every group are kept in registers");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int Mp = p.Mp, QH = Mp * D;
