@@ -1394,15 +1394,15 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
   const int xrow = (blockIdx.x % nblk) * TOK + wave * 32 + c;
   const bool xok = xrow < p.N;
 
-  // X and the stages of the first two groups first: group hg reads stage
-  // hg + 1 too (the key weights of the next group's projection), so stage
-  // hg + 1 is in LDS before group hg starts, and stage hg + 2 is issued then
+  // X and every stage at once (group hg also reads stage hg + 1: the key
+  // weights of the next group's projection); one wait, and no barrier inside
+  // the group loop, where the waves drift apart by up to a microsecond
   F xf[KSC];
 #pragma unroll
   for (int ks = 0; ks < KSC; ++ks)
     xf[ks] = load_frag((const T*)p.x + ((int64_t)b * p.N + min(xrow, p.N - 1)) * C + 16 * ks + 8 * g);
-  dec2_stage_issue<T, D, KSC>(p, smem, b, 0);
-  if (HG > 1) dec2_stage_issue<T, D, KSC>(p, smem + SB, b, 1);
+#pragma unroll
+  for (int s0 = 0; s0 < HG; ++s0) dec2_stage_issue<T, D, KSC>(p, smem + s0 * SB, b, s0);
   if (ONES_ROW && threadIdx.x < 2) store_frag<T>(cst + 8 * threadIdx.x, threadIdx.x == 0 ? fill_frag<T>(1.f) : zero_frag<T>());
   lds_wait_barrier();
 
@@ -1441,8 +1441,6 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 
   const bool partial = p.M < 32 * RT;  // the last route tile is partial
   for (int hg = 0; hg < HG; ++hg) {
-    if (hg > 0 && hg + 1 < HG) lds_wait_barrier();  // stage hg + 1 is in
-    if (hg + 2 < HG) dec2_stage_issue<T, D, KSC>(p, smem + (hg + 2) * SB, b, hg + 2);
     const int so = hg * SB;
     const T* st = reinterpret_cast<const T*>(smem + so);
     F kf[HPG][KS];
