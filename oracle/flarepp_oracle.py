@@ -1,4 +1,4 @@
-"""Float64 CPU oracle for the FLARE++ mixer forward.
+"""Float64 CPU oracle for the FLARE++ mixer forward and backward.
 
 TEST INFRASTRUCTURE ONLY.  This module is the correctness reference that the
 HIP path is compared against.  Only the tests, the package's ``smoke()`` and
@@ -22,6 +22,15 @@ It computes the plain definitions, in float64, in the paper's order:
                   Eqs. (24)-(28), including the empty-row convention).
 * ``materialised_operator`` W_eff = W_dec W_enc per head (Sec. 3.1, Eq. (6);
                   Sec. 3.2, Eq. (12)), for small N only.
+* ``sdpa_backward`` the gradient of one SDPA call from its global output and
+                  log-normaliser (App. A.5): P = exp(s S - L), c = <dO, O>
+                  per row, dV = P^T dO, dS = P (dO V^T - c), dK = s dS^T Q,
+                  dQ = s dS K.
+* ``mixer_backward`` the reverse pass of the whole mixer (App. A.5): W_O and
+                  the merge, the decode (call 3), the physical-value encode
+                  (call 2), the summed query gradient through the query
+                  synthesis (call 1), the seeds (summed over the batch) and
+                  the four projections.
 
 Readings of points the paper leaves open (all fixed here, in the same way as
 in the input generator):
@@ -59,6 +68,9 @@ __all__ = [
     "partial_encode",
     "materialised_operator",
     "merge_heads",
+    "split_heads",
+    "sdpa_backward",
+    "mixer_backward",
 ]
 
 # Key chunk for the two-pass softmax and query chunk for independent rows;
@@ -91,6 +103,12 @@ def merge_heads(Yh: np.ndarray) -> np.ndarray:
     """Concatenate heads: [B, H, N, D] -> [B, N, H*D] (Sec. 3.1, after Eq. (2))."""
     B, H, N, D = Yh.shape
     return Yh.transpose(0, 2, 1, 3).reshape(B, N, H * D).copy()
+
+
+def split_heads(Y: np.ndarray, H: int) -> np.ndarray:
+    """Inverse of ``merge_heads``: [B, N, H*D] -> [B, H, N, D]."""
+    B, N, C = Y.shape
+    return _f64(Y).reshape(B, N, H, C // H).transpose(0, 2, 1, 3).copy()
 
 
 def sdpa(Q: np.ndarray, K: np.ndarray, V: np.ndarray,
@@ -238,3 +256,95 @@ def materialised_operator(X, Wk, Wv, Wkt, Wvt, seeds, H: int) -> Dict[str, np.nd
     W_enc = softmax_last(S)
     W_dec = softmax_last(np.swapaxes(S, -1, -2))  # [B,H,N,M]
     return {"W_enc": W_enc, "W_dec": W_dec, "W_eff": W_dec @ W_enc, "V": V, "Q": Q}
+
+
+def sdpa_backward(Q, K, V, O, L, dO, scale: float | None = None) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Gradient of ``O = SDPA(Q, K, V)`` (softmax over the keys) from the
+    global output O and log-normaliser L of the forward (App. A.5).
+
+    Q: [..., Nq, D]; K: [..., Nk, D]; V: [..., Nk, Dv]; O, dO: [..., Nq, Dv];
+    L: [..., Nq].  Leading dimensions broadcast; every gradient comes back
+    with the broadcast leading shape (a caller whose operand was shared over
+    a dimension sums over it).  With P = exp(s Q K^T - L) and c = <dO, O>
+    over the value dimension:
+
+        dV = P^T dO,   dS = P * (dO V^T - c),   dK = s dS^T Q,   dQ = s dS K.
+
+    The key axis is walked in chunks; every chunk reads the global L and c,
+    so a chunk's dK, dV are final and its dQ share is a plain sum.
+    Returns ``(dQ, dK, dV)``.
+    """
+    Q, K, V, O, L, dO = (_f64(a) for a in (Q, K, V, O, L, dO))
+    D = Q.shape[-1]
+    s = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    lead = np.broadcast_shapes(Q.shape[:-2], K.shape[:-2], V.shape[:-2], O.shape[:-2], dO.shape[:-2])
+    Nq, Nk = Q.shape[-2], K.shape[-2]
+    Q = np.broadcast_to(Q, lead + Q.shape[-2:])
+    K = np.broadcast_to(K, lead + K.shape[-2:])
+    V = np.broadcast_to(V, lead + V.shape[-2:])
+    c = (dO * O).sum(axis=-1)  # [..., Nq]
+    dQ = np.zeros(lead + (Nq, D))
+    dK = np.zeros(lead + (Nk, D))
+    dV = np.zeros(lead + (Nk, V.shape[-1]))
+    for k0 in range(0, Nk, _KEY_CHUNK):
+        k1 = min(Nk, k0 + _KEY_CHUNK)
+        Kc, Vc = K[..., k0:k1, :], V[..., k0:k1, :]
+        P = np.exp(s * (Q @ np.swapaxes(Kc, -1, -2)) - L[..., None])  # [..., Nq, nk]
+        dV[..., k0:k1, :] = np.swapaxes(P, -1, -2) @ dO
+        dS = P * (dO @ np.swapaxes(Vc, -1, -2) - c[..., None])
+        dK[..., k0:k1, :] = s * (np.swapaxes(dS, -1, -2) @ Q)
+        dQ += s * (dS @ Kc)
+    return dQ, dK, dV
+
+
+def mixer_backward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int, dO) -> Dict[str, np.ndarray]:
+    """Reverse pass of the FLARE++ mixer (App. A.5) for the output gradient
+    dO [B, N, C].
+
+    Runs the forward (``mixer_forward``) for the operands and the global
+    log-normalisers, then, in reverse order of the forward:
+
+    * merge: dW_O = Y^T dO (summed over batch and tokens), dY = dO W_O^T;
+    * call 3 (decode; queries K, keys Q, values Z): ``sdpa_backward`` gives
+      the token-key gradient and the decoder's share of dQ and dZ;
+    * call 2 (encode; queries Q, keys K, values V) with the summed dZ gives
+      the encoder's share of dQ and the local dK, dV;
+    * call 1 (query synthesis; seeds shared over the batch, keys K~, values
+      V~) with dQ = decoder share + encoder share gives d(seeds), summed over
+      the batch, and the local dK~, dV~;
+    * the projections: dX = sum_j dG_j W_j^T, dW_j = X^T dG_j over the four
+      projected tensors (heads merged back to channels).
+
+    Returns the parameter and input gradients ``dX, dWk, dWv, dWkt, dWvt,
+    dWo, dseeds`` and the intermediates ``dY, dZ, dQ, dQ3, dK, dV, dKt, dVt``
+    ([B, H, *, D] for the per-head ones; dY is [B, N, C]).
+    """
+    X = _f64(X)
+    dO = _f64(dO)
+    f = mixer_forward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, H)
+    Q, Z, K, V, Kt, Vt = f["Q"], f["Z"], f["K"], f["V"], f["Kt"], f["Vt"]
+    B, N, C = X.shape
+    # merge
+    dWo = np.einsum("bni,bno->io", f["Y"], dO)
+    dYh = split_heads(dO @ _f64(Wo).T, H)
+    # call 3: the decode's own log-normaliser (per token)
+    Yh, L3 = sdpa(K, Q, Z)
+    dK3, dQ3, dZ = sdpa_backward(K, Q, Z, Yh, L3, dYh)
+    # call 2
+    dQ2, dK2, dV = sdpa_backward(Q, K, V, Z, f["L2"], dZ)
+    dQ = dQ3 + dQ2
+    dK = dK3 + dK2
+    # call 1: the seeds are shared over the batch
+    dS1, dKt, dVt = sdpa_backward(_f64(seeds)[None], Kt, Vt, Q, f["L1"], dQ)
+    dseeds = dS1.sum(axis=0)
+    # projections
+    grads = {}
+    dX = np.zeros_like(X)
+    for name, W, G in (("dWk", Wk, dK), ("dWv", Wv, dV), ("dWkt", Wkt, dKt), ("dWvt", Wvt, dVt)):
+        Gm = merge_heads(G)  # [B, N, C]
+        dX += Gm @ _f64(W).T
+        grads[name] = np.einsum("bni,bno->io", X, Gm)
+    out = {"dX": dX, "dWo": dWo, "dseeds": dseeds, "dY": merge_heads(dYh), "dZ": dZ, "dQ": dQ,
+           "dQ3": dQ3, "dK": dK, "dV": dV, "dKt": dKt, "dVt": dVt}
+    out.update(grads)
+    return out

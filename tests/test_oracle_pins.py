@@ -451,3 +451,128 @@ def test_lse_outputs_match_bruteforce():
     for h in range(w.H):
         _, L = _brute_sdpa(d["seeds"][h].astype(np.float64), Kt[0, h], Kt[0, h])
         np.testing.assert_allclose(r["L1"][0, h], L, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# backward (App. A.5)
+# ---------------------------------------------------------------------------
+
+def _library_mixer_grads(d, w, dO):
+    """Gradients of <O, dO> through three library SDPA calls, by autograd in
+    float64 (independent of the oracle's explicit backward)."""
+    t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64)).clone().requires_grad_(True)
+    X, Wk, Wv, Wkt, Wvt, Wo, seeds = (t(d[k]) for k in ("X", "Wk", "Wv", "Wkt", "Wvt", "Wo", "seeds"))
+    B, N, C, H, D = w.B, w.N, w.C, w.H, w.D
+
+    def heads(W):
+        return (X @ W).view(B, N, H, D).permute(0, 2, 1, 3)
+
+    sd = torch.nn.functional.scaled_dot_product_attention
+    K, V, Kt, Vt = heads(Wk), heads(Wv), heads(Wkt), heads(Wvt)
+    Q = sd(seeds.unsqueeze(0).expand(B, -1, -1, -1), Kt, Vt)
+    Z = sd(Q, K, V)
+    Y = sd(K, Q, Z).permute(0, 2, 1, 3).reshape(B, N, C)
+    O = Y @ Wo
+    (O * torch.from_numpy(dO)).sum().backward()
+    return {"dX": X.grad, "dWk": Wk.grad, "dWv": Wv.grad, "dWkt": Wkt.grad, "dWvt": Wvt.grad,
+            "dWo": Wo.grad, "dseeds": seeds.grad}
+
+
+@pytest.mark.parametrize("seed,seed_scale", [(11, 1.0), (12, 8.0)])
+def test_backward_matches_library_autograd(seed, seed_scale):
+    w, d = _small(seed=seed, seed_scale=seed_scale)
+    dO = _rng(seed + 100).standard_normal((w.B, w.N, w.C))
+    r = orc.mixer_backward(*_args(d), w.H, dO)
+    ref = _library_mixer_grads(d, w, dO)
+    for k, v in ref.items():
+        v = v.numpy()
+        assert np.abs(r[k] - v).max() <= 1e-10 * max(1.0, np.abs(v).max()), k
+
+
+def test_backward_directional_finite_difference():
+    # <grad, u> against the central difference of <O(theta + e u), dO>
+    w, d = _small(seed=13, seed_scale=4.0)
+    rng = _rng(14)
+    dO = rng.standard_normal((w.B, w.N, w.C))
+    r = orc.mixer_backward(*_args(d), w.H, dO)
+    keys = ("X", "Wk", "Wv", "Wkt", "Wvt", "Wo", "seeds")
+    u = {k: rng.standard_normal(np.shape(d[k])) for k in keys}
+    eps = 1e-5
+
+    def f(sign):
+        a = {k: np.asarray(d[k], dtype=np.float64) + sign * eps * u[k] for k in keys}
+        return float((orc.mixer_forward(*(a[k] for k in keys), w.H)["O"] * dO).sum())
+
+    fd = (f(1.0) - f(-1.0)) / (2 * eps)
+    an = sum(float((r["d" + k] * u[k]).sum()) for k in keys)
+    assert abs(fd - an) <= 1e-7 * max(1.0, abs(an)), (fd, an)
+
+
+def test_backward_single_token_closed_form():
+    # N = 1: every softmax over tokens has one key, Q and Z are that token's
+    # V~ and V, and O = X W_V W_O whatever the keys: the key, tilde and seed
+    # gradients vanish and the rest is the two-GEMM chain rule
+    w, d = _small(seed=15, N=1)
+    dO = _rng(16).standard_normal((w.B, 1, w.C))
+    r = orc.mixer_backward(*_args(d), w.H, dO)
+    X, Wv, Wo = (np.asarray(d[k], dtype=np.float64) for k in ("X", "Wv", "Wo"))
+    G = dO @ Wo.T
+    np.testing.assert_allclose(r["dX"], G @ Wv.T, atol=1e-12)
+    np.testing.assert_allclose(r["dWv"], np.einsum("bni,bno->io", X, G), atol=1e-12)
+    np.testing.assert_allclose(r["dWo"], np.einsum("bni,bno->io", X @ Wv, dO), atol=1e-12)
+    for k in ("dWk", "dWkt", "dWvt", "dseeds"):
+        assert np.abs(r[k]).max() <= 1e-12, k
+
+
+def _sdpa_case(seed, lead=(2, 3), Nq=5, Nk=7, D=4, Dv=3, scale=2.0):
+    g = _rng(seed)
+    Q = g.standard_normal(lead + (Nq, D)) * scale
+    K = g.standard_normal(lead + (Nk, D))
+    V = g.standard_normal(lead + (Nk, Dv))
+    dO = g.standard_normal(lead + (Nq, Dv))
+    O, L = orc.sdpa(Q, K, V)
+    return Q, K, V, O, L, dO
+
+
+def test_sdpa_backward_bruteforce_loops():
+    # every gradient element from its scalar definition, summed with fsum
+    Q, K, V, O, L, dO = _sdpa_case(21, lead=(), Nq=3, Nk=4, D=2, Dv=2)
+    dQ, dK, dV = orc.sdpa_backward(Q, K, V, O, L, dO)
+    s = 1.0 / math.sqrt(2)
+    Nq, Nk = 3, 4
+    P = [[math.exp(s * math.fsum(Q[i, t] * K[j, t] for t in range(2)) - L[i]) for j in range(Nk)] for i in range(Nq)]
+    dP = [[math.fsum(dO[i, t] * V[j, t] for t in range(2)) for j in range(Nk)] for i in range(Nq)]
+    c = [math.fsum(P[i][j] * dP[i][j] for j in range(Nk)) for i in range(Nq)]
+    dS = [[P[i][j] * (dP[i][j] - c[i]) for j in range(Nk)] for i in range(Nq)]
+    for j in range(Nk):
+        for t in range(2):
+            assert abs(dV[j, t] - math.fsum(P[i][j] * dO[i, t] for i in range(Nq))) < 1e-13
+            assert abs(dK[j, t] - s * math.fsum(dS[i][j] * Q[i, t] for i in range(Nq))) < 1e-13
+    for i in range(Nq):
+        for t in range(2):
+            assert abs(dQ[i, t] - s * math.fsum(dS[i][j] * K[j, t] for j in range(Nk))) < 1e-13
+
+
+def test_sdpa_backward_invariants():
+    Q, K, V, O, L, dO = _sdpa_case(22)
+    dQ, dK, dV = orc.sdpa_backward(Q, K, V, O, L, dO)
+    # adding one vector to every key shifts each query's scores by a
+    # constant: the key gradients sum to zero
+    assert np.abs(dK.sum(axis=-2)).max() < 1e-12
+    # the softmax weights of a query sum to one: the value gradients sum to
+    # the output gradients
+    np.testing.assert_allclose(dV.sum(axis=-2), dO.sum(axis=-2), atol=1e-12)
+    # constant values make the output independent of the scores
+    Vc = np.ones_like(V) * 0.7
+    Oc, Lc = orc.sdpa(Q, K, Vc)
+    dQc, dKc, _ = orc.sdpa_backward(Q, K, Vc, Oc, Lc, dO)
+    assert np.abs(dQc).max() < 1e-12 and np.abs(dKc).max() < 1e-12
+
+
+def test_sdpa_backward_chunked_key_axis(monkeypatch):
+    Q, K, V, O, L, dO = _sdpa_case(23, Nk=50)
+    a = orc.sdpa_backward(Q, K, V, O, L, dO)
+    monkeypatch.setattr(orc, "_KEY_CHUNK", 7)
+    b = orc.sdpa_backward(Q, K, V, O, L, dO)
+    for x, y in zip(a, b):
+        np.testing.assert_allclose(x, y, atol=1e-13)
