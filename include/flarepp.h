@@ -1,6 +1,6 @@
 /*
- * flarepp.h -- C ABI of libflarepp.so, the FLARE++ mixer forward on AMD
- * MI355X (gfx950).
+ * flarepp.h -- C ABI of libflarepp.so, the FLARE++ mixer forward and
+ * backward on AMD MI355X (gfx950).
  *
  * The operations follow "FLARE++: Low-rank attention with dynamic attention
  * routing" (arXiv 2608.11519):
@@ -182,6 +182,54 @@ FLAREPP_API int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int
                                             const void* Wv, const void* Wo, const void* queries,
                                             void* O, float* Z_out, void* Y_out, void* ws,
                                             size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Mixer backward (App. A.5): the gradients of the scalar <O, dO> with respect
+ * to every input of flarepp_mixer_forward, for the output gradient
+ * dO [B][N][C] (dtype).
+ *
+ * Each routing call is differentiated from its global output and
+ * log-normaliser: with P = exp(s S - L) and c = <dOut, Out> per query row,
+ * dV = P^T dOut, dS = P (dOut V^T - c), dK = s dS^T Q, dQ = s dS K.  The
+ * decode's query gradient (on the synthesised queries Q) is added to the
+ * physical-value encode's before the query-synthesis encode is
+ * differentiated; the seed gradient is summed over the batch.  The call runs
+ * the forward again itself (nothing needs to be kept from an earlier
+ * forward), then the merge, call 3, call 2, call 1 and the projections in
+ * reverse order.  Reductions over tokens and key chunks use fixed orders:
+ * the results are bitwise reproducible.
+ *
+ * Inputs as for flarepp_mixer_forward, plus dO.  Outputs, all fp32 and
+ * row-major, overwritten: dX [B][N][C]; dWk, dWv, dWkt, dWvt, dWo [C][C]
+ * (the layout of the weights, out = X W); dseeds [H][M][D].  With bf16 the
+ * MFMA operands (including the gradients fed to the next product) are
+ * rounded to bf16; accumulation is fp32.
+ *
+ * Sizes as for the mixer; in addition B*N <= 2^30, and a head's M x D route
+ * gradients (two of them, fp32) must fit in LDS: M <= 512 for D <= 32, M <=
+ * 256 for D = 64 (FLAREPP_ERR_UNSUPPORTED otherwise).  Workspace:
+ * flarepp_mixer_backward_workspace_bytes(...) bytes (0 for an invalid or
+ * unsupported shape); it holds the forward's K, V, K~, V~, Y and the fp32
+ * token gradients, about (4 * bytes(dtype) + 20) * B * N * C bytes.
+ * flarepp_mixer_backward_debug also writes the summed latent gradient dZ and
+ * the summed query gradient dQ (fp32 [B][H][M][D] each) when non-null.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_mixer_backward_workspace_bytes(int dtype, int64_t B, int64_t N,
+                                                          int64_t C, int64_t H, int64_t M);
+FLAREPP_API int flarepp_mixer_backward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                       int64_t M, const void* X, const void* Wk, const void* Wv,
+                                       const void* Wkt, const void* Wvt, const void* Wo,
+                                       const void* seeds, const void* dO, float* dX, float* dWk,
+                                       float* dWv, float* dWkt, float* dWvt, float* dWo,
+                                       float* dseeds, void* ws, size_t ws_bytes, void* stream);
+FLAREPP_API int flarepp_mixer_backward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                             int64_t M, const void* X, const void* Wk,
+                                             const void* Wv, const void* Wkt, const void* Wvt,
+                                             const void* Wo, const void* seeds, const void* dO,
+                                             float* dX, float* dWk, float* dWv, float* dWkt,
+                                             float* dWvt, float* dWo, float* dseeds, float* dZ_out,
+                                             float* dQ_out, void* ws, size_t ws_bytes,
+                                             void* stream);
 
 /* ---------------------------------------------------------------------------
  * Profiling variant of flarepp_mixer_forward for timing each stage on the

@@ -14,7 +14,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libflarepp.so")
-SOURCES = ["flarepp_kernels.hip", "flarepp_fused.hip", "flarepp_api.hip"]
+SOURCES = ["flarepp_kernels.hip", "flarepp_fused.hip", "flarepp_backward.hip", "flarepp_api.hip"]
 ARCH = "gfx950"
 
 

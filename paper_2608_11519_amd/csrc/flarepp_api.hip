@@ -8,6 +8,8 @@
 #include <cstdio>
 #include <cstdlib>
 #include <string>
+#include <type_traits>
+#include <algorithm>
 
 #include "../../include/flarepp.h"
 #include "flarepp_internal.hpp"
@@ -566,6 +568,298 @@ int route_impl(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M, 
   return ok();
 }
 
+
+// ---- backward (App. A.5) ----------------------------------------------------
+// Work split of the SDPA backward over the long axis (keys of an encode,
+// tokens of the decode): chunks per (b, h) and 32-position tiles per wave.
+struct BwdSplit {
+  int waves, R, tpw;
+};
+
+BwdSplit bwd_split(int64_t BH, int64_t Nl, int D, int Mp, bool dec, int elem_bytes) {
+  BwdSplit sp{};
+  sp.waves = flarepp::attn_bwd_waves(D, Mp, dec, elem_bytes);
+  if (sp.waves == 0) return sp;
+  const int64_t tiles = cdiv(Nl, 32);
+  int64_t R = std::max<int64_t>(1, std::min<int64_t>(cdiv(2048, BH), cdiv(tiles, sp.waves)));
+  const int64_t tpw = cdiv(tiles, R * sp.waves);
+  R = cdiv(tiles, tpw * sp.waves);
+  sp.R = (int)R;
+  sp.tpw = (int)tpw;
+  return sp;
+}
+
+// Split-K of the token reductions dW = X^T dG (K = B N tokens).
+int gemm_splits(int64_t T, int64_t C, int* kchunk) {
+  const int64_t tiles = cdiv(C, 64) * cdiv(C, 64);
+  int64_t splits = std::max<int64_t>(1, std::min<int64_t>(cdiv(T, 256), cdiv(1024, tiles)));
+  const int64_t kc = round_up(cdiv(T, splits), 32);
+  *kchunk = (int)kc;
+  return (int)cdiv(T, kc);
+}
+
+struct BwdWs {
+  void *wf[4], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *Y, *q_op, *z_op;
+  float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2;
+  float *dY, *dK, *dV, *dKt, *dVt, *dZf, *dQ3, *dQf, *c1, *c2, *pa, *pg, *gpart;
+  void *Qr, *Qt, *Zr, *dZr, *dZt, *dQr, *dQt, *Sr, *St;
+  BwdSplit dec, enc;
+  int splits, kchunk;
+  size_t bytes;
+};
+
+BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32), DB = cdiv(D, 32);
+  const size_t bs = dtype_bytes(dtype), f4 = sizeof(float);
+  const int64_t T = B * N, BH = B * H;
+  const EncPlan e = encode_plan(B, H, N, Mp, D);
+  Carver cv(base);
+  BwdWs w{};
+  for (int i = 0; i < 4; ++i) w.wf[i] = cv.take(bs * C * C);
+  w.seeds_op = cv.take(bs * H * Mp * D);
+  w.K = cv.take(bs * BH * N * D);
+  w.Kt = cv.take(bs * BH * N * D);
+  w.Vdm = cv.take(bs * BH * D * Np);
+  w.Vtdm = cv.take(bs * BH * D * Np);
+  w.Y = cv.take(bs * T * C);
+  w.q_op = cv.take(bs * BH * Mp * D);
+  w.z_op = cv.take(bs * BH * D * Mp);
+  w.part_ml = (float*)cv.take(f4 * e.nchunks * BH * Mp * 2);
+  w.part_acc = (float*)cv.take(f4 * e.nchunks * BH * Mp * D);
+  w.Qf = (float*)cv.take(f4 * BH * M * D);
+  w.Zf = (float*)cv.take(f4 * BH * M * D);
+  w.L1 = (float*)cv.take(f4 * BH * M);
+  w.L2 = (float*)cv.take(f4 * BH * M);
+  w.dY = (float*)cv.take(f4 * T * C);
+  w.dK = (float*)cv.take(f4 * T * C);
+  w.dV = (float*)cv.take(f4 * T * C);
+  w.dKt = (float*)cv.take(f4 * T * C);
+  w.dVt = (float*)cv.take(f4 * T * C);
+  w.dZf = (float*)cv.take(f4 * BH * M * D);
+  w.dQ3 = (float*)cv.take(f4 * BH * M * D);
+  w.dQf = (float*)cv.take(f4 * BH * M * D);
+  w.c1 = (float*)cv.take(f4 * BH * Mp);
+  w.c2 = (float*)cv.take(f4 * BH * Mp);
+  w.Qr = cv.take(bs * BH * Mp * D);
+  w.Qt = cv.take(bs * BH * Mp * 32 * DB);
+  w.Zr = cv.take(bs * BH * Mp * D);
+  w.dZr = cv.take(bs * BH * Mp * D);
+  w.dZt = cv.take(bs * BH * Mp * 32 * DB);
+  w.dQr = cv.take(bs * BH * Mp * D);
+  w.dQt = cv.take(bs * BH * Mp * 32 * DB);
+  w.Sr = cv.take(bs * H * Mp * D);
+  w.St = cv.take(bs * H * Mp * 32 * DB);
+  w.dec = bwd_split(BH, N, (int)D, (int)Mp, true, (int)bs);
+  w.enc = bwd_split(BH, N, (int)D, (int)Mp, false, (int)bs);
+  const int64_t R = std::max<int64_t>(std::max(w.dec.R, w.enc.R), 1);
+  w.pa = (float*)cv.take(f4 * BH * R * Mp * D);
+  w.pg = (float*)cv.take(f4 * BH * R * Mp * D);
+  w.splits = gemm_splits(T, C, &w.kchunk);
+  w.gpart = (float*)cv.take(f4 * w.splits * C * C);
+  w.bytes = cv.off;
+  return w;
+}
+
+int check_backward_shape(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  TRY(check_mixer_shape(dtype, B, N, C, H, M));
+  const int64_t D = C / H, Mp = round_up(M, 32);
+  const int bs = dtype_bytes(dtype);
+  if (flarepp::attn_bwd_waves((int)D, (int)Mp, true, bs) == 0)
+    return fail(FLAREPP_ERR_UNSUPPORTED, "the backward keeps M x D route gradients of a head in LDS: "
+                "M=%lld with D=%lld does not fit", (long long)M, (long long)D);
+  if (B * N > (int64_t(1) << 30)) return fail(FLAREPP_ERR_UNSUPPORTED, "B*N too large for the backward");
+  return FLAREPP_OK;
+}
+
+// The mixer's reverse pass: the forward again (unfused kernels, which keep
+// K, V, K~, V~, Y and the log-normalisers of both encodes), then the merge,
+// call 3, call 2, call 1 and the projections in reverse order.
+template <typename T>
+int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
+                  const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
+                  const void* seeds, const void* dO, float* dX, float* dWk, float* dWv, float* dWkt,
+                  float* dWvt, float* dWo, float* dseeds, float* dZ_out, float* dQ_out, void* ws,
+                  size_t ws_bytes, hipStream_t s) {
+  using namespace flarepp;
+  const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32), DB = cdiv(D, 32);
+  const int64_t NT = B * N, BH = B * H;
+  const BwdWs w = bwd_ws(ws, dtype, B, N, C, H, M);
+  if (ws_bytes < w.bytes)
+    return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
+  const float qscale = route_qscale(D);
+  const float sc = (float)(1.0 / std::sqrt((double)D));
+  const bool f32 = std::is_same<T, float>::value;
+
+  // ---- forward with its statistics ----
+  WeightFragParams wp{};
+  wp.C = (int)C;
+  const void* w_in[4] = {Wk, Wv, Wkt, Wvt};
+  for (int i = 0; i < 4; ++i) { wp.w[i] = w_in[i]; wp.out[i] = w.wf[i]; }
+  wp.nw = 4;
+  HIPTRY(launch_weight_frags<T>(wp, s));
+  RoutePrepParams sp{};
+  sp.src = seeds; sp.src_bstride = 0; sp.B = 1; sp.H = (int)H; sp.M = (int)M; sp.Mp = (int)Mp;
+  sp.D = (int)D; sp.qscale = qscale; sp.q_op = w.seeds_op; sp.z_op = nullptr;
+  HIPTRY((launch_route_prep<T, T>(sp, s)));
+  ProjParams pp{};
+  pp.x = X; pp.B = (int)B; pp.N = (int)N; pp.Np = (int)Np; pp.C = (int)C; pp.H = (int)H; pp.D = (int)D;
+  pp.nw = 4;
+  pp.wf[0] = w.wf[0]; pp.out[0] = w.K;    pp.layout[0] = kHeadsTokenMajor;
+  pp.wf[1] = w.wf[1]; pp.out[1] = w.Vdm;  pp.layout[1] = kHeadsDMajor;
+  pp.wf[2] = w.wf[2]; pp.out[2] = w.Kt;   pp.layout[2] = kHeadsTokenMajor;
+  pp.wf[3] = w.wf[3]; pp.out[3] = w.Vtdm; pp.layout[3] = kHeadsDMajor;
+  HIPTRY(launch_project<T>(pp, s));
+  const EncPlan e = encode_plan(B, H, N, Mp, D);
+  const int64_t tokHS = N * D, tokBS = H * N * D, dmHS = D * Np, dmBS = H * D * Np;
+  const int64_t rtHS = Mp * D, rtBS = H * Mp * D;
+  RouteParams r1 = encode_params(e, B, H, N, Mp, D);
+  r1.ka = w.Kt; r1.ka_sb = tokBS; r1.ka_sh = tokHS; r1.ka_rows = (int)N;
+  r1.va = w.Vtdm; r1.va_sb = dmBS; r1.va_sh = dmHS; r1.va_ld = (int)Np;
+  r1.qs = w.seeds_op; r1.qs_sb = 0; r1.qs_sh = rtHS; r1.qs_rows = (int)Mp;
+  r1.part_ml = w.part_ml; r1.part_acc = w.part_acc;
+  HIPTRY(launch_route<T>(r1, (int)D, false, s));
+  CombineParams c1{};
+  c1.part_ml = w.part_ml; c1.part_acc = w.part_acc; c1.BH = BH; c1.R = e.nchunks;
+  c1.M = (int)M; c1.Mp = (int)Mp; c1.D = (int)D; c1.qscale = qscale;
+  c1.out32 = w.Qf; c1.lse = w.L1; c1.q_op = w.q_op; c1.z_op = nullptr;
+  HIPTRY(launch_combine_par<T>(c1, s));
+  RouteParams r2 = r1;
+  r2.ka = w.K; r2.va = w.Vdm;
+  r2.qs = w.q_op; r2.qs_sb = rtBS; r2.qs_sh = rtHS; r2.qs_rows = (int)Mp;
+  HIPTRY(launch_route<T>(r2, (int)D, false, s));
+  CombineParams c2 = c1;
+  c2.out32 = w.Zf; c2.lse = w.L2; c2.q_op = nullptr; c2.z_op = w.z_op;
+  HIPTRY(launch_combine_par<T>(c2, s));
+  RouteParams r3 = decode_params(B, H, N, M, D);
+  r3.ka = w.q_op; r3.ka_sb = rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
+  r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;
+  r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
+  r3.y = w.Y; r3.y_sb = N * C; r3.y_row = C;
+  HIPTRY(launch_route<T>(r3, (int)D, true, s));
+
+  // ---- merge: dY = dO W_O^T, dW_O = Y^T dO ----
+  const int types_tt = kGemmTT;
+  GemmParams g{};
+  g.M = (int)NT; g.N = (int)C; g.K = (int)C; g.nseg = 1;
+  g.a[0] = dO; g.a_m = C; g.a_k = 1;
+  g.b[0] = Wo; g.b_k = 1; g.b_n = C;
+  g.kchunk = (int)round_up(C, 32); g.c = w.dY; g.ldc = C; g.split_stride = 0;
+  HIPTRY(launch_gemm<T>(g, types_tt, 1, s));
+  auto weight_grad = [&](const void* A, const void* G, int types, float* out) -> int {
+    GemmParams q{};
+    q.M = (int)C; q.N = (int)C; q.K = (int)NT; q.nseg = 1;
+    q.a[0] = A; q.a_m = 1; q.a_k = C;
+    q.b[0] = G; q.b_k = C; q.b_n = 1;
+    q.kchunk = w.kchunk; q.c = w.gpart; q.ldc = C; q.split_stride = C * C;
+    HIPTRY(launch_gemm<T>(q, types, w.splits, s));
+    HIPTRY(launch_sum_splits(w.gpart, out, C * C, w.splits, s));
+    return FLAREPP_OK;
+  };
+  TRY(weight_grad(w.Y, dO, types_tt, dWo));
+
+  // ---- call 3 (decode): queries K, keys Q, values Z ----
+  BwdPrepParams bp{};
+  bp.src = w.Qf; bp.src_is_f32 = 1; bp.dot = nullptr; bp.O = (int)BH; bp.M = (int)M; bp.Mp = (int)Mp;
+  bp.D = (int)D; bp.rows = w.Qr; bp.tfrag = w.Qt; bp.c = nullptr;
+  HIPTRY(launch_bwd_prep<T>(bp, s));
+  bp.src = w.Zf; bp.rows = w.Zr; bp.tfrag = nullptr;
+  HIPTRY(launch_bwd_prep<T>(bp, s));
+  const int64_t tfS = Mp * 32 * DB;  // elements per head of a transposed-fragment operand
+  AttnBwdParams a3{};
+  a3.B = (int)B; a3.H = (int)H; a3.Nl = (int)N; a3.M = (int)M; a3.Mp = (int)Mp;
+  a3.R = w.dec.R; a3.tpw = w.dec.tpw; a3.s = sc; a3.sl2 = sc * 1.4426950408889634f;
+  a3.ash = w.Qr; a3.ash_sb = rtBS; a3.ash_sh = rtHS;
+  a3.asht = w.Qt; a3.asht_sb = H * tfS; a3.asht_sh = tfS;
+  a3.gsh = w.Zr; a3.gsh_sb = rtBS; a3.gsh_sh = rtHS;
+  a3.blo = w.K; a3.blo_sb = tokBS; a3.blo_sh = tokHS; a3.blo_sn = D; a3.blo_sd = 1;
+  a3.glo = w.dY; a3.glo_sb = N * C; a3.glo_sh = D; a3.glo_sn = C; a3.glo_sd = 1;
+  a3.ylo = w.Y; a3.ylo_sb = N * C; a3.ylo_sh = D; a3.ylo_sn = C;
+  a3.dout_b = w.dK; a3.acc_b = 0;
+  a3.part_a = w.pa; a3.part_g = w.pg;
+  HIPTRY(launch_attn_bwd<T>(a3, (int)D, true, s));
+  BwdReduceParams rd{};
+  rd.P = 1; rd.O = (int)BH; rd.R = w.dec.R; rd.M = (int)M; rd.Mp = (int)Mp; rd.D = (int)D;
+  rd.part = w.pg; rd.base = nullptr; rd.out = dZ_out ? dZ_out : w.dZf;
+  HIPTRY(launch_bwd_reduce(rd, s));
+  float* dZf = rd.out;
+  rd.part = w.pa; rd.out = w.dQ3;
+  HIPTRY(launch_bwd_reduce(rd, s));
+
+  // ---- call 2 (encode): queries Q, keys K, values V; dOut = dZ ----
+  bp.src = dZf; bp.dot = w.Zf; bp.rows = w.dZr; bp.tfrag = w.dZt; bp.c = w.c2;
+  HIPTRY(launch_bwd_prep<T>(bp, s));
+  AttnBwdParams a2{};
+  a2.B = (int)B; a2.H = (int)H; a2.Nl = (int)N; a2.M = (int)M; a2.Mp = (int)Mp;
+  a2.R = w.enc.R; a2.tpw = w.enc.tpw; a2.s = sc; a2.sl2 = a3.sl2;
+  a2.ash = w.Qr; a2.ash_sb = rtBS; a2.ash_sh = rtHS;
+  a2.asht = w.Qt; a2.asht_sb = H * tfS; a2.asht_sh = tfS;
+  a2.gsh = w.dZr; a2.gsh_sb = rtBS; a2.gsh_sh = rtHS;
+  a2.gsht = w.dZt; a2.gsht_sb = H * tfS; a2.gsht_sh = tfS;
+  a2.lrow = w.L2; a2.crow = w.c2;
+  a2.blo = w.K; a2.blo_sb = tokBS; a2.blo_sh = tokHS; a2.blo_sn = D; a2.blo_sd = 1;
+  a2.glo = w.Vdm; a2.glo_sb = dmBS; a2.glo_sh = dmHS; a2.glo_sn = 1; a2.glo_sd = Np;
+  a2.dout_b = w.dK; a2.acc_b = 1; a2.dout_g = w.dV;
+  a2.part_a = w.pa;
+  HIPTRY(launch_attn_bwd<T>(a2, (int)D, false, s));
+  rd.R = w.enc.R; rd.part = w.pa; rd.base = w.dQ3; rd.out = dQ_out ? dQ_out : w.dQf;
+  HIPTRY(launch_bwd_reduce(rd, s));
+  float* dQf = rd.out;
+
+  // ---- call 1 (query synthesis): queries = seeds (shared), keys K~, values V~ ----
+  bp.src = dQf; bp.dot = w.Qf; bp.rows = w.dQr; bp.tfrag = w.dQt; bp.c = w.c1;
+  HIPTRY(launch_bwd_prep<T>(bp, s));
+  BwdPrepParams sp2{};
+  sp2.src = seeds; sp2.src_is_f32 = f32 ? 1 : 0; sp2.dot = nullptr; sp2.O = (int)H; sp2.M = (int)M;
+  sp2.Mp = (int)Mp; sp2.D = (int)D; sp2.rows = w.Sr; sp2.tfrag = w.St; sp2.c = nullptr;
+  HIPTRY(launch_bwd_prep<T>(sp2, s));
+  AttnBwdParams a1 = a2;
+  a1.ash = w.Sr; a1.ash_sb = 0; a1.ash_sh = rtHS;
+  a1.asht = w.St; a1.asht_sb = 0; a1.asht_sh = tfS;
+  a1.gsh = w.dQr; a1.gsht = w.dQt;
+  a1.lrow = w.L1; a1.crow = w.c1;
+  a1.blo = w.Kt; a1.glo = w.Vtdm;
+  a1.dout_b = w.dKt; a1.acc_b = 0; a1.dout_g = w.dVt;
+  HIPTRY(launch_attn_bwd<T>(a1, (int)D, false, s));
+  rd.P = (int)B; rd.O = (int)H; rd.R = w.enc.R; rd.part = w.pa; rd.base = nullptr; rd.out = dseeds;
+  HIPTRY(launch_bwd_reduce(rd, s));
+
+  // ---- projections: dX = sum_j dG_j W_j^T, dW_j = X^T dG_j ----
+  GemmParams gx{};
+  gx.M = (int)NT; gx.N = (int)C; gx.K = (int)C; gx.nseg = 4;
+  const float* G[4] = {w.dK, w.dV, w.dKt, w.dVt};
+  for (int j = 0; j < 4; ++j) { gx.a[j] = G[j]; gx.b[j] = w_in[j]; }
+  gx.a_m = C; gx.a_k = 1; gx.b_k = 1; gx.b_n = C;
+  gx.kchunk = (int)round_up(C, 32); gx.c = dX; gx.ldc = C; gx.split_stride = 0;
+  HIPTRY(launch_gemm<T>(gx, kGemmFT, 1, s));
+  float* dW[4] = {dWk, dWv, dWkt, dWvt};
+  for (int j = 0; j < 4; ++j) TRY(weight_grad(X, G[j], kGemmTF, dW[j]));
+  return ok();
+}
+
+int backward_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
+                   const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
+                   const void* seeds, const void* dO, float* dX, float* dWk, float* dWv, float* dWkt,
+                   float* dWvt, float* dWo, float* dseeds, float* dZ_out, float* dQ_out, void* ws,
+                   size_t ws_bytes, void* stream) {
+  TRY(check_backward_shape(dtype, B, N, C, H, M));
+  const void* in[] = {X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO};
+  const char* in_names[] = {"X", "Wk", "Wv", "Wkt", "Wvt", "Wo", "seeds", "dO"};
+  for (int i = 0; i < 8; ++i) TRY(check_ptr(in[i], in_names[i]));
+  const float* out[] = {dX, dWk, dWv, dWkt, dWvt, dWo, dseeds};
+  const char* out_names[] = {"dX", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds"};
+  for (int i = 0; i < 7; ++i) TRY(check_ptr(out[i], out_names[i]));
+  TRY(check_ptr(dZ_out, "dZ_out", true));
+  TRY(check_ptr(dQ_out, "dQ_out", true));
+  if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
+  TRY(check_ptr(ws, "ws"));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FLAREPP_F32)
+    return backward_impl<float>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt,
+                                dWvt, dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, s);
+  return backward_impl<__bf16>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt,
+                               dWvt, dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -720,6 +1014,31 @@ int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int6
                                 size_t ws_bytes, void* stream) {
   return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, nullptr, nullptr, Wo, queries, O, nullptr, Z_out,
                      Y_out, ws, ws_bytes, stream, nullptr, 0, 0, true);
+}
+
+size_t flarepp_mixer_backward_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                              int64_t M) {
+  if (check_backward_shape(dtype, B, N, C, H, M) != FLAREPP_OK) return 0;
+  return bwd_ws(nullptr, dtype, B, N, C, H, M).bytes;
+}
+
+int flarepp_mixer_backward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                           const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                           const void* Wvt, const void* Wo, const void* seeds, const void* dO,
+                           float* dX, float* dWk, float* dWv, float* dWkt, float* dWvt, float* dWo,
+                           float* dseeds, void* ws, size_t ws_bytes, void* stream) {
+  return backward_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt, dWvt,
+                        dWo, dseeds, nullptr, nullptr, ws, ws_bytes, stream);
+}
+
+int flarepp_mixer_backward_debug(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                 const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                                 const void* Wvt, const void* Wo, const void* seeds, const void* dO,
+                                 float* dX, float* dWk, float* dWv, float* dWkt, float* dWvt,
+                                 float* dWo, float* dseeds, float* dZ_out, float* dQ_out, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  return backward_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt, dWvt,
+                        dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

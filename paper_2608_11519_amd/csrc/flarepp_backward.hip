@@ -1,0 +1,473 @@
+// Backward of the FLARE++ mixer (App. A.5) on gfx950.
+//
+// * k_gemm: C = sum_seg A B on MFMA 32x32 tiles through LDS, for the
+//   projection and W_O gradients (dY = dO W_O^T, dW_O = Y^T dO,
+//   dX = sum_j dG_j W_j^T, dW_j = X^T dG_j).  Either operand may be fp32 (the
+//   gradients) and is rounded to the compute type on its way into LDS; the
+//   reductions over tokens are split over workgroups (split-K) and summed in
+//   a fixed order by k_sum_splits.
+// * k_attn_bwd: the SDPA backward of one routing call from its global output
+//   and log-normaliser, over a chunk of the long axis (keys of an encode,
+//   tokens of the decode).  Each wave owns 32 positions of the long axis and
+//   walks the route blocks; the long-side gradients stay in registers, the
+//   short-side (route) gradients are summed in the wave's LDS slot and, at
+//   the end, over the waves in a fixed order into the chunk's partial.
+// * k_bwd_reduce sums those partials over the chunks (and over the batch for
+//   the shared seeds) in a fixed order; k_bwd_prep lays out the route-side
+//   operands of the next call (rows, transposed fragments, c = <dOut, Out>).
+// No float atomics anywhere: every result is bitwise reproducible.
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "flarepp_device.hpp"
+#include "flarepp_internal.hpp"
+
+namespace flarepp {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ---------------------------------------------------------------------------
+// GEMM
+// ---------------------------------------------------------------------------
+constexpr int kGemmTile = 64, kGemmK = 32;
+// LDS row pitch (elements): 32 k values plus 16 bytes, so that fragment rows
+// start 16-byte aligned and neighbouring rows fall in different banks
+template <typename T> constexpr int gemm_pitch() { return kGemmK + 16 / (int)sizeof(T); }
+
+// One 64 x 32 operand tile into LDS as rows of k: row i, column k holds
+// X(row0 + i, k0 + k) where X(i, k) = x[i * s_i + k * s_k].  Each thread loads
+// 8 elements along whichever axis has unit stride, so neighbouring threads
+// read neighbouring addresses.
+template <typename T, typename TX>
+__device__ __forceinline__ void gemm_stage(T* dst, const TX* x, int64_t s_i, int64_t s_k, int row0, int nrows,
+                                           int k0, int kend) {
+  constexpr int PITCH = gemm_pitch<T>();
+  const int t = threadIdx.x;
+  int ii, kk, di, dk;
+  if (s_k == 1) {
+    ii = t >> 2; kk = (t & 3) * 8; di = 0; dk = 1;
+  } else {
+    kk = t >> 3; ii = (t & 7) * 8; di = 1; dk = 0;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = row0 + ii + j * di, k = k0 + kk + j * dk;
+    const float v = (i < nrows && k < kend) ? to_f32(x[(int64_t)i * s_i + (int64_t)k * s_k]) : 0.f;
+    dst[(ii + j * di) * PITCH + kk + j * dk] = from_f32<T>(v);
+  }
+}
+
+template <typename T, typename TA, typename TB>
+__global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
+  constexpr int PITCH = gemm_pitch<T>();
+  __shared__ __attribute__((aligned(16))) T As[kGemmTile * PITCH];
+  __shared__ __attribute__((aligned(16))) T Bs[kGemmTile * PITCH];
+  const int lane = lane_id(), wave = wave_id(), g = lane >> 5, c = lane & 31;
+  const int m0 = blockIdx.y * kGemmTile, n0 = blockIdx.x * kGemmTile;
+  const int kbeg = blockIdx.z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
+  const int mw = wave >> 1, nw = wave & 1;  // this wave's 32 x 32 quarter
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  for (int seg = 0; seg < p.nseg; ++seg) {
+    const TA* A = static_cast<const TA*>(p.a[seg]);
+    const TB* Bm = static_cast<const TB*>(p.b[seg]);
+    for (int k0 = kbeg; k0 < kend; k0 += kGemmK) {
+      gemm_stage<T>(As, A, p.a_m, p.a_k, m0, p.M, k0, kend);
+      gemm_stage<T>(Bs, Bm, p.b_n, p.b_k, n0, p.N, k0, kend);
+      __syncthreads();
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        mma(acc, load_frag(As + (32 * mw + c) * PITCH + 16 * ks + 8 * g),
+            load_frag(Bs + (32 * nw + c) * PITCH + 16 * ks + 8 * g));
+      __syncthreads();
+    }
+  }
+  float* out = p.c + (int64_t)blockIdx.z * p.split_stride;
+  const int n = n0 + 32 * nw + c;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int m = m0 + 32 * mw + acc_row(lane, r);
+    if (m < p.M && n < p.N) out[(int64_t)m * p.ldc + n] = acc[r];
+  }
+}
+
+__global__ __launch_bounds__(256) void k_sum_splits(const float* part, float* out, int64_t n, int splits) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + i];
+  out[i] = s;
+}
+
+// ---------------------------------------------------------------------------
+// SDPA backward over a chunk of the long axis
+// ---------------------------------------------------------------------------
+// LDS per wave: the short-side slot(s) [D][Mp + 4] fp32 (route index fastest,
+// padded so that the lanes' rows fall in different banks) and two transpose
+// tiles [32][32 + 16 bytes] of T.
+template <typename T> constexpr int tb_pitch() { return 32 + 16 / (int)sizeof(T); }
+size_t attn_bwd_wave_bytes(int D, int Mp, bool dec, int elem_bytes) {
+  const int tbp = 32 + 16 / elem_bytes;
+  return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (Mp + 4) + (size_t)2 * 32 * tbp * elem_bytes;
+}
+
+template <typename T, int D, bool DEC>
+__global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
+  using F = typename Frag<T>::type;
+  using TG = typename std::conditional<DEC, float, T>::type;
+  constexpr int KS = D / 16, DB = (D + 31) / 32, TBP = tb_pitch<T>();
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
+  const int W = blockDim.x >> 6;
+  const int bh = blockIdx.x / p.R, r = blockIdx.x % p.R;
+  const int b = bh / p.H, h = bh % p.H;
+  const int SP = p.Mp + 4, NS = p.Mp / 32;
+  const int slot_floats = (DEC ? 2 : 1) * D * SP;
+  float* slot_a = reinterpret_cast<float*>(smem) + wave * slot_floats;
+  float* slot_g = slot_a + D * SP;
+  T* tb = reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) + wave * 2 * 32 * TBP;
+  T* tb2 = tb + 32 * TBP;
+  for (int i = lane; i < slot_floats; i += 64) slot_a[i] = 0.f;
+
+  const T* ash = static_cast<const T*>(p.ash) + b * p.ash_sb + h * p.ash_sh;
+  const T* asht = static_cast<const T*>(p.asht) + b * p.asht_sb + h * p.asht_sh;
+  const T* gsh = static_cast<const T*>(p.gsh) + b * p.gsh_sb + h * p.gsh_sh;
+  const T* gsht = DEC ? nullptr : static_cast<const T*>(p.gsht) + b * p.gsht_sb + h * p.gsht_sh;
+  const T* blo = static_cast<const T*>(p.blo) + b * p.blo_sb + h * p.blo_sh;
+  const TG* glo = static_cast<const TG*>(p.glo) + b * p.glo_sb + h * p.glo_sh;
+  const float* lrow = DEC ? nullptr : p.lrow + (int64_t)bh * p.M;
+  const float* crow = DEC ? nullptr : p.crow + (int64_t)bh * p.Mp;
+
+  for (int i = 0; i < p.tpw; ++i) {
+    const int n0 = ((r * p.tpw + i) * W + wave) * 32;  // wave-uniform
+    if (n0 >= p.Nl) break;
+    const int n = n0 + c;
+    const bool nok = n < p.Nl;
+    const int nc = nok ? n : p.Nl - 1;
+    // long-side B operands of S (keys) and dP (values), one lane per position
+    F kb[KS], gb[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int d = 16 * ks + 8 * g + j;
+        kb[ks][j] = from_f32<T>(nok ? to_f32(blo[(int64_t)nc * p.blo_sn + (int64_t)d * p.blo_sd]) : 0.f);
+        gb[ks][j] = from_f32<T>(nok ? to_f32(glo[(int64_t)nc * p.glo_sn + (int64_t)d * p.glo_sd]) : 0.f);
+      }
+    // long-side B operands of the short-side products (k = position, n = d)
+    F kt[2][DB], gt[2][DB];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int nn = n0 + 16 * kk + 8 * g + j, d = 32 * db + c;
+          const bool ok = nn < p.Nl && d < D;
+          kt[kk][db][j] = from_f32<T>(ok ? to_f32(blo[(int64_t)nn * p.blo_sn + (int64_t)d * p.blo_sd]) : 0.f);
+          if (DEC) gt[kk][db][j] = from_f32<T>(ok ? to_f32(glo[(int64_t)nn * p.glo_sn + (int64_t)d * p.glo_sd]) : 0.f);
+        }
+    // decode: c = <dY_n, Y_n> over the head's channels, and the token's
+    // log-normaliser over the routes (log2 units), online over route blocks
+    float Ll = 0.f, cl = 0.f;
+    if constexpr (DEC) {
+      const T* y = static_cast<const T*>(p.ylo) + b * p.ylo_sb + h * p.ylo_sh;
+      float sacc = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int d = 16 * ks + 8 * g + j;
+          if (nok) sacc += glo[(int64_t)nc * p.glo_sn + (int64_t)d * p.glo_sd] * to_f32(y[(int64_t)nc * p.ylo_sn + d]);
+        }
+      cl = sacc + other_half(sacc);
+      float mx = -INFINITY, sm = 0.f;
+      for (int sb = 0; sb < NS; ++sb) {
+        f32x16 sc;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) mma(sc, load_frag(ash + (32 * sb + c) * D + 16 * ks + 8 * g), kb[ks]);
+        float tm = -INFINITY;
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr)
+          if (32 * sb + acc_row(lane, rr) < p.M) tm = fmaxf(tm, sc[rr] * p.sl2);
+        tm = fmaxf(tm, other_half(tm));
+        const float nm = fmaxf(mx, tm);
+        float ts = 0.f;
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr)
+          if (32 * sb + acc_row(lane, rr) < p.M) ts += exp2f(sc[rr] * p.sl2 - nm);
+        ts += other_half(ts);
+        sm = sm * exp2f(mx - nm) + ts;
+        mx = nm;
+      }
+      Ll = mx + log2f(sm);
+    }
+
+    f32x16 dk[DB], dv[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.f;
+    for (int sb = 0; sb < NS; ++sb) {
+      f32x16 sc, dp;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[e] = dp[e] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        mma(sc, load_frag(ash + (32 * sb + c) * D + 16 * ks + 8 * g), kb[ks]);
+        mma(dp, load_frag(gsh + (32 * sb + c) * D + 16 * ks + 8 * g), gb[ks]);
+      }
+      // P = exp(s S - L), dS = P (dP - c); rows past M and columns past the
+      // long length are zero
+      f32x16 P, dS;
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int m = 32 * sb + acc_row(lane, rr);
+        const bool ok = nok && m < p.M;
+        float L, cc;
+        if constexpr (DEC) {
+          L = Ll; cc = cl;
+        } else {
+          L = m < p.M ? lrow[m] * kLog2e : 0.f;
+          cc = crow[m];
+        }
+        const float pv = ok ? exp2f(sc[rr] * p.sl2 - L) : 0.f;
+        P[rr] = pv;
+        dS[rr] = pv * (dp[rr] - cc);
+      }
+      // P and dS as B operands (k = route, in the accumulator's row order)
+      F pb[2], dsb[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          pb[kk][j] = from_f32<T>(P[8 * kk + j]);
+          dsb[kk][j] = from_f32<T>(dS[8 * kk + j]);
+        }
+      // long side: dB^T += A^T dS, dG^T += G^T P (encode)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int fo = (((sb * 2 + kk) * DB + db) * 64 + lane) * 8;
+          mma(dk[db], load_frag(asht + fo), dsb[kk]);
+          if (!DEC) mma(dv[db], load_frag(gsht + fo), pb[kk]);
+        }
+      // short side: dS (and P) transposed through LDS, tile [position][route]
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        store4(tb + c * TBP + 8 * a + 4 * g, dS[4 * a], dS[4 * a + 1], dS[4 * a + 2], dS[4 * a + 3]);
+        if (DEC) store4(tb2 + c * TBP + 8 * a + 4 * g, P[4 * a], P[4 * a + 1], P[4 * a + 2], P[4 * a + 3]);
+      }
+      __builtin_amdgcn_wave_barrier();
+      F dsa[2], pa[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          dsa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
+          if (DEC) pa[kk][j] = tb2[(16 * kk + 8 * g + j) * TBP + c];
+        }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        f32x16 o, o2;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[e] = o2[e] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          mma(o, dsa[kk], kt[kk][db]);
+          if (DEC) mma(o2, pa[kk], gt[kk][db]);
+        }
+        if (32 * db + c < D) {
+          float* sa = slot_a + (32 * db + c) * SP + 32 * sb + 4 * g;
+          float* sg = slot_g + (32 * db + c) * SP + 32 * sb + 4 * g;
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            f32x4 v = *reinterpret_cast<f32x4*>(sa + 8 * a);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] += o[4 * a + q];
+            *reinterpret_cast<f32x4*>(sa + 8 * a) = v;
+            if (DEC) {
+              f32x4 u = *reinterpret_cast<f32x4*>(sg + 8 * a);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) u[q] += o2[4 * a + q];
+              *reinterpret_cast<f32x4*>(sg + 8 * a) = u;
+            }
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    // long-side results for this wave's 32 positions: rows d, column = lane
+    if (nok) {
+      const int64_t row = ((int64_t)b * p.Nl + n) * (int64_t)(p.H * D) + h * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const int d = 32 * db + 8 * a + 4 * g;
+          if (d < D) {
+            float* ob = p.dout_b + row + d;
+            f32x4 v;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] = p.s * dk[db][4 * a + q];
+            if (p.acc_b) {
+              const f32x4 old = *reinterpret_cast<const f32x4*>(ob);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) v[q] += old[q];
+            }
+            *reinterpret_cast<f32x4*>(ob) = v;
+            if (!DEC) store4(p.dout_g + row + d, dv[db][4 * a], dv[db][4 * a + 1], dv[db][4 * a + 2], dv[db][4 * a + 3]);
+          }
+        }
+    }
+  }
+  __syncthreads();
+  // fixed-order sum of the waves' slots: this chunk's short-side partials
+  const int64_t po = ((int64_t)bh * p.R + r) * p.Mp * D;
+  for (int e = threadIdx.x; e < p.Mp * D; e += blockDim.x) {
+    const int m = e / D, d = e % D;
+    float sa = 0.f, sg = 0.f;
+    for (int w = 0; w < W; ++w) {
+      const float* sw = reinterpret_cast<const float*>(smem) + w * slot_floats;
+      sa += sw[d * SP + m];
+      if (DEC) sg += sw[D * SP + d * SP + m];
+    }
+    p.part_a[po + e] = sa * p.s;
+    if (DEC) p.part_g[po + e] = sg;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// reductions and operand preparation
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_bwd_reduce(BwdReduceParams p) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n = (int64_t)p.O * p.M * p.D;
+  if (i >= n) return;
+  const int o = (int)(i / ((int64_t)p.M * p.D)), md = (int)(i % ((int64_t)p.M * p.D));
+  float s = p.base ? p.base[i] : 0.f;
+  for (int q = 0; q < p.P; ++q)
+    for (int r = 0; r < p.R; ++r) s += p.part[(((int64_t)q * p.O + o) * p.R + r) * p.Mp * p.D + md];
+  p.out[i] = s;
+}
+
+template <typename T, typename TS>
+__global__ __launch_bounds__(256) void k_bwd_prep(BwdPrepParams p) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int D = p.D, DB = (D + 31) / 32;
+  const TS* src = static_cast<const TS*>(p.src);
+  const int64_t nrows = (int64_t)p.O * p.Mp;
+  if (i < nrows) {
+    // one padded row: T copy and c
+    const int o = (int)(i / p.Mp), m = (int)(i % p.Mp);
+    T* dst = static_cast<T*>(p.rows) + i * D;
+    float cs = 0.f;
+    for (int d = 0; d < D; ++d) {
+      const float v = m < p.M ? to_f32(src[((int64_t)o * p.M + m) * D + d]) : 0.f;
+      dst[d] = from_f32<T>(v);
+      if (p.dot && m < p.M) cs += v * p.dot[((int64_t)o * p.M + m) * D + d];
+    }
+    if (p.c) p.c[i] = cs;
+    return;
+  }
+  // one lane of a transposed fragment: [O][Mp / 32][2][DB][64][8]
+  if (!p.tfrag) return;
+  const int64_t f = i - nrows;
+  const int64_t nfl = (int64_t)p.O * (p.Mp / 32) * 2 * DB * 64;
+  if (f >= nfl) return;
+  const int lane = (int)(f % 64);
+  int64_t q = f / 64;
+  const int db = (int)(q % DB); q /= DB;
+  const int kk = (int)(q % 2); q /= 2;
+  const int sb = (int)(q % (p.Mp / 32));
+  const int o = (int)(q / (p.Mp / 32));
+  const int g = lane >> 5, c = lane & 31, d = 32 * db + c;
+  T* dst = static_cast<T*>(p.tfrag) + f * 8;
+  for (int j = 0; j < 8; ++j) {
+    const int m = 32 * sb + 16 * kk + acc_row16(g, j);
+    const float v = (m < p.M && d < D) ? to_f32(src[((int64_t)o * p.M + m) * D + d]) : 0.f;
+    dst[j] = from_f32<T>(v);
+  }
+}
+
+template <typename T, int D, bool DEC>
+hipError_t attn_bwd_go(const AttnBwdParams& p, hipStream_t s) {
+  const int W = attn_bwd_waves(D, p.Mp, DEC, (int)sizeof(T));
+  const size_t lds = attn_bwd_lds_bytes(D, p.Mp, DEC, W, (int)sizeof(T));
+  const void* fn = reinterpret_cast<const void*>(&k_attn_bwd<T, D, DEC>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  k_attn_bwd<T, D, DEC><<<(int64_t)p.B * p.H * p.R, 64 * W, lds, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int attn_bwd_waves(int D, int Mp, bool dec, int elem_bytes) {
+  for (int w = 4; w >= 1; w /= 2)
+    if (attn_bwd_lds_bytes(D, Mp, dec, w, elem_bytes) <= 160 * 1024) return w;
+  return 0;
+}
+
+size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes) {
+  return (size_t)waves * attn_bwd_wave_bytes(D, Mp, dec, elem_bytes);
+}
+
+template <typename T>
+hipError_t launch_gemm(const GemmParams& p, int types, int splits, hipStream_t s) {
+  dim3 grid((p.N + kGemmTile - 1) / kGemmTile, (p.M + kGemmTile - 1) / kGemmTile, splits);
+  switch (types) {
+    case kGemmFT: k_gemm<T, float, T><<<grid, 256, 0, s>>>(p); break;
+    case kGemmTF: k_gemm<T, T, float><<<grid, 256, 0, s>>>(p); break;
+    default: k_gemm<T, T, T><<<grid, 256, 0, s>>>(p); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_splits(const float* part, float* out, int64_t n, int splits, hipStream_t s) {
+  k_sum_splits<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, out, n, splits);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_attn_bwd(const AttnBwdParams& p, int D, bool dec, hipStream_t s) {
+  if (dec) {
+    if (D == 16) return attn_bwd_go<T, 16, true>(p, s);
+    if (D == 32) return attn_bwd_go<T, 32, true>(p, s);
+    return attn_bwd_go<T, 64, true>(p, s);
+  }
+  if (D == 16) return attn_bwd_go<T, 16, false>(p, s);
+  if (D == 32) return attn_bwd_go<T, 32, false>(p, s);
+  return attn_bwd_go<T, 64, false>(p, s);
+}
+
+hipError_t launch_bwd_reduce(const BwdReduceParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.O * p.M * p.D;
+  k_bwd_reduce<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_bwd_prep(const BwdPrepParams& p, hipStream_t s) {
+  const int DB = (p.D + 31) / 32;
+  const int64_t n = (int64_t)p.O * p.Mp + (p.tfrag ? (int64_t)p.O * (p.Mp / 32) * 2 * DB * 64 : 0);
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (p.src_is_f32) k_bwd_prep<T, float><<<blocks, 256, 0, s>>>(p);
+  else k_bwd_prep<T, T><<<blocks, 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template hipError_t launch_gemm<float>(const GemmParams&, int, int, hipStream_t);
+template hipError_t launch_gemm<__bf16>(const GemmParams&, int, int, hipStream_t);
+template hipError_t launch_attn_bwd<float>(const AttnBwdParams&, int, bool, hipStream_t);
+template hipError_t launch_attn_bwd<__bf16>(const AttnBwdParams&, int, bool, hipStream_t);
+template hipError_t launch_bwd_prep<float>(const BwdPrepParams&, hipStream_t);
+template hipError_t launch_bwd_prep<__bf16>(const BwdPrepParams&, hipStream_t);
+
+}  // namespace flarepp

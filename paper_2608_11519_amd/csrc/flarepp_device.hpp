@@ -35,6 +35,9 @@ __device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfi
 __device__ __forceinline__ int acc_row(int lane, int r) {
   return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 }
+// Row (within a 16-row group) of element j of half g: the accumulator row
+// order of a 32x32 MFMA result, 8 (j / 4) + 4 g + j % 4.
+__device__ __forceinline__ int acc_row16(int g, int j) { return 8 * (j >> 2) + 4 * g + (j & 3); }
 
 __device__ __forceinline__ void mma(f32x16& c, const bf16x8& a, const bf16x8& b) {
   c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);

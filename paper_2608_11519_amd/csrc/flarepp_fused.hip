@@ -53,9 +53,6 @@ constexpr int kFrag = 512;  // elements of one 64-lane x 8 fragment
 __device__ __forceinline__ int key_perm(int rho) {
   return 16 * (rho >> 4) + 8 * ((rho >> 2) & 1) + 4 * ((rho & 15) >> 3) + (rho & 3);
 }
-// Row (within a 16-row group) of element j of half g: the accumulator row
-// order of a 32x32 MFMA result, 8 (j / 4) + 4 g + j % 4.
-__device__ __forceinline__ int acc_row16(int g, int j) { return 8 * (j >> 2) + 4 * g + (j & 3); }
 
 __device__ __forceinline__ void lds_wait_barrier() {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");

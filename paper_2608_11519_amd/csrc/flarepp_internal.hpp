@@ -180,6 +180,80 @@ constexpr int route_nq(int D, bool decode) {
   return decode ? (D <= 32 ? 2 : 1) : (D == 16 ? 4 : (D == 32 ? 2 : 1));
 }
 
+// ---- backward (App. A.5) ---------------------------------------------------
+// C[M][N] (fp32) = sum over segments of sum_k A(m, k) B(k, n), with
+// A(m, k) = a[m * a_m + k * a_k] and B(k, n) = b[k * b_k + n * b_n] (elements).
+// Split-K: blockIdx.z covers k in [z * kchunk, (z + 1) * kchunk) and writes
+// c + z * split_stride.
+struct GemmParams {
+  int M, N, K, nseg;
+  const void* a[4];
+  const void* b[4];
+  int64_t a_m, a_k, b_k, b_n;
+  int kchunk;
+  float* c;
+  int64_t ldc, split_stride;
+};
+// Which operand types a GEMM reads: A and B in the compute type T, or one of
+// them in fp32 (converted to T on the way into LDS).
+enum GemmTypes { kGemmTT = 0, kGemmFT = 1, kGemmTF = 2 };
+
+// SDPA backward over one (batch, head) pair and one chunk of the long axis
+// (keys of an encode, tokens of the decode).  The tile orientation is
+// rows = short axis (the M routes), columns = long axis, so that
+//   S = A_sh B_lo^T, dP = G_sh G_lo^T, dS = P (dP - c),
+//   long side:  dB_lo^T = s A_sh^T dS (both),  dG_lo^T = G_sh^T P (encode),
+//   short side: dA_sh = s dS B_lo (both),      dG_sh = P G_lo (decode).
+// Encode: A_sh = queries, G_sh = dOut, B_lo = keys, G_lo = values, L and c
+// per route.  Decode: A_sh = routes (its keys), G_sh = latents (its values),
+// B_lo = token keys (its queries), G_lo = dY, L and c per token (computed
+// in the kernel).
+struct AttnBwdParams {
+  int B, H, Nl, M, Mp, R, tpw;   // long length, routes, chunks per (b, h), long tiles per wave
+  float s, sl2;                  // 1/sqrt(D), and times log2(e)
+  // short side, per (b, h) at b * sb + h * sh (elements)
+  const void* ash; int64_t ash_sb, ash_sh;    // rows [Mp][D]
+  const void* asht; int64_t asht_sb, asht_sh; // A fragments of A_sh^T
+  const void* gsh; int64_t gsh_sb, gsh_sh;    // rows [Mp][D]
+  const void* gsht; int64_t gsht_sb, gsht_sh; // A fragments of G_sh^T (encode)
+  const float* lrow;  // encode: [B * H][M], natural log
+  const float* crow;  // encode: [B * H][Mp]
+  // long side: element (b, h, n, d) at b * sb + h * sh + n * sn + d * sd
+  const void* blo; int64_t blo_sb, blo_sh, blo_sn, blo_sd;  // type T
+  const void* glo; int64_t glo_sb, glo_sh, glo_sn, glo_sd;  // T (encode) or fp32 (decode)
+  const void* ylo; int64_t ylo_sb, ylo_sh, ylo_sn;          // decode: forward output rows (T)
+  // outputs: long side [B][Nl][H * D] fp32 (dout_b added to what is there
+  // when acc_b); short side partials [B][H][R][Mp][D] fp32
+  float* dout_b; int acc_b;
+  float* dout_g;
+  float* part_a; float* part_g;
+};
+int attn_bwd_waves(int D, int Mp, bool dec, int elem_bytes);
+size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes);
+
+// Fixed-order sums of backward partials: out[o][m][d] = base[o][m][d] +
+// sum_{p < P} sum_{r < R} part[((p * O + o) * R + r) * Mp * D + m * D + d].
+struct BwdReduceParams {
+  const float* part; const float* base; float* out;
+  int P, O, R, M, Mp, D;
+};
+// Short-side operands of a backward call from fp32 (or T) rows src[O][M][D]:
+// T rows [O][Mp][D] (zero padded), the A fragments of src^T
+// [O][Mp / 32][2][DB][64][8] (lane (c, g), element j holds
+// src[32 sb + 16 kk + acc_row16(g, j)][32 db + c]), and, when dot is given,
+// c[O][Mp] = sum_d src[m][d] dot[m][d].
+struct BwdPrepParams {
+  const void* src; int src_is_f32;
+  const float* dot;
+  int O, M, Mp, D;
+  void* rows; void* tfrag; float* c;
+};
+template <typename T> hipError_t launch_gemm(const GemmParams&, int types, int splits, hipStream_t);
+template <typename T> hipError_t launch_attn_bwd(const AttnBwdParams&, int D, bool dec, hipStream_t);
+hipError_t launch_sum_splits(const float* part, float* out, int64_t n, int splits, hipStream_t);
+hipError_t launch_bwd_reduce(const BwdReduceParams&, hipStream_t);
+template <typename T> hipError_t launch_bwd_prep(const BwdPrepParams&, hipStream_t);
+
 template <typename T> hipError_t launch_weight_frags(const WeightFragParams&, hipStream_t);
 template <typename Ts, typename T> hipError_t launch_route_prep(const RoutePrepParams&, hipStream_t);
 template <typename T> hipError_t launch_dmajor(const DmajorParams&, hipStream_t);

@@ -33,6 +33,7 @@ EXPORTS = (
     "flarepp_mixer_workspace_bytes", "flarepp_mixer_forward", "flarepp_mixer_forward_debug",
     "flarepp_mixer_forward_profiled", "flarepp_mixer_path", "flarepp_mixer_stage",
     "flarepp_flare_workspace_bytes", "flarepp_flare_forward", "flarepp_flare_forward_debug",
+    "flarepp_mixer_backward_workspace_bytes", "flarepp_mixer_backward", "flarepp_mixer_backward_debug",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -93,6 +94,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_flare_forward_debug.restype = i32
     lib.flarepp_flare_forward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 6
                                                 + [fp, vp] + [vp, sz, vp])
+    lib.flarepp_mixer_backward_workspace_bytes.restype = sz
+    lib.flarepp_mixer_backward_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
+    lib.flarepp_mixer_backward.restype = i32
+    lib.flarepp_mixer_backward.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8 + [fp] * 7
+                                           + [vp, sz, vp])
+    lib.flarepp_mixer_backward_debug.restype = i32
+    lib.flarepp_mixer_backward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8 + [fp] * 9
+                                                 + [vp, sz, vp])
     _lib = lib
     return lib
 
@@ -335,6 +344,48 @@ def flarepp_flare_forward_debug(X, Wk, Wv, Wo, queries, *, H: int,
     return O, Z, Y
 
 
+def flarepp_mixer_backward_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
+    return int(load().flarepp_mixer_backward_workspace_bytes(dtype, B, N, C, H, M))
+
+
+def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws):
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    D = C // H
+    dt = _dtype_code(X)
+    f32 = dict(dtype=torch.float32, device=X.device)
+    g = {"dX": torch.empty((B, N, C), **f32)}
+    for k in ("dWk", "dWv", "dWkt", "dWvt", "dWo"):
+        g[k] = torch.empty((C, C), **f32)
+    g["dseeds"] = torch.empty((H, M, D), **f32)
+    outs = [g[k] for k in ("dX", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds")]
+    if debug:
+        g["dZ"] = torch.empty((B, H, M, D), **f32)
+        g["dQ"] = torch.empty((B, H, M, D), **f32)
+        outs += [g["dZ"], g["dQ"]]
+    w = _workspace(flarepp_mixer_backward_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    fn = lib.flarepp_mixer_backward_debug if debug else lib.flarepp_mixer_backward
+    rc = fn(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt), _ptr(Wvt), _ptr(Wo), _ptr(seeds),
+            _ptr(dO), *[_ptr(t) for t in outs], _ptr(w), w.numel(), _stream(X.device))
+    _check(rc)
+    return g
+
+
+def flarepp_mixer_backward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,
+                           ws: Optional[torch.Tensor] = None):
+    """Gradients of <O, dO> for the FLARE++ mixer: a dict of fp32 tensors
+    dX [B, N, C], dWk, dWv, dWkt, dWvt, dWo [C, C] and dseeds [H, M, D]."""
+    return _backward(False, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws)
+
+
+def flarepp_mixer_backward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,
+                                 ws: Optional[torch.Tensor] = None):
+    """``flarepp_mixer_backward`` plus the summed latent and query gradients
+    dZ, dQ [B, H, M, D]."""
+    return _backward(True, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws)
+
+
 # short aliases
 project = flarepp_project
 route = flarepp_route
@@ -342,3 +393,5 @@ mixer_forward = flarepp_mixer_forward
 mixer_forward_debug = flarepp_mixer_forward_debug
 flare_forward = flarepp_flare_forward
 flare_forward_debug = flarepp_flare_forward_debug
+mixer_backward = flarepp_mixer_backward
+mixer_backward_debug = flarepp_mixer_backward_debug

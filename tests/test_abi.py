@@ -188,3 +188,45 @@ def test_flare_rejects_null_and_misaligned_pointers():
         assert _flare(ptrs=ptrs) == fp.ERR_INVALID_ARG
         ptrs[i] = ctypes.c_void_p(4096 + 4)
         assert _flare(ptrs=ptrs) == fp.ERR_INVALID_ARG
+
+
+def _backward(dtype=fp.BF16, B=1, N=64, C=64, H=4, M=32, ptrs=None, ws=_P, ws_bytes=1 << 40):
+    lib = _lib()
+    p = ptrs or [_P] * 15  # X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt, dWvt, dWo, dseeds
+    return lib.flarepp_mixer_backward(dtype, B, N, C, H, M, *p, ws, ws_bytes, None)
+
+
+def test_backward_workspace_sizes():
+    for dt in (fp.F32, fp.BF16):
+        bs = 4 if dt == fp.F32 else 2
+        n = fp.flarepp_mixer_backward_workspace_bytes(dt, 4, 16384, 128, 8, 128)
+        # K, K~, V, V~, Y in the storage type and five fp32 token gradients
+        assert n >= 4 * 16384 * 128 * (5 * bs + 5 * 4)
+    # a head's route gradients must fit in LDS: M = 512 with D = 64 does not
+    assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 2, 512) == 0
+    assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 2, 256) > 0
+    assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 8, 512) > 0
+    assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 10, 100, 3, 4) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), fp.ERR_INVALID_ARG),
+    (dict(N=0), fp.ERR_INVALID_ARG),
+    (dict(C=96, H=2), fp.ERR_UNSUPPORTED),
+    (dict(C=128, H=2, M=512), fp.ERR_UNSUPPORTED),
+    (dict(dtype=3), fp.ERR_UNSUPPORTED),
+    (dict(ws=None), fp.ERR_WORKSPACE),
+    (dict(ws_bytes=100), fp.ERR_WORKSPACE),
+])
+def test_backward_rejects_invalid_arguments(kw, code):
+    assert _backward(**kw) == code
+    assert fp.last_error() != ""
+
+
+def test_backward_rejects_null_and_misaligned_pointers():
+    for i in range(15):
+        ptrs = [_P] * 15
+        ptrs[i] = None
+        assert _backward(ptrs=ptrs) == fp.ERR_INVALID_ARG
+        ptrs[i] = ctypes.c_void_p(4096 + 4)
+        assert _backward(ptrs=ptrs) == fp.ERR_INVALID_ARG

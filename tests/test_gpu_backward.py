@@ -1,0 +1,107 @@
+"""GPU parity of the mixer backward (App. A.5) against the float64 oracle,
+through the C ABI.
+
+The output gradient dO is a seeded N(0, 1) tensor in the storage type; both
+sides see the same rounded values.  Gates as for the forward: every gradient
+(dX, the five weight gradients, the seed gradient) and the summed latent and
+query gradients dZ, dQ within 1e-4 (fp32) or 2e-2 (bf16) of the reference's
+max |.|.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import flarepp_oracle as orc
+from paper_2608_11519_amd import flarepp as fp
+from paper_2608_11519_amd import inputs as inp
+
+from gpu_util import TOL, assert_close, upload
+
+pytestmark = pytest.mark.gpu
+
+GRADS = ("dX", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fp.load()
+    yield
+
+
+def _run(w, d, dO, debug=True):
+    t = upload(d, w)
+    dOt = torch.from_numpy(dO).to("cuda", t["X"].dtype)
+    args = (t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"], t["seeds"], dOt)
+    g = fp.flarepp_mixer_backward_debug(*args, H=w.H) if debug else fp.flarepp_mixer_backward(*args, H=w.H)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in g.items()}
+
+
+def _check(w, d, label, dO_seed=100, tol=None):
+    print(f"[case] backward {label} {inp.describe(w)}", flush=True)
+    dO = inp.make_tensor((w.B, w.N, w.C), dO_seed, w.dtype)
+    got = _run(w, d, dO)
+    ref = orc.mixer_backward(d["X"], d["Wk"], d["Wv"], d["Wkt"], d["Wvt"], d["Wo"], d["seeds"], w.H, dO)
+    tol = TOL[w.dtype] if tol is None else tol
+    for k in GRADS + ("dZ", "dQ"):
+        assert_close(k, got[k], ref[k], tol, label)
+    return got, ref
+
+
+def test_backward_tiny_fp32():
+    w = inp.workload("tiny")
+    _check(w, inp.make_inputs(w, 0, seed_scale=4.0), "tiny")
+
+
+def test_backward_grid2d_full_size():
+    w = inp.workload("grid2d")
+    _check(w, inp.make_inputs(w, 0), "grid2d")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_backward_sharp_seeds(dtype):
+    # seeds x8: far-from-uniform routing weights, so dS = P (dP - c) is not
+    # dominated by the mean-field term
+    w = inp.Workload("bwd-sharp", 2, 1500, 64, 4, 64, dtype, "normal")
+    _check(w, inp.make_inputs(w, 2, seed_scale=8.0), "sharp")
+
+
+@pytest.mark.parametrize("N,M", [(33, 100), (1000, 1), (777, 48), (5, 3)])
+def test_backward_tails_and_route_counts(N, M):
+    w = inp.Workload("bwd-tail", 2, N, 64, 4, M, "f32", "normal")
+    _check(w, inp.make_inputs(w, 3, seed_scale=4.0), f"N{N}-M{M}")
+
+
+@pytest.mark.parametrize("D,dtype", [(32, "bf16"), (64, "bf16"), (32, "f32"), (64, "f32")])
+def test_backward_head_widths(D, dtype):
+    w = inp.Workload("bwd-width", 2, 600, 2 * D, 2, 40, dtype, "normal")
+    _check(w, inp.make_inputs(w, 5, seed_scale=4.0), f"D{D}")
+
+
+def test_backward_wide_channels_bf16():
+    # C = 256 (eight heads of 32), the mesh workload's width, at a small N
+    w = inp.Workload("bwd-c256", 1, 2000, 256, 8, 96, "bf16", "fourier")
+    _check(w, inp.make_inputs(w, 6), "C256")
+
+
+def test_backward_plain_entry_matches_debug():
+    w = inp.Workload("bwd-plain", 1, 700, 64, 4, 32, "bf16", "normal")
+    d = inp.make_inputs(w, 7, seed_scale=4.0)
+    dO = inp.make_tensor((w.B, w.N, w.C), 8, w.dtype)
+    a = _run(w, d, dO, debug=True)
+    b = _run(w, d, dO, debug=False)
+    for k in GRADS:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_backward_deterministic_bitwise():
+    w = inp.Workload("bwd-det", 2, 3000, 128, 8, 64, "bf16", "normal")
+    d = inp.make_inputs(w, 9)
+    dO = inp.make_tensor((w.B, w.N, w.C), 10, w.dtype)
+    a = _run(w, d, dO)
+    b = _run(w, d, dO)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
