@@ -45,6 +45,7 @@ def parse_args(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-graph", action="store_true", help="launch every step eagerly")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-backward", action="store_true", help="skip the mixer-backward timing")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host seconds spent timing the oracle")
     ap.add_argument("--stage-reps", type=int, default=20,
@@ -235,21 +236,10 @@ def cpu_baseline(w, d, min_seconds):
                       f"{el:.1f} s on {len(os.sched_getaffinity(0))} host cores"}
 
 
-def time_flare(args, w, t, use_graph):
-    """The fixed-query FLARE mixer (Sec. 3.1) on the same workload and
-    weights (its learned queries: the seeds), timed like the FLARE++ step:
-    the paper's cost comparison of the two mixers (Sec. 3.2 end; App. C.3)."""
+def _time_steps(args, step, use_graph):
+    """Mean ms of `step` over args.steps runs after args.warmup, replayed from
+    a HIP graph when use_graph."""
     import torch
-
-    from paper_2608_11519_amd import flarepp as fp
-
-    dcode = fp.BF16 if w.dtype == "bf16" else fp.F32
-    O = torch.empty_like(t["X"])
-    ws = torch.empty(fp.flarepp_flare_workspace_bytes(dcode, w.B, w.N, w.C, w.H, w.M),
-                     dtype=torch.uint8, device=t["X"].device)
-
-    def step():
-        fp.flarepp_flare_forward(t["X"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], H=w.H, out=O, ws=ws)
 
     for _ in range(args.warmup):
         step()
@@ -271,7 +261,66 @@ def time_flare(args, w, t, use_graph):
             step()
     e1.record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    return e0.elapsed_time(e1) / args.steps
+
+
+def backward_flops(w):
+    """Algorithmic flops of the mixer backward (App. A.5), per token: the
+    merge (dY, dW_O: 4 C^2), each routing call's recomputed scores and its
+    four gradient products (5 x 2 M C, three calls), and the projections
+    (dX, dW over four weights: 16 C^2).  The forward that the entry point
+    runs again to recover its statistics is not counted."""
+    return (20.0 * w.C * w.C + 30.0 * w.M * w.C) * w.B * w.N
+
+
+def time_backward(args, w, t, use_graph):
+    """The mixer backward on the same workload: gradients of <O, dO> for a
+    seeded dO, one complete call (forward again, then the reverse pass)."""
+    import torch
+
+    from paper_2608_11519_amd import flarepp as fp
+    from paper_2608_11519_amd import inputs as inp
+
+    dcode = fp.BF16 if w.dtype == "bf16" else fp.F32
+    dev = t["X"].device
+    dO = torch.from_numpy(inp.make_tensor((w.B, w.N, w.C), 100, w.dtype)).to(dev, t["X"].dtype)
+    ws = torch.empty(fp.flarepp_mixer_backward_workspace_bytes(dcode, w.B, w.N, w.C, w.H, w.M),
+                     dtype=torch.uint8, device=dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = {"dX": torch.empty((w.B, w.N, w.C), **f32), "dseeds": torch.empty((w.H, w.M, w.D), **f32)}
+    for k in ("dWk", "dWv", "dWkt", "dWvt", "dWo"):
+        out[k] = torch.empty((w.C, w.C), **f32)
+    args6 = (t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"], t["seeds"], dO)
+
+    def step():
+        fp.flarepp_mixer_backward(*args6, H=w.H, ws=ws, out=out)
+
+    ms = _time_steps(args, step, use_graph)
+    fl = backward_flops(w)
+    peak = PEAK_MFMA_BF16_TFLOPS if w.dtype == "bf16" else PEAK_MFMA_F32_TFLOPS
+    tf = fl / (ms * 1e-3) / 1e12
+    return {"ms_per_step": round(ms, 5), "tokens_per_s": round(w.B * w.N / (ms * 1e-3), 1),
+            "algorithmic_tflop": round(fl / 1e12, 4), "achieved_tflops": round(tf, 2),
+            "mfma_frac": round(tf / peak, 4)}
+
+
+def time_flare(args, w, t, use_graph):
+    """The fixed-query FLARE mixer (Sec. 3.1) on the same workload and
+    weights (its learned queries: the seeds), timed like the FLARE++ step:
+    the paper's cost comparison of the two mixers (Sec. 3.2 end; App. C.3)."""
+    import torch
+
+    from paper_2608_11519_amd import flarepp as fp
+
+    dcode = fp.BF16 if w.dtype == "bf16" else fp.F32
+    O = torch.empty_like(t["X"])
+    ws = torch.empty(fp.flarepp_flare_workspace_bytes(dcode, w.B, w.N, w.C, w.H, w.M),
+                     dtype=torch.uint8, device=t["X"].device)
+
+    def step():
+        fp.flarepp_flare_forward(t["X"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], H=w.H, out=O, ws=ws)
+
+    ms = _time_steps(args, step, use_graph)
     return {"ms_per_step": round(ms, 5), "tokens_per_s": round(w.B * w.N / (ms * 1e-3), 1)}
 
 
@@ -376,6 +425,7 @@ def main(argv=None):
     step()  # leave the workspace and O as one complete step wrote them
     torch.cuda.synchronize()
     flare = time_flare(args, w, t, graph is not None)
+    backward = None if args.no_backward else time_backward(args, w, t, graph is not None)
     work = stage_work(w, fused)
     stages = {n: {"ms": round(stage_ms[n], 5), **roofline(work[n], stage_ms[n], w.dtype)}
               for n in fp.PROFILE_STAGES if n not in empty}
@@ -418,6 +468,8 @@ def main(argv=None):
         "wall_ms_timed_region": round(wall_ms, 3),
         "flare": {**flare, "flarepp_over_flare_time": round(ms_per_step / flare["ms_per_step"], 3)},
     }
+    if backward is not None:
+        out["backward"] = backward
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, d, args.cpu_seconds)

@@ -202,15 +202,15 @@ FLAREPP_API int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int
  * Inputs as for flarepp_mixer_forward, plus dO.  Outputs, all fp32 and
  * row-major, overwritten: dX [B][N][C]; dWk, dWv, dWkt, dWvt, dWo [C][C]
  * (the layout of the weights, out = X W); dseeds [H][M][D].  With bf16 the
- * MFMA operands (including the gradients fed to the next product) are
- * rounded to bf16; accumulation is fp32.
+ * MFMA operands, and the token gradients dY, dK, dV, dK~, dV~ kept between
+ * the kernels, are rounded to bf16; accumulation is fp32.
  *
  * Sizes as for the mixer; in addition B*N <= 2^30, and a head's M x D route
  * gradients (two of them, fp32) must fit in LDS: M <= 512 for D <= 32, M <=
  * 256 for D = 64 (FLAREPP_ERR_UNSUPPORTED otherwise).  Workspace:
  * flarepp_mixer_backward_workspace_bytes(...) bytes (0 for an invalid or
- * unsupported shape); it holds the forward's K, V, K~, V~, Y and the fp32
- * token gradients, about (4 * bytes(dtype) + 20) * B * N * C bytes.
+ * unsupported shape); it holds the forward's K, V, K~, V~, Y and the token
+ * gradients dY, dK, dV, dK~, dV~, about 10 * bytes(dtype) * B * N * C bytes.
  * flarepp_mixer_backward_debug also writes the summed latent gradient dZ and
  * the summed query gradient dQ (fp32 [B][H][M][D] each) when non-null.
  * ------------------------------------------------------------------------- */

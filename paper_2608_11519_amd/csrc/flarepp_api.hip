@@ -581,7 +581,7 @@ BwdSplit bwd_split(int64_t BH, int64_t Nl, int D, int Mp, bool dec, int elem_byt
   sp.waves = flarepp::attn_bwd_waves(D, Mp, dec, elem_bytes);
   if (sp.waves == 0) return sp;
   const int64_t tiles = cdiv(Nl, 32);
-  int64_t R = std::max<int64_t>(1, std::min<int64_t>(cdiv(2048, BH), cdiv(tiles, sp.waves)));
+  int64_t R = std::max<int64_t>(1, std::min<int64_t>(cdiv(512, BH), cdiv(tiles, sp.waves)));
   const int64_t tpw = cdiv(tiles, R * sp.waves);
   R = cdiv(tiles, tpw * sp.waves);
   sp.R = (int)R;
@@ -589,11 +589,12 @@ BwdSplit bwd_split(int64_t BH, int64_t Nl, int D, int Mp, bool dec, int elem_byt
   return sp;
 }
 
-// Split-K of the token reductions dW = X^T dG (K = B N tokens).
+// Split-K of the five token reductions dW = X^T dG, dW_O = Y^T dO (K = B N
+// tokens), computed in one launch: about 1024 workgroups in all.
 int gemm_splits(int64_t T, int64_t C, int* kchunk) {
   const int64_t tiles = cdiv(C, 64) * cdiv(C, 64);
-  int64_t splits = std::max<int64_t>(1, std::min<int64_t>(cdiv(T, 256), cdiv(1024, tiles)));
-  const int64_t kc = round_up(cdiv(T, splits), 32);
+  int64_t splits = std::max<int64_t>(1, std::min<int64_t>(cdiv(T, 256), cdiv(1024, 5 * tiles)));
+  const int64_t kc = round_up(cdiv(T, splits), 64);
   *kchunk = (int)kc;
   return (int)cdiv(T, kc);
 }
@@ -601,7 +602,8 @@ int gemm_splits(int64_t T, int64_t C, int* kchunk) {
 struct BwdWs {
   void *wf[4], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *Y, *q_op, *z_op;
   float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2;
-  float *dY, *dK, *dV, *dKt, *dVt, *dZf, *dQ3, *dQf, *c1, *c2, *pa, *pg, *gpart;
+  float *dZf, *dQ3, *dQf, *c1, *c2, *l1, *l2, *pa, *pg, *gpart;
+  void *dY, *dK, *dV, *dKt, *dVt;
   void *Qr, *Qt, *Zr, *dZr, *dZt, *dQr, *dQt, *Sr, *St;
   BwdSplit dec, enc;
   int splits, kchunk;
@@ -630,16 +632,18 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   w.Zf = (float*)cv.take(f4 * BH * M * D);
   w.L1 = (float*)cv.take(f4 * BH * M);
   w.L2 = (float*)cv.take(f4 * BH * M);
-  w.dY = (float*)cv.take(f4 * T * C);
-  w.dK = (float*)cv.take(f4 * T * C);
-  w.dV = (float*)cv.take(f4 * T * C);
-  w.dKt = (float*)cv.take(f4 * T * C);
-  w.dVt = (float*)cv.take(f4 * T * C);
+  w.dY = cv.take(bs * T * C);
+  w.dK = cv.take(bs * T * C);
+  w.dV = cv.take(bs * T * C);
+  w.dKt = cv.take(bs * T * C);
+  w.dVt = cv.take(bs * T * C);
   w.dZf = (float*)cv.take(f4 * BH * M * D);
   w.dQ3 = (float*)cv.take(f4 * BH * M * D);
   w.dQf = (float*)cv.take(f4 * BH * M * D);
   w.c1 = (float*)cv.take(f4 * BH * Mp);
   w.c2 = (float*)cv.take(f4 * BH * Mp);
+  w.l1 = (float*)cv.take(f4 * BH * Mp);
+  w.l2 = (float*)cv.take(f4 * BH * Mp);
   w.Qr = cv.take(bs * BH * Mp * D);
   w.Qt = cv.take(bs * BH * Mp * 32 * DB);
   w.Zr = cv.take(bs * BH * Mp * D);
@@ -655,7 +659,7 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   w.pa = (float*)cv.take(f4 * BH * R * Mp * D);
   w.pg = (float*)cv.take(f4 * BH * R * Mp * D);
   w.splits = gemm_splits(T, C, &w.kchunk);
-  w.gpart = (float*)cv.take(f4 * w.splits * C * C);
+  w.gpart = (float*)cv.take(f4 * 5 * w.splits * C * C);
   w.bytes = cv.off;
   return w;
 }
@@ -737,25 +741,13 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   r3.y = w.Y; r3.y_sb = N * C; r3.y_row = C;
   HIPTRY(launch_route<T>(r3, (int)D, true, s));
 
-  // ---- merge: dY = dO W_O^T, dW_O = Y^T dO ----
-  const int types_tt = kGemmTT;
+  // ---- merge: dY = dO W_O^T (dW_O is computed with the weight gradients) ----
   GemmParams g{};
-  g.M = (int)NT; g.N = (int)C; g.K = (int)C; g.nseg = 1;
+  g.M = (int)NT; g.N = (int)C; g.K = (int)C; g.nseg = 1; g.nprob = 1; g.splits = 1;
   g.a[0] = dO; g.a_m = C; g.a_k = 1;
   g.b[0] = Wo; g.b_k = 1; g.b_n = C;
-  g.kchunk = (int)round_up(C, 32); g.c = w.dY; g.ldc = C; g.split_stride = 0;
-  HIPTRY(launch_gemm<T>(g, types_tt, 1, s));
-  auto weight_grad = [&](const void* A, const void* G, int types, float* out) -> int {
-    GemmParams q{};
-    q.M = (int)C; q.N = (int)C; q.K = (int)NT; q.nseg = 1;
-    q.a[0] = A; q.a_m = 1; q.a_k = C;
-    q.b[0] = G; q.b_k = C; q.b_n = 1;
-    q.kchunk = w.kchunk; q.c = w.gpart; q.ldc = C; q.split_stride = C * C;
-    HIPTRY(launch_gemm<T>(q, types, w.splits, s));
-    HIPTRY(launch_sum_splits(w.gpart, out, C * C, w.splits, s));
-    return FLAREPP_OK;
-  };
-  TRY(weight_grad(w.Y, dO, types_tt, dWo));
+  g.kchunk = (int)round_up(C, 64); g.c = w.dY; g.c_t = 1; g.ldc = C; g.split_stride = 0;
+  HIPTRY(launch_gemm<T>(g, s));
 
   // ---- call 3 (decode): queries K, keys Q, values Z ----
   BwdPrepParams bp{};
@@ -786,7 +778,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   HIPTRY(launch_bwd_reduce(rd, s));
 
   // ---- call 2 (encode): queries Q, keys K, values V; dOut = dZ ----
-  bp.src = dZf; bp.dot = w.Zf; bp.rows = w.dZr; bp.tfrag = w.dZt; bp.c = w.c2;
+  bp.src = dZf; bp.dot = w.Zf; bp.rows = w.dZr; bp.tfrag = w.dZt; bp.c = w.c2; bp.lse = w.L2; bp.l2 = w.l2;
   HIPTRY(launch_bwd_prep<T>(bp, s));
   AttnBwdParams a2{};
   a2.B = (int)B; a2.H = (int)H; a2.Nl = (int)N; a2.M = (int)M; a2.Mp = (int)Mp;
@@ -795,7 +787,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a2.asht = w.Qt; a2.asht_sb = H * tfS; a2.asht_sh = tfS;
   a2.gsh = w.dZr; a2.gsh_sb = rtBS; a2.gsh_sh = rtHS;
   a2.gsht = w.dZt; a2.gsht_sb = H * tfS; a2.gsht_sh = tfS;
-  a2.lrow = w.L2; a2.crow = w.c2;
+  a2.lrow = w.l2; a2.crow = w.c2;
   a2.blo = w.K; a2.blo_sb = tokBS; a2.blo_sh = tokHS; a2.blo_sn = D; a2.blo_sd = 1;
   a2.glo = w.Vdm; a2.glo_sb = dmBS; a2.glo_sh = dmHS; a2.glo_sn = 1; a2.glo_sd = Np;
   a2.dout_b = w.dK; a2.acc_b = 1; a2.dout_g = w.dV;
@@ -806,7 +798,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   float* dQf = rd.out;
 
   // ---- call 1 (query synthesis): queries = seeds (shared), keys K~, values V~ ----
-  bp.src = dQf; bp.dot = w.Qf; bp.rows = w.dQr; bp.tfrag = w.dQt; bp.c = w.c1;
+  bp.src = dQf; bp.dot = w.Qf; bp.rows = w.dQr; bp.tfrag = w.dQt; bp.c = w.c1; bp.lse = w.L1; bp.l2 = w.l1;
   HIPTRY(launch_bwd_prep<T>(bp, s));
   BwdPrepParams sp2{};
   sp2.src = seeds; sp2.src_is_f32 = f32 ? 1 : 0; sp2.dot = nullptr; sp2.O = (int)H; sp2.M = (int)M;
@@ -816,23 +808,32 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a1.ash = w.Sr; a1.ash_sb = 0; a1.ash_sh = rtHS;
   a1.asht = w.St; a1.asht_sb = 0; a1.asht_sh = tfS;
   a1.gsh = w.dQr; a1.gsht = w.dQt;
-  a1.lrow = w.L1; a1.crow = w.c1;
+  a1.lrow = w.l1; a1.crow = w.c1;
   a1.blo = w.Kt; a1.glo = w.Vtdm;
   a1.dout_b = w.dKt; a1.acc_b = 0; a1.dout_g = w.dVt;
   HIPTRY(launch_attn_bwd<T>(a1, (int)D, false, s));
   rd.P = (int)B; rd.O = (int)H; rd.R = w.enc.R; rd.part = w.pa; rd.base = nullptr; rd.out = dseeds;
   HIPTRY(launch_bwd_reduce(rd, s));
 
-  // ---- projections: dX = sum_j dG_j W_j^T, dW_j = X^T dG_j ----
+  // ---- projections: dX = sum_j dG_j W_j^T; the weight gradients
+  // dW_j = X^T dG_j and dW_O = Y^T dO in one split-K launch ----
   GemmParams gx{};
-  gx.M = (int)NT; gx.N = (int)C; gx.K = (int)C; gx.nseg = 4;
-  const float* G[4] = {w.dK, w.dV, w.dKt, w.dVt};
+  gx.M = (int)NT; gx.N = (int)C; gx.K = (int)C; gx.nseg = 4; gx.nprob = 1; gx.splits = 1;
+  const void* G[4] = {w.dK, w.dV, w.dKt, w.dVt};
   for (int j = 0; j < 4; ++j) { gx.a[j] = G[j]; gx.b[j] = w_in[j]; }
   gx.a_m = C; gx.a_k = 1; gx.b_k = 1; gx.b_n = C;
-  gx.kchunk = (int)round_up(C, 32); gx.c = dX; gx.ldc = C; gx.split_stride = 0;
-  HIPTRY(launch_gemm<T>(gx, kGemmFT, 1, s));
-  float* dW[4] = {dWk, dWv, dWkt, dWvt};
-  for (int j = 0; j < 4; ++j) TRY(weight_grad(X, G[j], kGemmTF, dW[j]));
+  gx.kchunk = (int)round_up(C, 64); gx.c = dX; gx.c_t = 0; gx.ldc = C; gx.split_stride = 0;
+  HIPTRY(launch_gemm<T>(gx, s));
+  GemmParams gw{};
+  gw.M = (int)C; gw.N = (int)C; gw.K = (int)NT; gw.nseg = 1; gw.nprob = 5; gw.splits = w.splits;
+  const void* wa[5] = {X, X, X, X, w.Y};
+  const void* wb[5] = {w.dK, w.dV, w.dKt, w.dVt, dO};
+  for (int j = 0; j < 5; ++j) { gw.a[j] = wa[j]; gw.b[j] = wb[j]; }
+  gw.a_m = 1; gw.a_k = C; gw.b_k = C; gw.b_n = 1;
+  gw.kchunk = w.kchunk; gw.c = w.gpart; gw.c_t = 0; gw.ldc = C; gw.split_stride = C * C;
+  HIPTRY(launch_gemm<T>(gw, s));
+  float* dW[5] = {dWk, dWv, dWkt, dWvt, dWo};
+  HIPTRY(launch_sum_splits(w.gpart, dW, C * C, w.splits, 5, s));
   return ok();
 }
 

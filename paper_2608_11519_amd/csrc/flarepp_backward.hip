@@ -1,11 +1,10 @@
 // Backward of the FLARE++ mixer (App. A.5) on gfx950.
 //
 // * k_gemm: C = sum_seg A B on MFMA 32x32 tiles through LDS, for the
-//   projection and W_O gradients (dY = dO W_O^T, dW_O = Y^T dO,
-//   dX = sum_j dG_j W_j^T, dW_j = X^T dG_j).  Either operand may be fp32 (the
-//   gradients) and is rounded to the compute type on its way into LDS; the
-//   reductions over tokens are split over workgroups (split-K) and summed in
-//   a fixed order by k_sum_splits.
+//   projection and W_O gradients (dY = dO W_O^T, dX = sum_j dG_j W_j^T, and
+//   in one launch the five weight gradients dW_j = X^T dG_j, dW_O = Y^T dO);
+//   the reductions over tokens are split over workgroups (split-K) and summed
+//   in a fixed order by k_sum_splits.
 // * k_attn_bwd: the SDPA backward of one routing call from its global output
 //   and log-normaliser, over a chunk of the long axis (keys of an encode,
 //   tokens of the decode).  Each wave owns 32 positions of the long axis and
@@ -31,75 +30,125 @@ constexpr float kLog2e = 1.4426950408889634f;
 // ---------------------------------------------------------------------------
 // GEMM
 // ---------------------------------------------------------------------------
-constexpr int kGemmTile = 64, kGemmK = 32;
-// LDS row pitch (elements): 32 k values plus 16 bytes, so that fragment rows
+constexpr int kGemmTile = 64, kGemmK = 64;
+// LDS row pitch (elements): 64 k values plus 16 bytes, so that fragment rows
 // start 16-byte aligned and neighbouring rows fall in different banks
 template <typename T> constexpr int gemm_pitch() { return kGemmK + 16 / (int)sizeof(T); }
 
-// One 64 x 32 operand tile into LDS as rows of k: row i, column k holds
-// X(row0 + i, k0 + k) where X(i, k) = x[i * s_i + k * s_k].  Each thread loads
-// 8 elements along whichever axis has unit stride, so neighbouring threads
-// read neighbouring addresses.
+__device__ __forceinline__ void load8(const __bf16* p, float (&v)[8]) {
+  const bf16x8 x = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = (float)x[j];
+}
+__device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) { v[j] = a[j]; v[4 + j] = b[j]; }
+}
+__device__ __forceinline__ void store8(__bf16* p, const float (&v)[8]) {
+  bf16x8 x;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = (__bf16)v[j];
+  *reinterpret_cast<bf16x8*>(p) = x;
+}
+__device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
+  f32x4 a, b;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) { a[j] = v[j]; b[j] = v[4 + j]; }
+  *reinterpret_cast<f32x4*>(p) = a;
+  *reinterpret_cast<f32x4*>(p + 4) = b;
+}
+
+// One 64 x 64 operand tile into LDS as rows of k: row i, column k holds
+// X(row0 + i, k0 + k) where X(i, k) = x[i * s_i + k * s_k].  Each thread
+// loads two runs of 8 elements along the unit-stride axis (16-byte loads when
+// the run is in range; the host keeps unit-stride rows 8-element aligned).
 template <typename T, typename TX>
 __device__ __forceinline__ void gemm_stage(T* dst, const TX* x, int64_t s_i, int64_t s_k, int row0, int nrows,
                                            int k0, int kend) {
   constexpr int PITCH = gemm_pitch<T>();
   const int t = threadIdx.x;
-  int ii, kk, di, dk;
-  if (s_k == 1) {
-    ii = t >> 2; kk = (t & 3) * 8; di = 0; dk = 1;
-  } else {
-    kk = t >> 3; ii = (t & 7) * 8; di = 1; dk = 0;
-  }
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int i = row0 + ii + j * di, k = k0 + kk + j * dk;
-    const float v = (i < nrows && k < kend) ? to_f32(x[(int64_t)i * s_i + (int64_t)k * s_k]) : 0.f;
-    dst[(ii + j * di) * PITCH + kk + j * dk] = from_f32<T>(v);
+  for (int q = 0; q < 2; ++q) {
+    float v[8];
+    if (s_k == 1) {
+      const int ii = (t >> 3) + 32 * q, kk = (t & 7) * 8;
+      const int i = row0 + ii, k = k0 + kk;
+      if (i < nrows && k + 8 <= kend) {
+        load8(x + (int64_t)i * s_i + k, v);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (i < nrows && k + j < kend) ? to_f32(x[(int64_t)i * s_i + k + j]) : 0.f;
+      }
+      store8(dst + ii * PITCH + kk, v);
+    } else {
+      const int kk = (t >> 3) + 32 * q, ii = (t & 7) * 8;
+      const int i = row0 + ii, k = k0 + kk;
+      if (s_i == 1 && i + 8 <= nrows && k < kend) {
+        load8(x + (int64_t)k * s_k + i, v);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          v[j] = (i + j < nrows && k < kend) ? to_f32(x[(int64_t)(i + j) * s_i + (int64_t)k * s_k]) : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dst[(ii + j) * PITCH + kk] = from_f32<T>(v[j]);
+    }
   }
 }
 
-template <typename T, typename TA, typename TB>
+template <typename T>
 __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
   constexpr int PITCH = gemm_pitch<T>();
   __shared__ __attribute__((aligned(16))) T As[kGemmTile * PITCH];
   __shared__ __attribute__((aligned(16))) T Bs[kGemmTile * PITCH];
   const int lane = lane_id(), wave = wave_id(), g = lane >> 5, c = lane & 31;
   const int m0 = blockIdx.y * kGemmTile, n0 = blockIdx.x * kGemmTile;
-  const int kbeg = blockIdx.z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
+  const int prob = blockIdx.z / p.splits, z = blockIdx.z % p.splits;
+  const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
   const int mw = wave >> 1, nw = wave & 1;  // this wave's 32 x 32 quarter
   f32x16 acc;
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-  for (int seg = 0; seg < p.nseg; ++seg) {
-    const TA* A = static_cast<const TA*>(p.a[seg]);
-    const TB* Bm = static_cast<const TB*>(p.b[seg]);
+  const int seg0 = p.nprob > 1 ? prob : 0, seg1 = p.nprob > 1 ? prob + 1 : p.nseg;
+  for (int seg = seg0; seg < seg1; ++seg) {
+    const T* A = static_cast<const T*>(p.a[seg]);
+    const T* Bm = static_cast<const T*>(p.b[seg]);
     for (int k0 = kbeg; k0 < kend; k0 += kGemmK) {
       gemm_stage<T>(As, A, p.a_m, p.a_k, m0, p.M, k0, kend);
       gemm_stage<T>(Bs, Bm, p.b_n, p.b_k, n0, p.N, k0, kend);
       __syncthreads();
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
+      for (int ks = 0; ks < kGemmK / 16; ++ks)
         mma(acc, load_frag(As + (32 * mw + c) * PITCH + 16 * ks + 8 * g),
             load_frag(Bs + (32 * nw + c) * PITCH + 16 * ks + 8 * g));
       __syncthreads();
     }
   }
-  float* out = p.c + (int64_t)blockIdx.z * p.split_stride;
+  const int64_t base = ((int64_t)prob * p.splits + z) * p.split_stride;
   const int n = n0 + 32 * nw + c;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int m = m0 + 32 * mw + acc_row(lane, r);
-    if (m < p.M && n < p.N) out[(int64_t)m * p.ldc + n] = acc[r];
+    if (m < p.M && n < p.N) {
+      if (p.c_t) static_cast<T*>(p.c)[base + (int64_t)m * p.ldc + n] = from_f32<T>(acc[r]);
+      else static_cast<float*>(p.c)[base + (int64_t)m * p.ldc + n] = acc[r];
+    }
   }
 }
 
-__global__ __launch_bounds__(256) void k_sum_splits(const float* part, float* out, int64_t n, int splits) {
+struct SumOuts {
+  float* out[5];
+};
+
+__global__ __launch_bounds__(256) void k_sum_splits(const float* part, SumOuts o, int64_t n, int splits, int nprob) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+  if (i >= n * nprob) return;
+  const int pr = (int)(i / n);
+  const int64_t e = i % n;
   float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + i];
-  out[i] = s;
+  for (int z = 0; z < splits; ++z) s += part[((int64_t)pr * splits + z) * n + e];
+  o.out[pr][e] = s;
 }
 
 // ---------------------------------------------------------------------------
@@ -114,10 +163,59 @@ size_t attn_bwd_wave_bytes(int D, int Mp, bool dec, int elem_bytes) {
   return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (Mp + 4) + (size_t)2 * 32 * tbp * elem_bytes;
 }
 
+// Fragment of a long-side row: element j = x[n * sn + (d0 + j) * sd] (one
+// 16-byte load when the row is contiguous), zero when !ok.
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type long_frag(const T* x, int64_t sn, int64_t sd, int n, int d0, bool ok) {
+  typename Frag<T>::type f;
+  if (sd == 1) {
+    f = ok ? load_frag(x + (int64_t)n * sn + d0) : zero_frag<T>();
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = ok ? x[(int64_t)n * sn + (int64_t)(d0 + j) * sd] : from_f32<T>(0.f);
+  }
+  return f;
+}
+
+// Route-side operands of one block of 32 routes, loaded one block ahead.
+template <typename T, int D, bool DEC>
+struct ShortBlock {
+  static constexpr int KS = D / 16, DB = (D + 31) / 32;
+  typename Frag<T>::type a[KS], gr[KS];       // rows of A_sh and G_sh
+  typename Frag<T>::type at[2][DB], gt[2][DB];  // transposed fragments (gt: encode)
+  f32x4 l[4], cc[4];                          // encode: L (log2) and c of this lane's rows
+};
+
+template <typename T, int D, bool DEC>
+__device__ __forceinline__ void load_short(ShortBlock<T, D, DEC>& s, const T* ash, const T* gsh, const T* asht,
+                                           const T* gsht, const float* lrow, const float* crow, int sb, int lane) {
+  constexpr int KS = D / 16, DB = (D + 31) / 32;
+  const int g = lane >> 5, c = lane & 31;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    s.a[ks] = load_frag(ash + (32 * sb + c) * D + 16 * ks + 8 * g);
+    s.gr[ks] = load_frag(gsh + (32 * sb + c) * D + 16 * ks + 8 * g);
+  }
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int fo = (((sb * 2 + kk) * DB + db) * 64 + lane) * 8;
+      s.at[kk][db] = load_frag(asht + fo);
+      if constexpr (!DEC) s.gt[kk][db] = load_frag(gsht + fo);
+    }
+  if constexpr (!DEC) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      s.l[a] = *reinterpret_cast<const f32x4*>(lrow + 32 * sb + 8 * a + 4 * g);
+      s.cc[a] = *reinterpret_cast<const f32x4*>(crow + 32 * sb + 8 * a + 4 * g);
+    }
+  }
+}
+
 template <typename T, int D, bool DEC>
 __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
   using F = typename Frag<T>::type;
-  using TG = typename std::conditional<DEC, float, T>::type;
   constexpr int KS = D / 16, DB = (D + 31) / 32, TBP = tb_pitch<T>();
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
@@ -137,26 +235,24 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
   const T* gsh = static_cast<const T*>(p.gsh) + b * p.gsh_sb + h * p.gsh_sh;
   const T* gsht = DEC ? nullptr : static_cast<const T*>(p.gsht) + b * p.gsht_sb + h * p.gsht_sh;
   const T* blo = static_cast<const T*>(p.blo) + b * p.blo_sb + h * p.blo_sh;
-  const TG* glo = static_cast<const TG*>(p.glo) + b * p.glo_sb + h * p.glo_sh;
-  const float* lrow = DEC ? nullptr : p.lrow + (int64_t)bh * p.M;
+  const T* glo = static_cast<const T*>(p.glo) + b * p.glo_sb + h * p.glo_sh;
+  const float* lrow = DEC ? nullptr : p.lrow + (int64_t)bh * p.Mp;
   const float* crow = DEC ? nullptr : p.crow + (int64_t)bh * p.Mp;
+  T* dout_b = static_cast<T*>(p.dout_b);
+  T* dout_g = static_cast<T*>(p.dout_g);
 
   for (int i = 0; i < p.tpw; ++i) {
     const int n0 = ((r * p.tpw + i) * W + wave) * 32;  // wave-uniform
     if (n0 >= p.Nl) break;
     const int n = n0 + c;
     const bool nok = n < p.Nl;
-    const int nc = nok ? n : p.Nl - 1;
     // long-side B operands of S (keys) and dP (values), one lane per position
     F kb[KS], gb[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int d = 16 * ks + 8 * g + j;
-        kb[ks][j] = from_f32<T>(nok ? to_f32(blo[(int64_t)nc * p.blo_sn + (int64_t)d * p.blo_sd]) : 0.f);
-        gb[ks][j] = from_f32<T>(nok ? to_f32(glo[(int64_t)nc * p.glo_sn + (int64_t)d * p.glo_sd]) : 0.f);
-      }
+    for (int ks = 0; ks < KS; ++ks) {
+      kb[ks] = long_frag(blo, p.blo_sn, p.blo_sd, n, 16 * ks + 8 * g, nok);
+      gb[ks] = long_frag(glo, p.glo_sn, p.glo_sd, n, 16 * ks + 8 * g, nok);
+    }
     // long-side B operands of the short-side products (k = position, n = d)
     F kt[2][DB], gt[2][DB];
 #pragma unroll
@@ -167,8 +263,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         for (int j = 0; j < 8; ++j) {
           const int nn = n0 + 16 * kk + 8 * g + j, d = 32 * db + c;
           const bool ok = nn < p.Nl && d < D;
-          kt[kk][db][j] = from_f32<T>(ok ? to_f32(blo[(int64_t)nn * p.blo_sn + (int64_t)d * p.blo_sd]) : 0.f);
-          if (DEC) gt[kk][db][j] = from_f32<T>(ok ? to_f32(glo[(int64_t)nn * p.glo_sn + (int64_t)d * p.glo_sd]) : 0.f);
+          kt[kk][db][j] = ok ? blo[(int64_t)nn * p.blo_sn + (int64_t)d * p.blo_sd] : from_f32<T>(0.f);
+          if (DEC) gt[kk][db][j] = ok ? glo[(int64_t)nn * p.glo_sn + (int64_t)d * p.glo_sd] : from_f32<T>(0.f);
         }
     // decode: c = <dY_n, Y_n> over the head's channels, and the token's
     // log-normaliser over the routes (log2 units), online over route blocks
@@ -177,12 +273,11 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
       const T* y = static_cast<const T*>(p.ylo) + b * p.ylo_sb + h * p.ylo_sh;
       float sacc = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
+      for (int ks = 0; ks < KS; ++ks) {
+        const F yf = long_frag(y, p.ylo_sn, (int64_t)1, n, 16 * ks + 8 * g, nok);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int d = 16 * ks + 8 * g + j;
-          if (nok) sacc += glo[(int64_t)nc * p.glo_sn + (int64_t)d * p.glo_sd] * to_f32(y[(int64_t)nc * p.ylo_sn + d]);
-        }
+        for (int j = 0; j < 8; ++j) sacc += to_f32(gb[ks][j]) * to_f32(yf[j]);
+      }
       cl = sacc + other_half(sacc);
       float mx = -INFINITY, sm = 0.f;
       for (int sb = 0; sb < NS; ++sb) {
@@ -213,14 +308,17 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.f;
+    ShortBlock<T, D, DEC> cur, nxt;
+    load_short(cur, ash, gsh, asht, gsht, lrow, crow, 0, lane);
     for (int sb = 0; sb < NS; ++sb) {
+      if (sb + 1 < NS) load_short(nxt, ash, gsh, asht, gsht, lrow, crow, sb + 1, lane);
       f32x16 sc, dp;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[e] = dp[e] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        mma(sc, load_frag(ash + (32 * sb + c) * D + 16 * ks + 8 * g), kb[ks]);
-        mma(dp, load_frag(gsh + (32 * sb + c) * D + 16 * ks + 8 * g), gb[ks]);
+        mma(sc, cur.a[ks], kb[ks]);
+        mma(dp, cur.gr[ks], gb[ks]);
       }
       // P = exp(s S - L), dS = P (dP - c); rows past M and columns past the
       // long length are zero
@@ -233,8 +331,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         if constexpr (DEC) {
           L = Ll; cc = cl;
         } else {
-          L = m < p.M ? lrow[m] * kLog2e : 0.f;
-          cc = crow[m];
+          L = cur.l[rr >> 2][rr & 3]; cc = cur.cc[rr >> 2][rr & 3];
         }
         const float pv = ok ? exp2f(sc[rr] * p.sl2 - L) : 0.f;
         P[rr] = pv;
@@ -254,9 +351,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          const int fo = (((sb * 2 + kk) * DB + db) * 64 + lane) * 8;
-          mma(dk[db], load_frag(asht + fo), dsb[kk]);
-          if (!DEC) mma(dv[db], load_frag(gsht + fo), pb[kk]);
+          mma(dk[db], cur.at[kk][db], dsb[kk]);
+          if constexpr (!DEC) mma(dv[db], cur.gt[kk][db], pb[kk]);
         }
       // short side: dS (and P) transposed through LDS, tile [position][route]
 #pragma unroll
@@ -302,6 +398,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         }
       }
       __builtin_amdgcn_wave_barrier();
+      if (sb + 1 < NS) cur = nxt;
     }
     // long-side results for this wave's 32 positions: rows d, column = lane
     if (nok) {
@@ -312,17 +409,16 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         for (int a = 0; a < 4; ++a) {
           const int d = 32 * db + 8 * a + 4 * g;
           if (d < D) {
-            float* ob = p.dout_b + row + d;
-            f32x4 v;
+            float v[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) v[q] = p.s * dk[db][4 * a + q];
             if (p.acc_b) {
-              const f32x4 old = *reinterpret_cast<const f32x4*>(ob);
+              const typename Frag<T>::half old = load_half(dout_b + row + d);
 #pragma unroll
-              for (int q = 0; q < 4; ++q) v[q] += old[q];
+              for (int q = 0; q < 4; ++q) v[q] += to_f32(old[q]);
             }
-            *reinterpret_cast<f32x4*>(ob) = v;
-            if (!DEC) store4(p.dout_g + row + d, dv[db][4 * a], dv[db][4 * a + 1], dv[db][4 * a + 2], dv[db][4 * a + 3]);
+            store4(dout_b + row + d, v[0], v[1], v[2], v[3]);
+            if (!DEC) store4(dout_g + row + d, dv[db][4 * a], dv[db][4 * a + 1], dv[db][4 * a + 2], dv[db][4 * a + 3]);
           }
         }
     }
@@ -374,6 +470,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(BwdPrepParams p) {
       if (p.dot && m < p.M) cs += v * p.dot[((int64_t)o * p.M + m) * D + d];
     }
     if (p.c) p.c[i] = cs;
+    if (p.l2) p.l2[i] = m < p.M ? p.lse[(int64_t)o * p.M + m] * kLog2e : 0.f;
     return;
   }
   // one lane of a transposed fragment: [O][Mp / 32][2][DB][64][8]
@@ -420,18 +517,16 @@ size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes) {
 }
 
 template <typename T>
-hipError_t launch_gemm(const GemmParams& p, int types, int splits, hipStream_t s) {
-  dim3 grid((p.N + kGemmTile - 1) / kGemmTile, (p.M + kGemmTile - 1) / kGemmTile, splits);
-  switch (types) {
-    case kGemmFT: k_gemm<T, float, T><<<grid, 256, 0, s>>>(p); break;
-    case kGemmTF: k_gemm<T, T, float><<<grid, 256, 0, s>>>(p); break;
-    default: k_gemm<T, T, T><<<grid, 256, 0, s>>>(p); break;
-  }
+hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
+  dim3 grid((p.N + kGemmTile - 1) / kGemmTile, (p.M + kGemmTile - 1) / kGemmTile, p.nprob * p.splits);
+  k_gemm<T><<<grid, 256, 0, s>>>(p);
   return hipGetLastError();
 }
 
-hipError_t launch_sum_splits(const float* part, float* out, int64_t n, int splits, hipStream_t s) {
-  k_sum_splits<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, out, n, splits);
+hipError_t launch_sum_splits(const float* part, float* const* out, int64_t n, int splits, int nprob, hipStream_t s) {
+  SumOuts o{};
+  for (int i = 0; i < nprob && i < 5; ++i) o.out[i] = out[i];
+  k_sum_splits<<<(unsigned)((n * nprob + 255) / 256), 256, 0, s>>>(part, o, n, splits, nprob);
   return hipGetLastError();
 }
 
@@ -463,8 +558,8 @@ hipError_t launch_bwd_prep(const BwdPrepParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-template hipError_t launch_gemm<float>(const GemmParams&, int, int, hipStream_t);
-template hipError_t launch_gemm<__bf16>(const GemmParams&, int, int, hipStream_t);
+template hipError_t launch_gemm<float>(const GemmParams&, hipStream_t);
+template hipError_t launch_gemm<__bf16>(const GemmParams&, hipStream_t);
 template hipError_t launch_attn_bwd<float>(const AttnBwdParams&, int, bool, hipStream_t);
 template hipError_t launch_attn_bwd<__bf16>(const AttnBwdParams&, int, bool, hipStream_t);
 template hipError_t launch_bwd_prep<float>(const BwdPrepParams&, hipStream_t);

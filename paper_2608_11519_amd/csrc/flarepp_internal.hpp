@@ -181,22 +181,23 @@ constexpr int route_nq(int D, bool decode) {
 }
 
 // ---- backward (App. A.5) ---------------------------------------------------
-// C[M][N] (fp32) = sum over segments of sum_k A(m, k) B(k, n), with
+// C[M][N] = sum over segments of sum_k A(m, k) B(k, n) (A, B in T), with
 // A(m, k) = a[m * a_m + k * a_k] and B(k, n) = b[k * b_k + n * b_n] (elements).
-// Split-K: blockIdx.z covers k in [z * kchunk, (z + 1) * kchunk) and writes
-// c + z * split_stride.
+// Either nseg segments accumulate into one product (nprob = 1), or nprob
+// independent products of one segment each share the shapes and strides.
+// Split-K: product p, split z covers k in [z * kchunk, (z + 1) * kchunk) and
+// writes c + (p * splits + z) * split_stride (fp32), or, with c_t and a
+// single split, the compute type T.
 struct GemmParams {
-  int M, N, K, nseg;
-  const void* a[4];
-  const void* b[4];
+  int M, N, K, nseg, nprob, splits;
+  const void* a[5];
+  const void* b[5];
   int64_t a_m, a_k, b_k, b_n;
   int kchunk;
-  float* c;
+  void* c;
+  int c_t;
   int64_t ldc, split_stride;
 };
-// Which operand types a GEMM reads: A and B in the compute type T, or one of
-// them in fp32 (converted to T on the way into LDS).
-enum GemmTypes { kGemmTT = 0, kGemmFT = 1, kGemmTF = 2 };
 
 // SDPA backward over one (batch, head) pair and one chunk of the long axis
 // (keys of an encode, tokens of the decode).  The tile orientation is
@@ -216,16 +217,16 @@ struct AttnBwdParams {
   const void* asht; int64_t asht_sb, asht_sh; // A fragments of A_sh^T
   const void* gsh; int64_t gsh_sb, gsh_sh;    // rows [Mp][D]
   const void* gsht; int64_t gsht_sb, gsht_sh; // A fragments of G_sh^T (encode)
-  const float* lrow;  // encode: [B * H][M], natural log
+  const float* lrow;  // encode: [B * H][Mp], log-normaliser in log2 units
   const float* crow;  // encode: [B * H][Mp]
   // long side: element (b, h, n, d) at b * sb + h * sh + n * sn + d * sd
   const void* blo; int64_t blo_sb, blo_sh, blo_sn, blo_sd;  // type T
-  const void* glo; int64_t glo_sb, glo_sh, glo_sn, glo_sd;  // T (encode) or fp32 (decode)
+  const void* glo; int64_t glo_sb, glo_sh, glo_sn, glo_sd;  // type T
   const void* ylo; int64_t ylo_sb, ylo_sh, ylo_sn;          // decode: forward output rows (T)
-  // outputs: long side [B][Nl][H * D] fp32 (dout_b added to what is there
+  // outputs: long side [B][Nl][H * D] in T (dout_b added to what is there
   // when acc_b); short side partials [B][H][R][Mp][D] fp32
-  float* dout_b; int acc_b;
-  float* dout_g;
+  void* dout_b; int acc_b;
+  void* dout_g;
   float* part_a; float* part_g;
 };
 int attn_bwd_waves(int D, int Mp, bool dec, int elem_bytes);
@@ -240,17 +241,20 @@ struct BwdReduceParams {
 // Short-side operands of a backward call from fp32 (or T) rows src[O][M][D]:
 // T rows [O][Mp][D] (zero padded), the A fragments of src^T
 // [O][Mp / 32][2][DB][64][8] (lane (c, g), element j holds
-// src[32 sb + 16 kk + acc_row16(g, j)][32 db + c]), and, when dot is given,
-// c[O][Mp] = sum_d src[m][d] dot[m][d].
+// src[32 sb + 16 kk + acc_row16(g, j)][32 db + c]) when tfrag is given,
+// c[O][Mp] = sum_d src[m][d] dot[m][d] when dot is given, and
+// l2[O][Mp] = lse[O][M] * log2(e) when lse is given (zero padded).
 struct BwdPrepParams {
   const void* src; int src_is_f32;
   const float* dot;
+  const float* lse;
   int O, M, Mp, D;
-  void* rows; void* tfrag; float* c;
+  void* rows; void* tfrag; float* c; float* l2;
 };
-template <typename T> hipError_t launch_gemm(const GemmParams&, int types, int splits, hipStream_t);
+template <typename T> hipError_t launch_gemm(const GemmParams&, hipStream_t);
 template <typename T> hipError_t launch_attn_bwd(const AttnBwdParams&, int D, bool dec, hipStream_t);
-hipError_t launch_sum_splits(const float* part, float* out, int64_t n, int splits, hipStream_t);
+// out[p][i] = sum_z part[(p * splits + z) * n + i], p < nprob (at most 5)
+hipError_t launch_sum_splits(const float* part, float* const* out, int64_t n, int splits, int nprob, hipStream_t);
 hipError_t launch_bwd_reduce(const BwdReduceParams&, hipStream_t);
 template <typename T> hipError_t launch_bwd_prep(const BwdPrepParams&, hipStream_t);
 

@@ -348,17 +348,20 @@ def flarepp_mixer_backward_workspace_bytes(dtype: int, B: int, N: int, C: int, H
     return int(load().flarepp_mixer_backward_workspace_bytes(dtype, B, N, C, H, M))
 
 
-def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws):
+def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out=None):
     lib = load()
     B, N, C = X.shape
     M = seeds.shape[1]
     D = C // H
     dt = _dtype_code(X)
     f32 = dict(dtype=torch.float32, device=X.device)
-    g = {"dX": torch.empty((B, N, C), **f32)}
-    for k in ("dWk", "dWv", "dWkt", "dWvt", "dWo"):
-        g[k] = torch.empty((C, C), **f32)
-    g["dseeds"] = torch.empty((H, M, D), **f32)
+    if out is not None:
+        g = dict(out)
+    else:
+        g = {"dX": torch.empty((B, N, C), **f32)}
+        for k in ("dWk", "dWv", "dWkt", "dWvt", "dWo"):
+            g[k] = torch.empty((C, C), **f32)
+        g["dseeds"] = torch.empty((H, M, D), **f32)
     outs = [g[k] for k in ("dX", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds")]
     if debug:
         g["dZ"] = torch.empty((B, H, M, D), **f32)
@@ -373,10 +376,11 @@ def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws):
 
 
 def flarepp_mixer_backward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,
-                           ws: Optional[torch.Tensor] = None):
+                           ws: Optional[torch.Tensor] = None, out: Optional[dict] = None):
     """Gradients of <O, dO> for the FLARE++ mixer: a dict of fp32 tensors
-    dX [B, N, C], dWk, dWv, dWkt, dWvt, dWo [C, C] and dseeds [H, M, D]."""
-    return _backward(False, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws)
+    dX [B, N, C], dWk, dWv, dWkt, dWvt, dWo [C, C] and dseeds [H, M, D]
+    (written into ``out``'s tensors when given)."""
+    return _backward(False, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out)
 
 
 def flarepp_mixer_backward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,

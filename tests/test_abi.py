@@ -200,8 +200,8 @@ def test_backward_workspace_sizes():
     for dt in (fp.F32, fp.BF16):
         bs = 4 if dt == fp.F32 else 2
         n = fp.flarepp_mixer_backward_workspace_bytes(dt, 4, 16384, 128, 8, 128)
-        # K, K~, V, V~, Y in the storage type and five fp32 token gradients
-        assert n >= 4 * 16384 * 128 * (5 * bs + 5 * 4)
+        # K, K~, V, V~, Y and the five token gradients dY, dK, dV, dK~, dV~
+        assert n >= 4 * 16384 * 128 * 10 * bs
     # a head's route gradients must fit in LDS: M = 512 with D = 64 does not
     assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 2, 512) == 0
     assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 2, 256) > 0
