@@ -601,7 +601,7 @@ int gemm_splits(int64_t T, int64_t C, int* kchunk) {
 
 struct BwdWs {
   void *wf[4], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *Y, *q_op, *z_op;
-  float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2;
+  float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2, *L3;
   float *dZf, *dQ3, *dQf, *c1, *c2, *l1, *l2, *pa, *pg, *gpart;
   void *dY, *dK, *dV, *dKt, *dVt;
   void *Qr, *Qt, *Zr, *dZr, *dZt, *dQr, *dQt, *Sr, *St;
@@ -632,6 +632,7 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   w.Zf = (float*)cv.take(f4 * BH * M * D);
   w.L1 = (float*)cv.take(f4 * BH * M);
   w.L2 = (float*)cv.take(f4 * BH * M);
+  w.L3 = (float*)cv.take(f4 * BH * N);
   w.dY = cv.take(bs * T * C);
   w.dK = cv.take(bs * T * C);
   w.dV = cv.take(bs * T * C);
@@ -738,7 +739,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   r3.ka = w.q_op; r3.ka_sb = rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
   r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;
   r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
-  r3.y = w.Y; r3.y_sb = N * C; r3.y_row = C;
+  r3.y = w.Y; r3.y_sb = N * C; r3.y_row = C; r3.lse2 = w.L3;
   HIPTRY(launch_route<T>(r3, (int)D, true, s));
 
   // ---- merge: dY = dO W_O^T (dW_O is computed with the weight gradients) ----
@@ -765,7 +766,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a3.gsh = w.Zr; a3.gsh_sb = rtBS; a3.gsh_sh = rtHS;
   a3.blo = w.K; a3.blo_sb = tokBS; a3.blo_sh = tokHS; a3.blo_sn = D; a3.blo_sd = 1;
   a3.glo = w.dY; a3.glo_sb = N * C; a3.glo_sh = D; a3.glo_sn = C; a3.glo_sd = 1;
-  a3.ylo = w.Y; a3.ylo_sb = N * C; a3.ylo_sh = D; a3.ylo_sn = C;
+  a3.ylo = w.Y; a3.ylo_sb = N * C; a3.ylo_sh = D; a3.ylo_sn = C; a3.lcol = w.L3;
   a3.dout_b = w.dK; a3.acc_b = 0;
   a3.part_a = w.pa; a3.part_g = w.pg;
   HIPTRY(launch_attn_bwd<T>(a3, (int)D, true, s));

@@ -26,6 +26,7 @@ namespace flarepp {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 
 // ---------------------------------------------------------------------------
 // GEMM
@@ -59,6 +60,17 @@ __device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
   *reinterpret_cast<f32x4*>(p + 4) = b;
 }
 
+__device__ __forceinline__ void store_pair(__bf16* p, float a, float b) {
+  bf16x2_t v;
+  v[0] = (__bf16)a; v[1] = (__bf16)b;
+  *reinterpret_cast<bf16x2_t*>(p) = v;
+}
+__device__ __forceinline__ void store_pair(float* p, float a, float b) {
+  f32x2 v;
+  v[0] = a; v[1] = b;
+  *reinterpret_cast<f32x2*>(p) = v;
+}
+
 // One 64 x 64 operand tile into LDS as rows of k: row i, column k holds
 // X(row0 + i, k0 + k) where X(i, k) = x[i * s_i + k * s_k].  Each thread
 // loads two runs of 8 elements along the unit-stride axis (16-byte loads when
@@ -82,17 +94,24 @@ __device__ __forceinline__ void gemm_stage(T* dst, const TX* x, int64_t s_i, int
       }
       store8(dst + ii * PITCH + kk, v);
     } else {
-      const int kk = (t >> 3) + 32 * q, ii = (t & 7) * 8;
+      // two neighbouring k rows per thread, so that each LDS store writes
+      // the pair (k, k + 1) of one row i
+      if (q == 1) break;
+      const int kk = 2 * (t >> 3), ii = (t & 7) * 8;
       const int i = row0 + ii, k = k0 + kk;
-      if (s_i == 1 && i + 8 <= nrows && k < kend) {
+      float w[8];
+      if (s_i == 1 && i + 8 <= nrows && k + 2 <= kend) {
         load8(x + (int64_t)k * s_k + i, v);
+        load8(x + (int64_t)(k + 1) * s_k + i, w);
       } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < 8; ++j) {
           v[j] = (i + j < nrows && k < kend) ? to_f32(x[(int64_t)(i + j) * s_i + (int64_t)k * s_k]) : 0.f;
+          w[j] = (i + j < nrows && k + 1 < kend) ? to_f32(x[(int64_t)(i + j) * s_i + (int64_t)(k + 1) * s_k]) : 0.f;
+        }
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) dst[(ii + j) * PITCH + kk] = from_f32<T>(v[j]);
+      for (int j = 0; j < 8; ++j) store_pair(dst + (ii + j) * PITCH + kk, v[j], w[j]);
     }
   }
 }
@@ -164,16 +183,19 @@ size_t attn_bwd_wave_bytes(int D, int Mp, bool dec, int elem_bytes) {
 }
 
 // Fragment of a long-side row: element j = x[n * sn + (d0 + j) * sd] (one
-// 16-byte load when the row is contiguous), zero when !ok.
+// 16-byte load when the row is contiguous), zero when !ok.  The caller passes
+// an in-range row n even when !ok, so the loads need no branch.
 template <typename T>
 __device__ __forceinline__ typename Frag<T>::type long_frag(const T* x, int64_t sn, int64_t sd, int n, int d0, bool ok) {
   typename Frag<T>::type f;
   if (sd == 1) {
-    f = ok ? load_frag(x + (int64_t)n * sn + d0) : zero_frag<T>();
+    f = load_frag(x + (int64_t)n * sn + d0);
   } else {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) f[j] = ok ? x[(int64_t)n * sn + (int64_t)(d0 + j) * sd] : from_f32<T>(0.f);
+    for (int j = 0; j < 8; ++j) f[j] = x[(int64_t)n * sn + (int64_t)(d0 + j) * sd];
   }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = ok ? f[j] : from_f32<T>(0.f);
   return f;
 }
 
@@ -246,12 +268,14 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
     if (n0 >= p.Nl) break;
     const int n = n0 + c;
     const bool nok = n < p.Nl;
+    const int nc = nok ? n : p.Nl - 1;        // in-range row for the loads
+    const bool full_tile = n0 + 32 <= p.Nl;  // wave-uniform: no position masked
     // long-side B operands of S (keys) and dP (values), one lane per position
     F kb[KS], gb[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      kb[ks] = long_frag(blo, p.blo_sn, p.blo_sd, n, 16 * ks + 8 * g, nok);
-      gb[ks] = long_frag(glo, p.glo_sn, p.glo_sd, n, 16 * ks + 8 * g, nok);
+      kb[ks] = long_frag(blo, p.blo_sn, p.blo_sd, nc, 16 * ks + 8 * g, nok);
+      gb[ks] = long_frag(glo, p.glo_sn, p.glo_sd, nc, 16 * ks + 8 * g, nok);
     }
     // long-side B operands of the short-side products (k = position, n = d)
     F kt[2][DB], gt[2][DB];
@@ -263,44 +287,28 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         for (int j = 0; j < 8; ++j) {
           const int nn = n0 + 16 * kk + 8 * g + j, d = 32 * db + c;
           const bool ok = nn < p.Nl && d < D;
-          kt[kk][db][j] = ok ? blo[(int64_t)nn * p.blo_sn + (int64_t)d * p.blo_sd] : from_f32<T>(0.f);
-          if (DEC) gt[kk][db][j] = ok ? glo[(int64_t)nn * p.glo_sn + (int64_t)d * p.glo_sd] : from_f32<T>(0.f);
+          const int64_t at = (int64_t)min(nn, p.Nl - 1) * p.blo_sn + (int64_t)min(d, D - 1) * p.blo_sd;
+          const T kv = blo[at];
+          kt[kk][db][j] = ok ? kv : from_f32<T>(0.f);
+          if (DEC) {
+            const T gv = glo[(int64_t)min(nn, p.Nl - 1) * p.glo_sn + (int64_t)min(d, D - 1) * p.glo_sd];
+            gt[kk][db][j] = ok ? gv : from_f32<T>(0.f);
+          }
         }
     // decode: c = <dY_n, Y_n> over the head's channels, and the token's
-    // log-normaliser over the routes (log2 units), online over route blocks
+    // log-normaliser over the routes (log2 units) from the forward
     float Ll = 0.f, cl = 0.f;
     if constexpr (DEC) {
       const T* y = static_cast<const T*>(p.ylo) + b * p.ylo_sb + h * p.ylo_sh;
       float sacc = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const F yf = long_frag(y, p.ylo_sn, (int64_t)1, n, 16 * ks + 8 * g, nok);
+        const F yf = long_frag(y, p.ylo_sn, (int64_t)1, nc, 16 * ks + 8 * g, nok);
 #pragma unroll
         for (int j = 0; j < 8; ++j) sacc += to_f32(gb[ks][j]) * to_f32(yf[j]);
       }
       cl = sacc + other_half(sacc);
-      float mx = -INFINITY, sm = 0.f;
-      for (int sb = 0; sb < NS; ++sb) {
-        f32x16 sc;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sc[e] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) mma(sc, load_frag(ash + (32 * sb + c) * D + 16 * ks + 8 * g), kb[ks]);
-        float tm = -INFINITY;
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr)
-          if (32 * sb + acc_row(lane, rr) < p.M) tm = fmaxf(tm, sc[rr] * p.sl2);
-        tm = fmaxf(tm, other_half(tm));
-        const float nm = fmaxf(mx, tm);
-        float ts = 0.f;
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr)
-          if (32 * sb + acc_row(lane, rr) < p.M) ts += exp2f(sc[rr] * p.sl2 - nm);
-        ts += other_half(ts);
-        sm = sm * exp2f(mx - nm) + ts;
-        mx = nm;
-      }
-      Ll = mx + log2f(sm);
+      Ll = p.lcol[(int64_t)bh * p.Nl + nc];
     }
 
     f32x16 dk[DB], dv[DB];
@@ -311,7 +319,9 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
     ShortBlock<T, D, DEC> cur, nxt;
     load_short(cur, ash, gsh, asht, gsht, lrow, crow, 0, lane);
     for (int sb = 0; sb < NS; ++sb) {
-      if (sb + 1 < NS) load_short(nxt, ash, gsh, asht, gsht, lrow, crow, sb + 1, lane);
+      // the next block (the last block again at the end: the same number of
+      // loads in flight on every iteration)
+      load_short(nxt, ash, gsh, asht, gsht, lrow, crow, min(sb + 1, NS - 1), lane);
       f32x16 sc, dp;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[e] = dp[e] = 0.f;
@@ -323,17 +333,17 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
       // P = exp(s S - L), dS = P (dP - c); rows past M and columns past the
       // long length are zero
       f32x16 P, dS;
+      const bool full = full_tile && 32 * (sb + 1) <= p.M;  // wave-uniform
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
-        const int m = 32 * sb + acc_row(lane, rr);
-        const bool ok = nok && m < p.M;
         float L, cc;
         if constexpr (DEC) {
           L = Ll; cc = cl;
         } else {
           L = cur.l[rr >> 2][rr & 3]; cc = cur.cc[rr >> 2][rr & 3];
         }
-        const float pv = ok ? exp2f(sc[rr] * p.sl2 - L) : 0.f;
+        float pv = __builtin_amdgcn_exp2f(sc[rr] * p.sl2 - L);
+        if (!full && !(nok && 32 * sb + acc_row(lane, rr) < p.M)) pv = 0.f;
         P[rr] = pv;
         dS[rr] = pv * (dp[rr] - cc);
       }
@@ -398,7 +408,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         }
       }
       __builtin_amdgcn_wave_barrier();
-      if (sb + 1 < NS) cur = nxt;
+      cur = nxt;
     }
     // long-side results for this wave's 32 positions: rows d, column = lane
     if (nok) {

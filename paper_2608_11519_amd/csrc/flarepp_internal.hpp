@@ -53,8 +53,10 @@ struct RouteParams {
   float fast_lim;
   // encode output: partials [B][H][nchunks][Mp] x {(m, l), acc[D]}
   float* part_ml; float* part_acc; int Mp;
-  // decode output: y[b*y_sb + n*y_row + h*D + d]
+  // decode output: y[b*y_sb + n*y_row + h*D + d], and optionally each
+  // token's log-normaliser over the routes in log2 units, lse2[b*H + h][n]
   void* y; int64_t y_sb, y_row;
+  float* lse2;
 };
 
 struct PrepFusedParams {
@@ -207,8 +209,8 @@ struct GemmParams {
 //   short side: dA_sh = s dS B_lo (both),      dG_sh = P G_lo (decode).
 // Encode: A_sh = queries, G_sh = dOut, B_lo = keys, G_lo = values, L and c
 // per route.  Decode: A_sh = routes (its keys), G_sh = latents (its values),
-// B_lo = token keys (its queries), G_lo = dY, L and c per token (computed
-// in the kernel).
+// B_lo = token keys (its queries), G_lo = dY, L per token from the forward
+// and c per token computed in the kernel.
 struct AttnBwdParams {
   int B, H, Nl, M, Mp, R, tpw;   // long length, routes, chunks per (b, h), long tiles per wave
   float s, sl2;                  // 1/sqrt(D), and times log2(e)
@@ -223,6 +225,7 @@ struct AttnBwdParams {
   const void* blo; int64_t blo_sb, blo_sh, blo_sn, blo_sd;  // type T
   const void* glo; int64_t glo_sb, glo_sh, glo_sn, glo_sd;  // type T
   const void* ylo; int64_t ylo_sb, ylo_sh, ylo_sn;          // decode: forward output rows (T)
+  const float* lcol;  // decode: [B * H][Nl], each position's log-normaliser in log2 units
   // outputs: long side [B][Nl][H * D] in T (dout_b added to what is there
   // when acc_b); short side partials [B][H][R][Mp][D] fp32
   void* dout_b; int acc_b;

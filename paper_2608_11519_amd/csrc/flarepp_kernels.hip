@@ -272,6 +272,7 @@ __global__ __launch_bounds__(256) void k_route(RouteParams p) {
         p.part_ml[pidx * 2 + 1] = l;
       }
     } else if (qrow < p.qs_rows) {
+      if (p.lse2 && g == 0) p.lse2[bh * p.qs_rows + qrow] = m[i] + __log2f(l);
       const float inv = 1.f / l;
       T* yp = (T*)p.y + (int64_t)b * p.y_sb + (int64_t)qrow * p.y_row + h * D;
 #pragma unroll
