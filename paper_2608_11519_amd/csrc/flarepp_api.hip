@@ -602,7 +602,7 @@ int gemm_splits(int64_t T, int64_t C, int* kchunk) {
 struct BwdWs {
   void *wf[4], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *Y, *q_op, *z_op;
   float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2, *L3;
-  float *dZf, *dQ3, *dQf, *c1, *c2, *l1, *l2, *pa, *pg, *gpart;
+  float *dZf, *dQf, *c1, *c2, *l1, *l2, *pa, *pg, *pq, *gpart;
   void *dY, *dK, *dV, *dKt, *dVt;
   void *Qr, *Qt, *Zr, *dZr, *dZt, *dQr, *dQt, *Sr, *St;
   BwdSplit dec, enc;
@@ -639,7 +639,6 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   w.dKt = cv.take(bs * T * C);
   w.dVt = cv.take(bs * T * C);
   w.dZf = (float*)cv.take(f4 * BH * M * D);
-  w.dQ3 = (float*)cv.take(f4 * BH * M * D);
   w.dQf = (float*)cv.take(f4 * BH * M * D);
   w.c1 = (float*)cv.take(f4 * BH * Mp);
   w.c2 = (float*)cv.take(f4 * BH * Mp);
@@ -659,6 +658,7 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   const int64_t R = std::max<int64_t>(std::max(w.dec.R, w.enc.R), 1);
   w.pa = (float*)cv.take(f4 * BH * R * Mp * D);
   w.pg = (float*)cv.take(f4 * BH * R * Mp * D);
+  w.pq = (float*)cv.take(f4 * BH * R * Mp * D);
   w.splits = gemm_splits(T, C, &w.kchunk);
   w.gpart = (float*)cv.take(f4 * 5 * w.splits * C * C);
   w.bytes = cv.off;
@@ -750,13 +750,18 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   g.kchunk = (int)round_up(C, 64); g.c = w.dY; g.c_t = 1; g.ldc = C; g.split_stride = 0;
   HIPTRY(launch_gemm<T>(g, s));
 
-  // ---- call 3 (decode): queries K, keys Q, values Z ----
+  // ---- route-side operands of the calls: Q (rows and transposed), Z rows,
+  // the seeds (rows and transposed) ----
   BwdPrepParams bp{};
-  bp.src = w.Qf; bp.src_is_f32 = 1; bp.dot = nullptr; bp.O = (int)BH; bp.M = (int)M; bp.Mp = (int)Mp;
-  bp.D = (int)D; bp.rows = w.Qr; bp.tfrag = w.Qt; bp.c = nullptr;
+  bp.M = (int)M; bp.Mp = (int)Mp; bp.D = (int)D; bp.njobs = 3;
+  bp.job[0].src = w.Qf; bp.job[0].src_is_f32 = 1; bp.job[0].O = (int)BH;
+  bp.job[0].rows = w.Qr; bp.job[0].tfrag = w.Qt;
+  bp.job[1].src = w.Zf; bp.job[1].src_is_f32 = 1; bp.job[1].O = (int)BH; bp.job[1].rows = w.Zr;
+  bp.job[2].src = seeds; bp.job[2].src_is_f32 = f32 ? 1 : 0; bp.job[2].O = (int)H;
+  bp.job[2].rows = w.Sr; bp.job[2].tfrag = w.St;
   HIPTRY(launch_bwd_prep<T>(bp, s));
-  bp.src = w.Zf; bp.rows = w.Zr; bp.tfrag = nullptr;
-  HIPTRY(launch_bwd_prep<T>(bp, s));
+
+  // ---- call 3 (decode): queries K, keys Q, values Z ----
   const int64_t tfS = Mp * 32 * DB;  // elements per head of a transposed-fragment operand
   AttnBwdParams a3{};
   a3.B = (int)B; a3.H = (int)H; a3.Nl = (int)N; a3.M = (int)M; a3.Mp = (int)Mp;
@@ -770,16 +775,18 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a3.dout_b = w.dK; a3.acc_b = 0;
   a3.part_a = w.pa; a3.part_g = w.pg;
   HIPTRY(launch_attn_bwd<T>(a3, (int)D, true, s));
-  BwdReduceParams rd{};
-  rd.P = 1; rd.O = (int)BH; rd.R = w.dec.R; rd.M = (int)M; rd.Mp = (int)Mp; rd.D = (int)D;
-  rd.part = w.pg; rd.base = nullptr; rd.out = dZ_out ? dZ_out : w.dZf;
-  HIPTRY(launch_bwd_reduce(rd, s));
-  float* dZf = rd.out;
-  rd.part = w.pa; rd.out = w.dQ3;
-  HIPTRY(launch_bwd_reduce(rd, s));
 
-  // ---- call 2 (encode): queries Q, keys K, values V; dOut = dZ ----
-  bp.src = dZf; bp.dot = w.Zf; bp.rows = w.dZr; bp.tfrag = w.dZt; bp.c = w.c2; bp.lse = w.L2; bp.l2 = w.l2;
+  // ---- call 2 (encode): queries Q, keys K, values V; dOut = dZ, the sum of
+  // the decode's partials ----
+  BwdReduceParams rd{};
+  rd.P = 1; rd.O = (int)BH; rd.M = (int)M; rd.Mp = (int)Mp; rd.D = (int)D;
+  rd.part0 = w.pg; rd.R0 = w.dec.R; rd.out = dZ_out ? dZ_out : w.dZf;
+  HIPTRY(launch_bwd_reduce(rd, s));
+  bp = BwdPrepParams{};
+  bp.M = (int)M; bp.Mp = (int)Mp; bp.D = (int)D; bp.njobs = 1;
+  bp.job[0].src = rd.out; bp.job[0].src_is_f32 = 1; bp.job[0].O = (int)BH;
+  bp.job[0].rows = w.dZr; bp.job[0].tfrag = w.dZt; bp.job[0].dot = w.Zf; bp.job[0].c = w.c2;
+  bp.job[0].lse = w.L2; bp.job[0].l2 = w.l2;
   HIPTRY(launch_bwd_prep<T>(bp, s));
   AttnBwdParams a2{};
   a2.B = (int)B; a2.H = (int)H; a2.Nl = (int)N; a2.M = (int)M; a2.Mp = (int)Mp;
@@ -792,19 +799,19 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a2.blo = w.K; a2.blo_sb = tokBS; a2.blo_sh = tokHS; a2.blo_sn = D; a2.blo_sd = 1;
   a2.glo = w.Vdm; a2.glo_sb = dmBS; a2.glo_sh = dmHS; a2.glo_sn = 1; a2.glo_sd = Np;
   a2.dout_b = w.dK; a2.acc_b = 1; a2.dout_g = w.dV;
-  a2.part_a = w.pa;
+  a2.part_a = w.pq;
   HIPTRY(launch_attn_bwd<T>(a2, (int)D, false, s));
-  rd.R = w.enc.R; rd.part = w.pa; rd.base = w.dQ3; rd.out = dQ_out ? dQ_out : w.dQf;
-  HIPTRY(launch_bwd_reduce(rd, s));
-  float* dQf = rd.out;
 
-  // ---- call 1 (query synthesis): queries = seeds (shared), keys K~, values V~ ----
-  bp.src = dQf; bp.dot = w.Qf; bp.rows = w.dQr; bp.tfrag = w.dQt; bp.c = w.c1; bp.lse = w.L1; bp.l2 = w.l1;
+  // ---- call 1 (query synthesis): queries = seeds (shared), keys K~, values
+  // V~; dOut = dQ, the decode's and the encode's shares summed ----
+  rd.part0 = w.pa; rd.R0 = w.dec.R; rd.part1 = w.pq; rd.R1 = w.enc.R; rd.out = dQ_out ? dQ_out : w.dQf;
+  HIPTRY(launch_bwd_reduce(rd, s));
+  bp = BwdPrepParams{};
+  bp.M = (int)M; bp.Mp = (int)Mp; bp.D = (int)D; bp.njobs = 1;
+  bp.job[0].src = rd.out; bp.job[0].src_is_f32 = 1; bp.job[0].O = (int)BH;
+  bp.job[0].rows = w.dQr; bp.job[0].tfrag = w.dQt; bp.job[0].dot = w.Qf; bp.job[0].c = w.c1;
+  bp.job[0].lse = w.L1; bp.job[0].l2 = w.l1;
   HIPTRY(launch_bwd_prep<T>(bp, s));
-  BwdPrepParams sp2{};
-  sp2.src = seeds; sp2.src_is_f32 = f32 ? 1 : 0; sp2.dot = nullptr; sp2.O = (int)H; sp2.M = (int)M;
-  sp2.Mp = (int)Mp; sp2.D = (int)D; sp2.rows = w.Sr; sp2.tfrag = w.St; sp2.c = nullptr;
-  HIPTRY(launch_bwd_prep<T>(sp2, s));
   AttnBwdParams a1 = a2;
   a1.ash = w.Sr; a1.ash_sb = 0; a1.ash_sh = rtHS;
   a1.asht = w.St; a1.asht_sb = 0; a1.asht_sh = tfS;
@@ -812,8 +819,11 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a1.lrow = w.l1; a1.crow = w.c1;
   a1.blo = w.Kt; a1.glo = w.Vtdm;
   a1.dout_b = w.dKt; a1.acc_b = 0; a1.dout_g = w.dVt;
+  a1.part_a = w.pa;
   HIPTRY(launch_attn_bwd<T>(a1, (int)D, false, s));
-  rd.P = (int)B; rd.O = (int)H; rd.R = w.enc.R; rd.part = w.pa; rd.base = nullptr; rd.out = dseeds;
+  rd = BwdReduceParams{};
+  rd.P = (int)B; rd.O = (int)H; rd.M = (int)M; rd.Mp = (int)Mp; rd.D = (int)D;
+  rd.part0 = w.pa; rd.R0 = w.enc.R; rd.out = dseeds;
   HIPTRY(launch_bwd_reduce(rd, s));
 
   // ---- projections: dX = sum_j dG_j W_j^T; the weight gradients

@@ -13,7 +13,8 @@
 //   the end, over the waves in a fixed order into the chunk's partial.
 // * k_bwd_reduce sums those partials over the chunks (and over the batch for
 //   the shared seeds) in a fixed order; k_bwd_prep lays out the route-side
-//   operands of the next call (rows, transposed fragments, c = <dOut, Out>).
+//   operands of the next call (rows, transposed fragments, c = <dOut, Out>,
+//   the log2 normaliser).
 // No float atomics anywhere: every result is bitwise reproducible.
 #include <hip/hip_runtime.h>
 
@@ -458,48 +459,59 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdReduceParams p) {
   if (i >= n) return;
   const int o = (int)(i / ((int64_t)p.M * p.D)), md = (int)(i % ((int64_t)p.M * p.D));
   float s = p.base ? p.base[i] : 0.f;
-  for (int q = 0; q < p.P; ++q)
-    for (int r = 0; r < p.R; ++r) s += p.part[(((int64_t)q * p.O + o) * p.R + r) * p.Mp * p.D + md];
+  for (int q = 0; q < p.P; ++q) {
+    for (int r = 0; r < p.R0; ++r) s += p.part0[(((int64_t)q * p.O + o) * p.R0 + r) * p.Mp * p.D + md];
+    for (int r = 0; r < p.R1; ++r) s += p.part1[(((int64_t)q * p.O + o) * p.R1 + r) * p.Mp * p.D + md];
+  }
   p.out[i] = s;
 }
 
-template <typename T, typename TS>
+// Source value src[o][m][d] of a prep job (m < M).
+template <typename T>
+__device__ __forceinline__ float prep_value(const BwdPrepJob& J, int M, int D, int o, int m, int d) {
+  const int64_t i = ((int64_t)o * M + m) * D + d;
+  return J.src_is_f32 ? static_cast<const float*>(J.src)[i] : to_f32(static_cast<const T*>(J.src)[i]);
+}
+
+template <typename T>
 __global__ __launch_bounds__(256) void k_bwd_prep(BwdPrepParams p) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int D = p.D, DB = (D + 31) / 32;
-  const TS* src = static_cast<const TS*>(p.src);
-  const int64_t nrows = (int64_t)p.O * p.Mp;
-  if (i < nrows) {
-    // one padded row: T copy and c
-    const int o = (int)(i / p.Mp), m = (int)(i % p.Mp);
-    T* dst = static_cast<T*>(p.rows) + i * D;
-    float cs = 0.f;
-    for (int d = 0; d < D; ++d) {
-      const float v = m < p.M ? to_f32(src[((int64_t)o * p.M + m) * D + d]) : 0.f;
-      dst[d] = from_f32<T>(v);
-      if (p.dot && m < p.M) cs += v * p.dot[((int64_t)o * p.M + m) * D + d];
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int D = p.D, DB = (D + 31) / 32, NS = p.Mp / 32;
+  for (int jb = 0; jb < p.njobs; ++jb) {
+    const BwdPrepJob& J = p.job[jb];
+    const int64_t nrows = (int64_t)J.O * p.Mp;
+    const int64_t nfl = J.tfrag ? (int64_t)J.O * NS * 2 * DB * 64 : 0;
+    if (i < nrows) {
+      // one padded row: T copy, c and the log2 normaliser
+      const int o = (int)(i / p.Mp), m = (int)(i % p.Mp);
+      float cs = 0.f;
+      for (int d = 0; d < D; ++d) {
+        const float v = m < p.M ? prep_value<T>(J, p.M, D, o, m, d) : 0.f;
+        if (J.rows) static_cast<T*>(J.rows)[i * D + d] = from_f32<T>(v);
+        if (J.dot && m < p.M) cs += v * J.dot[((int64_t)o * p.M + m) * D + d];
+      }
+      if (J.c) J.c[i] = cs;
+      if (J.l2) J.l2[i] = m < p.M ? J.lse[(int64_t)o * p.M + m] * kLog2e : 0.f;
+      return;
     }
-    if (p.c) p.c[i] = cs;
-    if (p.l2) p.l2[i] = m < p.M ? p.lse[(int64_t)o * p.M + m] * kLog2e : 0.f;
-    return;
-  }
-  // one lane of a transposed fragment: [O][Mp / 32][2][DB][64][8]
-  if (!p.tfrag) return;
-  const int64_t f = i - nrows;
-  const int64_t nfl = (int64_t)p.O * (p.Mp / 32) * 2 * DB * 64;
-  if (f >= nfl) return;
-  const int lane = (int)(f % 64);
-  int64_t q = f / 64;
-  const int db = (int)(q % DB); q /= DB;
-  const int kk = (int)(q % 2); q /= 2;
-  const int sb = (int)(q % (p.Mp / 32));
-  const int o = (int)(q / (p.Mp / 32));
-  const int g = lane >> 5, c = lane & 31, d = 32 * db + c;
-  T* dst = static_cast<T*>(p.tfrag) + f * 8;
-  for (int j = 0; j < 8; ++j) {
-    const int m = 32 * sb + 16 * kk + acc_row16(g, j);
-    const float v = (m < p.M && d < D) ? to_f32(src[((int64_t)o * p.M + m) * D + d]) : 0.f;
-    dst[j] = from_f32<T>(v);
+    i -= nrows;
+    if (i < nfl) {
+      // one lane of a transposed fragment: [O][Mp / 32][2][DB][64][8]
+      const int lane = (int)(i % 64);
+      int64_t q = i / 64;
+      const int db = (int)(q % DB); q /= DB;
+      const int kk = (int)(q % 2); q /= 2;
+      const int sb = (int)(q % NS);
+      const int o = (int)(q / NS);
+      const int g = lane >> 5, c = lane & 31, d = 32 * db + c;
+      T* dst = static_cast<T*>(J.tfrag) + i * 8;
+      for (int j = 0; j < 8; ++j) {
+        const int m = 32 * sb + 16 * kk + acc_row16(g, j);
+        dst[j] = from_f32<T>((m < p.M && d < D) ? prep_value<T>(J, p.M, D, o, m, d) : 0.f);
+      }
+      return;
+    }
+    i -= nfl;
   }
 }
 
@@ -558,13 +570,17 @@ hipError_t launch_bwd_reduce(const BwdReduceParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
+int64_t bwd_prep_items(const BwdPrepParams& p, int jb) {
+  const BwdPrepJob& J = p.job[jb];
+  const int DB = (p.D + 31) / 32;
+  return (int64_t)J.O * p.Mp + (J.tfrag ? (int64_t)J.O * (p.Mp / 32) * 2 * DB * 64 : 0);
+}
+
 template <typename T>
 hipError_t launch_bwd_prep(const BwdPrepParams& p, hipStream_t s) {
-  const int DB = (p.D + 31) / 32;
-  const int64_t n = (int64_t)p.O * p.Mp + (p.tfrag ? (int64_t)p.O * (p.Mp / 32) * 2 * DB * 64 : 0);
-  const unsigned blocks = (unsigned)((n + 255) / 256);
-  if (p.src_is_f32) k_bwd_prep<T, float><<<blocks, 256, 0, s>>>(p);
-  else k_bwd_prep<T, T><<<blocks, 256, 0, s>>>(p);
+  int64_t n = 0;
+  for (int jb = 0; jb < p.njobs; ++jb) n += bwd_prep_items(p, jb);
+  k_bwd_prep<T><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
   return hipGetLastError();
 }
 

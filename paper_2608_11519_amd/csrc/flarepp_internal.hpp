@@ -236,23 +236,30 @@ int attn_bwd_waves(int D, int Mp, bool dec, int elem_bytes);
 size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes);
 
 // Fixed-order sums of backward partials: out[o][m][d] = base[o][m][d] +
-// sum_{p < P} sum_{r < R} part[((p * O + o) * R + r) * Mp * D + m * D + d].
+// sum_{p < P} (sum_{r < R0} part0[p][o][r][m][d] + sum_{r < R1} part1[p][o][r][m][d]),
+// partials laid out [P][O][R][Mp][D] fp32 (part1 and base optional).
 struct BwdReduceParams {
-  const float* part; const float* base; float* out;
-  int P, O, R, M, Mp, D;
+  const float* part0; int R0;
+  const float* part1; int R1;
+  const float* base; float* out;
+  int P, O, M, Mp, D;
 };
-// Short-side operands of a backward call from fp32 (or T) rows src[O][M][D]:
-// T rows [O][Mp][D] (zero padded), the A fragments of src^T
-// [O][Mp / 32][2][DB][64][8] (lane (c, g), element j holds
-// src[32 sb + 16 kk + acc_row16(g, j)][32 db + c]) when tfrag is given,
-// c[O][Mp] = sum_d src[m][d] dot[m][d] when dot is given, and
-// l2[O][Mp] = lse[O][M] * log2(e) when lse is given (zero padded).
-struct BwdPrepParams {
+// Short-side operands of a backward call from rows src[O][M][D] (fp32 or T),
+// each output optional: T rows [O][Mp][D] (zero padded); the A fragments of
+// src^T [O][Mp / 32][2][DB][64][8] (lane (c, g), element j holds
+// src[32 sb + 16 kk + acc_row16(g, j)][32 db + c]); c[O][Mp] = sum_d
+// src[m][d] dot[m][d]; l2[O][Mp] = lse[O][M] * log2(e) (zero padded).  Up to
+// three jobs run in one launch.
+struct BwdPrepJob {
   const void* src; int src_is_f32;
   const float* dot;
   const float* lse;
-  int O, M, Mp, D;
+  int O;
   void* rows; void* tfrag; float* c; float* l2;
+};
+struct BwdPrepParams {
+  int M, Mp, D, njobs;
+  BwdPrepJob job[3];
 };
 template <typename T> hipError_t launch_gemm(const GemmParams&, hipStream_t);
 template <typename T> hipError_t launch_attn_bwd(const AttnBwdParams&, int D, bool dec, hipStream_t);
@@ -260,6 +267,7 @@ template <typename T> hipError_t launch_attn_bwd(const AttnBwdParams&, int D, bo
 hipError_t launch_sum_splits(const float* part, float* const* out, int64_t n, int splits, int nprob, hipStream_t);
 hipError_t launch_bwd_reduce(const BwdReduceParams&, hipStream_t);
 template <typename T> hipError_t launch_bwd_prep(const BwdPrepParams&, hipStream_t);
+int64_t bwd_prep_items(const BwdPrepParams&, int job);
 
 template <typename T> hipError_t launch_weight_frags(const WeightFragParams&, hipStream_t);
 template <typename Ts, typename T> hipError_t launch_route_prep(const RoutePrepParams&, hipStream_t);
