@@ -157,6 +157,21 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
   }
 }
 
+// s + x[0] + x[st] + ... + x[(n - 1) st], added in that order; the loads of
+// a group of 8 are issued before its adds.
+__device__ __forceinline__ float sum_run(float s, const float* x, int64_t st, int n) {
+  int r = 0;
+  for (; r + 8 <= n; r += 8) {
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = x[(int64_t)(r + j) * st];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += v[j];
+  }
+  for (; r < n; ++r) s += x[(int64_t)r * st];
+  return s;
+}
+
 struct SumOuts {
   float* out[5];
 };
@@ -166,21 +181,19 @@ __global__ __launch_bounds__(256) void k_sum_splits(const float* part, SumOuts o
   if (i >= n * nprob) return;
   const int pr = (int)(i / n);
   const int64_t e = i % n;
-  float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += part[((int64_t)pr * splits + z) * n + e];
-  o.out[pr][e] = s;
+  o.out[pr][e] = sum_run(0.f, part + (int64_t)pr * splits * n + e, n, splits);
 }
 
 // ---------------------------------------------------------------------------
 // SDPA backward over a chunk of the long axis
 // ---------------------------------------------------------------------------
 // LDS per wave: the short-side slot(s) [D][Mp + 4] fp32 (route index fastest,
-// padded so that the lanes' rows fall in different banks) and two transpose
-// tiles [32][32 + 16 bytes] of T.
+// padded so that the lanes' rows fall in different banks) and one transpose
+// tile [32][32 + 16 bytes] of T (dS, then P in the decode).
 template <typename T> constexpr int tb_pitch() { return 32 + 16 / (int)sizeof(T); }
 size_t attn_bwd_wave_bytes(int D, int Mp, bool dec, int elem_bytes) {
   const int tbp = 32 + 16 / elem_bytes;
-  return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (Mp + 4) + (size_t)2 * 32 * tbp * elem_bytes;
+  return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (Mp + 4) + (size_t)32 * tbp * elem_bytes;
 }
 
 // Fragment of a long-side row: element j = x[n * sn + (d0 + j) * sd] (one
@@ -249,8 +262,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
   const int slot_floats = (DEC ? 2 : 1) * D * SP;
   float* slot_a = reinterpret_cast<float*>(smem) + wave * slot_floats;
   float* slot_g = slot_a + D * SP;
-  T* tb = reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) + wave * 2 * 32 * TBP;
-  T* tb2 = tb + 32 * TBP;
+  T* tb = reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) + wave * 32 * TBP;
   for (int i = lane; i < slot_floats; i += 64) slot_a[i] = 0.f;
 
   const T* ash = static_cast<const T*>(p.ash) + b * p.ash_sb + h * p.ash_sh;
@@ -365,21 +377,28 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
           mma(dk[db], cur.at[kk][db], dsb[kk]);
           if constexpr (!DEC) mma(dv[db], cur.gt[kk][db], pb[kk]);
         }
-      // short side: dS (and P) transposed through LDS, tile [position][route]
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        store4(tb + c * TBP + 8 * a + 4 * g, dS[4 * a], dS[4 * a + 1], dS[4 * a + 2], dS[4 * a + 3]);
-        if (DEC) store4(tb2 + c * TBP + 8 * a + 4 * g, P[4 * a], P[4 * a + 1], P[4 * a + 2], P[4 * a + 3]);
-      }
-      __builtin_amdgcn_wave_barrier();
+      // short side: dS (then P in the decode) transposed through the wave's
+      // LDS tile [position][route]
       F dsa[2], pa[2];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+        store4(tb + c * TBP + 8 * a + 4 * g, dS[4 * a], dS[4 * a + 1], dS[4 * a + 2], dS[4 * a + 3]);
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          dsa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
-          if (DEC) pa[kk][j] = tb2[(16 * kk + 8 * g + j) * TBP + c];
-        }
+        for (int j = 0; j < 8; ++j) dsa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
+      if constexpr (DEC) {
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+          store4(tb + c * TBP + 8 * a + 4 * g, P[4 * a], P[4 * a + 1], P[4 * a + 2], P[4 * a + 3]);
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) pa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
+      }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         f32x16 o, o2;
@@ -459,9 +478,10 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdReduceParams p) {
   if (i >= n) return;
   const int o = (int)(i / ((int64_t)p.M * p.D)), md = (int)(i % ((int64_t)p.M * p.D));
   float s = p.base ? p.base[i] : 0.f;
+  const int64_t st = (int64_t)p.Mp * p.D;
   for (int q = 0; q < p.P; ++q) {
-    for (int r = 0; r < p.R0; ++r) s += p.part0[(((int64_t)q * p.O + o) * p.R0 + r) * p.Mp * p.D + md];
-    for (int r = 0; r < p.R1; ++r) s += p.part1[(((int64_t)q * p.O + o) * p.R1 + r) * p.Mp * p.D + md];
+    s = sum_run(s, p.part0 + (((int64_t)q * p.O + o) * p.R0) * st + md, st, p.R0);
+    if (p.part1) s = sum_run(s, p.part1 + (((int64_t)q * p.O + o) * p.R1) * st + md, st, p.R1);
   }
   p.out[i] = s;
 }
@@ -482,13 +502,24 @@ __global__ __launch_bounds__(256) void k_bwd_prep(BwdPrepParams p) {
     const int64_t nrows = (int64_t)J.O * p.Mp;
     const int64_t nfl = J.tfrag ? (int64_t)J.O * NS * 2 * DB * 64 : 0;
     if (i < nrows) {
-      // one padded row: T copy, c and the log2 normaliser
+      // one padded row: T copy, c and the log2 normaliser, 8 channels at a
+      // time (D is a multiple of 16)
       const int o = (int)(i / p.Mp), m = (int)(i % p.Mp);
+      const int64_t si = ((int64_t)o * p.M + m) * D;
       float cs = 0.f;
-      for (int d = 0; d < D; ++d) {
-        const float v = m < p.M ? prep_value<T>(J, p.M, D, o, m, d) : 0.f;
-        if (J.rows) static_cast<T*>(J.rows)[i * D + d] = from_f32<T>(v);
-        if (J.dot && m < p.M) cs += v * J.dot[((int64_t)o * p.M + m) * D + d];
+      for (int d0 = 0; d0 < D; d0 += 8) {
+        float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        if (m < p.M) {
+          if (J.src_is_f32) load8(static_cast<const float*>(J.src) + si + d0, v);
+          else load8(static_cast<const T*>(J.src) + si + d0, v);
+          if (J.dot) {
+            float w[8];
+            load8(J.dot + si + d0, w);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) cs += v[j] * w[j];
+          }
+        }
+        if (J.rows) store8(static_cast<T*>(J.rows) + i * D + d0, v);
       }
       if (J.c) J.c[i] = cs;
       if (J.l2) J.l2[i] = m < p.M ? J.lse[(int64_t)o * p.M + m] * kLog2e : 0.f;

@@ -96,52 +96,67 @@ __global__ void k_dmajor(DmajorParams p) {
 //   kHeadsDMajor     [B][H][D][Np]  (zero padded to Np tokens)
 //   kPlain           [B][N][C]
 // ---------------------------------------------------------------------------
+// One wave: 32 tokens of one weight's product, up to four 32-column output
+// blocks at once (independent accumulators), the token fragments loaded once.
+constexpr int kProjBlocks = 4;
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_project(ProjParams p) {
   using F = typename Frag<T>::type;
   const int lane = lane_id(), g = lane >> 5, c = lane & 31;
-  const int CB = p.C / 32, KS = p.C / 16, NB = p.Np / 32;
+  const int CB = p.C / 32, KS = p.C / 16, NB = p.Np / 32, CG = (CB + kProjBlocks - 1) / kProjBlocks;
   const int64_t u = (int64_t)blockIdx.x * 4 + wave_id();
-  const int64_t total = (int64_t)p.B * NB * CB * p.nw;
+  const int64_t total = (int64_t)p.B * NB * CG * p.nw;
   if (u >= total) return;
-  const int cb = (int)(u % CB);
-  const int w = (int)((u / CB) % p.nw);
-  const int64_t bn = u / ((int64_t)CB * p.nw);
+  const int cg = (int)(u % CG);
+  const int w = (int)((u / CG) % p.nw);
+  const int64_t bn = u / ((int64_t)CG * p.nw);
   const int b = (int)(bn / NB), n0 = (int)(bn % NB) * 32;
   const int layout = p.layout[w];
   const T* X = (const T*)p.x + ((int64_t)b * p.N) * p.C;
-  const T* wf = (const T*)p.wf[w] + (int64_t)cb * KS * 512;
   const int xrow = n0 + c;
   const bool xok = xrow < p.N;
-  f32x16 acc;
+  f32x16 acc[kProjBlocks];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  for (int q = 0; q < kProjBlocks; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[q][r] = 0.f;
   for (int ks = 0; ks < KS; ++ks) {
-    F xf = xok ? load_frag(X + (int64_t)xrow * p.C + 16 * ks + 8 * g) : zero_frag<T>();
-    F wv = load_frag(wf + ((int64_t)ks * 64 + lane) * 8);
-    if (layout == kHeadsDMajor) mma(acc, xf, wv);   // rows = tokens, cols = channels
-    else mma(acc, wv, xf);                          // rows = channels, cols = tokens
+    const F xf = xok ? load_frag(X + (int64_t)xrow * p.C + 16 * ks + 8 * g) : zero_frag<T>();
+#pragma unroll
+    for (int q = 0; q < kProjBlocks; ++q) {
+      const int cb = cg * kProjBlocks + q;
+      if (cb >= CB) break;  // wave-uniform
+      const F wv = load_frag((const T*)p.wf[w] + ((int64_t)cb * KS + ks) * 512 + lane * 8);
+      if (layout == kHeadsDMajor) mma(acc[q], xf, wv);   // rows = tokens, cols = channels
+      else mma(acc[q], wv, xf);                          // rows = channels, cols = tokens
+    }
   }
   T* out = (T*)p.out[w];
   const int D = p.D;
-  if (layout == kHeadsDMajor) {
-    const int col = 32 * cb + c, h = col / D, d = col % D;
-    T* o = out + (((int64_t)b * p.H + h) * D + d) * p.Np + n0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      store4(o + 8 * q + 4 * g, acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
-  } else if (xok) {
+  for (int q = 0; q < kProjBlocks; ++q) {
+    const int cb = cg * kProjBlocks + q;
+    if (cb >= CB) break;  // wave-uniform
+    if (layout == kHeadsDMajor) {
+      const int col = 32 * cb + c, h = col / D, d = col % D;
+      T* o = out + (((int64_t)b * p.H + h) * D + d) * p.Np + n0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int col = 32 * cb + 8 * q + 4 * g;
-      T* o;
-      if (layout == kPlain) {
-        o = out + ((int64_t)b * p.N + xrow) * p.C + col;
-      } else {
-        const int h = col / D, d = col % D;
-        o = out + (((int64_t)b * p.H + h) * p.N + xrow) * D + d;
+      for (int r4 = 0; r4 < 4; ++r4)
+        store4(o + 8 * r4 + 4 * g, acc[q][4 * r4], acc[q][4 * r4 + 1], acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
+    } else if (xok) {
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = 32 * cb + 8 * r4 + 4 * g;
+        T* o;
+        if (layout == kPlain) {
+          o = out + ((int64_t)b * p.N + xrow) * p.C + col;
+        } else {
+          const int h = col / D, d = col % D;
+          o = out + (((int64_t)b * p.H + h) * p.N + xrow) * D + d;
+        }
+        store4(o, acc[q][4 * r4], acc[q][4 * r4 + 1], acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
       }
-      store4(o, acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
     }
   }
 }
@@ -313,7 +328,7 @@ hipError_t launch_dmajor(const DmajorParams& p, hipStream_t s) {
 
 template <typename T>
 hipError_t launch_project(const ProjParams& p, hipStream_t s) {
-  const int64_t units = (int64_t)p.B * (p.Np / 32) * (p.C / 32) * p.nw;
+  const int64_t units = (int64_t)p.B * (p.Np / 32) * ((p.C / 32 + kProjBlocks - 1) / kProjBlocks) * p.nw;
   k_project<T><<<blocks_for(units, 4), 256, 0, s>>>(p);
   return hipGetLastError();
 }
