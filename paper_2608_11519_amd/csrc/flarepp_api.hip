@@ -590,10 +590,12 @@ BwdSplit bwd_split(int64_t BH, int64_t Nl, int D, int Mp, bool dec, int elem_byt
 }
 
 // Split-K of the five token reductions dW = X^T dG, dW_O = Y^T dO (K = B N
-// tokens), computed in one launch: about 1024 workgroups in all.
+// tokens), computed in one launch: about 512 workgroups in all (the GEMM's
+// workgroup tile is 128 x 128 for C >= 128, else 64 x 64).
 int gemm_splits(int64_t T, int64_t C, int* kchunk) {
-  const int64_t tiles = cdiv(C, 64) * cdiv(C, 64);
-  int64_t splits = std::max<int64_t>(1, std::min<int64_t>(cdiv(T, 256), cdiv(1024, 5 * tiles)));
+  const int64_t tile = C >= 128 ? 128 : 64;
+  const int64_t tiles = cdiv(C, tile) * cdiv(C, tile);
+  int64_t splits = std::max<int64_t>(1, std::min<int64_t>(cdiv(T, 256), cdiv(512, 5 * tiles)));
   const int64_t kc = round_up(cdiv(T, splits), 64);
   *kchunk = (int)kc;
   return (int)cdiv(T, kc);

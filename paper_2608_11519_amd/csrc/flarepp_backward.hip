@@ -32,10 +32,20 @@ typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 // ---------------------------------------------------------------------------
 // GEMM
 // ---------------------------------------------------------------------------
-constexpr int kGemmTile = 64, kGemmK = 64;
-// LDS row pitch (elements): 64 k values plus 16 bytes, so that fragment rows
+// k step per LDS stage: 64 for bf16, 32 for fp32 (same bytes)
+template <typename T> constexpr int gemm_k() { return sizeof(T) == 2 ? 64 : 32; }
+// LDS row pitch (elements): the k step plus 16 bytes, so that fragment rows
 // start 16-byte aligned and neighbouring rows fall in different banks
-template <typename T> constexpr int gemm_pitch() { return kGemmK + 16 / (int)sizeof(T); }
+template <typename T> constexpr int gemm_pitch() { return gemm_k<T>() + 16 / (int)sizeof(T); }
+// LDS offset of element (row i, k) of a staged tile: the 8-element blocks of
+// a row are permuted by the row's group of 8 (block ^ (i / 8)), so that the
+// k-pair stores of eight rows 8 apart fall in different banks; a fragment
+// (8 consecutive k from a multiple of 8) stays contiguous.
+template <typename T>
+__device__ __forceinline__ int gemm_lds(int i, int k) {
+  constexpr int NB = gemm_k<T>() / 8;
+  return i * gemm_pitch<T>() + ((((k >> 3) ^ (i >> 3)) & (NB - 1)) << 3) + (k & 7);
+}
 
 __device__ __forceinline__ void load8(const __bf16* p, float (&v)[8]) {
   const bf16x8 x = *reinterpret_cast<const bf16x8*>(p);
@@ -60,7 +70,6 @@ __device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
   *reinterpret_cast<f32x4*>(p) = a;
   *reinterpret_cast<f32x4*>(p + 4) = b;
 }
-
 __device__ __forceinline__ void store_pair(__bf16* p, float a, float b) {
   bf16x2_t v;
   v[0] = (__bf16)a; v[1] = (__bf16)b;
@@ -72,89 +81,181 @@ __device__ __forceinline__ void store_pair(float* p, float a, float b) {
   *reinterpret_cast<f32x2*>(p) = v;
 }
 
-// One 64 x 64 operand tile into LDS as rows of k: row i, column k holds
-// X(row0 + i, k0 + k) where X(i, k) = x[i * s_i + k * s_k].  Each thread
-// loads two runs of 8 elements along the unit-stride axis (16-byte loads when
-// the run is in range; the host keeps unit-stride rows 8-element aligned).
-template <typename T, typename TX>
-__device__ __forceinline__ void gemm_stage(T* dst, const TX* x, int64_t s_i, int64_t s_k, int row0, int nrows,
-                                           int k0, int kend) {
-  constexpr int PITCH = gemm_pitch<T>();
-  const int t = threadIdx.x;
+// One ROWS x K operand tile, staged through registers into LDS as rows of k:
+// row i, column k holds X(row0 + i, k0 + k) where X(i, k) = x[i * s_i + k *
+// s_k].  Unit stride along k: runs of 8 k values (16-byte loads and stores).
+// Otherwise (unit stride along i): runs of 8 rows for two neighbouring k,
+// stored as k pairs.  The host keeps unit-stride runs 8-element aligned.
+// gemm_load issues the global loads of a tile; gemm_store writes them to LDS
+// later, so the loads of the next k step overlap the current one's MFMAs.
+template <typename T, int ROWS>
+struct GemmStage {
+  static constexpr int K = gemm_k<T>();
+  static constexpr int NK = (ROWS * (K / 8) + 255) / 256;      // k runs per thread
+  static constexpr int NP = ((ROWS / 8) * (K / 2) + 255) / 256;  // row-run pairs per thread
+  static constexpr int NF = NK > 2 * NP ? NK : 2 * NP;
+  typename Frag<T>::type f[NF];
+};
+
+// 16-byte aligned stores of a fragment (fp32: two 16-byte halves)
+__device__ __forceinline__ void store_frag8(__bf16* p, const bf16x8& f) { *reinterpret_cast<bf16x8*>(p) = f; }
+__device__ __forceinline__ void store_frag8(float* p, const f32x8& f) {
+  f32x4 a, b;
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    float v[8];
-    if (s_k == 1) {
-      const int ii = (t >> 3) + 32 * q, kk = (t & 7) * 8;
+  for (int j = 0; j < 4; ++j) { a[j] = f[j]; b[j] = f[4 + j]; }
+  *reinterpret_cast<f32x4*>(p) = a;
+  *reinterpret_cast<f32x4*>(p + 4) = b;
+}
+
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type frag_from(const float (&v)[8]) {
+  typename Frag<T>::type f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = from_f32<T>(v[j]);
+  return f;
+}
+
+template <typename T, int ROWS>
+__device__ __forceinline__ void gemm_load(GemmStage<T, ROWS>& st, const T* x, int64_t s_i, int64_t s_k, int row0,
+                                          int nrows, int k0, int kend) {
+  constexpr int K = gemm_k<T>();
+  const int t = threadIdx.x;
+  if (s_k == 1) {
+    constexpr int RPR = K / 8;  // runs per row
+#pragma unroll
+    for (int q = 0; q < GemmStage<T, ROWS>::NK; ++q) {
+      const int r = t + 256 * q;
+      if (r >= ROWS * RPR) break;
+      const int ii = r / RPR, kk = (r % RPR) * 8;
       const int i = row0 + ii, k = k0 + kk;
       if (i < nrows && k + 8 <= kend) {
-        load8(x + (int64_t)i * s_i + k, v);
+        st.f[q] = load_frag(x + (int64_t)i * s_i + k);
       } else {
+        float v[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) v[j] = (i < nrows && k + j < kend) ? to_f32(x[(int64_t)i * s_i + k + j]) : 0.f;
+        st.f[q] = frag_from<T>(v);
       }
-      store8(dst + ii * PITCH + kk, v);
-    } else {
-      // two neighbouring k rows per thread, so that each LDS store writes
-      // the pair (k, k + 1) of one row i
-      if (q == 1) break;
-      const int kk = 2 * (t >> 3), ii = (t & 7) * 8;
+    }
+  } else {
+    constexpr int IG = ROWS / 8;  // groups of 8 rows
+#pragma unroll
+    for (int q = 0; q < GemmStage<T, ROWS>::NP; ++q) {
+      const int r = t + 256 * q;
+      if (r >= IG * (K / 2)) break;
+      const int ii = (r % IG) * 8, kk = 2 * (r / IG);
       const int i = row0 + ii, k = k0 + kk;
-      float w[8];
       if (s_i == 1 && i + 8 <= nrows && k + 2 <= kend) {
-        load8(x + (int64_t)k * s_k + i, v);
-        load8(x + (int64_t)(k + 1) * s_k + i, w);
+        st.f[2 * q] = load_frag(x + (int64_t)k * s_k + i);
+        st.f[2 * q + 1] = load_frag(x + (int64_t)(k + 1) * s_k + i);
       } else {
+        float v[8], w[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           v[j] = (i + j < nrows && k < kend) ? to_f32(x[(int64_t)(i + j) * s_i + (int64_t)k * s_k]) : 0.f;
           w[j] = (i + j < nrows && k + 1 < kend) ? to_f32(x[(int64_t)(i + j) * s_i + (int64_t)(k + 1) * s_k]) : 0.f;
         }
+        st.f[2 * q] = frag_from<T>(v);
+        st.f[2 * q + 1] = frag_from<T>(w);
       }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) store_pair(dst + (ii + j) * PITCH + kk, v[j], w[j]);
     }
   }
 }
 
-template <typename T>
+template <typename T, int ROWS>
+__device__ __forceinline__ void gemm_store(const GemmStage<T, ROWS>& st, T* dst, int64_t s_k) {
+  constexpr int K = gemm_k<T>();
+  const int t = threadIdx.x;
+  if (s_k == 1) {
+    constexpr int RPR = K / 8;
+#pragma unroll
+    for (int q = 0; q < GemmStage<T, ROWS>::NK; ++q) {
+      const int r = t + 256 * q;
+      if (r >= ROWS * RPR) break;
+      store_frag8(dst + gemm_lds<T>(r / RPR, (r % RPR) * 8), st.f[q]);
+    }
+  } else {
+    constexpr int IG = ROWS / 8;
+#pragma unroll
+    for (int q = 0; q < GemmStage<T, ROWS>::NP; ++q) {
+      const int r = t + 256 * q;
+      if (r >= IG * (K / 2)) break;
+      const int ii = (r % IG) * 8, kk = 2 * (r / IG);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        store_pair(dst + gemm_lds<T>(ii + j, kk), to_f32(st.f[2 * q][j]), to_f32(st.f[2 * q + 1][j]));
+    }
+  }
+}
+
+// Workgroup tile TM x TN (64 or 128 each), four waves in a 2 x 2 grid, each
+// wave (TM / 64) x (TN / 64) accumulators of 32 x 32.  The global loads of
+// k step s + 1 are in flight while step s runs on the MFMAs.
+template <typename T, int TM, int TN>
 __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
-  constexpr int PITCH = gemm_pitch<T>();
-  __shared__ __attribute__((aligned(16))) T As[kGemmTile * PITCH];
-  __shared__ __attribute__((aligned(16))) T Bs[kGemmTile * PITCH];
+  constexpr int K = gemm_k<T>(), PITCH = gemm_pitch<T>(), MT = TM / 64, NT = TN / 64;
+  static_assert(gemm_k<T>() % 16 == 0, "k step");
+  __shared__ __attribute__((aligned(16))) T As[TM * PITCH];
+  __shared__ __attribute__((aligned(16))) T Bs[TN * PITCH];
   const int lane = lane_id(), wave = wave_id(), g = lane >> 5, c = lane & 31;
-  const int m0 = blockIdx.y * kGemmTile, n0 = blockIdx.x * kGemmTile;
+  const int m0 = blockIdx.y * TM, n0 = blockIdx.x * TN;
   const int prob = blockIdx.z / p.splits, z = blockIdx.z % p.splits;
   const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
-  const int mw = wave >> 1, nw = wave & 1;  // this wave's 32 x 32 quarter
-  f32x16 acc;
+  const int mw = wave >> 1, nw = wave & 1;
+  f32x16 acc[MT][NT];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  for (int a = 0; a < MT; ++a)
+#pragma unroll
+    for (int b = 0; b < NT; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
   const int seg0 = p.nprob > 1 ? prob : 0, seg1 = p.nprob > 1 ? prob + 1 : p.nseg;
-  for (int seg = seg0; seg < seg1; ++seg) {
-    const T* A = static_cast<const T*>(p.a[seg]);
-    const T* Bm = static_cast<const T*>(p.b[seg]);
-    for (int k0 = kbeg; k0 < kend; k0 += kGemmK) {
-      gemm_stage<T>(As, A, p.a_m, p.a_k, m0, p.M, k0, kend);
-      gemm_stage<T>(Bs, Bm, p.b_n, p.b_k, n0, p.N, k0, kend);
-      __syncthreads();
+  // the (segment, k step) sequence of this workgroup, walked with a one-step
+  // register prefetch
+  const int nk = kend > kbeg ? (kend - kbeg + K - 1) / K : 0;
+  const int nsteps = (seg1 - seg0) * nk;
+  GemmStage<T, TM> sa;
+  GemmStage<T, TN> sb;
+  auto load_step = [&](int it) __attribute__((always_inline)) {
+    const int seg = seg0 + it / nk, k0 = kbeg + (it % nk) * K;
+    gemm_load(sa, static_cast<const T*>(p.a[seg]), p.a_m, p.a_k, m0, p.M, k0, kend);
+    gemm_load(sb, static_cast<const T*>(p.b[seg]), p.b_n, p.b_k, n0, p.N, k0, kend);
+  };
+  if (nsteps > 0) load_step(0);
+  for (int it = 0; it < nsteps; ++it) {
+    gemm_store(sa, As, p.a_k);
+    gemm_store(sb, Bs, p.b_k);
+    __syncthreads();
+    if (it + 1 < nsteps) load_step(it + 1);
 #pragma unroll
-      for (int ks = 0; ks < kGemmK / 16; ++ks)
-        mma(acc, load_frag(As + (32 * mw + c) * PITCH + 16 * ks + 8 * g),
-            load_frag(Bs + (32 * nw + c) * PITCH + 16 * ks + 8 * g));
-      __syncthreads();
+    for (int ks = 0; ks < K / 16; ++ks) {
+      typename Frag<T>::type af[MT], bfr[NT];
+#pragma unroll
+      for (int a = 0; a < MT; ++a) af[a] = load_frag(As + gemm_lds<T>(32 * (MT * mw + a) + c, 16 * ks + 8 * g));
+#pragma unroll
+      for (int b = 0; b < NT; ++b) bfr[b] = load_frag(Bs + gemm_lds<T>(32 * (NT * nw + b) + c, 16 * ks + 8 * g));
+#pragma unroll
+      for (int a = 0; a < MT; ++a)
+#pragma unroll
+        for (int b = 0; b < NT; ++b) mma(acc[a][b], af[a], bfr[b]);
     }
+    __syncthreads();
   }
   const int64_t base = ((int64_t)prob * p.splits + z) * p.split_stride;
-  const int n = n0 + 32 * nw + c;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int m = m0 + 32 * mw + acc_row(lane, r);
-    if (m < p.M && n < p.N) {
-      if (p.c_t) static_cast<T*>(p.c)[base + (int64_t)m * p.ldc + n] = from_f32<T>(acc[r]);
-      else static_cast<float*>(p.c)[base + (int64_t)m * p.ldc + n] = acc[r];
+  for (int a = 0; a < MT; ++a)
+#pragma unroll
+    for (int b = 0; b < NT; ++b) {
+      const int n = n0 + 32 * (NT * nw + b) + c;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + 32 * (MT * mw + a) + acc_row(lane, r);
+        if (m < p.M && n < p.N) {
+          if (p.c_t) static_cast<T*>(p.c)[base + (int64_t)m * p.ldc + n] = from_f32<T>(acc[a][b][r]);
+          else static_cast<float*>(p.c)[base + (int64_t)m * p.ldc + n] = acc[a][b][r];
+        }
+      }
     }
-  }
 }
 
 // s + x[0] + x[st] + ... + x[(n - 1) st], added in that order; the loads of
@@ -569,10 +670,16 @@ size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes) {
   return (size_t)waves * attn_bwd_wave_bytes(D, Mp, dec, elem_bytes);
 }
 
+int gemm_tile(int n) { return n >= 128 ? 128 : 64; }
+
 template <typename T>
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
-  dim3 grid((p.N + kGemmTile - 1) / kGemmTile, (p.M + kGemmTile - 1) / kGemmTile, p.nprob * p.splits);
-  k_gemm<T><<<grid, 256, 0, s>>>(p);
+  const int tm = gemm_tile(p.M), tn = gemm_tile(p.N);
+  dim3 grid((p.N + tn - 1) / tn, (p.M + tm - 1) / tm, p.nprob * p.splits);
+  if (tm == 128 && tn == 128) k_gemm<T, 128, 128><<<grid, 256, 0, s>>>(p);
+  else if (tm == 128) k_gemm<T, 128, 64><<<grid, 256, 0, s>>>(p);
+  else if (tn == 128) k_gemm<T, 64, 128><<<grid, 256, 0, s>>>(p);
+  else k_gemm<T, 64, 64><<<grid, 256, 0, s>>>(p);
   return hipGetLastError();
 }
 
