@@ -895,9 +895,9 @@ __device__ __forceinline__ void pipelined_routes2(int RT, int rt_full, Score&& s
 // ---------------------------------------------------------------------------
 // Decode with the key projection and the merge fused (call 3 + W_O).
 // ---------------------------------------------------------------------------
-// Waves (of 32 tokens) per decode workgroup: 8, or 4 at C = 256 where the
-// resident X and Y fragments need more than 256 registers.
-constexpr int dec_waves(int C) { return C >= 256 ? 4 : 8; }
+// Waves (of 32 tokens) per decode workgroup: 8, two per SIMD (at C = 256 the
+// resident X and Y fragments take 128 of each wave's 256 registers).
+constexpr int dec_waves(int) { return 8; }
 
 int decode_stage_elems(int C, int D, int Mp) {
   const int hpg = D == 16 ? 2 : 1, gb = D == 64 ? 2 : 1;
