@@ -1680,7 +1680,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 // ---------------------------------------------------------------------------
 template <typename T, int D, int KSC, int NQW, int W>
 static hipError_t enc_one(const EncFusedParams& p, hipStream_t s) {
-  if constexpr (NQW > enc_nqw_cap(D, W) || (W == 8 && (D != 16 || KSC > 8)) ||
+  if constexpr (NQW > enc_nqw_cap(D, W) || (W == 8 && !((D == 16 && KSC <= 8) || (D == 32 && KSC == 16))) ||
                 !fused_width_ok(16 * KSC, sizeof(T))) {
     return hipErrorInvalidValue;
   } else {
@@ -1721,6 +1721,7 @@ template <typename T>
 hipError_t launch_encode_fused(const EncFusedParams& p, int D, int waves, hipStream_t s) {
   if (waves == 8) {
     if (D == 16) return enc_ksc<T, 16, 8>(p, s);
+    if (D == 32) return enc_ksc<T, 32, 8>(p, s);
     return hipErrorInvalidValue;
   }
   switch (D) {

@@ -148,12 +148,15 @@ struct DecFusedParams {
 
 // Fused path coverage.  bf16: C in {64, 128, 256}; fp32 (a correctness path):
 // C = 64.  Query blocks per wave of the fused encode: a power of two up to
-// enc_nqw_cap; waves per encode workgroup: enc_waves.
+// enc_nqw_cap; waves per encode workgroup: enc_waves (eight, two per SIMD,
+// where the registers allow it with at least eight query slots).
 constexpr bool fused_width_ok(int C, int elem_bytes) {
   return elem_bytes == 2 ? (C == 64 || C == 128 || C == 256) : C == 64;
 }
 constexpr int enc_nqw_cap(int D, int waves) { return D == 16 ? (waves == 8 ? 2 : 4) : (D == 32 ? 2 : 1); }
-constexpr int enc_waves(int D, int C, int slots) { return (D == 16 && C <= 128 && slots >= 8) ? 8 : 4; }
+constexpr int enc_waves(int D, int C, int slots) {
+  return ((D == 16 && C <= 128) || (D == 32 && C == 256)) && slots >= 8 ? 8 : 4;
+}
 constexpr bool dec_fused_ok(int elem_bytes, int D, int ksc) { return !(elem_bytes == 4 && D == 64 && ksc >= 8); }
 size_t enc_fused_lds_bytes(int C, int D, int waves, int elem_bytes);
 int decode_stage_elems(int C, int D, int Mp);
