@@ -290,7 +290,8 @@ __global__ __launch_bounds__(256) void k_sum_splits(const float* part, SumOuts o
 // ---------------------------------------------------------------------------
 // LDS per wave: the short-side slot(s) [D][Mp + 4] fp32 (route index fastest,
 // padded so that the lanes' rows fall in different banks) and one transpose
-// tile [32][32 + 16 bytes] of T (dS, then P in the decode).
+// tile [32][32 + 16 bytes] of T (dS, then P in the decode); per workgroup
+// (encode) the routes' L and c.
 template <typename T> constexpr int tb_pitch() { return 32 + 16 / (int)sizeof(T); }
 size_t attn_bwd_wave_bytes(int D, int Mp, bool dec, int elem_bytes) {
   const int tbp = 32 + 16 / elem_bytes;
@@ -320,12 +321,11 @@ struct ShortBlock {
   static constexpr int KS = D / 16, DB = (D + 31) / 32;
   typename Frag<T>::type a[KS], gr[KS];       // rows of A_sh and G_sh
   typename Frag<T>::type at[2][DB], gt[2][DB];  // transposed fragments (gt: encode)
-  f32x4 l[4], cc[4];                          // encode: L (log2) and c of this lane's rows
 };
 
 template <typename T, int D, bool DEC>
 __device__ __forceinline__ void load_short(ShortBlock<T, D, DEC>& s, const T* ash, const T* gsh, const T* asht,
-                                           const T* gsht, const float* lrow, const float* crow, int sb, int lane) {
+                                           const T* gsht, int sb, int lane) {
   constexpr int KS = D / 16, DB = (D + 31) / 32;
   const int g = lane >> 5, c = lane & 31;
 #pragma unroll
@@ -341,13 +341,6 @@ __device__ __forceinline__ void load_short(ShortBlock<T, D, DEC>& s, const T* as
       s.at[kk][db] = load_frag(asht + fo);
       if constexpr (!DEC) s.gt[kk][db] = load_frag(gsht + fo);
     }
-  if constexpr (!DEC) {
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      s.l[a] = *reinterpret_cast<const f32x4*>(lrow + 32 * sb + 8 * a + 4 * g);
-      s.cc[a] = *reinterpret_cast<const f32x4*>(crow + 32 * sb + 8 * a + 4 * g);
-    }
-  }
 }
 
 template <typename T, int D, bool DEC>
@@ -364,7 +357,16 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
   float* slot_a = reinterpret_cast<float*>(smem) + wave * slot_floats;
   float* slot_g = slot_a + D * SP;
   T* tb = reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) + wave * 32 * TBP;
+  // encode: the routes' L (log2) and c of this (b, h), [2][Mp], after the
+  // waves' transpose tiles
+  float* lc_lds = reinterpret_cast<float*>(reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) +
+                                           W * 32 * TBP);
   for (int i = lane; i < slot_floats; i += 64) slot_a[i] = 0.f;
+  if constexpr (!DEC) {
+    for (int i = threadIdx.x; i < 2 * p.Mp; i += blockDim.x)
+      lc_lds[i] = i < p.Mp ? p.lrow[(int64_t)bh * p.Mp + i] : p.crow[(int64_t)bh * p.Mp + i - p.Mp];
+    __syncthreads();
+  }
 
   const T* ash = static_cast<const T*>(p.ash) + b * p.ash_sb + h * p.ash_sh;
   const T* asht = static_cast<const T*>(p.asht) + b * p.asht_sb + h * p.asht_sh;
@@ -372,8 +374,6 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
   const T* gsht = DEC ? nullptr : static_cast<const T*>(p.gsht) + b * p.gsht_sb + h * p.gsht_sh;
   const T* blo = static_cast<const T*>(p.blo) + b * p.blo_sb + h * p.blo_sh;
   const T* glo = static_cast<const T*>(p.glo) + b * p.glo_sb + h * p.glo_sh;
-  const float* lrow = DEC ? nullptr : p.lrow + (int64_t)bh * p.Mp;
-  const float* crow = DEC ? nullptr : p.crow + (int64_t)bh * p.Mp;
   T* dout_b = static_cast<T*>(p.dout_b);
   T* dout_g = static_cast<T*>(p.dout_g);
 
@@ -430,37 +430,48 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.f;
-    ShortBlock<T, D, DEC> cur, nxt;
-    load_short(cur, ash, gsh, asht, gsht, lrow, crow, 0, lane);
-    for (int sb = 0; sb < NS; ++sb) {
-      // the next block (the last block again at the end: the same number of
-      // loads in flight on every iteration)
-      load_short(nxt, ash, gsh, asht, gsht, lrow, crow, min(sb + 1, NS - 1), lane);
+    // one block of 32 routes; the operands of the next block are loaded into
+    // the other buffer first (the last block again at the end, so the same
+    // number of loads is in flight on every block)
+    auto route_block = [&](const ShortBlock<T, D, DEC>& cb, int sb) __attribute__((always_inline)) {
       f32x16 sc, dp;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[e] = dp[e] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        mma(sc, cur.a[ks], kb[ks]);
-        mma(dp, cur.gr[ks], gb[ks]);
+        mma(sc, cb.a[ks], kb[ks]);
+        mma(dp, cb.gr[ks], gb[ks]);
       }
       // P = exp(s S - L), dS = P (dP - c); rows past M and columns past the
       // long length are zero
       f32x16 P, dS;
-      const bool full = full_tile && 32 * (sb + 1) <= p.M;  // wave-uniform
+      // encode: L (log2) and c of this lane's 16 routes, from LDS
+      f32x4 lq[4], cq[4];
+      if constexpr (!DEC) {
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        float L, cc;
-        if constexpr (DEC) {
-          L = Ll; cc = cl;
-        } else {
-          L = cur.l[rr >> 2][rr & 3]; cc = cur.cc[rr >> 2][rr & 3];
+        for (int a = 0; a < 4; ++a) {
+          lq[a] = *reinterpret_cast<const f32x4*>(lc_lds + 32 * sb + 8 * a + 4 * g);
+          cq[a] = *reinterpret_cast<const f32x4*>(lc_lds + p.Mp + 32 * sb + 8 * a + 4 * g);
         }
-        float pv = __builtin_amdgcn_exp2f(sc[rr] * p.sl2 - L);
-        if (!full && !(nok && 32 * sb + acc_row(lane, rr) < p.M)) pv = 0.f;
-        P[rr] = pv;
-        dS[rr] = pv * (dp[rr] - cc);
       }
+      auto softmax_grad = [&](auto masked) __attribute__((always_inline)) {
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          float L, cc;
+          if constexpr (DEC) {
+            L = Ll; cc = cl;
+          } else {
+            L = lq[rr >> 2][rr & 3]; cc = cq[rr >> 2][rr & 3];
+          }
+          float pv = __builtin_amdgcn_exp2f(sc[rr] * p.sl2 - L);
+          if constexpr (decltype(masked)::value)
+            if (!(nok && 32 * sb + acc_row(lane, rr) < p.M)) pv = 0.f;
+          P[rr] = pv;
+          dS[rr] = pv * (dp[rr] - cc);
+        }
+      };
+      if (full_tile && 32 * (sb + 1) <= p.M) softmax_grad(std::false_type{});  // wave-uniform
+      else softmax_grad(std::true_type{});
       // P and dS as B operands (k = route, in the accumulator's row order)
       F pb[2], dsb[2];
 #pragma unroll
@@ -475,8 +486,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          mma(dk[db], cur.at[kk][db], dsb[kk]);
-          if constexpr (!DEC) mma(dv[db], cur.gt[kk][db], pb[kk]);
+          mma(dk[db], cb.at[kk][db], dsb[kk]);
+          if constexpr (!DEC) mma(dv[db], cb.gt[kk][db], pb[kk]);
         }
       // short side: dS (then P in the decode) transposed through the wave's
       // LDS tile [position][route]
@@ -529,7 +540,16 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         }
       }
       __builtin_amdgcn_wave_barrier();
-      cur = nxt;
+    };
+    ShortBlock<T, D, DEC> b0, b1;
+    load_short(b0, ash, gsh, asht, gsht, 0, lane);
+    for (int sb = 0; sb < NS; sb += 2) {
+      load_short(b1, ash, gsh, asht, gsht, min(sb + 1, NS - 1), lane);
+      route_block(b0, sb);
+      if (sb + 1 < NS) {  // wave-uniform
+        load_short(b0, ash, gsh, asht, gsht, min(sb + 2, NS - 1), lane);
+        route_block(b1, sb + 1);
+      }
     }
     // long-side results for this wave's 32 positions: rows d, column = lane
     if (nok) {
@@ -667,7 +687,7 @@ int attn_bwd_waves(int D, int Mp, bool dec, int elem_bytes) {
 }
 
 size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes) {
-  return (size_t)waves * attn_bwd_wave_bytes(D, Mp, dec, elem_bytes);
+  return (size_t)waves * attn_bwd_wave_bytes(D, Mp, dec, elem_bytes) + (dec ? 0 : 2 * sizeof(float) * (size_t)Mp);
 }
 
 int gemm_tile(int n) { return n >= 128 ? 128 : 64; }
