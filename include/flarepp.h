@@ -184,6 +184,21 @@ FLAREPP_API int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int
                                             size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Shared-projection mixer: FLARE++ with the query-synthesis keys and values
+ * tied to the physical ones (K~ = K, V~ = V), the variant the paper's cost
+ * model leaves open (App. C.2): call 1 is Q = SDPA(Q~, K, V).  Same
+ * arguments, workspace (flarepp_mixer_workspace_bytes) and errors as
+ * flarepp_mixer_forward without Wkt and Wvt; the result equals
+ * flarepp_mixer_forward(..., Wkt = Wk, Wvt = Wv, ...) bit for bit.  Every
+ * routing kernel projects its own operands from X, so no projection work is
+ * saved on this path; what the variant removes is the two C x C parameters.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API int flarepp_mixer_forward_shared(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                             int64_t M, const void* X, const void* Wk,
+                                             const void* Wv, const void* Wo, const void* seeds,
+                                             void* O, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Mixer backward (App. A.5): the gradients of the scalar <O, dO> with respect
  * to every input of flarepp_mixer_forward, for the output gradient
  * dO [B][N][C] (dtype).

@@ -1030,6 +1030,13 @@ int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int6
                      Y_out, ws, ws_bytes, stream, nullptr, 0, 0, true);
 }
 
+int flarepp_mixer_forward_shared(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                 const void* X, const void* Wk, const void* Wv, const void* Wo,
+                                 const void* seeds, void* O, void* ws, size_t ws_bytes, void* stream) {
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wk, Wv, Wo, seeds, O, nullptr, nullptr, nullptr, ws,
+                     ws_bytes, stream, nullptr, 0);
+}
+
 size_t flarepp_mixer_backward_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
                                               int64_t M) {
   if (check_backward_shape(dtype, B, N, C, H, M) != FLAREPP_OK) return 0;

@@ -34,6 +34,7 @@ EXPORTS = (
     "flarepp_mixer_forward_profiled", "flarepp_mixer_path", "flarepp_mixer_stage",
     "flarepp_flare_workspace_bytes", "flarepp_flare_forward", "flarepp_flare_forward_debug",
     "flarepp_mixer_backward_workspace_bytes", "flarepp_mixer_backward", "flarepp_mixer_backward_debug",
+    "flarepp_mixer_forward_shared",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -94,6 +95,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_flare_forward_debug.restype = i32
     lib.flarepp_flare_forward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 6
                                                 + [fp, vp] + [vp, sz, vp])
+    lib.flarepp_mixer_forward_shared.restype = i32
+    lib.flarepp_mixer_forward_shared.argtypes = [i32, i64, i64, i64, i64, i64] + [vp] * 6 + [vp, sz, vp]
     lib.flarepp_mixer_backward_workspace_bytes.restype = sz
     lib.flarepp_mixer_backward_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
     lib.flarepp_mixer_backward.restype = i32
@@ -344,6 +347,23 @@ def flarepp_flare_forward_debug(X, Wk, Wv, Wo, queries, *, H: int,
     return O, Z, Y
 
 
+def flarepp_mixer_forward_shared(X, Wk, Wv, Wo, seeds, *, H: int,
+                                 out: Optional[torch.Tensor] = None,
+                                 ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """FLARE++ with the query-synthesis keys and values tied to K and V
+    (K~ = K, V~ = V): O [B, N, C] in X's dtype."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    dt = _dtype_code(X)
+    O = out if out is not None else torch.empty_like(X)
+    w = _workspace(flarepp_mixer_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_mixer_forward_shared(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wo), _ptr(seeds),
+                                          _ptr(O), _ptr(w), w.numel(), _stream(X.device))
+    _check(rc)
+    return O
+
+
 def flarepp_mixer_backward_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
     return int(load().flarepp_mixer_backward_workspace_bytes(dtype, B, N, C, H, M))
 
@@ -397,5 +417,6 @@ mixer_forward = flarepp_mixer_forward
 mixer_forward_debug = flarepp_mixer_forward_debug
 flare_forward = flarepp_flare_forward
 flare_forward_debug = flarepp_flare_forward_debug
+mixer_forward_shared = flarepp_mixer_forward_shared
 mixer_backward = flarepp_mixer_backward
 mixer_backward_debug = flarepp_mixer_backward_debug

@@ -230,3 +230,10 @@ def test_backward_rejects_null_and_misaligned_pointers():
         assert _backward(ptrs=ptrs) == fp.ERR_INVALID_ARG
         ptrs[i] = ctypes.c_void_p(4096 + 4)
         assert _backward(ptrs=ptrs) == fp.ERR_INVALID_ARG
+
+
+def test_shared_variant_rejects_invalid_arguments():
+    lib = _lib()
+    assert lib.flarepp_mixer_forward_shared(fp.BF16, 0, 64, 64, 4, 32, *([_P] * 6), _P, 1 << 30, None) == fp.ERR_INVALID_ARG
+    assert lib.flarepp_mixer_forward_shared(fp.BF16, 1, 64, 64, 4, 32, None, *([_P] * 5), _P, 1 << 30, None) == fp.ERR_INVALID_ARG
+    assert lib.flarepp_mixer_forward_shared(fp.BF16, 1, 64, 64, 4, 32, *([_P] * 6), _P, 16, None) == fp.ERR_WORKSPACE

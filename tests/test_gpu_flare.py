@@ -121,3 +121,20 @@ def test_flare_deterministic_bitwise():
     b = fp.flarepp_flare_forward(t["X"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], H=w.H)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("name", ["tiny", "grid2d"])
+def test_shared_projection_variant(name):
+    # K~, V~ tied to K, V (the variant of App. C.2): the oracle's mixer with
+    # W~_K = W_K and W~_V = W_V, and bitwise the mixer entry point given the
+    # tied weights
+    w = inp.workload(name)
+    d = inp.make_inputs(w, 11, seed_scale=4.0)
+    print(f"[case] shared {inp.describe(w)}", flush=True)
+    t = upload(d, w)
+    O = fp.flarepp_mixer_forward_shared(t["X"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], H=w.H)
+    O2 = fp.flarepp_mixer_forward(t["X"], t["Wk"], t["Wv"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], H=w.H)
+    torch.cuda.synchronize()
+    assert torch.equal(O, O2)
+    ref = orc.mixer_forward(d["X"], d["Wk"], d["Wv"], d["Wk"], d["Wv"], d["Wo"], d["seeds"], w.H)
+    assert_close("O", O.float().cpu().numpy(), ref["O"], TOL[w.dtype], "shared")
