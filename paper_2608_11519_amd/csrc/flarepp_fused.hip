@@ -1063,10 +1063,27 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
         if (SF) tile_shift_free<T, RB, ONES_ROW, MASK>(acc[hh], ls[hh], sc, zv, nvalid, lane);
         else tile_online<T, RB, ONES_ROW, MASK>(acc[hh], m[hh], ls[hh], sc, zv, nvalid, lane);
       };
-      pipelined_routes2<HPG>(RT, rt_full, score, finish);
+      if constexpr (KSC >= 16) {
+        // C = 256: one score tile in flight (the software-pipelined order's
+        // second tile would push the X and Y fragments out of registers)
+        for (int rt = 0; rt < rt_full; ++rt)
+#pragma unroll
+          for (int hh = 0; hh < HPG; ++hh) finish(rt, hh, score(rt, hh), std::false_type{});
+        if (rt_full < RT)
+#pragma unroll
+          for (int hh = 0; hh < HPG; ++hh) finish(rt_full, hh, score(rt_full, hh), std::true_type{});
+      } else {
+        pipelined_routes2<HPG>(RT, rt_full, score, finish);
+      }
     };
     if (fast) routes(std::true_type{});
     else routes(std::false_type{});
+    // the decoded tokens of the finished groups, oldest first: a shift
+    // register, so that every index is a compile-time constant (the group
+    // loop is not unrolled) and yf stays in registers
+    constexpr int GKS = HPG * KS;  // fragments per group
+#pragma unroll
+    for (int u = 0; u + GKS < KSC; ++u) yf[u] = yf[u + GKS];
 #pragma unroll
     for (int hh = 0; hh < HPG; ++hh) {
       const int h = hg * HPG + hh;
@@ -1075,7 +1092,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
-          if (rb * 32 + 16 * hf < D) yf[h * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
+          if (rb * 32 + 16 * hf < D) yf[KSC - GKS + hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
       if (p.y && xok) {
         T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + h * D;
         constexpr int NQ4 = ONES_ROW ? 2 : 4;
