@@ -220,9 +220,8 @@ FLAREPP_API int flarepp_mixer_forward_shared(int dtype, int64_t B, int64_t N, in
  * MFMA operands, and the token gradients dY, dK, dV, dK~, dV~ kept between
  * the kernels, are rounded to bf16; accumulation is fp32.
  *
- * Sizes as for the mixer; in addition B*N <= 2^30, and a head's M x D route
- * gradients (two of them, fp32) must fit in LDS: M <= 512 for D <= 32, M <=
- * 256 for D = 64 (FLAREPP_ERR_UNSUPPORTED otherwise).  Workspace:
+ * Sizes as for the mixer; in addition B*N <= 2^30 (FLAREPP_ERR_UNSUPPORTED
+ * otherwise).  Workspace:
  * flarepp_mixer_backward_workspace_bytes(...) bytes (0 for an invalid or
  * unsupported shape); it holds the forward's K, V, K~, V~, Y and the token
  * gradients dY, dK, dV, dK~, dV~, about 10 * bytes(dtype) * B * N * C bytes.

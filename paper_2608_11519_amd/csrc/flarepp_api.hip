@@ -571,15 +571,22 @@ int route_impl(int kind, int dtype, int64_t B, int64_t H, int64_t N, int64_t M, 
 
 // ---- backward (App. A.5) ----------------------------------------------------
 // Work split of the SDPA backward over the long axis (keys of an encode,
-// tokens of the decode): chunks per (b, h) and 32-position tiles per wave.
+// tokens of the decode): chunks per (b, h) and 32-position tiles per wave;
+// and over the routes: a launch covers nsb route blocks (a window), sized so
+// that four waves' route-gradient slots take at most 80 KB of LDS (two
+// workgroups per CU); the windows run one after another.
 struct BwdSplit {
-  int waves, R, tpw;
+  int waves, R, tpw, nsb;
 };
 
 BwdSplit bwd_split(int64_t BH, int64_t Nl, int D, int Mp, bool dec, int elem_bytes) {
   BwdSplit sp{};
-  sp.waves = flarepp::attn_bwd_waves(D, Mp, dec, elem_bytes);
-  if (sp.waves == 0) return sp;
+  const int NS = Mp / 32;
+  int nwin = 1;
+  while (nwin < NS && flarepp::attn_bwd_lds_bytes(D, (int)cdiv(NS, nwin), Mp, dec, 4, elem_bytes) > 80 * 1024)
+    ++nwin;
+  sp.nsb = (int)cdiv(NS, nwin);
+  sp.waves = flarepp::attn_bwd_waves(D, sp.nsb, Mp, dec, elem_bytes);
   const int64_t tiles = cdiv(Nl, 32);
   int64_t R = std::max<int64_t>(1, std::min<int64_t>(cdiv(512, BH), cdiv(tiles, sp.waves)));
   const int64_t tpw = cdiv(tiles, R * sp.waves);
@@ -669,11 +676,6 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
 
 int check_backward_shape(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
   TRY(check_mixer_shape(dtype, B, N, C, H, M));
-  const int64_t D = C / H, Mp = round_up(M, 32);
-  const int bs = dtype_bytes(dtype);
-  if (flarepp::attn_bwd_waves((int)D, (int)Mp, true, bs) == 0)
-    return fail(FLAREPP_ERR_UNSUPPORTED, "the backward keeps M x D route gradients of a head in LDS: "
-                "M=%lld with D=%lld does not fit", (long long)M, (long long)D);
   if (B * N > (int64_t(1) << 30)) return fail(FLAREPP_ERR_UNSUPPORTED, "B*N too large for the backward");
   return FLAREPP_OK;
 }
@@ -752,6 +754,20 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   g.kchunk = (int)round_up(C, 64); g.c = w.dY; g.c_t = 1; g.ldc = C; g.split_stride = 0;
   HIPTRY(launch_gemm<T>(g, s));
 
+  // one SDPA backward, launched once per window of route blocks; the later
+  // windows add to the long-side gradients of the earlier ones
+  auto attn_windows = [&](const AttnBwdParams& a, const BwdSplit& sp, bool dec) -> int {
+    const int NS = (int)(Mp / 32);
+    for (int w0 = 0; w0 < NS; w0 += sp.nsb) {
+      AttnBwdParams q = a;
+      q.sb0 = w0;
+      q.nsb = std::min(sp.nsb, NS - w0);
+      if (w0 > 0) q.acc_b = q.acc_g = 1;
+      HIPTRY(launch_attn_bwd<T>(q, (int)D, dec, s));
+    }
+    return FLAREPP_OK;
+  };
+
   // ---- route-side operands of the calls: Q (rows and transposed), Z rows,
   // the seeds (rows and transposed) ----
   BwdPrepParams bp{};
@@ -776,7 +792,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a3.ylo = w.Y; a3.ylo_sb = N * C; a3.ylo_sh = D; a3.ylo_sn = C; a3.lcol = w.L3;
   a3.dout_b = w.dK; a3.acc_b = 0;
   a3.part_a = w.pa; a3.part_g = w.pg;
-  HIPTRY(launch_attn_bwd<T>(a3, (int)D, true, s));
+  TRY(attn_windows(a3, w.dec, true));
 
   // ---- call 2 (encode): queries Q, keys K, values V; dOut = dZ, the sum of
   // the decode's partials ----
@@ -802,7 +818,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a2.glo = w.Vdm; a2.glo_sb = dmBS; a2.glo_sh = dmHS; a2.glo_sn = 1; a2.glo_sd = Np;
   a2.dout_b = w.dK; a2.acc_b = 1; a2.dout_g = w.dV;
   a2.part_a = w.pq;
-  HIPTRY(launch_attn_bwd<T>(a2, (int)D, false, s));
+  TRY(attn_windows(a2, w.enc, false));
 
   // ---- call 1 (query synthesis): queries = seeds (shared), keys K~, values
   // V~; dOut = dQ, the decode's and the encode's shares summed ----
@@ -822,7 +838,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a1.blo = w.Kt; a1.glo = w.Vtdm;
   a1.dout_b = w.dKt; a1.acc_b = 0; a1.dout_g = w.dVt;
   a1.part_a = w.pa;
-  HIPTRY(launch_attn_bwd<T>(a1, (int)D, false, s));
+  TRY(attn_windows(a1, w.enc, false));
   rd = BwdReduceParams{};
   rd.P = (int)B; rd.O = (int)H; rd.M = (int)M; rd.Mp = (int)Mp; rd.D = (int)D;
   rd.part0 = w.pa; rd.R0 = w.enc.R; rd.out = dseeds;

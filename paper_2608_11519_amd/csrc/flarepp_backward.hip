@@ -293,9 +293,9 @@ __global__ __launch_bounds__(256) void k_sum_splits(const float* part, SumOuts o
 // tile [32][32 + 16 bytes] of T (dS, then P in the decode); per workgroup
 // (encode) the routes' L and c.
 template <typename T> constexpr int tb_pitch() { return 32 + 16 / (int)sizeof(T); }
-size_t attn_bwd_wave_bytes(int D, int Mp, bool dec, int elem_bytes) {
+size_t attn_bwd_wave_bytes(int D, int nsb, bool dec, int elem_bytes) {
   const int tbp = 32 + 16 / elem_bytes;
-  return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (Mp + 4) + (size_t)32 * tbp * elem_bytes;
+  return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (32 * nsb + 4) + (size_t)32 * tbp * elem_bytes;
 }
 
 // Fragment of a long-side row: element j = x[n * sn + (d0 + j) * sd] (one
@@ -352,7 +352,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
   const int W = blockDim.x >> 6;
   const int bh = blockIdx.x / p.R, r = blockIdx.x % p.R;
   const int b = bh / p.H, h = bh % p.H;
-  const int SP = p.Mp + 4, NS = p.Mp / 32;
+  const int SB0 = p.sb0, NS = p.nsb, SP = 32 * NS + 4;  // this launch's route blocks
   const int slot_floats = (DEC ? 2 : 1) * D * SP;
   float* slot_a = reinterpret_cast<float*>(smem) + wave * slot_floats;
   float* slot_g = slot_a + D * SP;
@@ -450,8 +450,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
       if constexpr (!DEC) {
 #pragma unroll
         for (int a = 0; a < 4; ++a) {
-          lq[a] = *reinterpret_cast<const f32x4*>(lc_lds + 32 * sb + 8 * a + 4 * g);
-          cq[a] = *reinterpret_cast<const f32x4*>(lc_lds + p.Mp + 32 * sb + 8 * a + 4 * g);
+          lq[a] = *reinterpret_cast<const f32x4*>(lc_lds + 32 * (SB0 + sb) + 8 * a + 4 * g);
+          cq[a] = *reinterpret_cast<const f32x4*>(lc_lds + p.Mp + 32 * (SB0 + sb) + 8 * a + 4 * g);
         }
       }
       auto softmax_grad = [&](auto masked) __attribute__((always_inline)) {
@@ -465,12 +465,12 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
           }
           float pv = __builtin_amdgcn_exp2f(sc[rr] * p.sl2 - L);
           if constexpr (decltype(masked)::value)
-            if (!(nok && 32 * sb + acc_row(lane, rr) < p.M)) pv = 0.f;
+            if (!(nok && 32 * (SB0 + sb) + acc_row(lane, rr) < p.M)) pv = 0.f;
           P[rr] = pv;
           dS[rr] = pv * (dp[rr] - cc);
         }
       };
-      if (full_tile && 32 * (sb + 1) <= p.M) softmax_grad(std::false_type{});  // wave-uniform
+      if (full_tile && 32 * (SB0 + sb + 1) <= p.M) softmax_grad(std::false_type{});  // wave-uniform
       else softmax_grad(std::true_type{});
       // P and dS as B operands (k = route, in the accumulator's row order)
       F pb[2], dsb[2];
@@ -542,12 +542,12 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
       __builtin_amdgcn_wave_barrier();
     };
     ShortBlock<T, D, DEC> b0, b1;
-    load_short(b0, ash, gsh, asht, gsht, 0, lane);
+    load_short(b0, ash, gsh, asht, gsht, SB0, lane);
     for (int sb = 0; sb < NS; sb += 2) {
-      load_short(b1, ash, gsh, asht, gsht, min(sb + 1, NS - 1), lane);
+      load_short(b1, ash, gsh, asht, gsht, SB0 + min(sb + 1, NS - 1), lane);
       route_block(b0, sb);
       if (sb + 1 < NS) {  // wave-uniform
-        load_short(b0, ash, gsh, asht, gsht, min(sb + 2, NS - 1), lane);
+        load_short(b0, ash, gsh, asht, gsht, SB0 + min(sb + 2, NS - 1), lane);
         route_block(b1, sb + 1);
       }
     }
@@ -569,16 +569,26 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
               for (int q = 0; q < 4; ++q) v[q] += to_f32(old[q]);
             }
             store4(dout_b + row + d, v[0], v[1], v[2], v[3]);
-            if (!DEC) store4(dout_g + row + d, dv[db][4 * a], dv[db][4 * a + 1], dv[db][4 * a + 2], dv[db][4 * a + 3]);
+            if (!DEC) {
+              float u[4];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) u[q] = dv[db][4 * a + q];
+              if (p.acc_g) {
+                const typename Frag<T>::half old = load_half(dout_g + row + d);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) u[q] += to_f32(old[q]);
+              }
+              store4(dout_g + row + d, u[0], u[1], u[2], u[3]);
+            }
           }
         }
     }
   }
   __syncthreads();
   // fixed-order sum of the waves' slots: this chunk's short-side partials
-  const int64_t po = ((int64_t)bh * p.R + r) * p.Mp * D;
-  for (int e = threadIdx.x; e < p.Mp * D; e += blockDim.x) {
-    const int m = e / D, d = e % D;
+  const int64_t po = ((int64_t)bh * p.R + r) * p.Mp * D + (int64_t)32 * SB0 * D;
+  for (int e = threadIdx.x; e < 32 * NS * D; e += blockDim.x) {
+    const int m = e / D, d = e % D;  // m: route within the window
     float sa = 0.f, sg = 0.f;
     for (int w = 0; w < W; ++w) {
       const float* sw = reinterpret_cast<const float*>(smem) + w * slot_floats;
@@ -669,8 +679,8 @@ __global__ __launch_bounds__(256) void k_bwd_prep(BwdPrepParams p) {
 
 template <typename T, int D, bool DEC>
 hipError_t attn_bwd_go(const AttnBwdParams& p, hipStream_t s) {
-  const int W = attn_bwd_waves(D, p.Mp, DEC, (int)sizeof(T));
-  const size_t lds = attn_bwd_lds_bytes(D, p.Mp, DEC, W, (int)sizeof(T));
+  const int W = attn_bwd_waves(D, p.nsb, p.Mp, DEC, (int)sizeof(T));
+  const size_t lds = attn_bwd_lds_bytes(D, p.nsb, p.Mp, DEC, W, (int)sizeof(T));
   const void* fn = reinterpret_cast<const void*>(&k_attn_bwd<T, D, DEC>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
@@ -680,14 +690,14 @@ hipError_t attn_bwd_go(const AttnBwdParams& p, hipStream_t s) {
 
 }  // namespace
 
-int attn_bwd_waves(int D, int Mp, bool dec, int elem_bytes) {
+int attn_bwd_waves(int D, int nsb, int Mp, bool dec, int elem_bytes) {
   for (int w = 4; w >= 1; w /= 2)
-    if (attn_bwd_lds_bytes(D, Mp, dec, w, elem_bytes) <= 160 * 1024) return w;
+    if (attn_bwd_lds_bytes(D, nsb, Mp, dec, w, elem_bytes) <= 160 * 1024) return w;
   return 0;
 }
 
-size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes) {
-  return (size_t)waves * attn_bwd_wave_bytes(D, Mp, dec, elem_bytes) + (dec ? 0 : 2 * sizeof(float) * (size_t)Mp);
+size_t attn_bwd_lds_bytes(int D, int nsb, int Mp, bool dec, int waves, int elem_bytes) {
+  return (size_t)waves * attn_bwd_wave_bytes(D, nsb, dec, elem_bytes) + (dec ? 0 : 2 * sizeof(float) * (size_t)Mp);
 }
 
 int gemm_tile(int n) { return n >= 128 ? 128 : 64; }

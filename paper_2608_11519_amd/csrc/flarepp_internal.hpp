@@ -216,6 +216,7 @@ struct GemmParams {
 // and c per token computed in the kernel.
 struct AttnBwdParams {
   int B, H, Nl, M, Mp, R, tpw;   // long length, routes, chunks per (b, h), long tiles per wave
+  int sb0, nsb;                  // the window of route blocks [sb0, sb0 + nsb) of this launch
   float s, sl2;                  // 1/sqrt(D), and times log2(e)
   // short side, per (b, h) at b * sb + h * sh (elements)
   const void* ash; int64_t ash_sb, ash_sh;    // rows [Mp][D]
@@ -229,14 +230,16 @@ struct AttnBwdParams {
   const void* glo; int64_t glo_sb, glo_sh, glo_sn, glo_sd;  // type T
   const void* ylo; int64_t ylo_sb, ylo_sh, ylo_sn;          // decode: forward output rows (T)
   const float* lcol;  // decode: [B * H][Nl], each position's log-normaliser in log2 units
-  // outputs: long side [B][Nl][H * D] in T (dout_b added to what is there
-  // when acc_b); short side partials [B][H][R][Mp][D] fp32
+  // outputs: long side [B][Nl][H * D] in T (added to what is there when
+  // acc_b / acc_g); short side partials [B][H][R][Mp][D] fp32 (this window's
+  // rows)
   void* dout_b; int acc_b;
-  void* dout_g;
+  void* dout_g; int acc_g;
   float* part_a; float* part_g;
 };
-int attn_bwd_waves(int D, int Mp, bool dec, int elem_bytes);
-size_t attn_bwd_lds_bytes(int D, int Mp, bool dec, int waves, int elem_bytes);
+// LDS of a launch over a window of nsb route blocks (Mp routes in all)
+int attn_bwd_waves(int D, int nsb, int Mp, bool dec, int elem_bytes);
+size_t attn_bwd_lds_bytes(int D, int nsb, int Mp, bool dec, int waves, int elem_bytes);
 
 // Fixed-order sums of backward partials: out[o][m][d] = base[o][m][d] +
 // sum_{p < P} (sum_{r < R0} part0[p][o][r][m][d] + sum_{r < R1} part1[p][o][r][m][d]),

@@ -202,8 +202,8 @@ def test_backward_workspace_sizes():
         n = fp.flarepp_mixer_backward_workspace_bytes(dt, 4, 16384, 128, 8, 128)
         # K, K~, V, V~, Y and the five token gradients dY, dK, dV, dK~, dV~
         assert n >= 4 * 16384 * 128 * 10 * bs
-    # a head's route gradients must fit in LDS: M = 512 with D = 64 does not
-    assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 2, 512) == 0
+    # every route count is covered (the kernel walks the routes in windows)
+    assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 2, 512) > 0
     assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 2, 256) > 0
     assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 100, 128, 8, 512) > 0
     assert fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 1, 10, 100, 3, 4) == 0
@@ -213,7 +213,6 @@ def test_backward_workspace_sizes():
     (dict(B=0), fp.ERR_INVALID_ARG),
     (dict(N=0), fp.ERR_INVALID_ARG),
     (dict(C=96, H=2), fp.ERR_UNSUPPORTED),
-    (dict(C=128, H=2, M=512), fp.ERR_UNSUPPORTED),
     (dict(dtype=3), fp.ERR_UNSUPPORTED),
     (dict(ws=None), fp.ERR_WORKSPACE),
     (dict(ws_bytes=100), fp.ERR_WORKSPACE),
