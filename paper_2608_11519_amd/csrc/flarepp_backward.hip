@@ -8,9 +8,11 @@
 // * k_attn_bwd: the SDPA backward of one routing call from its global output
 //   and log-normaliser, over a chunk of the long axis (keys of an encode,
 //   tokens of the decode).  Each wave owns 32 positions of the long axis and
-//   walks the route blocks; the long-side gradients stay in registers, the
-//   short-side (route) gradients are summed in the wave's LDS slot and, at
-//   the end, over the waves in a fixed order into the chunk's partial.
+//   walks the route blocks of a window (operands of the next block in flight
+//   in a second register buffer); the long-side gradients stay in registers,
+//   the short-side (route) gradients are summed in the wave's LDS slot and,
+//   at the end, over the waves in a fixed order into the chunk's partial.
+//   Large M x D is covered by several windows, one launch each.
 // * k_bwd_reduce sums those partials over the chunks (and over the batch for
 //   the shared seeds) in a fixed order; k_bwd_prep lays out the route-side
 //   operands of the next call (rows, transposed fragments, c = <dOut, Out>,
