@@ -324,6 +324,31 @@ def time_flare(args, w, t, use_graph):
     return {"ms_per_step": round(ms, 5), "tokens_per_s": round(w.B * w.N / (ms * 1e-3), 1)}
 
 
+def time_block(args, w, t, use_graph, mixer_ms):
+    """The pre-norm residual block X + mixer(LayerNorm(X)) on the same workload
+    and weights: what the layer-norm pass and the fused residual add to the
+    mixer step."""
+    import torch
+
+    from paper_2608_11519_amd import flarepp as fp
+
+    dcode = fp.BF16 if w.dtype == "bf16" else fp.F32
+    dev = t["X"].device
+    O = torch.empty_like(t["X"])
+    gamma = torch.ones(w.C, dtype=t["X"].dtype, device=dev)
+    beta = torch.zeros_like(gamma)
+    ws = torch.empty(fp.flarepp_block_workspace_bytes(dcode, w.B, w.N, w.C, w.H, w.M),
+                     dtype=torch.uint8, device=dev)
+
+    def step():
+        fp.flarepp_block_forward(t["X"], gamma, beta, t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"], t["seeds"],
+                                 H=w.H, out=O, ws=ws)
+
+    ms = _time_steps(args, step, use_graph)
+    return {"ms_per_step": round(ms, 5), "tokens_per_s": round(w.B * w.N / (ms * 1e-3), 1),
+            "over_mixer_ms": round(ms - mixer_ms, 5)}
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.pmc_summary:
@@ -426,6 +451,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     flare = time_flare(args, w, t, graph is not None)
     backward = None if args.no_backward else time_backward(args, w, t, graph is not None)
+    block = time_block(args, w, t, graph is not None, ms_per_step)
     work = stage_work(w, fused)
     stages = {n: {"ms": round(stage_ms[n], 5), **roofline(work[n], stage_ms[n], w.dtype)}
               for n in fp.PROFILE_STAGES if n not in empty}
@@ -467,6 +493,7 @@ def main(argv=None):
         "stages": stages,
         "wall_ms_timed_region": round(wall_ms, 3),
         "flare": {**flare, "flarepp_over_flare_time": round(ms_per_step / flare["ms_per_step"], 3)},
+        "block": block,
     }
     if backward is not None:
         out["backward"] = backward

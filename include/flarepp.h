@@ -184,6 +184,26 @@ FLAREPP_API int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int
                                             size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Mixer block: O = X + mixer(LN(X)), the pre-norm residual block around the
+ * mixer (the residual stream of Sec. 3.2 "What dynamic routing does not
+ * change").  LN normalises every token over its C channels:
+ * (x - mean) / sqrt(var + eps) * gamma + beta with the biased variance;
+ * gamma, beta [C] in dtype, eps > 0.  The normalised tokens go to a
+ * workspace buffer (one pass) and through the same kernels as
+ * flarepp_mixer_forward; the residual is added where O is stored (the
+ * decode's merge, or the merge product on the unfused path).  O must not
+ * alias X.  Workspace: flarepp_block_workspace_bytes(...) bytes.  Errors as
+ * for flarepp_mixer_forward, plus FLAREPP_ERR_INVALID_ARG for eps <= 0.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_block_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                                 int64_t M);
+FLAREPP_API int flarepp_block_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                      const void* X, const void* gamma, const void* beta, float eps,
+                                      const void* Wk, const void* Wv, const void* Wkt, const void* Wvt,
+                                      const void* Wo, const void* seeds, void* O, void* ws,
+                                      size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Shared-projection mixer: FLARE++ with the query-synthesis keys and values
  * tied to the physical ones (K~ = K, V~ = V), the variant the paper's cost
  * model leaves open (App. C.2): call 1 is Q = SDPA(Q~, K, V).  Same

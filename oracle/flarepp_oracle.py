@@ -26,6 +26,10 @@ It computes the plain definitions, in float64, in the paper's order:
                   log-normaliser (App. A.5): P = exp(s S - L), c = <dO, O>
                   per row, dV = P^T dO, dS = P (dO V^T - c), dK = s dS^T Q,
                   dQ = s dS K.
+* ``block_forward`` the pre-norm residual block around the mixer,
+                  X + mixer(LN(X)) (the residual stream the paper leaves
+                  unchanged, Sec. 3.2); ``layer_norm`` normalises each token
+                  over its channels with the biased variance.
 * ``mixer_backward`` the reverse pass of the whole mixer (App. A.5): W_O and
                   the merge, the decode (call 3), the physical-value encode
                   (call 2), the summed query gradient through the query
@@ -71,6 +75,8 @@ __all__ = [
     "split_heads",
     "sdpa_backward",
     "mixer_backward",
+    "layer_norm",
+    "block_forward",
 ]
 
 # Key chunk for the two-pass softmax and query chunk for independent rows;
@@ -348,3 +354,17 @@ def mixer_backward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int, dO) -> Dict[str, np.n
            "dQ3": dQ3, "dK": dK, "dV": dV, "dKt": dKt, "dVt": dVt}
     out.update(grads)
     return out
+
+
+def layer_norm(X, gamma, beta, eps: float) -> np.ndarray:
+    """Normalise every token over its channels: (x - mean) / sqrt(var + eps)
+    * gamma + beta, var the biased variance (mean of squared deviations)."""
+    X = _f64(X)
+    mean = X.mean(axis=-1, keepdims=True)
+    var = ((X - mean) ** 2).mean(axis=-1, keepdims=True)
+    return (X - mean) / np.sqrt(var + eps) * _f64(gamma) + _f64(beta)
+
+
+def block_forward(X, gamma, beta, eps: float, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int) -> np.ndarray:
+    """The pre-norm residual block around the mixer: X + mixer(LN(X))."""
+    return _f64(X) + mixer_forward(layer_norm(X, gamma, beta, eps), Wk, Wv, Wkt, Wvt, Wo, seeds, H)["O"]

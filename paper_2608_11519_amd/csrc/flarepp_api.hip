@@ -282,7 +282,8 @@ template <typename T>
 int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
                const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                const void* seeds, void* O, float* Q_out, float* Z_out, void* Y_out, void* ws,
-               size_t ws_bytes, hipStream_t s, hipEvent_t const* ev, int only, bool flare) {
+               size_t ws_bytes, hipStream_t s, hipEvent_t const* ev, int only, bool flare,
+               const void* res = nullptr) {
   using namespace flarepp;
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32);
   const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
@@ -347,7 +348,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     dp.x = X; dp.wkf = w.wf[0]; dp.wof = w.wf[4]; dp.q_op = flare ? w.seeds_op : w.q_op;
     dp.z_op = w.z_op; dp.qnorm2 = w.qnorm2;
     dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
-    dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O;
+    dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O; dp.res = res;
     dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);
     dp.stage_bytes = (int)dec2_stage_bytes((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype));
     dp.kind = dkind;
@@ -430,7 +431,7 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
   // 7. merge: O = Y W_O
   ProjParams mp{};
   mp.x = Y; mp.B = (int)B; mp.N = (int)N; mp.Np = (int)Np; mp.C = (int)C; mp.H = (int)H; mp.D = (int)D;
-  mp.nw = 1; mp.wf[0] = w.wf[4]; mp.out[0] = O; mp.layout[0] = kPlain;
+  mp.nw = 1; mp.wf[0] = w.wf[4]; mp.out[0] = O; mp.layout[0] = kPlain; mp.res = res;
   if (RUN(8)) HIPTRY(launch_project<T>(mp, s));
   STAGE(8);
 #undef RUN
@@ -1044,6 +1045,43 @@ int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int64_t C, int6
                                 size_t ws_bytes, void* stream) {
   return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, nullptr, nullptr, Wo, queries, O, nullptr, Z_out,
                      Y_out, ws, ws_bytes, stream, nullptr, 0, 0, true);
+}
+
+size_t flarepp_block_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  if (check_mixer_shape(dtype, B, N, C, H, M) != FLAREPP_OK) return 0;
+  return align256((size_t)dtype_bytes(dtype) * B * N * C) +
+         mixer_ws(nullptr, dtype, B, N, C, H, M, mixer_plan(dtype, B, N, C, H, M)).bytes;
+}
+
+int flarepp_block_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
+                          const void* gamma, const void* beta, float eps, const void* Wk, const void* Wv,
+                          const void* Wkt, const void* Wvt, const void* Wo, const void* seeds, void* O,
+                          void* ws, size_t ws_bytes, void* stream) {
+  TRY(check_mixer_shape(dtype, B, N, C, H, M));
+  const void* in[] = {X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, O};
+  const char* names[] = {"X", "gamma", "beta", "Wk", "Wv", "Wkt", "Wvt", "Wo", "seeds", "O"};
+  for (int i = 0; i < 10; ++i) TRY(check_ptr(in[i], names[i]));
+  if (!(eps > 0.f) || !std::isfinite(eps)) return fail(FLAREPP_ERR_INVALID_ARG, "eps=%g must be positive", (double)eps);
+  if (O == X) return fail(FLAREPP_ERR_INVALID_ARG, "O must not alias X (X is read again for the residual)");
+  if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
+  TRY(check_ptr(ws, "ws"));
+  const size_t xn_bytes = align256((size_t)dtype_bytes(dtype) * B * N * C);
+  const size_t need = flarepp_block_workspace_bytes(dtype, B, N, C, H, M);
+  if (ws_bytes < need)
+    return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* Xn = ws;
+  void* mws = static_cast<char*>(ws) + xn_bytes;
+  flarepp::LayerNormParams lp{};
+  lp.x = X; lp.gamma = gamma; lp.beta = beta; lp.y = Xn; lp.T = B * N; lp.C = (int)C; lp.eps = eps;
+  if (dtype == FLAREPP_F32) {
+    HIPTRY(flarepp::launch_layernorm<float>(lp, s));
+    return mixer_impl<float>(dtype, B, N, C, H, M, Xn, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr, nullptr,
+                             mws, ws_bytes - xn_bytes, s, nullptr, 0, false, X);
+  }
+  HIPTRY(flarepp::launch_layernorm<__bf16>(lp, s));
+  return mixer_impl<__bf16>(dtype, B, N, C, H, M, Xn, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr, nullptr,
+                            mws, ws_bytes - xn_bytes, s, nullptr, 0, false, X);
 }
 
 int flarepp_mixer_forward_shared(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,

@@ -116,6 +116,17 @@ __device__ __forceinline__ void store4(__bf16* p, float a, float b, float c, flo
   *reinterpret_cast<bf16x4*>(p) = v;
 }
 
+// store4 of a + r, b + r', ... where r.. are the 4 values at rp (the block's
+// residual), or of a, b, c, d when rp is null
+template <typename T>
+__device__ __forceinline__ void store4_res(T* p, const T* rp, float a, float b, float c, float d) {
+  if (rp) {
+    const typename Frag<T>::half r = load_half(rp);
+    a += to_f32(r[0]); b += to_f32(r[1]); c += to_f32(r[2]); d += to_f32(r[3]);
+  }
+  store4(p, a, b, c, d);
+}
+
 // ---- cross-lane helpers ------------------------------------------------------
 // Value held by lane l ^ 32 (the other half of the wave).
 __device__ __forceinline__ float other_half(float x) { return __shfl_xor(x, 32, 64); }

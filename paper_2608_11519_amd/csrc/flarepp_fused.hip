@@ -1119,9 +1119,12 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 #pragma unroll
     for (int ks = 0; ks < KSC; ++ks) mma(o, load_frag(sb + (ks * 64 + lane) * 8), yf[ks]);
     if (xok) {
-      T* op = (T*)p.o + ((int64_t)b * p.N + xrow) * C + 32 * cbo;
+      const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cbo;
+      T* op = (T*)p.o + oo;
+      const T* rp = p.res ? (const T*)p.res + oo : nullptr;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) store4(op + 8 * q + 4 * g, o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
+      for (int q = 0; q < 4; ++q)
+        store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
     }
     if (cbo + 1 < CB) lds_wait_barrier();
   }
@@ -1365,10 +1368,13 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode2(DecFusedPa
   if (xok) {
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
-      T* op = (T*)p.o + ((int64_t)b * p.N + xrow) * C + 32 * cb;
+      const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cb;
+      T* op = (T*)p.o + oo;
+      const T* rp = p.res ? (const T*)p.res + oo : nullptr;
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        store4(op + 8 * q + 4 * g, o[cb][4 * q], o[cb][4 * q + 1], o[cb][4 * q + 2], o[cb][4 * q + 3]);
+        store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, o[cb][4 * q], o[cb][4 * q + 1],
+                   o[cb][4 * q + 2], o[cb][4 * q + 3]);
     }
   }
 }
@@ -1685,9 +1691,13 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
       for (int j = 0; j < KPG; ++j) mma(oc, load_frag(wo + ((cb * KPG + j) * 64 + lane) * 8), yall[u][j]);
     }
     if (xok) {
-      T* op = (T*)p.o + ((int64_t)b * p.N + xrow) * C + 32 * cb;
+      const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cb;
+      T* op = (T*)p.o + oo;
+      const T* rp = p.res ? (const T*)p.res + oo : nullptr;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) store4(op + 8 * q + 4 * g, oc[4 * q], oc[4 * q + 1], oc[4 * q + 2], oc[4 * q + 3]);
+      for (int q = 0; q < 4; ++q)
+        store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, oc[4 * q], oc[4 * q + 1], oc[4 * q + 2],
+                   oc[4 * q + 3]);
     }
   }
 }

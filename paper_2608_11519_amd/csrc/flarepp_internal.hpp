@@ -36,6 +36,15 @@ struct ProjParams {
   const void* wf[5];
   void* out[5];
   int layout[5];
+  const void* res;  // kPlain outputs: [B][N][C] added to the product, or null
+};
+
+// Layer normalisation over the channels of every token: y = (x - mean) /
+// sqrt(var + eps) * gamma + beta (biased variance), one wave per token.
+struct LayerNormParams {
+  const void* x; const void* gamma; const void* beta; void* y;
+  int64_t T; int C;
+  float eps;
 };
 
 struct RouteParams {
@@ -141,6 +150,7 @@ struct DecFusedParams {
   float fast_lim;
   void* y;            // [B][N][C] decoded tokens, or null
   void* o;            // [B][N][C]
+  const void* res;    // [B][N][C] added to O (the block's residual), or null
   int stage_elems;    // elements per LDS stage buffer (k_decode_fused)
   int stage_bytes;    // bytes per head-group stage (k_decode2)
   int kind;           // DecodeKind
@@ -275,6 +285,7 @@ hipError_t launch_bwd_reduce(const BwdReduceParams&, hipStream_t);
 template <typename T> hipError_t launch_bwd_prep(const BwdPrepParams&, hipStream_t);
 int64_t bwd_prep_items(const BwdPrepParams&, int job);
 
+template <typename T> hipError_t launch_layernorm(const LayerNormParams&, hipStream_t);
 template <typename T> hipError_t launch_weight_frags(const WeightFragParams&, hipStream_t);
 template <typename Ts, typename T> hipError_t launch_route_prep(const RoutePrepParams&, hipStream_t);
 template <typename T> hipError_t launch_dmajor(const DmajorParams&, hipStream_t);

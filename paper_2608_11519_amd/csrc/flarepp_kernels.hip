@@ -149,13 +149,16 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
       for (int r4 = 0; r4 < 4; ++r4) {
         const int col = 32 * cb + 8 * r4 + 4 * g;
         T* o;
+        const T* rp = nullptr;
         if (layout == kPlain) {
-          o = out + ((int64_t)b * p.N + xrow) * p.C + col;
+          const int64_t oo = ((int64_t)b * p.N + xrow) * p.C + col;
+          o = out + oo;
+          if (p.res) rp = (const T*)p.res + oo;
         } else {
           const int h = col / D, d = col % D;
           o = out + (((int64_t)b * p.H + h) * p.N + xrow) * D + d;
         }
-        store4(o, acc[q][4 * r4], acc[q][4 * r4 + 1], acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
+        store4_res(o, rp, acc[q][4 * r4], acc[q][4 * r4 + 1], acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
       }
     }
   }
@@ -301,6 +304,56 @@ __global__ __launch_bounds__(256) void k_route(RouteParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// Layer normalisation (the block's pre-norm), one wave per token: the row in
+// registers (C / 64 values per lane), exact mean, then the variance of the
+// centred values, both reduced over the wave.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int k = 32; k >= 1; k >>= 1) x += __shfl_xor(x, k, 64);
+  return x;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_layernorm(LayerNormParams p) {
+  constexpr int MAXV = 64;  // C <= 4096
+  const int lane = lane_id();
+  // one wave per token; the grid is capped, so waves step over the tokens
+  for (int64_t row = (int64_t)blockIdx.x * 4 + wave_id(); row < p.T; row += (int64_t)gridDim.x * 4) {
+  const T* x = (const T*)p.x + row * p.C;
+  // C is a multiple of 32: the last group of 64 channels may be half full;
+  // lanes past C hold zero and stay out of the sums
+  const int nv = (p.C + 63) / 64;
+  float v[MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i)
+    if (i < nv) {
+      v[i] = i * 64 + lane < p.C ? to_f32(x[i * 64 + lane]) : 0.f;
+      s += v[i];
+    }
+  const float mean = wave_sum(s) / (float)p.C;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i)
+    if (i < nv && i * 64 + lane < p.C) {
+      v[i] -= mean;
+      q += v[i] * v[i];
+    }
+  const float rstd = 1.f / sqrtf(wave_sum(q) / (float)p.C + p.eps);
+  T* y = (T*)p.y + row * p.C;
+  const T* gm = (const T*)p.gamma;
+  const T* bt = (const T*)p.beta;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i)
+    if (i < nv && i * 64 + lane < p.C) {
+      const int ch = i * 64 + lane;
+      y[ch] = from_f32<T>(v[i] * rstd * to_f32(gm[ch]) + to_f32(bt[ch]));
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 static inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
@@ -323,6 +376,12 @@ template <typename T>
 hipError_t launch_dmajor(const DmajorParams& p, hipStream_t s) {
   const int64_t n = (int64_t)p.BH * p.D * p.Np;
   k_dmajor<T><<<blocks_for(n, 256), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_layernorm(const LayerNormParams& p, hipStream_t s) {
+  k_layernorm<T><<<(unsigned)std::min<int64_t>((p.T + 3) / 4, 1 << 16), 256, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -359,6 +418,8 @@ template hipError_t launch_route_prep<float, __bf16>(const RoutePrepParams&, hip
 template hipError_t launch_route_prep<__bf16, __bf16>(const RoutePrepParams&, hipStream_t);
 template hipError_t launch_dmajor<float>(const DmajorParams&, hipStream_t);
 template hipError_t launch_dmajor<__bf16>(const DmajorParams&, hipStream_t);
+template hipError_t launch_layernorm<float>(const LayerNormParams&, hipStream_t);
+template hipError_t launch_layernorm<__bf16>(const LayerNormParams&, hipStream_t);
 template hipError_t launch_project<float>(const ProjParams&, hipStream_t);
 template hipError_t launch_project<__bf16>(const ProjParams&, hipStream_t);
 template hipError_t launch_route<float>(const RouteParams&, int, bool, hipStream_t);

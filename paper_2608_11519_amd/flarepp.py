@@ -34,7 +34,7 @@ EXPORTS = (
     "flarepp_mixer_forward_profiled", "flarepp_mixer_path", "flarepp_mixer_stage",
     "flarepp_flare_workspace_bytes", "flarepp_flare_forward", "flarepp_flare_forward_debug",
     "flarepp_mixer_backward_workspace_bytes", "flarepp_mixer_backward", "flarepp_mixer_backward_debug",
-    "flarepp_mixer_forward_shared",
+    "flarepp_mixer_forward_shared", "flarepp_block_workspace_bytes", "flarepp_block_forward",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -105,6 +105,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_mixer_backward_debug.restype = i32
     lib.flarepp_mixer_backward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8 + [fp] * 9
                                                  + [vp, sz, vp])
+    lib.flarepp_block_workspace_bytes.restype = sz
+    lib.flarepp_block_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
+    lib.flarepp_block_forward.restype = i32
+    lib.flarepp_block_forward.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 3 + [ctypes.c_float]
+                                          + [vp] * 7 + [vp, sz, vp])
     _lib = lib
     return lib
 
@@ -410,6 +415,28 @@ def flarepp_mixer_backward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,
     return _backward(True, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws)
 
 
+def flarepp_block_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
+    return int(load().flarepp_block_workspace_bytes(dtype, B, N, C, H, M))
+
+
+def flarepp_block_forward(X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, eps: float = 1e-5,
+                          out: Optional[torch.Tensor] = None,
+                          ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The pre-norm residual block X + mixer(LayerNorm(X)): O [B, N, C] in
+    X's dtype; gamma, beta [C] in X's dtype."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    dt = _dtype_code(X)
+    O = out if out is not None else torch.empty_like(X)
+    w = _workspace(flarepp_block_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_block_forward(dt, B, N, C, H, M, _ptr(X), _ptr(gamma), _ptr(beta), float(eps), _ptr(Wk),
+                                   _ptr(Wv), _ptr(Wkt), _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(O), _ptr(w),
+                                   w.numel(), _stream(X.device))
+    _check(rc)
+    return O
+
+
 # short aliases
 project = flarepp_project
 route = flarepp_route
@@ -420,3 +447,4 @@ flare_forward_debug = flarepp_flare_forward_debug
 mixer_forward_shared = flarepp_mixer_forward_shared
 mixer_backward = flarepp_mixer_backward
 mixer_backward_debug = flarepp_mixer_backward_debug
+block_forward = flarepp_block_forward

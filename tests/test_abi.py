@@ -236,3 +236,42 @@ def test_shared_variant_rejects_invalid_arguments():
     assert lib.flarepp_mixer_forward_shared(fp.BF16, 0, 64, 64, 4, 32, *([_P] * 6), _P, 1 << 30, None) == fp.ERR_INVALID_ARG
     assert lib.flarepp_mixer_forward_shared(fp.BF16, 1, 64, 64, 4, 32, None, *([_P] * 5), _P, 1 << 30, None) == fp.ERR_INVALID_ARG
     assert lib.flarepp_mixer_forward_shared(fp.BF16, 1, 64, 64, 4, 32, *([_P] * 6), _P, 16, None) == fp.ERR_WORKSPACE
+
+
+def _block(dtype=fp.BF16, B=1, N=64, C=64, H=4, M=32, eps=1e-5, ptrs=None, ws=_P, ws_bytes=1 << 30):
+    # X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, O: O differs from X unless
+    # a test makes them alias
+    ptrs = ptrs if ptrs is not None else [_P] * 9 + [ctypes.c_void_p(8192)]
+    return _lib().flarepp_block_forward(dtype, B, N, C, H, M, *ptrs[:3], eps, *ptrs[3:], ws, ws_bytes, None)
+
+
+def test_block_workspace_adds_the_normalised_input():
+    for dt, bs in ((fp.F32, 4), (fp.BF16, 2)):
+        m = fp.flarepp_mixer_workspace_bytes(dt, 2, 1000, 128, 8, 64)
+        assert fp.flarepp_block_workspace_bytes(dt, 2, 1000, 128, 8, 64) >= m + 2 * 1000 * 128 * bs
+    assert fp.flarepp_block_workspace_bytes(fp.BF16, 1, 10, 100, 3, 4) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), fp.ERR_INVALID_ARG),
+    (dict(C=96, H=2), fp.ERR_UNSUPPORTED),
+    (dict(dtype=3), fp.ERR_UNSUPPORTED),
+    (dict(eps=0.0), fp.ERR_INVALID_ARG),
+    (dict(eps=-1.0), fp.ERR_INVALID_ARG),
+    (dict(eps=float("nan")), fp.ERR_INVALID_ARG),
+    (dict(ws=None), fp.ERR_WORKSPACE),
+    (dict(ws_bytes=100), fp.ERR_WORKSPACE),
+    (dict(ptrs=[_P] * 10), fp.ERR_INVALID_ARG),  # O aliases X
+])
+def test_block_rejects_invalid_arguments(kw, code):
+    assert _block(**kw) == code
+    assert fp.last_error() != ""
+
+
+def test_block_rejects_null_and_misaligned_pointers():
+    for i in range(10):
+        ptrs = [_P] * 9 + [ctypes.c_void_p(8192)]
+        ptrs[i] = None
+        assert _block(ptrs=ptrs) == fp.ERR_INVALID_ARG
+        ptrs[i] = ctypes.c_void_p(4096 + 4 if i != 9 else 8192 + 4)
+        assert _block(ptrs=ptrs) == fp.ERR_INVALID_ARG

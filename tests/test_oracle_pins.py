@@ -576,3 +576,31 @@ def test_sdpa_backward_chunked_key_axis(monkeypatch):
     b = orc.sdpa_backward(Q, K, V, O, L, dO)
     for x, y in zip(a, b):
         np.testing.assert_allclose(x, y, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# the pre-norm residual block around the mixer
+# ---------------------------------------------------------------------------
+
+def test_layer_norm_matches_library():
+    g = _rng(31)
+    X = g.standard_normal((2, 7, 32)) * 3 + 1
+    gamma, beta = g.standard_normal(32), g.standard_normal(32)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(X), (32,), torch.from_numpy(gamma),
+                                         torch.from_numpy(beta), eps=1e-5).numpy()
+    np.testing.assert_allclose(orc.layer_norm(X, gamma, beta, 1e-5), ref, atol=1e-12)
+
+
+def test_block_is_residual_plus_mixer_of_library_layer_norm():
+    w, d = _small(seed=32, seed_scale=4.0)
+    g = _rng(33)
+    gamma, beta = 1 + 0.1 * g.standard_normal(w.C), 0.1 * g.standard_normal(w.C)
+    out = orc.block_forward(d["X"], gamma, beta, 1e-5, *_args(d)[1:], w.H)
+    Xn = torch.nn.functional.layer_norm(torch.from_numpy(np.asarray(d["X"], dtype=np.float64)), (w.C,),
+                                        torch.from_numpy(gamma), torch.from_numpy(beta), eps=1e-5).numpy()
+    mix = orc.mixer_forward(Xn, *_args(d)[1:], w.H)["O"]
+    np.testing.assert_allclose(out, np.asarray(d["X"], dtype=np.float64) + mix, atol=1e-12)
+    # zero gamma and beta: the mixer sees zeros, every softmax is uniform and
+    # its values are zero, so the block is the identity
+    np.testing.assert_allclose(orc.block_forward(d["X"], 0 * gamma, 0 * beta, 1e-5, *_args(d)[1:], w.H),
+                               np.asarray(d["X"], dtype=np.float64), atol=1e-12)
