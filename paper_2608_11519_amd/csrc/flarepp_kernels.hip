@@ -314,42 +314,85 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Layer norm of one token per LPT lanes: each lane holds NCH runs of 8
+// channels (one 16- or 32-byte load each), so the row is read once, the two
+// sums are shuffles over the token's lanes, and a wave normalises 64 / LPT
+// tokens at a time.  Channel of lane li, run u: 8 (u LPT + li) + j.
+template <typename T, int LPT, int NCH>
+__global__ __launch_bounds__(256) void k_layernorm_vec(LayerNormParams p) {
+  using F = typename Frag<T>::type;
+  constexpr int TPW = 64 / LPT;
+  const int lane = lane_id(), li = lane % LPT;
+  F gm[NCH], bt[NCH];
+#pragma unroll
+  for (int u = 0; u < NCH; ++u) {
+    gm[u] = load_frag((const T*)p.gamma + 8 * (u * LPT + li));
+    bt[u] = load_frag((const T*)p.beta + 8 * (u * LPT + li));
+  }
+  const float inv_c = 1.f / (float)p.C;
+  for (int64_t t0 = ((int64_t)blockIdx.x * 4 + wave_id()) * TPW; t0 < p.T; t0 += (int64_t)gridDim.x * 4 * TPW) {
+    const int64_t row = min(t0 + lane / LPT, p.T - 1);  // past the end: a duplicate, not stored
+    const T* x = (const T*)p.x + row * p.C;
+    float v[NCH][8];
+    float s = 0.f;
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const F f = load_frag(x + 8 * (u * LPT + li));
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[u][j] = to_f32(f[j]);
+        s += v[u][j];
+      }
+    }
+#pragma unroll
+    for (int k = 1; k < LPT; k <<= 1) s += __shfl_xor(s, k, 64);
+    const float mean = s * inv_c;
+    float q = 0.f;
+#pragma unroll
+    for (int u = 0; u < NCH; ++u)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[u][j] -= mean;
+        q += v[u][j] * v[u][j];
+      }
+#pragma unroll
+    for (int k = 1; k < LPT; k <<= 1) q += __shfl_xor(q, k, 64);
+    const float rstd = 1.f / sqrtf(q * inv_c + p.eps);
+    if (t0 + lane / LPT < p.T) {
+      T* y = (T*)p.y + row * p.C;
+#pragma unroll
+      for (int u = 0; u < NCH; ++u) {
+        F o;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = from_f32<T>(v[u][j] * rstd * to_f32(gm[u][j]) + to_f32(bt[u][j]));
+        *reinterpret_cast<F*>(y + 8 * (u * LPT + li)) = o;
+      }
+    }
+  }
+}
+
+// Any C (a multiple of 32): one wave per token, the row read three times
+// (the sum, the centred squares and the output; the later reads hit the
+// cache).
 template <typename T>
 __global__ __launch_bounds__(256) void k_layernorm(LayerNormParams p) {
-  constexpr int MAXV = 64;  // C <= 4096
   const int lane = lane_id();
-  // one wave per token; the grid is capped, so waves step over the tokens
-  for (int64_t row = (int64_t)blockIdx.x * 4 + wave_id(); row < p.T; row += (int64_t)gridDim.x * 4) {
-  const T* x = (const T*)p.x + row * p.C;
-  // C is a multiple of 32: the last group of 64 channels may be half full;
-  // lanes past C hold zero and stay out of the sums
-  const int nv = (p.C + 63) / 64;
-  float v[MAXV];
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < MAXV; ++i)
-    if (i < nv) {
-      v[i] = i * 64 + lane < p.C ? to_f32(x[i * 64 + lane]) : 0.f;
-      s += v[i];
-    }
-  const float mean = wave_sum(s) / (float)p.C;
-  float q = 0.f;
-#pragma unroll
-  for (int i = 0; i < MAXV; ++i)
-    if (i < nv && i * 64 + lane < p.C) {
-      v[i] -= mean;
-      q += v[i] * v[i];
-    }
-  const float rstd = 1.f / sqrtf(wave_sum(q) / (float)p.C + p.eps);
-  T* y = (T*)p.y + row * p.C;
   const T* gm = (const T*)p.gamma;
   const T* bt = (const T*)p.beta;
-#pragma unroll
-  for (int i = 0; i < MAXV; ++i)
-    if (i < nv && i * 64 + lane < p.C) {
-      const int ch = i * 64 + lane;
-      y[ch] = from_f32<T>(v[i] * rstd * to_f32(gm[ch]) + to_f32(bt[ch]));
+  for (int64_t row = (int64_t)blockIdx.x * 4 + wave_id(); row < p.T; row += (int64_t)gridDim.x * 4) {
+    const T* x = (const T*)p.x + row * p.C;
+    float s = 0.f;
+    for (int ch = lane; ch < p.C; ch += 64) s += to_f32(x[ch]);
+    const float mean = wave_sum(s) / (float)p.C;
+    float q = 0.f;
+    for (int ch = lane; ch < p.C; ch += 64) {
+      const float d = to_f32(x[ch]) - mean;
+      q += d * d;
     }
+    const float rstd = 1.f / sqrtf(wave_sum(q) / (float)p.C + p.eps);
+    T* y = (T*)p.y + row * p.C;
+    for (int ch = lane; ch < p.C; ch += 64)
+      y[ch] = from_f32<T>((to_f32(x[ch]) - mean) * rstd * to_f32(gm[ch]) + to_f32(bt[ch]));
   }
 }
 
@@ -381,7 +424,21 @@ hipError_t launch_dmajor(const DmajorParams& p, hipStream_t s) {
 
 template <typename T>
 hipError_t launch_layernorm(const LayerNormParams& p, hipStream_t s) {
-  k_layernorm<T><<<(unsigned)std::min<int64_t>((p.T + 3) / 4, 1 << 16), 256, 0, s>>>(p);
+  // lanes per token for one run of 8 channels each (C = 32 .. 512), or 64
+  // lanes with 2 .. 8 runs (C = 1024 .. 4096); other widths take k_layernorm
+  const int runs = p.C / 8;
+  auto grid = [&](int tpw) { return (unsigned)std::min<int64_t>((p.T + 4 * tpw - 1) / (4 * tpw), 1 << 16); };
+  switch (p.C % 8 == 0 ? runs : 0) {
+    case 4: k_layernorm_vec<T, 4, 1><<<grid(16), 256, 0, s>>>(p); break;
+    case 8: k_layernorm_vec<T, 8, 1><<<grid(8), 256, 0, s>>>(p); break;
+    case 16: k_layernorm_vec<T, 16, 1><<<grid(4), 256, 0, s>>>(p); break;
+    case 32: k_layernorm_vec<T, 32, 1><<<grid(2), 256, 0, s>>>(p); break;
+    case 64: k_layernorm_vec<T, 64, 1><<<grid(1), 256, 0, s>>>(p); break;
+    case 128: k_layernorm_vec<T, 64, 2><<<grid(1), 256, 0, s>>>(p); break;
+    case 256: k_layernorm_vec<T, 64, 4><<<grid(1), 256, 0, s>>>(p); break;
+    case 512: k_layernorm_vec<T, 64, 8><<<grid(1), 256, 0, s>>>(p); break;
+    default: k_layernorm<T><<<grid(1), 256, 0, s>>>(p); break;
+  }
   return hipGetLastError();
 }
 

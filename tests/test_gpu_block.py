@@ -81,10 +81,11 @@ def test_block_every_decode_kernel(monkeypatch, kind):
     _check_block(w, inp.make_inputs(w, 16, seed_scale=4.0), f"decode-kind{kind}")
 
 
-@pytest.mark.parametrize("C,H,dtype", [(96, 3, "f32"), (32, 2, "bf16"), (512, 8, "bf16")])
+@pytest.mark.parametrize("C,H,dtype", [(96, 3, "f32"), (32, 2, "bf16"), (512, 8, "bf16"), (1024, 16, "bf16"), (2048, 32, "f32")])
 def test_block_widths(C, H, dtype):
-    # C = 96 and 32 leave the layer norm's last group of 64 channels half
-    # full; C = 512 spans eight groups
+    # the layer norm's kernels: C = 96 takes the one-wave-per-token kernel,
+    # C = 32 and 512 a single run of 8 channels per lane (16 and 1 tokens per
+    # wave), C = 1024 and 2048 two and four runs per lane
     w = inp.Workload("block-width", 1, 300, C, H, 32, dtype, "normal")
     _check_block(w, inp.make_inputs(w, 17, seed_scale=4.0), f"C{C}")
 
