@@ -46,6 +46,7 @@ def parse_args(argv=None):
     ap.add_argument("--no-graph", action="store_true", help="launch every step eagerly")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true", help="skip the mixer-backward timing")
+    ap.add_argument("--no-block", action="store_true", help="skip the pre-norm residual block timing")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host seconds spent timing the oracle")
     ap.add_argument("--stage-reps", type=int, default=20,
@@ -438,20 +439,25 @@ def main(argv=None):
         else:
             run_stage()
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        if sg is not None:
-            sg.replay()
-        else:
-            run_stage()
-        e1.record()
-        torch.cuda.synchronize()
-        stage_ms[name] = e0.elapsed_time(e1) / reps
+        # the median of five timed regions of `reps` launches each (a single
+        # region varies by a few microseconds per launch from run to run)
+        region_ms = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            if sg is not None:
+                sg.replay()
+            else:
+                run_stage()
+            e1.record()
+            torch.cuda.synchronize()
+            region_ms.append(e0.elapsed_time(e1) / reps)
+        stage_ms[name] = sorted(region_ms)[2]
     step()  # leave the workspace and O as one complete step wrote them
     torch.cuda.synchronize()
     flare = time_flare(args, w, t, graph is not None)
     backward = None if args.no_backward else time_backward(args, w, t, graph is not None)
-    block = time_block(args, w, t, graph is not None, ms_per_step)
+    block = None if args.no_block else time_block(args, w, t, graph is not None, ms_per_step)
     work = stage_work(w, fused)
     stages = {n: {"ms": round(stage_ms[n], 5), **roofline(work[n], stage_ms[n], w.dtype)}
               for n in fp.PROFILE_STAGES if n not in empty}
@@ -493,8 +499,9 @@ def main(argv=None):
         "stages": stages,
         "wall_ms_timed_region": round(wall_ms, 3),
         "flare": {**flare, "flarepp_over_flare_time": round(ms_per_step / flare["ms_per_step"], 3)},
-        "block": block,
     }
+    if block is not None:
+        out["block"] = block
     if backward is not None:
         out["backward"] = backward
     if not args.no_cpu_baseline:

@@ -237,14 +237,17 @@ FLAREPP_API int flarepp_mixer_forward_shared(int dtype, int64_t B, int64_t N, in
  * Inputs as for flarepp_mixer_forward, plus dO.  Outputs, all fp32 and
  * row-major, overwritten: dX [B][N][C]; dWk, dWv, dWkt, dWvt, dWo [C][C]
  * (the layout of the weights, out = X W); dseeds [H][M][D].  With bf16 the
- * MFMA operands, and the token gradients dY, dK, dV, dK~, dV~ kept between
- * the kernels, are rounded to bf16; accumulation is fp32.
+ * MFMA operands, and the token gradients dY, dK, dK~ kept between the
+ * kernels, are rounded to bf16; the value gradients dV, dV~ are kept as two
+ * bf16 parts (hi + lo, ~16 bits), because the weight gradients X^T dV are
+ * made of their small token-dependent part; accumulation is fp32.
  *
  * Sizes as for the mixer; in addition B*N <= 2^30 (FLAREPP_ERR_UNSUPPORTED
  * otherwise).  Workspace:
  * flarepp_mixer_backward_workspace_bytes(...) bytes (0 for an invalid or
  * unsupported shape); it holds the forward's K, V, K~, V~, Y and the token
- * gradients dY, dK, dV, dK~, dV~, about 10 * bytes(dtype) * B * N * C bytes.
+ * gradients dY, dK, dV, dK~, dV~ (and the low parts of dV, dV~ with bf16),
+ * about 10 * bytes(dtype) * B * N * C bytes (12 with bf16).
  * flarepp_mixer_backward_debug also writes the summed latent gradient dZ and
  * the summed query gradient dQ (fp32 [B][H][M][D] each) when non-null.
  * ------------------------------------------------------------------------- */

@@ -583,8 +583,15 @@ struct BwdSplit {
 BwdSplit bwd_split(int64_t BH, int64_t Nl, int D, int Mp, bool dec, int elem_bytes) {
   BwdSplit sp{};
   const int NS = Mp / 32;
+  // LDS budget of a window at 4 waves; FLAREPP_BWD_WINDOW_KB (testing and
+  // tuning) overrides the default of two workgroups per CU
+  size_t budget = 80 * 1024;
+  if (const char* f = std::getenv("FLAREPP_BWD_WINDOW_KB")) {
+    const long kb = std::atol(f);
+    if (kb >= 16 && kb <= 160) budget = (size_t)kb * 1024;
+  }
   int nwin = 1;
-  while (nwin < NS && flarepp::attn_bwd_lds_bytes(D, (int)cdiv(NS, nwin), Mp, dec, 4, elem_bytes) > 80 * 1024)
+  while (nwin < NS && flarepp::attn_bwd_lds_bytes(D, (int)cdiv(NS, nwin), Mp, dec, 4, elem_bytes) > budget)
     ++nwin;
   sp.nsb = (int)cdiv(NS, nwin);
   sp.waves = flarepp::attn_bwd_waves(D, sp.nsb, Mp, dec, elem_bytes);
@@ -614,11 +621,27 @@ struct BwdWs {
   float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2, *L3;
   float *dZf, *dQf, *c1, *c2, *l1, *l2, *pa, *pg, *pq, *gpart;
   void *dY, *dK, *dV, *dKt, *dVt;
+  void *dVlo, *dVtlo;  // bf16: the value gradients' low parts
   void *Qr, *Qt, *Zr, *dZr, *dZt, *dQr, *dQt, *Sr, *St;
   BwdSplit dec, enc;
   int splits, kchunk;
   size_t bytes;
 };
+
+// bf16: the encoders' value gradients (dV, dV~) are kept as bf16 pairs
+// hi + lo between the SDPA backward and the weight-gradient GEMMs.  A value
+// gradient P^T dOut over a near-uniform softmax is a common part (about the
+// mean of dOut over the routes) plus a small token-dependent part, which
+// falls below the bf16 step of the common part at large N; the weight
+// gradient X^T dV is made of exactly that part (with hi alone dW_V at 2^20
+// tokens is off by ~10% of its largest entry).  The key gradients
+// dK = s dS^T Q have no common part (dS sums to zero over the routes).
+// FLAREPP_BWD_NO_LO=1 (testing and tuning) keeps hi alone.
+bool bwd_lo_parts(int dtype) {
+  if (dtype != FLAREPP_BF16) return false;
+  const char* f = std::getenv("FLAREPP_BWD_NO_LO");
+  return !(f && std::atoi(f) != 0);
+}
 
 BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32), DB = cdiv(D, 32);
@@ -648,6 +671,10 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   w.dV = cv.take(bs * T * C);
   w.dKt = cv.take(bs * T * C);
   w.dVt = cv.take(bs * T * C);
+  if (bwd_lo_parts(dtype)) {
+    w.dVlo = cv.take(bs * T * C);
+    w.dVtlo = cv.take(bs * T * C);
+  }
   w.dZf = (float*)cv.take(f4 * BH * M * D);
   w.dQf = (float*)cv.take(f4 * BH * M * D);
   w.c1 = (float*)cv.take(f4 * BH * Mp);
@@ -817,7 +844,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a2.lrow = w.l2; a2.crow = w.c2;
   a2.blo = w.K; a2.blo_sb = tokBS; a2.blo_sh = tokHS; a2.blo_sn = D; a2.blo_sd = 1;
   a2.glo = w.Vdm; a2.glo_sb = dmBS; a2.glo_sh = dmHS; a2.glo_sn = 1; a2.glo_sd = Np;
-  a2.dout_b = w.dK; a2.acc_b = 1; a2.dout_g = w.dV;
+  a2.dout_b = w.dK; a2.acc_b = 1; a2.dout_g = w.dV; a2.dout_g_lo = w.dVlo;
   a2.part_a = w.pq;
   TRY(attn_windows(a2, w.enc, false));
 
@@ -837,7 +864,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   a1.gsh = w.dQr; a1.gsht = w.dQt;
   a1.lrow = w.l1; a1.crow = w.c1;
   a1.blo = w.Kt; a1.glo = w.Vtdm;
-  a1.dout_b = w.dKt; a1.acc_b = 0; a1.dout_g = w.dVt;
+  a1.dout_b = w.dKt; a1.acc_b = 0; a1.dout_g = w.dVt; a1.dout_g_lo = w.dVtlo;
   a1.part_a = w.pa;
   TRY(attn_windows(a1, w.enc, false));
   rd = BwdReduceParams{};
@@ -861,6 +888,17 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   for (int j = 0; j < 5; ++j) { gw.a[j] = wa[j]; gw.b[j] = wb[j]; }
   gw.a_m = 1; gw.a_k = C; gw.b_k = C; gw.b_n = 1;
   gw.kchunk = w.kchunk; gw.c = w.gpart; gw.c_t = 0; gw.ldc = C; gw.split_stride = C * C;
+  if (w.dVlo) {
+    // dW_V and dW~_V as X^T hi + X^T lo (two K segments); the other three
+    // problems have one (a null second segment)
+    const void* lo[5] = {nullptr, w.dVlo, nullptr, w.dVtlo, nullptr};
+    gw.nseg = 2;
+    for (int j = 0; j < 5; ++j) {
+      gw.a[2 * j] = gw.a[2 * j + 1] = wa[j];
+      gw.b[2 * j] = wb[j];
+      gw.b[2 * j + 1] = lo[j];
+    }
+  }
   HIPTRY(launch_gemm<T>(gw, s));
   float* dW[5] = {dWk, dWv, dWkt, dWvt, dWo};
   HIPTRY(launch_sum_splits(w.gpart, dW, C * C, w.splits, 5, s));

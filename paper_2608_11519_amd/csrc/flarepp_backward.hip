@@ -211,7 +211,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
     for (int b = 0; b < NT; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
-  const int seg0 = p.nprob > 1 ? prob : 0, seg1 = p.nprob > 1 ? prob + 1 : p.nseg;
+  // this problem's segments; a null b operand ends the list early
+  const int seg0 = prob * p.nseg;
+  int seg1 = seg0 + 1;
+  while (seg1 < seg0 + p.nseg && p.b[seg1]) ++seg1;
   // the (segment, k step) sequence of this workgroup, walked with a one-step
   // register prefetch
   const int nk = kend > kbeg ? (kend - kbeg + K - 1) / K : 0;
@@ -318,6 +321,32 @@ __device__ __forceinline__ typename Frag<T>::type long_frag(const T* x, int64_t 
 }
 
 // Route-side operands of one block of 32 routes, loaded one block ahead.
+// Store 4 long-side values at out[o], adding what is there when acc.  With a
+// lo buffer the value is kept as hi = T(v) in out and lo = T(v - hi) in lo:
+// about 16 mantissa bits in bf16, so the token reductions over it (the weight
+// gradients) do not lose the small token-dependent part of a gradient whose
+// tokens share a large common part.
+template <typename T>
+__device__ __forceinline__ void long_store(T* out, T* lo, int64_t o, int acc, float (&v)[4]) {
+  if (acc) {
+    const typename Frag<T>::half old = load_half(out + o);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] += to_f32(old[q]);
+    if (lo) {
+      const typename Frag<T>::half ol = load_half(lo + o);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] += to_f32(ol[q]);
+    }
+  }
+  store4(out + o, v[0], v[1], v[2], v[3]);
+  if (lo) {
+    float r[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[q] = v[q] - to_f32(from_f32<T>(v[q]));
+    store4(lo + o, r[0], r[1], r[2], r[3]);
+  }
+}
+
 template <typename T, int D, bool DEC>
 struct ShortBlock {
   static constexpr int KS = D / 16, DB = (D + 31) / 32;
@@ -565,22 +594,12 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
             float v[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) v[q] = p.s * dk[db][4 * a + q];
-            if (p.acc_b) {
-              const typename Frag<T>::half old = load_half(dout_b + row + d);
-#pragma unroll
-              for (int q = 0; q < 4; ++q) v[q] += to_f32(old[q]);
-            }
-            store4(dout_b + row + d, v[0], v[1], v[2], v[3]);
+            long_store(dout_b, static_cast<T*>(p.dout_b_lo), row + d, p.acc_b, v);
             if (!DEC) {
               float u[4];
 #pragma unroll
               for (int q = 0; q < 4; ++q) u[q] = dv[db][4 * a + q];
-              if (p.acc_g) {
-                const typename Frag<T>::half old = load_half(dout_g + row + d);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) u[q] += to_f32(old[q]);
-              }
-              store4(dout_g + row + d, u[0], u[1], u[2], u[3]);
+              long_store(dout_g, static_cast<T*>(p.dout_g_lo), row + d, p.acc_g, u);
             }
           }
         }

@@ -205,8 +205,8 @@ constexpr int route_nq(int D, bool decode) {
 // single split, the compute type T.
 struct GemmParams {
   int M, N, K, nseg, nprob, splits;
-  const void* a[5];
-  const void* b[5];
+  const void* a[10];  // operands of segment j of problem i at [i * nseg + j];
+  const void* b[10];  // a null b after the first segment ends the problem's list
   int64_t a_m, a_k, b_k, b_n;
   int kchunk;
   void* c;
@@ -242,9 +242,11 @@ struct AttnBwdParams {
   const float* lcol;  // decode: [B * H][Nl], each position's log-normaliser in log2 units
   // outputs: long side [B][Nl][H * D] in T (added to what is there when
   // acc_b / acc_g); short side partials [B][H][R][Mp][D] fp32 (this window's
-  // rows)
-  void* dout_b; int acc_b;
-  void* dout_g; int acc_g;
+  // rows).  With dout_b_lo / dout_g_lo (bf16 only) a long-side value v is
+  // kept as hi = bf16(v) in dout and lo = bf16(v - hi) there, and read back
+  // as hi + lo
+  void* dout_b; void* dout_b_lo; int acc_b;
+  void* dout_g; void* dout_g_lo; int acc_g;
   float* part_a; float* part_g;
 };
 // LDS of a launch over a window of nsb route blocks (Mp routes in all)

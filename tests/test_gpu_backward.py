@@ -16,7 +16,7 @@ from oracle import flarepp_oracle as orc
 from paper_2608_11519_amd import flarepp as fp
 from paper_2608_11519_amd import inputs as inp
 
-from gpu_util import TOL, assert_close, upload
+from gpu_util import TOL, assert_close, rel_err, upload
 
 pytestmark = pytest.mark.gpu
 
@@ -114,3 +114,25 @@ def test_backward_many_routes_in_windows(dtype):
     # partial) and the later windows add to the long-side gradients
     w = inp.Workload("bwd-windows", 1, 700, 128, 2, 300, dtype, "normal")
     _check(w, inp.make_inputs(w, 12, seed_scale=4.0), "M300")
+
+
+def test_value_gradients_keep_their_token_part_at_half_a_million_tokens(monkeypatch):
+    # N = 2^19, M = 512: the encoders' softmaxes over the tokens are near
+    # uniform, so a value gradient P^T dOut is a large common part plus a
+    # small token-dependent part, which bf16 alone rounds away; dW_V = X^T dV
+    # is made of that part.  The bf16 path keeps dV, dV~ as hi + lo pairs;
+    # checked against the fp32 path (itself held to the oracle above), and
+    # the same shape with hi alone must miss the gate (the case has power).
+    w = inp.Workload("bwd-halfmega", 1, 1 << 19, 128, 8, 512, "bf16", "normal")
+    print(f"[case] backward value-gradient precision {inp.describe(w)}", flush=True)
+    d = inp.make_inputs(w, 20)
+    dO = inp.make_tensor((w.B, w.N, w.C), 21, "bf16")  # exact in both types
+    ref = _run(w.replace(dtype="f32"), d, dO, debug=False)
+    got = _run(w, d, dO, debug=False)
+    for k in GRADS:
+        assert_close(k, got[k], ref[k], 1e-2, "halfmega")
+    monkeypatch.setenv("FLAREPP_BWD_NO_LO", "1")
+    hi = _run(w, d, dO, debug=False)
+    e = rel_err(hi["dWv"], ref["dWv"])
+    print(f"  hi alone: dWv {e:.3e}", flush=True)
+    assert e > TOL["bf16"], "with hi alone dW_V should miss the bf16 gate at this size"
