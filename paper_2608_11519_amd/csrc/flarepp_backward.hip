@@ -239,10 +239,12 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
       for (int a = 0; a < MT; ++a) af[a] = load_frag(As + gemm_lds<T>(32 * (MT * mw + a) + c, 16 * ks + 8 * g));
 #pragma unroll
       for (int b = 0; b < NT; ++b) bfr[b] = load_frag(Bs + gemm_lds<T>(32 * (NT * nw + b) + c, 16 * ks + 8 * g));
+      // C^T = B^T A^T: the accumulator's rows are output columns, so each
+      // lane holds runs of 4 consecutive columns of one output row
 #pragma unroll
       for (int a = 0; a < MT; ++a)
 #pragma unroll
-        for (int b = 0; b < NT; ++b) mma(acc[a][b], af[a], bfr[b]);
+        for (int b = 0; b < NT; ++b) mma(acc[a][b], bfr[b], af[a]);
     }
     __syncthreads();
   }
@@ -251,13 +253,23 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
   for (int a = 0; a < MT; ++a)
 #pragma unroll
     for (int b = 0; b < NT; ++b) {
-      const int n = n0 + 32 * (NT * nw + b) + c;
+      const int m = m0 + 32 * (MT * mw + a) + c;
+      if (m >= p.M) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + 32 * (MT * mw + a) + acc_row(lane, r);
-        if (m < p.M && n < p.N) {
-          if (p.c_t) static_cast<T*>(p.c)[base + (int64_t)m * p.ldc + n] = from_f32<T>(acc[a][b][r]);
-          else static_cast<float*>(p.c)[base + (int64_t)m * p.ldc + n] = acc[a][b][r];
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int n = n0 + 32 * (NT * nw + b) + acc_row(lane, 4 * r4);  // 4 columns n .. n + 3
+        const int64_t o = base + (int64_t)m * p.ldc + n;
+        const float v[4] = {acc[a][b][4 * r4], acc[a][b][4 * r4 + 1], acc[a][b][4 * r4 + 2], acc[a][b][4 * r4 + 3]};
+        if (n + 3 < p.N) {
+          if (p.c_t) store4(static_cast<T*>(p.c) + o, v[0], v[1], v[2], v[3]);
+          else store4(static_cast<float*>(p.c) + o, v[0], v[1], v[2], v[3]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (n + q < p.N) {
+              if (p.c_t) static_cast<T*>(p.c)[o + q] = from_f32<T>(v[q]);
+              else static_cast<float*>(p.c)[o + q] = v[q];
+            }
         }
       }
     }

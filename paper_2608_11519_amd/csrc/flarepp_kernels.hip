@@ -121,15 +121,32 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
   for (int q = 0; q < kProjBlocks; ++q)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[q][r] = 0.f;
+  // the operands of k step ks + 1 are loaded before the products of step ks;
+  // rows past N load row N - 1 and are zeroed (the d-major layout stores them
+  // as the zero padding)
+  const T* xr = X + (int64_t)min(xrow, p.N - 1) * p.C + 8 * g;
+  const T* wr = (const T*)p.wf[w] + (int64_t)cg * kProjBlocks * KS * 512 + lane * 8;
+  const int nq = min(kProjBlocks, CB - cg * kProjBlocks);  // wave-uniform
+  F xn = load_frag(xr), wn[kProjBlocks];
+#pragma unroll
+  for (int q = 0; q < kProjBlocks; ++q)
+    if (q < nq) wn[q] = load_frag(wr + (int64_t)q * KS * 512);
   for (int ks = 0; ks < KS; ++ks) {
-    const F xf = xok ? load_frag(X + (int64_t)xrow * p.C + 16 * ks + 8 * g) : zero_frag<T>();
+    const F xf = xok ? xn : zero_frag<T>();
+    F wv[kProjBlocks];
+#pragma unroll
+    for (int q = 0; q < kProjBlocks; ++q) wv[q] = wn[q];
+    if (ks + 1 < KS) {
+      xn = load_frag(xr + 16 * (ks + 1));
+#pragma unroll
+      for (int q = 0; q < kProjBlocks; ++q)
+        if (q < nq) wn[q] = load_frag(wr + ((int64_t)q * KS + ks + 1) * 512);
+    }
 #pragma unroll
     for (int q = 0; q < kProjBlocks; ++q) {
-      const int cb = cg * kProjBlocks + q;
-      if (cb >= CB) break;  // wave-uniform
-      const F wv = load_frag((const T*)p.wf[w] + ((int64_t)cb * KS + ks) * 512 + lane * 8);
-      if (layout == kHeadsDMajor) mma(acc[q], xf, wv);   // rows = tokens, cols = channels
-      else mma(acc[q], wv, xf);                          // rows = channels, cols = tokens
+      if (q >= nq) break;  // wave-uniform
+      if (layout == kHeadsDMajor) mma(acc[q], xf, wv[q]);   // rows = tokens, cols = channels
+      else mma(acc[q], wv[q], xf);                          // rows = channels, cols = tokens
     }
   }
   T* out = (T*)p.out[w];
