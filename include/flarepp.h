@@ -269,6 +269,21 @@ FLAREPP_API int flarepp_mixer_backward_debug(int dtype, int64_t B, int64_t N, in
                                              void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Backward of the shared-projection mixer (flarepp_mixer_forward_shared,
+ * K~ = K and V~ = V; App. C.2): the gradients of <O, dO> with respect to X,
+ * the tied W_K and W_V, W_O and the seeds.  A tied weight's gradient is the
+ * sum of its two uses, dWk = X^T (dK + dK~) and dWv = X^T (dV + dV~), formed
+ * in one fixed-order reduction.  Arguments, outputs, precision, workspace
+ * (flarepp_mixer_backward_workspace_bytes) and errors as for
+ * flarepp_mixer_backward without Wkt, Wvt, dWkt and dWvt.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API int flarepp_mixer_backward_shared(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                              int64_t M, const void* X, const void* Wk, const void* Wv,
+                                              const void* Wo, const void* seeds, const void* dO, float* dX,
+                                              float* dWk, float* dWv, float* dWo, float* dseeds, void* ws,
+                                              size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Profiling variant of flarepp_mixer_forward for timing each stage on the
  * device.  `events` holds FLAREPP_PROFILE_EVENTS caller-created hipEvent_t
  * handles (created with timing enabled); events[0] is recorded on `stream`

@@ -34,7 +34,9 @@ It computes the plain definitions, in float64, in the paper's order:
                   the merge, the decode (call 3), the physical-value encode
                   (call 2), the summed query gradient through the query
                   synthesis (call 1), the seeds (summed over the batch) and
-                  the four projections.
+                  the four projections.  ``mixer_backward_shared`` the same
+                  with K~ = K, V~ = V (App. C.2): a tied weight's gradient
+                  sums its two uses.
 
 Readings of points the paper leaves open (all fixed here, in the same way as
 in the input generator):
@@ -77,6 +79,7 @@ __all__ = [
     "mixer_backward",
     "layer_norm",
     "block_forward",
+    "mixer_backward_shared",
 ]
 
 # Key chunk for the two-pass softmax and query chunk for independent rows;
@@ -368,3 +371,12 @@ def layer_norm(X, gamma, beta, eps: float) -> np.ndarray:
 def block_forward(X, gamma, beta, eps: float, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int) -> np.ndarray:
     """The pre-norm residual block around the mixer: X + mixer(LN(X))."""
     return _f64(X) + mixer_forward(layer_norm(X, gamma, beta, eps), Wk, Wv, Wkt, Wvt, Wo, seeds, H)["O"]
+
+
+def mixer_backward_shared(X, Wk, Wv, Wo, seeds, H: int, dO) -> dict:
+    """Backward of the shared-projection mixer (K~ = K, V~ = V): the mixer's
+    backward with W~_K = W_K and W~_V = W_V, a tied weight's gradient being
+    the sum of the gradients of its two uses."""
+    g = mixer_backward(X, Wk, Wv, Wk, Wv, Wo, seeds, H, dO)
+    return {"dX": g["dX"], "dWk": g["dWk"] + g["dWkt"], "dWv": g["dWv"] + g["dWvt"], "dWo": g["dWo"],
+            "dseeds": g["dseeds"]}

@@ -888,6 +888,22 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   for (int j = 0; j < 5; ++j) { gw.a[j] = wa[j]; gw.b[j] = wb[j]; }
   gw.a_m = 1; gw.a_k = C; gw.b_k = C; gw.b_n = 1;
   gw.kchunk = w.kchunk; gw.c = w.gpart; gw.c_t = 0; gw.ldc = C; gw.split_stride = C * C;
+  if (!dWkt) {
+    // tied weights (W~_K = W_K, W~_V = W_V): dW_K = X^T (dK + dK~) and
+    // dW_V = X^T (dV + dV~) (with the low parts under bf16), each one problem
+    // over K segments; then dW_O
+    const void* seg[3][4] = {{w.dK, w.dKt, nullptr, nullptr},
+                             {w.dV, w.dVt, w.dVlo, w.dVtlo},
+                             {dO, nullptr, nullptr, nullptr}};
+    const void* sa[3] = {X, X, w.Y};
+    gw.nprob = 3; gw.nseg = 4;
+    for (int j = 0; j < 3; ++j)
+      for (int k = 0; k < 4; ++k) { gw.a[4 * j + k] = sa[j]; gw.b[4 * j + k] = seg[j][k]; }
+    HIPTRY(launch_gemm<T>(gw, s));
+    float* dW3[3] = {dWk, dWv, dWo};
+    HIPTRY(launch_sum_splits(w.gpart, dW3, C * C, w.splits, 3, s));
+    return ok();
+  }
   if (w.dVlo) {
     // dW_V and dW~_V as X^T hi + X^T lo (two K segments); the other three
     // problems have one (a null second segment)
@@ -909,14 +925,17 @@ int backward_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_
                    const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                    const void* seeds, const void* dO, float* dX, float* dWk, float* dWv, float* dWkt,
                    float* dWvt, float* dWo, float* dseeds, float* dZ_out, float* dQ_out, void* ws,
-                   size_t ws_bytes, void* stream) {
+                   size_t ws_bytes, void* stream, bool shared = false) {
   TRY(check_backward_shape(dtype, B, N, C, H, M));
+  if (shared) dWkt = dWvt = nullptr;
   const void* in[] = {X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO};
   const char* in_names[] = {"X", "Wk", "Wv", "Wkt", "Wvt", "Wo", "seeds", "dO"};
   for (int i = 0; i < 8; ++i) TRY(check_ptr(in[i], in_names[i]));
+  // shared: the tied weights' gradients land in dWk and dWv (dWkt, dWvt null)
   const float* out[] = {dX, dWk, dWv, dWkt, dWvt, dWo, dseeds};
   const char* out_names[] = {"dX", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds"};
-  for (int i = 0; i < 7; ++i) TRY(check_ptr(out[i], out_names[i]));
+  for (int i = 0; i < 7; ++i)
+    if (!(shared && (i == 3 || i == 4))) TRY(check_ptr(out[i], out_names[i]));
   TRY(check_ptr(dZ_out, "dZ_out", true));
   TRY(check_ptr(dQ_out, "dQ_out", true));
   if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
@@ -1152,6 +1171,14 @@ int flarepp_mixer_backward_debug(int dtype, int64_t B, int64_t N, int64_t C, int
                                  size_t ws_bytes, void* stream) {
   return backward_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt, dWvt,
                         dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, stream);
+}
+
+int flarepp_mixer_backward_shared(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                  const void* X, const void* Wk, const void* Wv, const void* Wo,
+                                  const void* seeds, const void* dO, float* dX, float* dWk, float* dWv,
+                                  float* dWo, float* dseeds, void* ws, size_t ws_bytes, void* stream) {
+  return backward_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wk, Wv, Wo, seeds, dO, dX, dWk, dWv, nullptr, nullptr,
+                        dWo, dseeds, nullptr, nullptr, ws, ws_bytes, stream, true);
 }
 
 }  // extern "C"

@@ -205,8 +205,8 @@ constexpr int route_nq(int D, bool decode) {
 // single split, the compute type T.
 struct GemmParams {
   int M, N, K, nseg, nprob, splits;
-  const void* a[10];  // operands of segment j of problem i at [i * nseg + j];
-  const void* b[10];  // a null b after the first segment ends the problem's list
+  const void* a[16];  // operands of segment j of problem i at [i * nseg + j];
+  const void* b[16];  // a null b after the first segment ends the problem's list
   int64_t a_m, a_k, b_k, b_n;
   int kchunk;
   void* c;

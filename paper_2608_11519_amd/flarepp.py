@@ -35,6 +35,7 @@ EXPORTS = (
     "flarepp_flare_workspace_bytes", "flarepp_flare_forward", "flarepp_flare_forward_debug",
     "flarepp_mixer_backward_workspace_bytes", "flarepp_mixer_backward", "flarepp_mixer_backward_debug",
     "flarepp_mixer_forward_shared", "flarepp_block_workspace_bytes", "flarepp_block_forward",
+    "flarepp_mixer_backward_shared",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -105,6 +106,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_mixer_backward_debug.restype = i32
     lib.flarepp_mixer_backward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8 + [fp] * 9
                                                  + [vp, sz, vp])
+    lib.flarepp_mixer_backward_shared.restype = i32
+    lib.flarepp_mixer_backward_shared.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 6 + [fp] * 5
+                                                  + [vp, sz, vp])
     lib.flarepp_block_workspace_bytes.restype = sz
     lib.flarepp_block_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
     lib.flarepp_block_forward.restype = i32
@@ -415,6 +419,31 @@ def flarepp_mixer_backward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,
     return _backward(True, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws)
 
 
+def flarepp_mixer_backward_shared(X, Wk, Wv, Wo, seeds, dO, *, H: int,
+                                  ws: Optional[torch.Tensor] = None, out: Optional[dict] = None):
+    """Gradients of <O, dO> for the shared-projection mixer (K~ = K, V~ = V):
+    a dict of fp32 tensors dX [B, N, C], dWk, dWv, dWo [C, C] (the tied
+    weights' gradients summed over both uses) and dseeds [H, M, D]."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    D = C // H
+    dt = _dtype_code(X)
+    f32 = dict(dtype=torch.float32, device=X.device)
+    if out is not None:
+        g = dict(out)
+    else:
+        g = {"dX": torch.empty((B, N, C), **f32), "dWk": torch.empty((C, C), **f32),
+             "dWv": torch.empty((C, C), **f32), "dWo": torch.empty((C, C), **f32),
+             "dseeds": torch.empty((H, M, D), **f32)}
+    w = _workspace(flarepp_mixer_backward_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_mixer_backward_shared(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wo), _ptr(seeds),
+                                           _ptr(dO), *[_ptr(g[k]) for k in ("dX", "dWk", "dWv", "dWo", "dseeds")],
+                                           _ptr(w), w.numel(), _stream(X.device))
+    _check(rc)
+    return g
+
+
 def flarepp_block_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
     return int(load().flarepp_block_workspace_bytes(dtype, B, N, C, H, M))
 
@@ -448,3 +477,4 @@ mixer_forward_shared = flarepp_mixer_forward_shared
 mixer_backward = flarepp_mixer_backward
 mixer_backward_debug = flarepp_mixer_backward_debug
 block_forward = flarepp_block_forward
+mixer_backward_shared = flarepp_mixer_backward_shared

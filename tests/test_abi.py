@@ -275,3 +275,16 @@ def test_block_rejects_null_and_misaligned_pointers():
         assert _block(ptrs=ptrs) == fp.ERR_INVALID_ARG
         ptrs[i] = ctypes.c_void_p(4096 + 4 if i != 9 else 8192 + 4)
         assert _block(ptrs=ptrs) == fp.ERR_INVALID_ARG
+
+
+def test_shared_backward_rejects_invalid_arguments():
+    lib = _lib()
+    args = lambda B=1, ptrs=None, ws=_P, nbytes=1 << 30: lib.flarepp_mixer_backward_shared(
+        fp.BF16, B, 64, 64, 4, 32, *(ptrs or [_P] * 11), ws, nbytes, None)
+    assert args(B=0) == fp.ERR_INVALID_ARG
+    assert args(ws=None) == fp.ERR_WORKSPACE
+    assert args(nbytes=16) == fp.ERR_WORKSPACE
+    for i in range(11):
+        ptrs = [_P] * 11
+        ptrs[i] = None
+        assert args(ptrs=ptrs) == fp.ERR_INVALID_ARG

@@ -136,3 +136,19 @@ def test_value_gradients_keep_their_token_part_at_half_a_million_tokens(monkeypa
     e = rel_err(hi["dWv"], ref["dWv"])
     print(f"  hi alone: dWv {e:.3e}", flush=True)
     assert e > TOL["bf16"], "with hi alone dW_V should miss the bf16 gate at this size"
+
+
+@pytest.mark.parametrize("name", ["tiny", "grid2d"])
+def test_shared_projection_backward(name):
+    # K~ = K, V~ = V: the tied weights' gradients sum their two uses
+    w = inp.workload(name)
+    d = inp.make_inputs(w, 22, seed_scale=4.0)
+    print(f"[case] backward shared {inp.describe(w)}", flush=True)
+    dO = inp.make_tensor((w.B, w.N, w.C), 23, w.dtype)
+    t = upload(d, w)
+    dOt = torch.from_numpy(dO).to("cuda", t["X"].dtype)
+    g = fp.flarepp_mixer_backward_shared(t["X"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], dOt, H=w.H)
+    torch.cuda.synchronize()
+    ref = orc.mixer_backward_shared(d["X"], d["Wk"], d["Wv"], d["Wo"], d["seeds"], w.H, dO)
+    for k in ("dX", "dWk", "dWv", "dWo", "dseeds"):
+        assert_close(k, g[k].cpu().numpy(), ref[k], TOL[w.dtype], f"shared-{name}")

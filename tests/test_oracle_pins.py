@@ -604,3 +604,28 @@ def test_block_is_residual_plus_mixer_of_library_layer_norm():
     # its values are zero, so the block is the identity
     np.testing.assert_allclose(orc.block_forward(d["X"], 0 * gamma, 0 * beta, 1e-5, *_args(d)[1:], w.H),
                                np.asarray(d["X"], dtype=np.float64), atol=1e-12)
+
+
+def test_shared_backward_matches_library_autograd_with_tied_weights():
+    # K~ = K, V~ = V: autograd through one tensor used twice sums its two
+    # gradients by itself
+    w, d = _small(seed=34, seed_scale=4.0)
+    dO = _rng(35).standard_normal((w.B, w.N, w.C))
+    tied = dict(d, Wkt=d["Wk"], Wvt=d["Wv"])
+    t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64)).clone().requires_grad_(True)
+    X, Wk, Wv, Wo, seeds = (t(d[k]) for k in ("X", "Wk", "Wv", "Wo", "seeds"))
+    B, N, C, H, D = w.B, w.N, w.C, w.H, w.D
+    heads = lambda W: (X @ W).view(B, N, H, D).permute(0, 2, 1, 3)
+    sd = torch.nn.functional.scaled_dot_product_attention
+    K, V = heads(Wk), heads(Wv)
+    Q = sd(seeds.unsqueeze(0).expand(B, -1, -1, -1), K, V)
+    Z = sd(Q, K, V)
+    O = sd(K, Q, Z).permute(0, 2, 1, 3).reshape(B, N, C) @ Wo
+    (O * torch.from_numpy(dO)).sum().backward()
+    r = orc.mixer_backward_shared(d["X"], d["Wk"], d["Wv"], d["Wo"], d["seeds"], w.H, dO)
+    for k, g in (("dX", X.grad), ("dWk", Wk.grad), ("dWv", Wv.grad), ("dWo", Wo.grad), ("dseeds", seeds.grad)):
+        g = g.numpy()
+        assert np.abs(r[k] - g).max() <= 1e-10 * max(1.0, np.abs(g).max()), k
+    # and it is not the untied gradient: the tilde uses contribute
+    u = orc.mixer_backward(*_args(tied), w.H, dO)
+    assert np.abs(r["dWk"] - u["dWk"]).max() > 1e-6 * np.abs(r["dWk"]).max()
