@@ -300,9 +300,20 @@ def time_backward(args, w, t, use_graph):
     fl = backward_flops(w)
     peak = PEAK_MFMA_BF16_TFLOPS if w.dtype == "bf16" else PEAK_MFMA_F32_TFLOPS
     tf = fl / (ms * 1e-3) / 1e12
+    # the training pair: a forward that keeps its statistics, then the
+    # backward from them (no second forward)
+    O = torch.empty_like(t["X"])
+    args7 = args6[:7]
+
+    def train_step():
+        fp.flarepp_mixer_forward_train(*args7, H=w.H, ws=ws, out=O)
+        fp.flarepp_mixer_backward_from_saved(*args6, H=w.H, ws=ws, out=out)
+
+    ms_train = _time_steps(args, train_step, use_graph)
     return {"ms_per_step": round(ms, 5), "tokens_per_s": round(w.B * w.N / (ms * 1e-3), 1),
             "algorithmic_tflop": round(fl / 1e12, 4), "achieved_tflops": round(tf, 2),
-            "mfma_frac": round(tf / peak, 4)}
+            "mfma_frac": round(tf / peak, 4),
+            "train_pair_ms": round(ms_train, 5)}
 
 
 def time_flare(args, w, t, use_graph):

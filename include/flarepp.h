@@ -284,6 +284,32 @@ FLAREPP_API int flarepp_mixer_backward_shared(int dtype, int64_t B, int64_t N, i
                                               size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Training pair: a forward that keeps what the backward needs, and a backward
+ * that reads it instead of running the forward again.
+ *
+ * flarepp_mixer_forward_train computes O like flarepp_mixer_forward (on the
+ * unfused kernels, the results agree within rounding) and leaves in `ws`
+ * (flarepp_mixer_backward_workspace_bytes bytes) the projections K, V, K~,
+ * V~, the decoded tokens Y, Q(X), Z and the three log-normalisers.
+ * flarepp_mixer_backward_from_saved then computes exactly what
+ * flarepp_mixer_backward computes for the same inputs (bit for bit), given a
+ * workspace that a flarepp_mixer_forward_train with the same sizes and inputs
+ * filled and that nothing has written since; it does not modify the saved
+ * state, so one forward can serve several output gradients.  Arguments,
+ * outputs and errors as for flarepp_mixer_forward and flarepp_mixer_backward.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API int flarepp_mixer_forward_train(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                            const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                                            const void* Wvt, const void* Wo, const void* seeds, void* O,
+                                            void* ws, size_t ws_bytes, void* stream);
+FLAREPP_API int flarepp_mixer_backward_from_saved(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                                  int64_t M, const void* X, const void* Wk, const void* Wv,
+                                                  const void* Wkt, const void* Wvt, const void* Wo,
+                                                  const void* seeds, const void* dO, float* dX, float* dWk,
+                                                  float* dWv, float* dWkt, float* dWvt, float* dWo,
+                                                  float* dseeds, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Profiling variant of flarepp_mixer_forward for timing each stage on the
  * device.  `events` holds FLAREPP_PROFILE_EVENTS caller-created hipEvent_t
  * handles (created with timing enabled); events[0] is recorded on `stream`

@@ -708,6 +708,12 @@ int check_backward_shape(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   return FLAREPP_OK;
 }
 
+// What backward_impl runs: the forward again and the reverse pass; the
+// forward alone, keeping its statistics in the workspace and writing O (the
+// training forward); or the reverse pass alone, on the statistics a training
+// forward left in the workspace.
+enum BwdMode { kBwdFull = 0, kBwdForward = 1, kBwdReverse = 2 };
+
 // The mixer's reverse pass: the forward again (unfused kernels, which keep
 // K, V, K~, V~, Y and the log-normalisers of both encodes), then the merge,
 // call 3, call 2, call 1 and the projections in reverse order.
@@ -716,7 +722,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
                   const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                   const void* seeds, const void* dO, float* dX, float* dWk, float* dWv, float* dWkt,
                   float* dWvt, float* dWo, float* dseeds, float* dZ_out, float* dQ_out, void* ws,
-                  size_t ws_bytes, hipStream_t s) {
+                  size_t ws_bytes, hipStream_t s, int mode = kBwdFull, void* O = nullptr) {
   using namespace flarepp;
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32), DB = cdiv(D, 32);
   const int64_t NT = B * N, BH = B * H;
@@ -727,10 +733,15 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   const float sc = (float)(1.0 / std::sqrt((double)D));
   const bool f32 = std::is_same<T, float>::value;
 
-  // ---- forward with its statistics ----
+  const void* w_in[4] = {Wk, Wv, Wkt, Wvt};
+  const EncPlan e = encode_plan(B, H, N, Mp, D);
+  const int64_t tokHS = N * D, tokBS = H * N * D, dmHS = D * Np, dmBS = H * D * Np;
+  const int64_t rtHS = Mp * D, rtBS = H * Mp * D;
+
+  // ---- forward with its statistics (kept in the workspace) ----
+  if (mode != kBwdReverse) {
   WeightFragParams wp{};
   wp.C = (int)C;
-  const void* w_in[4] = {Wk, Wv, Wkt, Wvt};
   for (int i = 0; i < 4; ++i) { wp.w[i] = w_in[i]; wp.out[i] = w.wf[i]; }
   wp.nw = 4;
   HIPTRY(launch_weight_frags<T>(wp, s));
@@ -746,9 +757,6 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   pp.wf[2] = w.wf[2]; pp.out[2] = w.Kt;   pp.layout[2] = kHeadsTokenMajor;
   pp.wf[3] = w.wf[3]; pp.out[3] = w.Vtdm; pp.layout[3] = kHeadsDMajor;
   HIPTRY(launch_project<T>(pp, s));
-  const EncPlan e = encode_plan(B, H, N, Mp, D);
-  const int64_t tokHS = N * D, tokBS = H * N * D, dmHS = D * Np, dmBS = H * D * Np;
-  const int64_t rtHS = Mp * D, rtBS = H * Mp * D;
   RouteParams r1 = encode_params(e, B, H, N, Mp, D);
   r1.ka = w.Kt; r1.ka_sb = tokBS; r1.ka_sh = tokHS; r1.ka_rows = (int)N;
   r1.va = w.Vtdm; r1.va_sb = dmBS; r1.va_sh = dmHS; r1.va_ld = (int)Np;
@@ -773,6 +781,16 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
   r3.y = w.Y; r3.y_sb = N * C; r3.y_row = C; r3.lse2 = w.L3;
   HIPTRY(launch_route<T>(r3, (int)D, true, s));
+  }
+  if (mode == kBwdForward) {  // the training forward's output O = Y W_O
+    GemmParams go{};
+    go.M = (int)NT; go.N = (int)C; go.K = (int)C; go.nseg = 1; go.nprob = 1; go.splits = 1;
+    go.a[0] = w.Y; go.a_m = C; go.a_k = 1;
+    go.b[0] = Wo; go.b_k = C; go.b_n = 1;
+    go.kchunk = (int)round_up(C, 64); go.c = O; go.c_t = 1; go.ldc = C; go.split_stride = 0;
+    HIPTRY(launch_gemm<T>(go, s));
+    return ok();
+  }
 
   // ---- merge: dY = dO W_O^T (dW_O is computed with the weight gradients) ----
   GemmParams g{};
@@ -925,7 +943,7 @@ int backward_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_
                    const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
                    const void* seeds, const void* dO, float* dX, float* dWk, float* dWv, float* dWkt,
                    float* dWvt, float* dWo, float* dseeds, float* dZ_out, float* dQ_out, void* ws,
-                   size_t ws_bytes, void* stream, bool shared = false) {
+                   size_t ws_bytes, void* stream, bool shared = false, int mode = kBwdFull) {
   TRY(check_backward_shape(dtype, B, N, C, H, M));
   if (shared) dWkt = dWvt = nullptr;
   const void* in[] = {X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO};
@@ -943,9 +961,28 @@ int backward_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == FLAREPP_F32)
     return backward_impl<float>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt,
-                                dWvt, dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, s);
+                                dWvt, dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, s, mode);
   return backward_impl<__bf16>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt,
-                               dWvt, dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, s);
+                               dWvt, dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, s, mode);
+}
+
+int forward_train_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
+                        const void* Wk, const void* Wv, const void* Wkt, const void* Wvt, const void* Wo,
+                        const void* seeds, void* O, void* ws, size_t ws_bytes, void* stream) {
+  TRY(check_backward_shape(dtype, B, N, C, H, M));
+  const void* in[] = {X, Wk, Wv, Wkt, Wvt, Wo, seeds, O};
+  const char* in_names[] = {"X", "Wk", "Wv", "Wkt", "Wvt", "Wo", "seeds", "O"};
+  for (int i = 0; i < 8; ++i) TRY(check_ptr(in[i], in_names[i]));
+  if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
+  TRY(check_ptr(ws, "ws"));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FLAREPP_F32)
+    return backward_impl<float>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, nullptr, nullptr, nullptr,
+                                nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes, s,
+                                kBwdForward, O);
+  return backward_impl<__bf16>(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, nullptr, nullptr, nullptr,
+                               nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes, s,
+                               kBwdForward, O);
 }
 
 }  // namespace
@@ -1171,6 +1208,22 @@ int flarepp_mixer_backward_debug(int dtype, int64_t B, int64_t N, int64_t C, int
                                  size_t ws_bytes, void* stream) {
   return backward_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt, dWvt,
                         dWo, dseeds, dZ_out, dQ_out, ws, ws_bytes, stream);
+}
+
+int flarepp_mixer_forward_train(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                const void* X, const void* Wk, const void* Wv, const void* Wkt, const void* Wvt,
+                                const void* Wo, const void* seeds, void* O, void* ws, size_t ws_bytes,
+                                void* stream) {
+  return forward_train_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, ws, ws_bytes, stream);
+}
+
+int flarepp_mixer_backward_from_saved(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                      const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                                      const void* Wvt, const void* Wo, const void* seeds, const void* dO,
+                                      float* dX, float* dWk, float* dWv, float* dWkt, float* dWvt, float* dWo,
+                                      float* dseeds, void* ws, size_t ws_bytes, void* stream) {
+  return backward_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, dX, dWk, dWv, dWkt, dWvt,
+                        dWo, dseeds, nullptr, nullptr, ws, ws_bytes, stream, false, kBwdReverse);
 }
 
 int flarepp_mixer_backward_shared(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,

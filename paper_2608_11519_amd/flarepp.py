@@ -35,7 +35,7 @@ EXPORTS = (
     "flarepp_flare_workspace_bytes", "flarepp_flare_forward", "flarepp_flare_forward_debug",
     "flarepp_mixer_backward_workspace_bytes", "flarepp_mixer_backward", "flarepp_mixer_backward_debug",
     "flarepp_mixer_forward_shared", "flarepp_block_workspace_bytes", "flarepp_block_forward",
-    "flarepp_mixer_backward_shared",
+    "flarepp_mixer_backward_shared", "flarepp_mixer_forward_train", "flarepp_mixer_backward_from_saved",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -106,6 +106,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_mixer_backward_debug.restype = i32
     lib.flarepp_mixer_backward_debug.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8 + [fp] * 9
                                                  + [vp, sz, vp])
+    lib.flarepp_mixer_forward_train.restype = i32
+    lib.flarepp_mixer_forward_train.argtypes = [i32, i64, i64, i64, i64, i64] + [vp] * 8 + [vp, sz, vp]
+    lib.flarepp_mixer_backward_from_saved.restype = i32
+    lib.flarepp_mixer_backward_from_saved.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 8 + [fp] * 7
+                                                      + [vp, sz, vp])
     lib.flarepp_mixer_backward_shared.restype = i32
     lib.flarepp_mixer_backward_shared.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 6 + [fp] * 5
                                                   + [vp, sz, vp])
@@ -377,7 +382,7 @@ def flarepp_mixer_backward_workspace_bytes(dtype: int, B: int, N: int, C: int, H
     return int(load().flarepp_mixer_backward_workspace_bytes(dtype, B, N, C, H, M))
 
 
-def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out=None):
+def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out=None, saved=False):
     lib = load()
     B, N, C = X.shape
     M = seeds.shape[1]
@@ -396,7 +401,16 @@ def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out=None):
         g["dZ"] = torch.empty((B, H, M, D), **f32)
         g["dQ"] = torch.empty((B, H, M, D), **f32)
         outs += [g["dZ"], g["dQ"]]
-    w = _workspace(flarepp_mixer_backward_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    need = flarepp_mixer_backward_workspace_bytes(dt, B, N, C, H, M)
+    if saved and (ws is None or ws.numel() * ws.element_size() < need):
+        raise ValueError("backward_from_saved needs the workspace its training forward filled")
+    w = _workspace(need, X.device, ws)
+    if saved:
+        rc = lib.flarepp_mixer_backward_from_saved(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt),
+                                                   _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(dO),
+                                                   *[_ptr(t) for t in outs], _ptr(w), w.numel(), _stream(X.device))
+        _check(rc)
+        return g
     fn = lib.flarepp_mixer_backward_debug if debug else lib.flarepp_mixer_backward
     rc = fn(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt), _ptr(Wvt), _ptr(Wo), _ptr(seeds),
             _ptr(dO), *[_ptr(t) for t in outs], _ptr(w), w.numel(), _stream(X.device))
@@ -410,6 +424,33 @@ def flarepp_mixer_backward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,
     dX [B, N, C], dWk, dWv, dWkt, dWvt, dWo [C, C] and dseeds [H, M, D]
     (written into ``out``'s tensors when given)."""
     return _backward(False, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out)
+
+
+def flarepp_mixer_forward_train(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, ws: torch.Tensor,
+                                out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Mixer forward that keeps in ``ws`` (at least
+    flarepp_mixer_backward_workspace_bytes bytes) what
+    flarepp_mixer_backward_from_saved reads: O [B, N, C] in X's dtype."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    dt = _dtype_code(X)
+    need = flarepp_mixer_backward_workspace_bytes(dt, B, N, C, H, M)
+    if ws.numel() * ws.element_size() < need:
+        raise ValueError(f"ws holds {ws.numel() * ws.element_size()} bytes, {need} needed")
+    O = out if out is not None else torch.empty_like(X)
+    rc = lib.flarepp_mixer_forward_train(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt), _ptr(Wvt),
+                                         _ptr(Wo), _ptr(seeds), _ptr(O), _ptr(ws), ws.numel() * ws.element_size(),
+                                         _stream(X.device))
+    _check(rc)
+    return O
+
+
+def flarepp_mixer_backward_from_saved(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int, ws: torch.Tensor,
+                                      out: Optional[dict] = None):
+    """``flarepp_mixer_backward`` on the state a flarepp_mixer_forward_train
+    with the same inputs left in ``ws`` (no forward is run again)."""
+    return _backward(False, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out, saved=True)
 
 
 def flarepp_mixer_backward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int,
@@ -478,3 +519,5 @@ mixer_backward = flarepp_mixer_backward
 mixer_backward_debug = flarepp_mixer_backward_debug
 block_forward = flarepp_block_forward
 mixer_backward_shared = flarepp_mixer_backward_shared
+mixer_forward_train = flarepp_mixer_forward_train
+mixer_backward_from_saved = flarepp_mixer_backward_from_saved

@@ -288,3 +288,24 @@ def test_shared_backward_rejects_invalid_arguments():
         ptrs = [_P] * 11
         ptrs[i] = None
         assert args(ptrs=ptrs) == fp.ERR_INVALID_ARG
+
+
+def test_training_pair_rejects_invalid_arguments():
+    lib = _lib()
+    fwd = lambda B=1, ptrs=None, ws=_P, nbytes=1 << 30: lib.flarepp_mixer_forward_train(
+        fp.BF16, B, 64, 64, 4, 32, *(ptrs or [_P] * 8), ws, nbytes, None)
+    assert fwd(B=0) == fp.ERR_INVALID_ARG
+    assert fwd(ws=None) == fp.ERR_WORKSPACE
+    assert fwd(nbytes=16) == fp.ERR_WORKSPACE
+    for i in range(8):
+        ptrs = [_P] * 8
+        ptrs[i] = None
+        assert fwd(ptrs=ptrs) == fp.ERR_INVALID_ARG
+    bwd = lambda B=1, ptrs=None, ws=_P, nbytes=1 << 30: lib.flarepp_mixer_backward_from_saved(
+        fp.BF16, B, 64, 64, 4, 32, *(ptrs or [_P] * 15), ws, nbytes, None)
+    assert bwd(B=0) == fp.ERR_INVALID_ARG
+    assert bwd(nbytes=16) == fp.ERR_WORKSPACE
+    for i in range(15):
+        ptrs = [_P] * 15
+        ptrs[i] = None
+        assert bwd(ptrs=ptrs) == fp.ERR_INVALID_ARG

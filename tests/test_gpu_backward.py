@@ -152,3 +152,29 @@ def test_shared_projection_backward(name):
     ref = orc.mixer_backward_shared(d["X"], d["Wk"], d["Wv"], d["Wo"], d["seeds"], w.H, dO)
     for k in ("dX", "dWk", "dWv", "dWo", "dseeds"):
         assert_close(k, g[k].cpu().numpy(), ref[k], TOL[w.dtype], f"shared-{name}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "grid2d"])
+def test_training_forward_then_backward_from_saved(name):
+    # the training forward's O against the oracle; the backward from its
+    # saved state bitwise equal to the backward that runs the forward again,
+    # for two output gradients from one forward
+    w = inp.workload(name)
+    d = inp.make_inputs(w, 24, seed_scale=4.0)
+    print(f"[case] training pair {inp.describe(w)}", flush=True)
+    t = upload(d, w)
+    args = (t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"], t["seeds"])
+    dt = fp.F32 if w.dtype == "f32" else fp.BF16
+    ws = torch.empty(fp.flarepp_mixer_backward_workspace_bytes(dt, w.B, w.N, w.C, w.H, w.M), dtype=torch.uint8,
+                     device="cuda")
+    O = fp.flarepp_mixer_forward_train(*args, H=w.H, ws=ws)
+    torch.cuda.synchronize()
+    ref = orc.mixer_forward(d["X"], d["Wk"], d["Wv"], d["Wkt"], d["Wvt"], d["Wo"], d["seeds"], w.H)
+    assert_close("O", O.float().cpu().numpy(), ref["O"], TOL[w.dtype], f"train-{name}")
+    for seed in (25, 26):
+        dO = torch.from_numpy(inp.make_tensor((w.B, w.N, w.C), seed, w.dtype)).to("cuda", t["X"].dtype)
+        a = fp.flarepp_mixer_backward_from_saved(*args, dO, H=w.H, ws=ws)
+        b = fp.flarepp_mixer_backward(*args, dO, H=w.H)
+        torch.cuda.synchronize()
+        for k in GRADS:
+            assert torch.equal(a[k], b[k]), k
