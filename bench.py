@@ -47,6 +47,8 @@ def parse_args(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true", help="skip the mixer-backward timing")
     ap.add_argument("--no-block", action="store_true", help="skip the pre-norm residual block timing")
+    ap.add_argument("--no-train-pair", action="store_true",
+                    help="skip the training forward + backward-from-saved timing")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host seconds spent timing the oracle")
     ap.add_argument("--stage-reps", type=int, default=20,
@@ -309,11 +311,11 @@ def time_backward(args, w, t, use_graph):
         fp.flarepp_mixer_forward_train(*args7, H=w.H, ws=ws, out=O)
         fp.flarepp_mixer_backward_from_saved(*args6, H=w.H, ws=ws, out=out)
 
-    ms_train = _time_steps(args, train_step, use_graph)
+    ms_train = None if args.no_train_pair else _time_steps(args, train_step, use_graph)
     return {"ms_per_step": round(ms, 5), "tokens_per_s": round(w.B * w.N / (ms * 1e-3), 1),
             "algorithmic_tflop": round(fl / 1e12, 4), "achieved_tflops": round(tf, 2),
             "mfma_frac": round(tf / peak, 4),
-            "train_pair_ms": round(ms_train, 5)}
+            "train_pair_ms": None if ms_train is None else round(ms_train, 5)}
 
 
 def time_flare(args, w, t, use_graph):
