@@ -204,6 +204,31 @@ FLAREPP_API int flarepp_block_forward(int dtype, int64_t B, int64_t N, int64_t C
                                       size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Backward of the pre-norm residual block O = X + mixer(LayerNorm(X)): the
+ * gradients of <O, dO> with respect to X, gamma, beta, the five weights and
+ * the seeds.  The layer norm runs again (keeping each token's mean and
+ * 1 / sqrt(var + eps)), the mixer backward runs on the normalised tokens, and
+ * dX = dO + rstd (g - mean_c(g) - xhat mean_c(g xhat)) with g = dXn * gamma,
+ * xhat the normalised token and dXn the mixer's input gradient; dgamma =
+ * sum_tokens dXn * xhat and dbeta = sum_tokens dXn in fixed-order sums.
+ * Inputs as for flarepp_block_forward plus dO [B][N][C] (dtype); outputs
+ * fp32, overwritten: dX [B][N][C], dgamma and dbeta [C], the rest as for
+ * flarepp_mixer_backward.  Workspace:
+ * flarepp_block_backward_workspace_bytes(...) bytes (0 for an invalid shape).
+ * Errors as for flarepp_mixer_backward, plus FLAREPP_ERR_INVALID_ARG for
+ * eps <= 0.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_block_backward_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C,
+                                                          int64_t H, int64_t M);
+FLAREPP_API int flarepp_block_backward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                       const void* X, const void* gamma, const void* beta, float eps,
+                                       const void* Wk, const void* Wv, const void* Wkt, const void* Wvt,
+                                       const void* Wo, const void* seeds, const void* dO, float* dX,
+                                       float* dgamma, float* dbeta, float* dWk, float* dWv, float* dWkt,
+                                       float* dWvt, float* dWo, float* dseeds, void* ws, size_t ws_bytes,
+                                       void* stream);
+
+/* ---------------------------------------------------------------------------
  * Shared-projection mixer: FLARE++ with the query-synthesis keys and values
  * tied to the physical ones (K~ = K, V~ = V), the variant the paper's cost
  * model leaves open (App. C.2): call 1 is Q = SDPA(Q~, K, V).  Same

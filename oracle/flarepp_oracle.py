@@ -30,6 +30,8 @@ It computes the plain definitions, in float64, in the paper's order:
                   X + mixer(LN(X)) (the residual stream the paper leaves
                   unchanged, Sec. 3.2); ``layer_norm`` normalises each token
                   over its channels with the biased variance.
+* ``block_backward`` the block's gradients: the mixer's backward on the
+                  normalised tokens, the layer norm's backward, the residual.
 * ``mixer_backward`` the reverse pass of the whole mixer (App. A.5): W_O and
                   the merge, the decode (call 3), the physical-value encode
                   (call 2), the summed query gradient through the query
@@ -80,6 +82,7 @@ __all__ = [
     "layer_norm",
     "block_forward",
     "mixer_backward_shared",
+    "block_backward",
 ]
 
 # Key chunk for the two-pass softmax and query chunk for independent rows;
@@ -380,3 +383,24 @@ def mixer_backward_shared(X, Wk, Wv, Wo, seeds, H: int, dO) -> dict:
     g = mixer_backward(X, Wk, Wv, Wk, Wv, Wo, seeds, H, dO)
     return {"dX": g["dX"], "dWk": g["dWk"] + g["dWkt"], "dWv": g["dWv"] + g["dWvt"], "dWo": g["dWo"],
             "dseeds": g["dseeds"]}
+
+
+def block_backward(X, gamma, beta, eps: float, Wk, Wv, Wkt, Wvt, Wo, seeds, H: int, dO) -> dict:
+    """Gradients of <O, dO> for O = X + mixer(LN(X)).  With xhat the
+    normalised token, r = 1 / sqrt(var + eps) and g = dXn * gamma (dXn the
+    mixer's input gradient): dX = dO + r (g - mean_c g - xhat mean_c(g xhat)),
+    dgamma = sum_tokens dXn xhat, dbeta = sum_tokens dXn."""
+    X = _f64(X)
+    mean = X.mean(axis=-1, keepdims=True)
+    var = ((X - mean) ** 2).mean(axis=-1, keepdims=True)
+    r = 1.0 / np.sqrt(var + eps)
+    xhat = (X - mean) * r
+    Xn = xhat * _f64(gamma) + _f64(beta)
+    g = mixer_backward(Xn, Wk, Wv, Wkt, Wvt, Wo, seeds, H, dO)
+    dXn = g["dX"]
+    gg = dXn * _f64(gamma)
+    dX = _f64(dO) + r * (gg - gg.mean(axis=-1, keepdims=True) - xhat * (gg * xhat).mean(axis=-1, keepdims=True))
+    out = {k: g[k] for k in ("dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds")}
+    out.update(dX=dX, dgamma=(dXn * xhat).reshape(-1, X.shape[-1]).sum(axis=0),
+               dbeta=dXn.reshape(-1, X.shape[-1]).sum(axis=0))
+    return out

@@ -1178,6 +1178,80 @@ int flarepp_block_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
                             mws, ws_bytes - xn_bytes, s, nullptr, 0, false, X);
 }
 
+// Block backward workspace: the normalised tokens, their statistics, the
+// mixer's input gradient (fp32), the dgamma / dbeta partials, then the mixer
+// backward's own workspace.
+struct BlockBwdWs {
+  void *xn, *ws;
+  float *mean, *rstd, *dxn, *part;
+  int nchunks;
+  int64_t chunk;
+  size_t bytes, ws_bytes;
+};
+
+BlockBwdWs block_bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  const int64_t T = B * N;
+  Carver cv(base);
+  BlockBwdWs w{};
+  w.chunk = std::max<int64_t>(1, cdiv(T, 1024));
+  w.nchunks = (int)cdiv(T, w.chunk);
+  w.xn = cv.take((size_t)dtype_bytes(dtype) * T * C);
+  w.mean = (float*)cv.take(sizeof(float) * T);
+  w.rstd = (float*)cv.take(sizeof(float) * T);
+  w.dxn = (float*)cv.take(sizeof(float) * T * C);
+  w.part = (float*)cv.take(sizeof(float) * 2 * w.nchunks * C);
+  w.ws_bytes = bwd_ws(nullptr, dtype, B, N, C, H, M).bytes;
+  w.ws = cv.take(w.ws_bytes);
+  w.bytes = cv.off;
+  return w;
+}
+
+size_t flarepp_block_backward_workspace_bytes(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
+  if (check_backward_shape(dtype, B, N, C, H, M) != FLAREPP_OK) return 0;
+  return block_bwd_ws(nullptr, dtype, B, N, C, H, M).bytes;
+}
+
+int flarepp_block_backward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M, const void* X,
+                           const void* gamma, const void* beta, float eps, const void* Wk, const void* Wv,
+                           const void* Wkt, const void* Wvt, const void* Wo, const void* seeds, const void* dO,
+                           float* dX, float* dgamma, float* dbeta, float* dWk, float* dWv, float* dWkt,
+                           float* dWvt, float* dWo, float* dseeds, void* ws, size_t ws_bytes, void* stream) {
+  TRY(check_backward_shape(dtype, B, N, C, H, M));
+  const void* in[] = {X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, dO};
+  const char* in_names[] = {"X", "gamma", "beta", "Wk", "Wv", "Wkt", "Wvt", "Wo", "seeds", "dO"};
+  for (int i = 0; i < 10; ++i) TRY(check_ptr(in[i], in_names[i]));
+  const float* out[] = {dX, dgamma, dbeta, dWk, dWv, dWkt, dWvt, dWo, dseeds};
+  const char* out_names[] = {"dX", "dgamma", "dbeta", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds"};
+  for (int i = 0; i < 9; ++i) TRY(check_ptr(out[i], out_names[i]));
+  if (!(eps > 0.f) || !std::isfinite(eps)) return fail(FLAREPP_ERR_INVALID_ARG, "eps=%g must be positive", (double)eps);
+  if (!ws) return fail(FLAREPP_ERR_WORKSPACE, "workspace is NULL");
+  TRY(check_ptr(ws, "ws"));
+  const BlockBwdWs w = block_bwd_ws(ws, dtype, B, N, C, H, M);
+  if (ws_bytes < w.bytes)
+    return fail(FLAREPP_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, w.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  flarepp::LayerNormParams lp{};
+  lp.x = X; lp.gamma = gamma; lp.beta = beta; lp.y = w.xn; lp.T = B * N; lp.C = (int)C; lp.eps = eps;
+  lp.mean = w.mean; lp.rstd = w.rstd;
+  flarepp::LayerNormBwdParams lb{};
+  lb.x = X; lb.gamma = gamma; lb.mean = w.mean; lb.rstd = w.rstd; lb.dxn = w.dxn; lb.dO = dO; lb.dx = dX;
+  lb.part = w.part; lb.T = B * N; lb.C = (int)C; lb.nchunks = w.nchunks; lb.chunk = w.chunk;
+  float* dgb[2] = {dgamma, dbeta};
+  if (dtype == FLAREPP_F32) {
+    HIPTRY(flarepp::launch_layernorm<float>(lp, s));
+    TRY(backward_impl<float>(dtype, B, N, C, H, M, w.xn, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, w.dxn, dWk, dWv, dWkt,
+                             dWvt, dWo, dseeds, nullptr, nullptr, w.ws, w.ws_bytes, s));
+    HIPTRY(flarepp::launch_layernorm_bwd<float>(lb, s));
+  } else {
+    HIPTRY(flarepp::launch_layernorm<__bf16>(lp, s));
+    TRY(backward_impl<__bf16>(dtype, B, N, C, H, M, w.xn, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, w.dxn, dWk, dWv, dWkt,
+                              dWvt, dWo, dseeds, nullptr, nullptr, w.ws, w.ws_bytes, s));
+    HIPTRY(flarepp::launch_layernorm_bwd<__bf16>(lb, s));
+  }
+  HIPTRY(flarepp::launch_sum_splits(w.part, dgb, C, w.nchunks, 2, s));
+  return ok();
+}
+
 int flarepp_mixer_forward_shared(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
                                  const void* X, const void* Wk, const void* Wv, const void* Wo,
                                  const void* seeds, void* O, void* ws, size_t ws_bytes, void* stream) {

@@ -45,6 +45,17 @@ struct LayerNormParams {
   const void* x; const void* gamma; const void* beta; void* y;
   int64_t T; int C;
   float eps;
+  float* mean; float* rstd;  // optional [T]: each token's mean and 1 / sqrt(var + eps)
+};
+// Layer-norm backward of the block O = X + mixer(LN(X)): dx = dO + the
+// layer norm's input gradient for the normalised-input gradient dxn (fp32);
+// per token chunk, the partial sums of dgamma = sum dxn * xhat and dbeta =
+// sum dxn over the chunk's tokens.
+struct LayerNormBwdParams {
+  const void* x; const void* gamma; const float* mean; const float* rstd;
+  const float* dxn; const void* dO; float* dx;
+  float* part;  // [2][nchunks][C]: dgamma partials, then dbeta partials
+  int64_t T; int C; int nchunks; int64_t chunk;
 };
 
 struct RouteParams {
@@ -288,6 +299,7 @@ template <typename T> hipError_t launch_bwd_prep(const BwdPrepParams&, hipStream
 int64_t bwd_prep_items(const BwdPrepParams&, int job);
 
 template <typename T> hipError_t launch_layernorm(const LayerNormParams&, hipStream_t);
+template <typename T> hipError_t launch_layernorm_bwd(const LayerNormBwdParams&, hipStream_t);
 template <typename T> hipError_t launch_weight_frags(const WeightFragParams&, hipStream_t);
 template <typename Ts, typename T> hipError_t launch_route_prep(const RoutePrepParams&, hipStream_t);
 template <typename T> hipError_t launch_dmajor(const DmajorParams&, hipStream_t);

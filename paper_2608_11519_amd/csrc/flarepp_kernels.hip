@@ -375,6 +375,10 @@ __global__ __launch_bounds__(256) void k_layernorm_vec(LayerNormParams p) {
 #pragma unroll
     for (int k = 1; k < LPT; k <<= 1) q += __shfl_xor(q, k, 64);
     const float rstd = 1.f / sqrtf(q * inv_c + p.eps);
+    if (p.mean && li == 0 && t0 + lane / LPT < p.T) {
+      p.mean[row] = mean;
+      p.rstd[row] = rstd;
+    }
     if (t0 + lane / LPT < p.T) {
       T* y = (T*)p.y + row * p.C;
 #pragma unroll
@@ -407,10 +411,60 @@ __global__ __launch_bounds__(256) void k_layernorm(LayerNormParams p) {
       q += d * d;
     }
     const float rstd = 1.f / sqrtf(wave_sum(q) / (float)p.C + p.eps);
+    if (p.mean && lane == 0) {
+      p.mean[row] = mean;
+      p.rstd[row] = rstd;
+    }
     T* y = (T*)p.y + row * p.C;
     for (int ch = lane; ch < p.C; ch += 64)
       y[ch] = from_f32<T>((to_f32(x[ch]) - mean) * rstd * to_f32(gm[ch]) + to_f32(bt[ch]));
   }
+}
+
+// Input gradient of the block's layer norm plus the residual, one wave per
+// token: with g = dxn * gamma and xhat = (x - mean) rstd,
+// dx = dO + rstd (g - mean_c(g) - xhat mean_c(g xhat)).
+template <typename T>
+__global__ __launch_bounds__(256) void k_layernorm_bwd_dx(LayerNormBwdParams p) {
+  const int lane = lane_id();
+  const T* gm = (const T*)p.gamma;
+  for (int64_t row = (int64_t)blockIdx.x * 4 + wave_id(); row < p.T; row += (int64_t)gridDim.x * 4) {
+    const T* x = (const T*)p.x + row * p.C;
+    const float* dxn = p.dxn + row * p.C;
+    const float mu = p.mean[row], rs = p.rstd[row];
+    float sg = 0.f, sgx = 0.f;
+    for (int ch = lane; ch < p.C; ch += 64) {
+      const float g = dxn[ch] * to_f32(gm[ch]);
+      sg += g;
+      sgx += g * (to_f32(x[ch]) - mu) * rs;
+    }
+    const float mg = wave_sum(sg) / (float)p.C, mgx = wave_sum(sgx) / (float)p.C;
+    const T* dO = (const T*)p.dO + row * p.C;
+    float* dx = p.dx + row * p.C;
+    for (int ch = lane; ch < p.C; ch += 64) {
+      const float g = dxn[ch] * to_f32(gm[ch]);
+      const float xh = (to_f32(x[ch]) - mu) * rs;
+      dx[ch] = to_f32(dO[ch]) + rs * (g - mg - xh * mgx);
+    }
+  }
+}
+
+// Partial sums of dgamma and dbeta over a chunk of tokens: one thread per
+// channel (coalesced across the block), tokens in order.
+template <typename T>
+__global__ __launch_bounds__(256) void k_layernorm_bwd_params(LayerNormBwdParams p) {
+  const int ch = blockIdx.x * 256 + threadIdx.x;
+  const int z = blockIdx.y;
+  if (ch >= p.C) return;
+  const int64_t t0 = (int64_t)z * p.chunk, t1 = min(p.T, t0 + p.chunk);
+  float sg = 0.f, sb = 0.f;
+  for (int64_t t = t0; t < t1; ++t) {
+    const float d = p.dxn[t * p.C + ch];
+    sg += d * (to_f32(((const T*)p.x)[t * p.C + ch]) - p.mean[t]) * p.rstd[t];
+    sb += d;
+  }
+  p.part[(int64_t)z * p.C + ch] = sg;
+  p.part[((int64_t)p.nchunks + z) * p.C + ch] = sb;
 }
 
 // ---------------------------------------------------------------------------
@@ -460,6 +514,14 @@ hipError_t launch_layernorm(const LayerNormParams& p, hipStream_t s) {
 }
 
 template <typename T>
+hipError_t launch_layernorm_bwd(const LayerNormBwdParams& p, hipStream_t s) {
+  k_layernorm_bwd_dx<T><<<(unsigned)std::min<int64_t>((p.T + 3) / 4, 1 << 16), 256, 0, s>>>(p);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  k_layernorm_bwd_params<T><<<dim3((unsigned)((p.C + 255) / 256), (unsigned)p.nchunks), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T>
 hipError_t launch_project(const ProjParams& p, hipStream_t s) {
   const int64_t units = (int64_t)p.B * (p.Np / 32) * ((p.C / 32 + kProjBlocks - 1) / kProjBlocks) * p.nw;
   k_project<T><<<blocks_for(units, 4), 256, 0, s>>>(p);
@@ -494,6 +556,8 @@ template hipError_t launch_dmajor<float>(const DmajorParams&, hipStream_t);
 template hipError_t launch_dmajor<__bf16>(const DmajorParams&, hipStream_t);
 template hipError_t launch_layernorm<float>(const LayerNormParams&, hipStream_t);
 template hipError_t launch_layernorm<__bf16>(const LayerNormParams&, hipStream_t);
+template hipError_t launch_layernorm_bwd<float>(const LayerNormBwdParams&, hipStream_t);
+template hipError_t launch_layernorm_bwd<__bf16>(const LayerNormBwdParams&, hipStream_t);
 template hipError_t launch_project<float>(const ProjParams&, hipStream_t);
 template hipError_t launch_project<__bf16>(const ProjParams&, hipStream_t);
 template hipError_t launch_route<float>(const RouteParams&, int, bool, hipStream_t);

@@ -36,6 +36,7 @@ EXPORTS = (
     "flarepp_mixer_backward_workspace_bytes", "flarepp_mixer_backward", "flarepp_mixer_backward_debug",
     "flarepp_mixer_forward_shared", "flarepp_block_workspace_bytes", "flarepp_block_forward",
     "flarepp_mixer_backward_shared", "flarepp_mixer_forward_train", "flarepp_mixer_backward_from_saved",
+    "flarepp_block_backward_workspace_bytes", "flarepp_block_backward",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -114,6 +115,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_mixer_backward_shared.restype = i32
     lib.flarepp_mixer_backward_shared.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 6 + [fp] * 5
                                                   + [vp, sz, vp])
+    lib.flarepp_block_backward_workspace_bytes.restype = sz
+    lib.flarepp_block_backward_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
+    lib.flarepp_block_backward.restype = i32
+    lib.flarepp_block_backward.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 3 + [ctypes.c_float]
+                                           + [vp] * 7 + [fp] * 9 + [vp, sz, vp])
     lib.flarepp_block_workspace_bytes.restype = sz
     lib.flarepp_block_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
     lib.flarepp_block_forward.restype = i32
@@ -507,6 +513,35 @@ def flarepp_block_forward(X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int
     return O
 
 
+def flarepp_block_backward_workspace_bytes(dtype: int, B: int, N: int, C: int, H: int, M: int) -> int:
+    return int(load().flarepp_block_backward_workspace_bytes(dtype, B, N, C, H, M))
+
+
+def flarepp_block_backward(X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H: int, eps: float = 1e-5,
+                           ws: Optional[torch.Tensor] = None):
+    """Gradients of <O, dO> for the pre-norm residual block: a dict of fp32
+    tensors dX [B, N, C], dgamma, dbeta [C], dWk, dWv, dWkt, dWvt, dWo [C, C]
+    and dseeds [H, M, D]."""
+    lib = load()
+    B, N, C = X.shape
+    M = seeds.shape[1]
+    D = C // H
+    dt = _dtype_code(X)
+    f32 = dict(dtype=torch.float32, device=X.device)
+    g = {"dX": torch.empty((B, N, C), **f32), "dgamma": torch.empty(C, **f32), "dbeta": torch.empty(C, **f32)}
+    for k in ("dWk", "dWv", "dWkt", "dWvt", "dWo"):
+        g[k] = torch.empty((C, C), **f32)
+    g["dseeds"] = torch.empty((H, M, D), **f32)
+    w = _workspace(flarepp_block_backward_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
+    rc = lib.flarepp_block_backward(dt, B, N, C, H, M, _ptr(X), _ptr(gamma), _ptr(beta), float(eps), _ptr(Wk),
+                                    _ptr(Wv), _ptr(Wkt), _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(dO),
+                                    *[_ptr(g[k]) for k in ("dX", "dgamma", "dbeta", "dWk", "dWv", "dWkt", "dWvt",
+                                                            "dWo", "dseeds")],
+                                    _ptr(w), w.numel(), _stream(X.device))
+    _check(rc)
+    return g
+
+
 # short aliases
 project = flarepp_project
 route = flarepp_route
@@ -521,3 +556,4 @@ block_forward = flarepp_block_forward
 mixer_backward_shared = flarepp_mixer_backward_shared
 mixer_forward_train = flarepp_mixer_forward_train
 mixer_backward_from_saved = flarepp_mixer_backward_from_saved
+block_backward = flarepp_block_backward

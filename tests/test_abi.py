@@ -309,3 +309,20 @@ def test_training_pair_rejects_invalid_arguments():
         ptrs = [_P] * 15
         ptrs[i] = None
         assert bwd(ptrs=ptrs) == fp.ERR_INVALID_ARG
+
+
+def test_block_backward_rejects_invalid_arguments():
+    lib = _lib()
+    call = lambda B=1, eps=1e-5, ptrs=None, ws=_P, nbytes=1 << 30: lib.flarepp_block_backward(
+        fp.BF16, B, 64, 64, 4, 32, *([_P] * 3 if ptrs is None else ptrs[:3]), eps, *([_P] * 7 if ptrs is None else ptrs[3:10]),
+        *([_P] * 9 if ptrs is None else ptrs[10:]), ws, nbytes, None)
+    assert call(B=0) == fp.ERR_INVALID_ARG
+    assert call(eps=0.0) == fp.ERR_INVALID_ARG
+    assert call(ws=None) == fp.ERR_WORKSPACE
+    assert call(nbytes=16) == fp.ERR_WORKSPACE
+    for i in range(19):
+        ptrs = [_P] * 19
+        ptrs[i] = None
+        assert call(ptrs=ptrs) == fp.ERR_INVALID_ARG
+    n = fp.flarepp_block_backward_workspace_bytes(fp.BF16, 2, 1000, 128, 8, 64)
+    assert n > fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 2, 1000, 128, 8, 64) + 4 * 2 * 1000 * 128

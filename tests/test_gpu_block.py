@@ -110,3 +110,29 @@ def test_block_workspace_and_output_reuse():
     b = fp.flarepp_block_forward(*args, H=w.H, ws=ws, out=out)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+BWD = ("dX", "dgamma", "dbeta", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dseeds")
+
+
+@pytest.mark.parametrize("name,C,H", [("tiny", None, None), ("grid2d", None, None), ("widths", 96, 3)])
+def test_block_backward(name, C, H):
+    # the layer norm's backward (both layer-norm kernel shapes: C = 64, 128
+    # take the vector kernel's statistics, C = 96 the one-wave-per-token one)
+    # and the residual on top of the mixer backward
+    w = inp.workload(name) if C is None else inp.Workload("block-bwd", 1, 300, C, H, 32, "f32", "normal")
+    d = inp.make_inputs(w, 27, seed_scale=4.0)
+    d = dict(d, X=np.asarray(d["X"], dtype=np.float32) * 0.25)
+    print(f"[case] block backward {name} {inp.describe(w)}", flush=True)
+    gamma = 1.0 + inp.make_tensor((w.C,), 28, w.dtype, scale=0.2)
+    gamma = inp.round_to_bf16(gamma.astype(np.float32)) if w.dtype == "bf16" else gamma.astype(np.float32)
+    beta = inp.make_tensor((w.C,), 29, w.dtype, scale=0.2)
+    dO = inp.make_tensor((w.B, w.N, w.C), 30, w.dtype)
+    t = upload(dict(d, gamma=gamma, beta=beta, dO=dO), w)
+    g = fp.flarepp_block_backward(t["X"], t["gamma"], t["beta"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"],
+                                  t["seeds"], t["dO"], H=w.H)
+    torch.cuda.synchronize()
+    ref = orc.block_backward(d["X"], gamma, beta, 1e-5, d["Wk"], d["Wv"], d["Wkt"], d["Wvt"], d["Wo"], d["seeds"],
+                             w.H, dO)
+    for k in BWD:
+        assert_close(k, g[k].cpu().numpy(), ref[k], TOL[w.dtype], f"block-bwd-{name}")

@@ -629,3 +629,27 @@ def test_shared_backward_matches_library_autograd_with_tied_weights():
     # and it is not the untied gradient: the tilde uses contribute
     u = orc.mixer_backward(*_args(tied), w.H, dO)
     assert np.abs(r["dWk"] - u["dWk"]).max() > 1e-6 * np.abs(r["dWk"]).max()
+
+
+def test_block_backward_matches_library_autograd():
+    w, d = _small(seed=36, seed_scale=4.0)
+    g0 = _rng(37)
+    gamma, beta = 1 + 0.2 * g0.standard_normal(w.C), 0.2 * g0.standard_normal(w.C)
+    dO = g0.standard_normal((w.B, w.N, w.C))
+    t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64)).clone().requires_grad_(True)
+    X, ga, be, Wk, Wv, Wkt, Wvt, Wo, seeds = (t(v) for v in (d["X"], gamma, beta, d["Wk"], d["Wv"], d["Wkt"],
+                                                             d["Wvt"], d["Wo"], d["seeds"]))
+    B, N, C, H, D = w.B, w.N, w.C, w.H, w.D
+    Xn = torch.nn.functional.layer_norm(X, (C,), ga, be, eps=1e-5)
+    heads = lambda W: (Xn @ W).view(B, N, H, D).permute(0, 2, 1, 3)
+    sd = torch.nn.functional.scaled_dot_product_attention
+    Q = sd(seeds.unsqueeze(0).expand(B, -1, -1, -1), heads(Wkt), heads(Wvt))
+    K = heads(Wk)
+    Z = sd(Q, K, heads(Wv))
+    O = X + sd(K, Q, Z).permute(0, 2, 1, 3).reshape(B, N, C) @ Wo
+    (O * torch.from_numpy(dO)).sum().backward()
+    r = orc.block_backward(d["X"], gamma, beta, 1e-5, *_args(d)[1:], w.H, dO)
+    for k, v in (("dX", X), ("dgamma", ga), ("dbeta", be), ("dWk", Wk), ("dWv", Wv), ("dWkt", Wkt),
+                 ("dWvt", Wvt), ("dWo", Wo), ("dseeds", seeds)):
+        ref = v.grad.numpy()
+        assert np.abs(r[k] - ref).max() <= 1e-10 * max(1.0, np.abs(ref).max()), k
