@@ -83,6 +83,19 @@ __device__ __forceinline__ void store_pair(float* p, float a, float b) {
   *reinterpret_cast<f32x2*>(p) = v;
 }
 
+// Element j of fragments a and b (k and k + 1 of one row) as one k pair.
+// bf16: the two 16-bit halves are picked by a byte permute, no conversion.
+__device__ __forceinline__ void store_kpair(__bf16* p, const bf16x8& a, const bf16x8& b, int j) {
+  typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+  const u32x4 ua = __builtin_bit_cast(u32x4, a), ub = __builtin_bit_cast(u32x4, b);
+  // result bytes {a.lo, b.lo} for even j, {a.hi, b.hi} for odd j
+  *reinterpret_cast<unsigned int*>(p) =
+      __builtin_amdgcn_perm(ub[j >> 1], ua[j >> 1], (j & 1) ? 0x07060302u : 0x05040100u);
+}
+__device__ __forceinline__ void store_kpair(float* p, const f32x8& a, const f32x8& b, int j) {
+  store_pair(p, a[j], b[j]);
+}
+
 // One ROWS x K operand tile, staged through registers into LDS as rows of k:
 // row i, column k holds X(row0 + i, k0 + k) where X(i, k) = x[i * s_i + k *
 // s_k].  Unit stride along k: runs of 8 k values (16-byte loads and stores).
@@ -184,8 +197,7 @@ __device__ __forceinline__ void gemm_store(const GemmStage<T, ROWS>& st, T* dst,
       if (r >= IG * (K / 2)) break;
       const int ii = (r % IG) * 8, kk = 2 * (r / IG);
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        store_pair(dst + gemm_lds<T>(ii + j, kk), to_f32(st.f[2 * q][j]), to_f32(st.f[2 * q + 1][j]));
+      for (int j = 0; j < 8; ++j) store_kpair(dst + gemm_lds<T>(ii + j, kk), st.f[2 * q], st.f[2 * q + 1], j);
     }
   }
 }
