@@ -185,8 +185,8 @@ FLAREPP_API int flarepp_flare_forward_debug(int dtype, int64_t B, int64_t N, int
 
 /* ---------------------------------------------------------------------------
  * Mixer block: O = X + mixer(LN(X)), the pre-norm residual block around the
- * mixer (the residual stream of Sec. 3.2 "What dynamic routing does not
- * change").  LN normalises every token over its C channels:
+ * mixer (the residual stream that Sec. 3.2 leaves as it is; only the mixer
+ * changes).  LN normalises every token over its C channels:
  * (x - mean) / sqrt(var + eps) * gamma + beta with the biased variance;
  * gamma, beta [C] in dtype, eps > 0.  The normalised tokens go to a
  * workspace buffer (one pass) and through the same kernels as

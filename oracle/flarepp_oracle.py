@@ -16,7 +16,7 @@ It computes the plain definitions, in float64, in the paper's order:
 * ``mixer_forward`` project; Q = SDPA(Q~, K~, V~) (Eq. (8));
                   Z = SDPA(Q, K, V) (Eq. (10)); Y = SDPA(K, Q, Z) (Eq. (11));
                   heads merged and multiplied by W_O (Sec. 3.1 after Eq. (2);
-                  Fig. 1 "merge(Y) @ Wo").
+                  Fig. 1).
 * ``split_merge`` the exact split-key merge of partial results
                   (App. A.2, Eqs. (22)-(23); stable form App. A.3,
                   Eqs. (24)-(28), including the empty-row convention).
