@@ -178,3 +178,32 @@ def test_training_forward_then_backward_from_saved(name):
         torch.cuda.synchronize()
         for k in GRADS:
             assert torch.equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("B,N,C,H,M,dtype", [(1, 2000, 256, 8, 96, "bf16"), (2, 33, 64, 4, 300, "f32"),
+                                             (1, 700, 128, 2, 300, "bf16")])
+def test_shared_and_training_pair_on_other_shapes(B, N, C, H, M, dtype):
+    # C = 256 (eight heads of 32), a token tail with M > N, and M = 300 at
+    # D = 64 (route windows): the shared backward against the oracle, the
+    # training pair bitwise against the full backward
+    w = inp.Workload("bwd-shapes", B, N, C, H, M, dtype, "normal")
+    d = inp.make_inputs(w, 31, seed_scale=4.0)
+    print(f"[case] shared + training pair {inp.describe(w)}", flush=True)
+    dO = inp.make_tensor((w.B, w.N, w.C), 32, w.dtype)
+    t = upload(d, w)
+    dOt = torch.from_numpy(dO).to("cuda", t["X"].dtype)
+    g = fp.flarepp_mixer_backward_shared(t["X"], t["Wk"], t["Wv"], t["Wo"], t["seeds"], dOt, H=w.H)
+    torch.cuda.synchronize()
+    ref = orc.mixer_backward_shared(d["X"], d["Wk"], d["Wv"], d["Wo"], d["seeds"], w.H, dO)
+    for k in ("dX", "dWk", "dWv", "dWo", "dseeds"):
+        assert_close(k, g[k].cpu().numpy(), ref[k], TOL[w.dtype], "shared-shapes")
+    args = (t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"], t["seeds"])
+    dt = fp.F32 if w.dtype == "f32" else fp.BF16
+    ws = torch.empty(fp.flarepp_mixer_backward_workspace_bytes(dt, w.B, w.N, w.C, w.H, w.M), dtype=torch.uint8,
+                     device="cuda")
+    fp.flarepp_mixer_forward_train(*args, H=w.H, ws=ws)
+    a = fp.flarepp_mixer_backward_from_saved(*args, dOt, H=w.H, ws=ws)
+    b = fp.flarepp_mixer_backward(*args, dOt, H=w.H)
+    torch.cuda.synchronize()
+    for k in GRADS:
+        assert torch.equal(a[k], b[k]), k

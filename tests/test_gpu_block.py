@@ -136,3 +136,23 @@ def test_block_backward(name, C, H):
                              w.H, dO)
     for k in BWD:
         assert_close(k, g[k].cpu().numpy(), ref[k], TOL[w.dtype], f"block-bwd-{name}")
+
+
+@pytest.mark.parametrize("B,N,C,H,M,dtype", [(2, 33, 64, 4, 100, "f32"), (1, 1500, 256, 8, 64, "bf16")])
+def test_block_backward_tail_and_wide(B, N, C, H, M, dtype):
+    w = inp.Workload("block-bwd-shapes", B, N, C, H, M, dtype, "normal")
+    d = inp.make_inputs(w, 33, seed_scale=4.0)
+    d = dict(d, X=np.asarray(d["X"], dtype=np.float32) * 0.25)
+    print(f"[case] block backward {inp.describe(w)}", flush=True)
+    gamma = 1.0 + inp.make_tensor((w.C,), 34, w.dtype, scale=0.2)
+    gamma = inp.round_to_bf16(gamma.astype(np.float32)) if w.dtype == "bf16" else gamma.astype(np.float32)
+    beta = inp.make_tensor((w.C,), 35, w.dtype, scale=0.2)
+    dO = inp.make_tensor((w.B, w.N, w.C), 36, w.dtype)
+    t = upload(dict(d, gamma=gamma, beta=beta, dO=dO), w)
+    g = fp.flarepp_block_backward(t["X"], t["gamma"], t["beta"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], t["Wo"],
+                                  t["seeds"], t["dO"], H=w.H)
+    torch.cuda.synchronize()
+    ref = orc.block_backward(d["X"], gamma, beta, 1e-5, d["Wk"], d["Wv"], d["Wkt"], d["Wvt"], d["Wo"], d["seeds"],
+                             w.H, dO)
+    for k in BWD:
+        assert_close(k, g[k].cpu().numpy(), ref[k], TOL[w.dtype], "block-bwd-shapes")
