@@ -448,22 +448,52 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
     }
     // long-side B operands of the short-side products (k = position, n = d)
     F kt[2][DB], gt[2][DB];
+    // row-major long side (unit stride along d): each lane stores its
+    // position's row of 32 columns into the wave's transpose tile with
+    // 16-byte loads, then reads one column (d = 32 db + c) of it
+    auto transpose_long = [&](const T* x, int64_t sn, F (&out)[2][DB]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
+      for (int db = 0; db < DB; ++db) {
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int nn = n0 + 16 * kk + 8 * g + j, d = 32 * db + c;
-          const bool ok = nn < p.Nl && d < D;
-          const int64_t at = (int64_t)min(nn, p.Nl - 1) * p.blo_sn + (int64_t)min(d, D - 1) * p.blo_sd;
-          const T kv = blo[at];
-          kt[kk][db][j] = ok ? kv : from_f32<T>(0.f);
-          if (DEC) {
-            const T gv = glo[(int64_t)min(nn, p.Nl - 1) * p.glo_sn + (int64_t)min(d, D - 1) * p.glo_sd];
-            gt[kk][db][j] = ok ? gv : from_f32<T>(0.f);
-          }
+        for (int h = 0; h < 2; ++h) {
+          const int d0 = 32 * db + 16 * g + 8 * h;  // D is a multiple of 16: d0 < D means d0 + 8 <= D
+          store_frag8(tb + c * TBP + 16 * g + 8 * h, d0 < D ? load_frag(x + (int64_t)nc * sn + d0) : zero_frag<T>());
         }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int pos = 16 * kk + 8 * g + j;
+            const T v = tb[pos * TBP + c];
+            out[kk][db][j] = n0 + pos < p.Nl ? v : from_f32<T>(0.f);
+          }
+        __builtin_amdgcn_wave_barrier();
+      }
+    };
+    // (D = 64 keeps the element loads: the staged rows would add to a
+    // register budget that is already full there)
+    if (D <= 32 && p.blo_sd == 1 && (!DEC || p.glo_sd == 1)) {  // wave-uniform
+      transpose_long(blo, p.blo_sn, kt);
+      if constexpr (DEC) transpose_long(glo, p.glo_sn, gt);
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int nn = n0 + 16 * kk + 8 * g + j, d = 32 * db + c;
+            const bool ok = nn < p.Nl && d < D;
+            const int64_t at = (int64_t)min(nn, p.Nl - 1) * p.blo_sn + (int64_t)min(d, D - 1) * p.blo_sd;
+            const T kv = blo[at];
+            kt[kk][db][j] = ok ? kv : from_f32<T>(0.f);
+            if (DEC) {
+              const T gv = glo[(int64_t)min(nn, p.Nl - 1) * p.glo_sn + (int64_t)min(d, D - 1) * p.glo_sd];
+              gt[kk][db][j] = ok ? gv : from_f32<T>(0.f);
+            }
+          }
+    }
     // decode: c = <dY_n, Y_n> over the head's channels, and the token's
     // log-normaliser over the routes (log2 units) from the forward
     float Ll = 0.f, cl = 0.f;
