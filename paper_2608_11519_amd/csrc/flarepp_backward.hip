@@ -442,9 +442,29 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
     // long-side B operands of S (keys) and dP (values), one lane per position
     F kb[KS], gb[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      kb[ks] = long_frag(blo, p.blo_sn, p.blo_sd, nc, 16 * ks + 8 * g, nok);
-      gb[ks] = long_frag(glo, p.glo_sn, p.glo_sd, nc, 16 * ks + 8 * g, nok);
+    for (int ks = 0; ks < KS; ++ks) kb[ks] = long_frag(blo, p.blo_sn, p.blo_sd, nc, 16 * ks + 8 * g, nok);
+    if (D == 32 && p.glo_sn == 1) {  // wave-uniform (at D = 16 the staging would cost the second wave per SIMD)
+      // d-major values (each head's rows padded to whole 32-position tiles):
+      // the tile's D rows of 32 positions go through the wave's transpose
+      // tile with 16-byte loads (chunk r: row r / 4, positions 8 (r % 4) ..
+      // + 7), then each lane reads its position's column
+#pragma unroll
+      for (int r0 = 0; r0 < D * 4; r0 += 64) {
+        const int r = r0 + lane, d = r >> 2, q = r & 3;
+        store_frag8(tb + d * TBP + 8 * q, load_frag(glo + (int64_t)d * p.glo_sd + n0 + 8 * q));
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const T v = tb[(16 * ks + 8 * g + j) * TBP + c];
+          gb[ks][j] = nok ? v : from_f32<T>(0.f);
+        }
+      __builtin_amdgcn_wave_barrier();
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) gb[ks] = long_frag(glo, p.glo_sn, p.glo_sd, nc, 16 * ks + 8 * g, nok);
     }
     // long-side B operands of the short-side products (k = position, n = d)
     F kt[2][DB], gt[2][DB];
