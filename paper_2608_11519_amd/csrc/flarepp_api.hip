@@ -583,9 +583,13 @@ struct BwdSplit {
 BwdSplit bwd_split(int64_t BH, int64_t Nl, int D, int Mp, bool dec, int elem_bytes) {
   BwdSplit sp{};
   const int NS = Mp / 32;
-  // LDS budget of a window at 4 waves; FLAREPP_BWD_WINDOW_KB (testing and
-  // tuning) overrides the default of two workgroups per CU
-  size_t budget = 80 * 1024;
+  // LDS budget of a window at 4 waves: the CU's LDS split over as many
+  // workgroups as the kernel's registers let run at once (bf16 at D = 16 fits
+  // two waves per SIMD, so two workgroups of 80 KB; the other variants hold
+  // one wave per SIMD, and a smaller window would only re-read the long side
+  // once more per window).  FLAREPP_BWD_WINDOW_KB (testing and tuning)
+  // overrides it.
+  size_t budget = (D == 16 && elem_bytes == 2) ? 80 * 1024 : 160 * 1024;
   if (const char* f = std::getenv("FLAREPP_BWD_WINDOW_KB")) {
     const long kb = std::atol(f);
     if (kb >= 16 && kb <= 160) budget = (size_t)kb * 1024;
