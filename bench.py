@@ -3,8 +3,9 @@
 
 One step = one complete mixer forward (project; query synthesis, encode and
 decode routing calls; merge) over one batch of synthetic inputs already
-resident in HBM.  Default workload: the 2D structured-grid surrogate layer
-(B=4, N=16384, C=128, H=8, D=16, M=128, bf16 storage, fp32 accumulation).
+resident in HBM.  Default workload: the large 3D-mesh layer, the largest
+configuration that fits one GPU (B=1, N=2^20, C=128, H=8, D=16, M=512, bf16
+storage, fp32 accumulation).
 
 Prints one JSON line with tokens/s, the per-stage device times measured with
 HIP events, the roofline of the dominant kernel and the float64 oracle timed
@@ -41,7 +42,7 @@ def parse_args(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="grid2d")
+    ap.add_argument("--workload", default="mesh3d")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-graph", action="store_true", help="launch every step eagerly")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -216,9 +217,24 @@ def pmc_summary(fetch_dir, write_dir, workload, copy_mib, command):
     print(json.dumps(out, indent=1))
 
 
+def cpu_sample_tokens(N, call_seconds, min_seconds, start=4096):
+    """Token count of the oracle's bounded sample: doubles from `start` while
+    a call at the current count took under a quarter of min_seconds (given
+    the time call_seconds(n) of one call over n tokens), up to N."""
+    n = min(start, N)
+    while n < N and call_seconds(n) < min_seconds / 4:
+        n = min(2 * n, N)
+    return n
+
+
 def cpu_baseline(w, d, min_seconds):
-    """Time the float64 oracle on the host (the full batch, repeated until
-    min_seconds have passed)."""
+    """Time the float64 oracle on the host on a bounded sample of the
+    workload: the mixer over the first n tokens of every batch entry (the
+    same C, H, M, weights and seeds), with n the whole sequence when one call
+    over it fits in a quarter of min_seconds, and calls repeated until
+    min_seconds have passed.  The oracle's work per token is the same at any
+    n (every token enters each routing call and projection once), so tokens/s
+    over the sample is the oracle's rate on the workload."""
     from oracle import flarepp_oracle as orc
 
     try:
@@ -226,17 +242,29 @@ def cpu_baseline(w, d, min_seconds):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover - optional dependency
         threads = os.cpu_count() or 1
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        orc.mixer_forward(d["X"], d["Wk"], d["Wv"], d["Wkt"], d["Wvt"], d["Wo"], d["seeds"], w.H)
+
+    def call(n):
+        X = d["X"][:, :n]
+        t0 = time.perf_counter()
+        orc.mixer_forward(X, d["Wk"], d["Wv"], d["Wkt"], d["Wvt"], d["Wo"], d["seeds"], w.H)
+        return time.perf_counter() - t0
+
+    n = cpu_sample_tokens(w.N, call, min_seconds)
+    reps, el = 0, 0.0
+    while el < min_seconds:
+        el += call(n)
         reps += 1
-        el = time.perf_counter() - t0
-        if el >= min_seconds:
-            break
-    return {"value": round(w.B * w.N * reps / el, 1), "unit": "tokens/s", "cores": threads,
+    what = "full batch" if n == w.N else f"first {n} of the {w.N} tokens of every batch entry"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "unknown")
+    except OSError:
+        model = "unknown"
+    return {"value": round(w.B * n * reps / el, 1), "unit": "tokens/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"full {w.name} batch (B={w.B}, N={w.N}) x {reps}, float64 NumPy, "
-                      f"{el:.1f} s on {len(os.sched_getaffinity(0))} host cores"}
+            "sample": f"{w.name} (B={w.B}, N={w.N}, C={w.C}, H={w.H}, M={w.M}): {what} x {reps} calls, "
+                      f"float64 NumPy, {el:.1f} s on {len(os.sched_getaffinity(0))} host cores ({model}), "
+                      f"{threads} BLAS threads"}
 
 
 def _time_steps(args, step, use_graph):

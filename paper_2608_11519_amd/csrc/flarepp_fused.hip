@@ -709,11 +709,15 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   }
 
   // ---- partials ----
+  // A chunk that starts at or past the last token holds no key: its partial
+  // is (-inf, 0, 0) (App. A.3), whatever shift the loops above left in m.
+  const bool empty_chunk = k1 <= k0;
   constexpr int NQ4 = ONES_ROW ? 2 : 4;
 #pragma unroll
   for (int i = 0; i < NQW; ++i) {
     const int s = slot0 + i;
     if (s >= nslots) continue;
+    if (empty_chunk) m[i] = -INFINITY;
     const int h = hg * HPG + hh, qb = s % p.QB;
     const float l = softmax_denominator<RB, ONES_ROW>(acc[i], ls[i], lane);
     const int64_t pidx = (((int64_t)b * p.H + h) * p.nchunks + r) * p.Mp + qb * 32 + c;

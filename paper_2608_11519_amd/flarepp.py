@@ -8,6 +8,7 @@ stream.  If the library is missing this module raises; there is no fallback.
 from __future__ import annotations
 
 import ctypes
+import operator
 import os
 from typing import Optional, Tuple
 
@@ -160,6 +161,69 @@ def _ptr(t: Optional[torch.Tensor]):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _same(t: torch.Tensor, name: str, shape, dtype: torch.dtype, device: torch.device) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device} (the device of X)")
+
+
+def _validate(X: torch.Tensor, H: int, *, mats=(), routes=None, tokens=(), vecs=(), ws=None,
+              f32_tokens=(), f32_mats=(), f32_routes=()):
+    """Check every tensor argument of a mixer-level entry point against X
+    before anything reaches the library (whose kernels trust the sizes they
+    are given): X is [B, N, C] in float32 or bfloat16; every other tensor is
+    on X's device, in X's dtype unless it is one of the float32 outputs, with
+    the shape its role implies: C x C weights, [H, M, C/H] seeds or queries,
+    [B, N, C] token tensors (outputs, output gradients), [C] vectors; the
+    workspace is uint8.  Raises TypeError or ValueError; returns
+    (B, N, C, M, D)."""
+    if not isinstance(X, torch.Tensor):
+        raise TypeError(f"X must be a torch.Tensor, got {type(X).__name__}")
+    _dtype_code(X)
+    if X.dim() != 3:
+        raise ValueError(f"X must be [B, N, C], got shape {tuple(X.shape)}")
+    B, N, C = X.shape
+    try:
+        H = operator.index(H)
+    except TypeError:
+        raise TypeError(f"H must be an integer, got {type(H).__name__}") from None
+    if isinstance(H, bool) or H < 1 or C % H:
+        raise ValueError(f"H={H!r} must be a positive integer dividing C={C}")
+    D = C // H
+    dev, dt = X.device, X.dtype
+    M = None
+    if routes is not None:
+        name, t = routes
+        if not isinstance(t, torch.Tensor) or t.dim() != 3:
+            raise ValueError(f"{name} must be a [H, M, D] tensor")
+        M = t.shape[1]
+        _same(t, name, (H, M, D), dt, dev)
+    for name, t in mats:
+        _same(t, name, (C, C), dt, dev)
+    for name, t in tokens:
+        if t is not None:
+            _same(t, name, (B, N, C), dt, dev)
+    for name, t in vecs:
+        _same(t, name, (C,), dt, dev)
+    for name, t in f32_tokens:
+        _same(t, name, (B, N, C), torch.float32, dev)
+    for name, t in f32_mats:
+        _same(t, name, (C, C), torch.float32, dev)
+    for name, t in f32_routes:
+        _same(t, name, (H, M, D), torch.float32, dev)
+    if ws is not None:
+        if not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8:
+            raise TypeError("ws must be a uint8 torch.Tensor")
+        if ws.device != dev:
+            raise ValueError(f"ws is on {ws.device}, expected {dev} (the device of X)")
+    return B, N, C, M, D
+
+
 def _stream(device: torch.device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
@@ -201,8 +265,8 @@ def flarepp_project(X: torch.Tensor, Wk=None, Wv=None, Wkt=None, Wvt=None, *, H:
                     ws: Optional[torch.Tensor] = None) -> Tuple[Optional[torch.Tensor], ...]:
     """K, V, K~, V~ = X W (heads split, [B, H, N, D]) for each weight given."""
     lib = load()
-    B, N, C = X.shape
-    D = C // H
+    B, N, C, _, D = _validate(X, H, mats=[(n, W) for n, W in (("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt))
+                                          if W is not None], ws=ws)
     dt = _dtype_code(X)
     outs = [None if W is None else torch.empty((B, H, N, D), dtype=X.dtype, device=X.device)
             for W in (Wk, Wv, Wkt, Wvt)]
@@ -224,20 +288,28 @@ def flarepp_route(kind: int, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, 
     out [B, N, H*D] in the tokens' dtype.
     """
     lib = load()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not isinstance(t, torch.Tensor) or t.dim() != 4:
+            raise ValueError(f"{name} must be a 4-D tensor")
+    tok, rt = (k, q) if kind == ENCODE else (q, k)
+    B, H, N, D = tok.shape
+    M = rt.shape[2]
     if kind == ENCODE:
-        B, H, N, D = k.shape
-        M = q.shape[-2]
+        _same(v, "v", tok.shape, tok.dtype, tok.device)
+        _same(q, "q", ((1 if shared_routes else B), H, M, D), torch.float32, tok.device)
+    elif kind == DECODE:
+        _same(k, "k", ((1 if shared_routes else B), H, M, D), torch.float32, tok.device)
+        _same(v, "v", k.shape, torch.float32, tok.device)
+    else:
+        raise ValueError(f"kind={kind!r} is neither ENCODE nor DECODE")
+    if ws is not None and (ws.dtype != torch.uint8 or ws.device != tok.device):
+        raise TypeError("ws must be a uint8 tensor on the tokens' device")
+    if kind == ENCODE:
         dt = _dtype_code(k)
-        if q.dtype != torch.float32:
-            raise TypeError("route-side tensors are float32")
         out = torch.empty((B, H, M, D), dtype=torch.float32, device=k.device)
         lse = torch.empty((B, H, M), dtype=torch.float32, device=k.device) if want_lse else None
     else:
-        B, H, N, D = q.shape
-        M = k.shape[-2]
         dt = _dtype_code(q)
-        if k.dtype != torch.float32 or v.dtype != torch.float32:
-            raise TypeError("route-side tensors are float32")
         out = torch.empty((B, N, H * D), dtype=q.dtype, device=q.device)
         lse = None
     stride = 0 if shared_routes else H * M * D
@@ -254,8 +326,8 @@ def flarepp_mixer_forward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int,
                           ws: Optional[torch.Tensor] = None) -> torch.Tensor:
     """The FLARE++ mixer forward: O [B, N, C] in X's dtype."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("out", out)], ws=ws)
     dt = _dtype_code(X)
     O = out if out is not None else torch.empty_like(X)
     w = _workspace(flarepp_mixer_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
@@ -270,9 +342,7 @@ def flarepp_mixer_forward_debug(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int,
                                 ws: Optional[torch.Tensor] = None):
     """Mixer forward that also returns the stage results: (O, Q, Z, Y)."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
-    D = C // H
+    B, N, C, M, D = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds), ws=ws)
     dt = _dtype_code(X)
     O = torch.empty_like(X)
     Q = torch.empty((B, H, M, D), dtype=torch.float32, device=X.device)
@@ -292,8 +362,8 @@ def flarepp_mixer_forward_profiled(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, ev
     """Mixer forward that records ``events`` (PROFILE_EVENTS torch.cuda.Event
     objects with timing enabled) around its stages on the current stream."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("out", out)], ws=ws)
     dt = _dtype_code(X)
     if len(events) != PROFILE_EVENTS:
         raise ValueError(f"need {PROFILE_EVENTS} events")
@@ -318,8 +388,8 @@ def flarepp_mixer_stage(stage: int, X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, o
     ``ws`` and ``out`` must be those of a complete mixer forward with the same
     arguments."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("out", out)], ws=ws)
     dt = _dtype_code(X)
     rc = lib.flarepp_mixer_stage(stage, dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt),
                                  _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(out), _ptr(ws), ws.numel(),
@@ -337,8 +407,8 @@ def flarepp_flare_forward(X, Wk, Wv, Wo, queries, *, H: int,
     """The fixed-query FLARE mixer forward: O [B, N, C] in X's dtype;
     ``queries`` [H, M, D] are the learned routing queries."""
     lib = load()
-    B, N, C = X.shape
-    M = queries.shape[1]
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wo", Wo)], routes=("queries", queries),
+                              tokens=[("out", out)], ws=ws)
     dt = _dtype_code(X)
     O = out if out is not None else torch.empty_like(X)
     w = _workspace(flarepp_flare_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
@@ -352,9 +422,7 @@ def flarepp_flare_forward_debug(X, Wk, Wv, Wo, queries, *, H: int,
                                 ws: Optional[torch.Tensor] = None):
     """Fixed-query FLARE forward that also returns the stage results: (O, Z, Y)."""
     lib = load()
-    B, N, C = X.shape
-    M = queries.shape[1]
-    D = C // H
+    B, N, C, M, D = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wo", Wo)], routes=("queries", queries), ws=ws)
     dt = _dtype_code(X)
     O = torch.empty_like(X)
     Z = torch.empty((B, H, M, D), dtype=torch.float32, device=X.device)
@@ -373,8 +441,8 @@ def flarepp_mixer_forward_shared(X, Wk, Wv, Wo, seeds, *, H: int,
     """FLARE++ with the query-synthesis keys and values tied to K and V
     (K~ = K, V~ = V): O [B, N, C] in X's dtype."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("out", out)], ws=ws)
     dt = _dtype_code(X)
     O = out if out is not None else torch.empty_like(X)
     w = _workspace(flarepp_mixer_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
@@ -390,9 +458,12 @@ def flarepp_mixer_backward_workspace_bytes(dtype: int, B: int, N: int, C: int, H
 
 def _backward(debug, X, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, H, ws, out=None, saved=False):
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
-    D = C // H
+    B, N, C, M, D = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("dO", dO)], ws=ws,
+                              f32_tokens=[("out['dX']", out["dX"])] if out else (),
+                              f32_mats=[(f"out[{k!r}]", out[k]) for k in ("dWk", "dWv", "dWkt", "dWvt", "dWo")]
+                              if out else (),
+                              f32_routes=[("out['dseeds']", out["dseeds"])] if out else ())
     dt = _dtype_code(X)
     f32 = dict(dtype=torch.float32, device=X.device)
     if out is not None:
@@ -438,8 +509,8 @@ def flarepp_mixer_forward_train(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int, ws: t
     flarepp_mixer_backward_workspace_bytes bytes) what
     flarepp_mixer_backward_from_saved reads: O [B, N, C] in X's dtype."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("out", out)], ws=ws)
     dt = _dtype_code(X)
     need = flarepp_mixer_backward_workspace_bytes(dt, B, N, C, H, M)
     if ws.numel() * ws.element_size() < need:
@@ -472,9 +543,11 @@ def flarepp_mixer_backward_shared(X, Wk, Wv, Wo, seeds, dO, *, H: int,
     a dict of fp32 tensors dX [B, N, C], dWk, dWv, dWo [C, C] (the tied
     weights' gradients summed over both uses) and dseeds [H, M, D]."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
-    D = C // H
+    B, N, C, M, D = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("dO", dO)], ws=ws,
+                              f32_tokens=[("out['dX']", out["dX"])] if out else (),
+                              f32_mats=[(f"out[{k!r}]", out[k]) for k in ("dWk", "dWv", "dWo")] if out else (),
+                              f32_routes=[("out['dseeds']", out["dseeds"])] if out else ())
     dt = _dtype_code(X)
     f32 = dict(dtype=torch.float32, device=X.device)
     if out is not None:
@@ -501,8 +574,8 @@ def flarepp_block_forward(X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int
     """The pre-norm residual block X + mixer(LayerNorm(X)): O [B, N, C] in
     X's dtype; gamma, beta [C] in X's dtype."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("out", out)], vecs=[("gamma", gamma), ("beta", beta)], ws=ws)
     dt = _dtype_code(X)
     O = out if out is not None else torch.empty_like(X)
     w = _workspace(flarepp_block_workspace_bytes(dt, B, N, C, H, M), X.device, ws)
@@ -523,9 +596,8 @@ def flarepp_block_backward(X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H
     tensors dX [B, N, C], dgamma, dbeta [C], dWk, dWv, dWkt, dWvt, dWo [C, C]
     and dseeds [H, M, D]."""
     lib = load()
-    B, N, C = X.shape
-    M = seeds.shape[1]
-    D = C // H
+    B, N, C, M, D = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)], routes=("seeds", seeds),
+                              tokens=[("dO", dO)], vecs=[("gamma", gamma), ("beta", beta)], ws=ws)
     dt = _dtype_code(X)
     f32 = dict(dtype=torch.float32, device=X.device)
     g = {"dX": torch.empty((B, N, C), **f32), "dgamma": torch.empty(C, **f32), "dbeta": torch.empty(C, **f32)}

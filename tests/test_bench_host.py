@@ -44,3 +44,17 @@ def test_decode_algorithmic_bytes_and_flops():
 def test_backward_flops_formula():
     w = inp.workload("grid2d")
     assert bench.backward_flops(w) == (20.0 * w.C ** 2 + 30.0 * w.M * w.C) * w.B * w.N
+
+
+def test_default_workload_is_the_largest_single_gpu_configuration():
+    args = bench.parse_args([])
+    w = inp.workload(args.workload)
+    assert w.name == "mesh3d" and w.B * w.N == max(v.B * v.N for v in inp.WORKLOADS.values())
+
+
+def test_cpu_sample_grows_until_a_call_takes_a_quarter_of_the_budget():
+    # a call over n tokens takes n / 1e4 seconds: with 12 s of budget the
+    # sample doubles from 4096 while a call is under 3 s
+    assert bench.cpu_sample_tokens(1 << 20, lambda n: n / 1e4, 12.0) == 32768
+    assert bench.cpu_sample_tokens(1000, lambda n: n / 1e4, 12.0) == 1000
+    assert bench.cpu_sample_tokens(20000, lambda n: n / 1e4, 1e9) == 20000

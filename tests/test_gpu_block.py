@@ -47,10 +47,11 @@ def _check_block(w, d, label, seed=40, eps=1e-5):
     tol = TOL[w.dtype]
     assert rel_err(np.asarray(d["X"], dtype=np.float64), ref) > 5 * tol, "the mixer term is too small to test"
     assert_close("O", got, ref, tol, label)
-    if w.dtype == "f32":
-        # fp32: the mixer's share on its own, O - X against mixer(LN(X))
-        assert_close("O-X", got - np.asarray(d["X"], dtype=np.float64), ref - np.asarray(d["X"], dtype=np.float64),
-                     tol, label)
+    # the mixer's share on its own, O - X against mixer(LN(X)), at the same
+    # gate relative to max |mixer(LN(X))| (with bf16 the difference also
+    # carries the rounding of O to its storage type, ~0.2% of max |O|)
+    assert_close("O-X", got - np.asarray(d["X"], dtype=np.float64), ref - np.asarray(d["X"], dtype=np.float64),
+                 tol, label)
     return got
 
 

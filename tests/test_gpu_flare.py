@@ -87,6 +87,48 @@ def test_flare_head_widths(D):
     _check_flare(w, inp.make_inputs(w, 5, seed_scale=4.0), f"D{D}")
 
 
+# C = 256, H = 8 (D = 32), M = 256, Fourier-feature tokens and a token tail:
+# the irregular-mesh workload's kernels away from near-uniform softmaxes
+_C256 = inp.Workload("flare-c256", 1, 5000, 256, 8, 256, "bf16", "fourier")
+
+
+@pytest.mark.parametrize("variant", ["sharp", "hot", "nofast"])
+def test_flare_c256_stress_bf16(monkeypatch, variant):
+    w = _C256
+    assert fp.flarepp_mixer_path(fp.BF16, w.B, w.N, w.C, w.H, w.M) == fp.PATH_FUSED
+    if variant == "sharp":
+        d = inp.make_inputs(w, 41, seed_scale=8.0)
+    elif variant == "hot":
+        d = inp.make_inputs(w, 42, x_scale=3.0, seed_scale=2.0)
+    else:
+        monkeypatch.setenv("FLAREPP_NO_FAST_PATH", "1")
+        d = inp.make_inputs(w, 43, seed_scale=4.0)
+    _check_flare(w, d, f"c256-{variant}")
+
+
+def test_flare_empty_chunks_with_very_negative_row_maxima(monkeypatch):
+    """Tokens with a common offset, and every fourth query pointing away from
+    the offset's key: those routes' scores are all far below zero (row maxima
+    between about -100 and -180 in log2 units), so their encode runs on the
+    online maximum.  With 40 forced chunks of 128 tokens over N = 1024 the
+    chunks past the last token start on super-tile boundaries; their partials
+    must be (-inf, 0, 0) (App. A.3), or the merge would scale those routes'
+    sums by 2^(max - 0), which underflows to zero."""
+    monkeypatch.setenv("FLAREPP_FORCE_CHUNKS", "40")
+    w = inp.Workload("flare-offset", 1, 1024, 64, 4, 64, "f32", "normal")
+    d = inp.make_inputs(w, 21, seed_scale=2.0)
+    off = np.float32(8.0)
+    d["X"] = (d["X"] + off).astype(np.float32)
+    # the key of the common offset, per head, and queries of length 16 against it
+    k0 = np.full(w.C, float(off)) @ d["Wk"].astype(np.float64)
+    q = d["seeds"].astype(np.float64).copy()
+    for h in range(w.H):
+        kh = k0[h * w.D:(h + 1) * w.D]
+        q[h, ::4] = -16.0 * kh / np.linalg.norm(kh)
+    d["seeds"] = q.astype(np.float32)
+    _check_flare(w, d, "offset-R40")
+
+
 def test_flare_online_max_path(monkeypatch):
     monkeypatch.setenv("FLAREPP_NO_FAST_PATH", "1")
     w = inp.Workload("flare-online", 2, 900, 64, 4, 40, "f32", "normal")
