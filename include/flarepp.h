@@ -132,6 +132,34 @@ FLAREPP_API int flarepp_mixer_forward(int dtype, int64_t B, int64_t N, int64_t C
                           const void* seeds, void* O, void* ws, size_t ws_bytes,
                           void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Allocation-free mixer forward, for callers that cannot allocate device
+ * memory (work recorded under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It computes exactly what
+ * flarepp_mixer_forward computes (bit for bit, same kernels) without a
+ * workspace argument: its workspace is a static scratch array of
+ * flarepp_mixer_noalloc_max_bytes() bytes (32 MiB) in the library's device
+ * code, so every device the library runs on holds its own copy until the
+ * process ends.  The caller passes inputs and outputs as for
+ * flarepp_mixer_forward; nothing is allocated or freed.
+ *
+ * The work runs on the current device, and `stream` (NULL = the null
+ * stream) must belong to it (FLAREPP_ERR_INVALID_ARG otherwise).  Every call
+ * on a device shares that device's array and leaves its contents behind:
+ * calls that overlap in time on one device (on two streams, or from two
+ * threads) race on it and must not be issued.  Only shapes that take the
+ * fused kernels are covered (FLAREPP_ERR_UNSUPPORTED otherwise, see
+ * flarepp_mixer_path), and only while flarepp_mixer_workspace_bytes(...) of
+ * the shape is at most the array's size (FLAREPP_ERR_WORKSPACE otherwise);
+ * both are checked before anything is enqueued.  Other errors as
+ * flarepp_mixer_forward.
+ * ------------------------------------------------------------------------- */
+FLAREPP_API size_t flarepp_mixer_noalloc_max_bytes(void);
+FLAREPP_API int flarepp_mixer_forward_noalloc(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
+                                              int64_t M, const void* X, const void* Wk, const void* Wv,
+                                              const void* Wkt, const void* Wvt, const void* Wo,
+                                              const void* seeds, void* O, void* stream);
+
 /* Which kernel sequence flarepp_mixer_forward runs for this shape:
  * FLAREPP_PATH_FUSED (projections inside the routing kernels, decode fused
  * with the merge; used when C is 64, 128 or 256 and the per-wave register

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <mutex>
 #include <string>
 #include <type_traits>
 #include <algorithm>
@@ -989,6 +990,42 @@ int forward_train_entry(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, i
                                kBwdForward, O);
 }
 
+// ---- allocation-free variant of the mixer forward ----------------------------
+// The workspace of flarepp_mixer_forward_noalloc is this file-scope device
+// array: every device the library runs on holds its own copy until the
+// process ends.  In host code the name is only a host-side stand-in; kernels
+// get the device address that hipGetSymbolAddress returns for the current
+// device, looked up once per device and kept in g_scratch.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxScratchDevices];
+
+// The scratch array's address on device `dev` (the current device).
+int scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(FLAREPP_ERR_UNSUPPORTED, "device %d is beyond the %d the library tracks", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(FLAREPP_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    // the runtime resolved the device copy: its size is the array's, and its
+    // address is not the host-side stand-in
+    size_t n = 0;
+    e = hipGetSymbolSize(&n, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || n != kScratchBytes || p == static_cast<void*>(scratch))
+      return fail(FLAREPP_ERR_HIP, "the scratch array did not resolve on device %d (%s, %zu bytes)", dev,
+                  hipGetErrorString(e), n);
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return FLAREPP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1096,6 +1133,38 @@ int flarepp_mixer_forward(int dtype, int64_t B, int64_t N, int64_t C, int64_t H,
                           size_t ws_bytes, void* stream) {
   return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr,
                      nullptr, ws, ws_bytes, stream, nullptr, 0);
+}
+
+size_t flarepp_mixer_noalloc_max_bytes(void) { return kScratchBytes; }
+
+int flarepp_mixer_forward_noalloc(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
+                                  const void* X, const void* Wk, const void* Wv, const void* Wkt,
+                                  const void* Wvt, const void* Wo, const void* seeds, void* O,
+                                  void* stream) {
+  TRY(check_mixer_shape(dtype, B, N, C, H, M));
+  const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
+  if (!pl.fused)
+    return fail(FLAREPP_ERR_UNSUPPORTED,
+                "the allocation-free mixer runs the fused kernels only; this shape (C=%lld, H=%lld, M=%lld) takes "
+                "the unfused path, whose workspace holds token-sized tensors",
+                (long long)C, (long long)H, (long long)M);
+  const size_t need = mixer_ws(nullptr, dtype, B, N, C, H, M, pl).bytes;
+  if (need > kScratchBytes)
+    return fail(FLAREPP_ERR_WORKSPACE,
+                "this shape needs %zu bytes of workspace, more than the %zu of the allocation-free mixer's scratch array",
+                need, kScratchBytes);
+  int dev = -1;
+  HIPTRY(hipGetDevice(&dev));
+  if (stream) {
+    hipDevice_t sdev = -1;
+    HIPTRY(hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev));
+    if (sdev != dev)
+      return fail(FLAREPP_ERR_INVALID_ARG, "the stream belongs to device %d, the current device is %d", (int)sdev, dev);
+  }
+  void* ws = nullptr;
+  TRY(scratch_address(dev, &ws));
+  return mixer_entry(dtype, B, N, C, H, M, X, Wk, Wv, Wkt, Wvt, Wo, seeds, O, nullptr, nullptr, nullptr, ws,
+                     kScratchBytes, stream, nullptr, 0);
 }
 
 int flarepp_mixer_forward_profiled(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,

@@ -38,6 +38,7 @@ EXPORTS = (
     "flarepp_mixer_forward_shared", "flarepp_block_workspace_bytes", "flarepp_block_forward",
     "flarepp_mixer_backward_shared", "flarepp_mixer_forward_train", "flarepp_mixer_backward_from_saved",
     "flarepp_block_backward_workspace_bytes", "flarepp_block_backward",
+    "flarepp_mixer_noalloc_max_bytes", "flarepp_mixer_forward_noalloc",
 )
 PATH_UNFUSED = 0
 PATH_FUSED = 1
@@ -126,6 +127,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flarepp_block_forward.restype = i32
     lib.flarepp_block_forward.argtypes = ([i32, i64, i64, i64, i64, i64] + [vp] * 3 + [ctypes.c_float]
                                           + [vp] * 7 + [vp, sz, vp])
+    lib.flarepp_mixer_noalloc_max_bytes.restype = sz
+    lib.flarepp_mixer_noalloc_max_bytes.argtypes = []
+    lib.flarepp_mixer_forward_noalloc.restype = i32
+    lib.flarepp_mixer_forward_noalloc.argtypes = [i32, i64, i64, i64, i64, i64] + [vp] * 8 + [vp]
     _lib = lib
     return lib
 
@@ -334,6 +339,27 @@ def flarepp_mixer_forward(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int,
     rc = lib.flarepp_mixer_forward(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt),
                                    _ptr(Wvt), _ptr(Wo), _ptr(seeds), _ptr(O), _ptr(w), w.numel(),
                                    _stream(X.device))
+    _check(rc)
+    return O
+
+
+def flarepp_mixer_noalloc_max_bytes() -> int:
+    return int(load().flarepp_mixer_noalloc_max_bytes())
+
+
+def flarepp_mixer_forward_noalloc(X, Wk, Wv, Wkt, Wvt, Wo, seeds, *, H: int,
+                                  out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The FLARE++ mixer forward on the library's own scratch array (no
+    workspace argument, nothing allocated by the library): O [B, N, C] in
+    X's dtype, bitwise equal to flarepp_mixer_forward.  Calls on one device
+    share the array and must not overlap."""
+    lib = load()
+    B, N, C, M, _ = _validate(X, H, mats=[("Wk", Wk), ("Wv", Wv), ("Wkt", Wkt), ("Wvt", Wvt), ("Wo", Wo)],
+                              routes=("seeds", seeds), tokens=[("out", out)])
+    dt = _dtype_code(X)
+    O = out if out is not None else torch.empty_like(X)
+    rc = lib.flarepp_mixer_forward_noalloc(dt, B, N, C, H, M, _ptr(X), _ptr(Wk), _ptr(Wv), _ptr(Wkt), _ptr(Wvt),
+                                           _ptr(Wo), _ptr(seeds), _ptr(O), _stream(X.device))
     _check(rc)
     return O
 
@@ -618,6 +644,7 @@ def flarepp_block_backward(X, gamma, beta, Wk, Wv, Wkt, Wvt, Wo, seeds, dO, *, H
 project = flarepp_project
 route = flarepp_route
 mixer_forward = flarepp_mixer_forward
+mixer_forward_noalloc = flarepp_mixer_forward_noalloc
 mixer_forward_debug = flarepp_mixer_forward_debug
 flare_forward = flarepp_flare_forward
 flare_forward_debug = flarepp_flare_forward_debug

@@ -326,3 +326,23 @@ def test_block_backward_rejects_invalid_arguments():
         assert call(ptrs=ptrs) == fp.ERR_INVALID_ARG
     n = fp.flarepp_block_backward_workspace_bytes(fp.BF16, 2, 1000, 128, 8, 64)
     assert n > fp.flarepp_mixer_backward_workspace_bytes(fp.BF16, 2, 1000, 128, 8, 64) + 4 * 2 * 1000 * 128
+
+
+def test_noalloc_rejects_shapes_beyond_its_scratch_array_before_any_hip_call():
+    lib = _lib()
+    cap = fp.flarepp_mixer_noalloc_max_bytes()
+    assert cap == 32 << 20
+    p = ctypes.c_void_p(256)  # aligned, never dereferenced: the checks come first
+    ptrs = [p] * 8
+    # a fused shape whose workspace exceeds the array
+    B, N, C, H, M = 64, 4096, 128, 8, 512
+    assert fp.flarepp_mixer_path(fp.BF16, B, N, C, H, M) == fp.PATH_FUSED
+    assert fp.flarepp_mixer_workspace_bytes(fp.BF16, B, N, C, H, M) > cap
+    rc = lib.flarepp_mixer_forward_noalloc(fp.BF16, B, N, C, H, M, *ptrs, None)
+    assert rc == fp.ERR_WORKSPACE and "scratch" in fp.last_error()
+    # a shape on the unfused path (C = 512)
+    assert fp.flarepp_mixer_path(fp.BF16, 1, 100, 512, 8, 32) == fp.PATH_UNFUSED
+    rc = lib.flarepp_mixer_forward_noalloc(fp.BF16, 1, 100, 512, 8, 32, *ptrs, None)
+    assert rc == fp.ERR_UNSUPPORTED
+    # invalid shapes as for the mixer
+    assert lib.flarepp_mixer_forward_noalloc(fp.BF16, 1, 100, 100, 3, 32, *ptrs, None) == fp.ERR_INVALID_ARG
