@@ -130,7 +130,7 @@ int decode_kind_for(int C, int D, int Mp, int elem_bytes) {
   const char* f = std::getenv("FLAREPP_DECODE_KIND");
   if (f) {
     const int want = std::atoi(f);
-    if (want >= 0 && want < k) k = want;
+    if (want >= 0 && want <= flarepp::kDecodePersist && flarepp::decode_kind_fits(want, C, D, Mp, elem_bytes)) k = want;
   }
   return k;
 }
@@ -351,7 +351,8 @@ int mixer_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M,
     dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
     dp.fast_lim = fast_limit(); dp.y = Y_out; dp.o = O; dp.res = res;
     dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);
-    dp.stage_bytes = (int)dec2_stage_bytes((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype));
+    dp.stage_bytes = (int)(dkind == kDecodePersist ? persist_stage_bytes((int)D, (int)Mp, (int)dtype_bytes(dtype))
+                                                   : dec2_stage_bytes((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype)));
     dp.kind = dkind;
     if (RUN(7)) HIPTRY(launch_decode_fused<T>(dp, (int)D, s));  // call 3 + merge
     STAGE(7);

@@ -38,6 +38,7 @@
 //                 (batch, 32 * waves tokens) one workgroup; the route operands
 //                 of each head group and the W_O blocks are staged through LDS
 //                 (direct global -> LDS copies), double buffered.
+#include <algorithm>
 #include <type_traits>
 
 #include "flarepp_device.hpp"
@@ -911,8 +912,7 @@ int decode_stage_elems(int C, int D, int Mp) {
 }
 
 bool decode_fused_fits(int C, int D, int Mp, int elem_bytes) {
-  const size_t se = (size_t)decode_stage_elems(C, D, Mp) * elem_bytes;
-  return decode_kind(C, D, Mp, elem_bytes) != kDecodeStaged || 2 * se + 16 * elem_bytes <= 160 * 1024;
+  return decode_kind_fits(decode_kind(C, D, Mp, elem_bytes), C, D, Mp, elem_bytes);
 }
 
 // Issue the global -> LDS copy of decode stage s into buffer s & 1: for
@@ -1155,9 +1155,35 @@ size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res) {
   return (res ? hg : 2) * dec2_stage_bytes(C, D, Mp, elem_bytes) + 16 * elem_bytes;
 }
 
+// LDS of k_decode_persist: [W_K fragments][W_O fragments][2 head stages]
+// [16 constant elements]; a head stage is [q][z][route-norm bounds].
+size_t persist_stage_bytes(int D, int Mp, int elem_bytes) {
+  return (size_t)2 * Mp * D * elem_bytes + (size_t)Mp;  // + Mp / 4 floats
+}
+size_t persist_lds_bytes(int C, int D, int Mp, int elem_bytes) {
+  return (size_t)2 * C * C * elem_bytes + 2 * persist_stage_bytes(D, Mp, elem_bytes) + 16 * elem_bytes;
+}
+
+bool decode_kind_fits(int kind, int C, int D, int Mp, int elem_bytes) {
+  switch (kind) {
+    case kDecodeGroupsResident: return C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, true) <= 160 * 1024;
+    case kDecodeGroupsStaged: return C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, false) <= 160 * 1024;
+    case kDecodePersist:
+      return elem_bytes == 2 && C <= 128 && (D == 16 || D == 32) && persist_lds_bytes(C, D, Mp, elem_bytes) <= 160 * 1024;
+    case kDecodeStaged: {
+      const size_t se = (size_t)decode_stage_elems(C, D, Mp) * elem_bytes;
+      return 2 * se + 16 * elem_bytes <= 160 * 1024;
+    }
+  }
+  return false;
+}
+
+// Every route stage resident when it fits (k_decode3 / k_decode2), else the
+// persistent decode with per-head stages, else the staged kernels.
 int decode_kind(int C, int D, int Mp, int elem_bytes) {
-  if (C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, true) <= 160 * 1024) return kDecodeGroupsResident;
-  if (C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, false) <= 160 * 1024) return kDecodeGroupsStaged;
+  if (decode_kind_fits(kDecodeGroupsResident, C, D, Mp, elem_bytes)) return kDecodeGroupsResident;
+  if (decode_kind_fits(kDecodePersist, C, D, Mp, elem_bytes)) return kDecodePersist;
+  if (decode_kind_fits(kDecodeGroupsStaged, C, D, Mp, elem_bytes)) return kDecodeGroupsStaged;
   return kDecodeStaged;
 }
 
@@ -1707,6 +1733,214 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 }
 
 // ---------------------------------------------------------------------------
+// Persistent decode (call 3 + merge) for C <= 128 when the route operands of
+// every head do not fit in LDS together.  One workgroup of 8 waves per CU
+// walks token blocks of 256 (t = blockIdx.x, blockIdx.x + gridDim.x, ...).
+// W_K and W_O stay resident in LDS for the whole launch; the route operands
+// of one head at a time ([q][z][route-norm bounds], one batch entry's head)
+// go through two alternating stages, so the stage sequence runs on across
+// token blocks: while head h is routed, the copy of the next head (or of head
+// 0 of the next token block) is in flight.  The X rows of the next token
+// block are loaded once the last head group has been projected.  Per token
+// block: HG key projections, H route loops, one merge O^T = W_O^T Y^T from
+// the resident W_O (no barrier), and one barrier per head.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int KSC>
+__device__ __forceinline__ void persist_stage_issue(const DecFusedParams& p, char* dst, int bh) {
+  constexpr int NT = 64 * dec_waves(16 * KSC), PER16 = 16 / (int)sizeof(T);
+  const int Mp = p.Mp;
+  const int QE = Mp * D, ZE = (int)z_frag_elems_per_head(Mp, D);
+  copy_to_lds((const T*)p.q_op + (int64_t)bh * QE, dst, QE / PER16, NT);
+  copy_to_lds((const T*)p.z_op + (int64_t)bh * ZE, dst + (size_t)QE * sizeof(T), ZE / PER16, NT);
+  copy_to_lds(p.qnorm2 + (int64_t)bh * (Mp / 4), dst + (size_t)(QE + ZE) * sizeof(T), Mp / 16, NT);
+}
+
+template <typename T, int D, int KSC>
+__global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(DecFusedParams p) {
+  using F = typename Frag<T>::type;
+  constexpr int HPG = (D == 16) ? 2 : 1, GB = (D == 64) ? 2 : 1;
+  constexpr int KS = D / 16, RB = (D + 31) / 32, KPG = 2 * GB;
+  constexpr bool ONES_ROW = (D == 16);
+  constexpr int C = KSC * 16, CB = C / 32, HG = CB / GB, H = C / D;
+  constexpr int WELEMS = GB * KSC * kFrag;  // key weight slice of one head group
+  constexpr int NW = dec_waves(C), TOK = 32 * NW;
+  constexpr int ZC = D < 32 ? D : 32;
+  constexpr int GKS = HPG * KS;  // decoded-token fragments per head group
+  static_assert(C <= 128 && GKS == KPG, "");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int Mp = p.Mp, RT = Mp / 32, QE = Mp * D;
+  const int SB = p.stage_bytes;
+  T* wk_l = reinterpret_cast<T*>(smem);
+  T* wo_l = wk_l + C * C;
+  char* stage0 = smem + (size_t)2 * C * C * sizeof(T);
+  T* cst = reinterpret_cast<T*>(stage0 + 2 * SB);  // 8 ones (row 16), 8 zeros
+
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
+  const int nblk = (p.N + TOK - 1) / TOK;
+  const int total = p.B * nblk;
+  int t = blockIdx.x;
+  if (t >= total) return;  // whole workgroup, before any barrier
+
+  // resident weights, the first head's stage and the first block's X
+  copy_to_lds(p.wkf, smem, C * C * (int)sizeof(T) / 16, 64 * NW);
+  copy_to_lds(p.wof, reinterpret_cast<char*>(wo_l), C * C * (int)sizeof(T) / 16, 64 * NW);
+  persist_stage_issue<T, D, KSC>(p, stage0, (t / nblk) * H);
+  if (ONES_ROW && threadIdx.x < 2) store_frag<T>(cst + 8 * threadIdx.x, threadIdx.x == 0 ? fill_frag<T>(1.f) : zero_frag<T>());
+  F xf[KSC];
+  auto load_x = [&](int tb) __attribute__((always_inline)) {
+    const int bb = tb / nblk, row = min((tb % nblk) * TOK + wave * 32 + c, p.N - 1);
+#pragma unroll
+    for (int ks = 0; ks < KSC; ++ks) xf[ks] = load_frag((const T*)p.x + ((int64_t)bb * p.N + row) * C + 16 * ks + 8 * g);
+  };
+  load_x(t);
+  lds_wait_barrier();  // the weights are read before the first head's barrier
+
+  // z operand lanes: value-row lanes walk the head's z fragments; on D = 16
+  // the lanes of rows 16 .. 31 read the constant block
+  const bool konst = ONES_ROW && c >= 16;
+  const uint32_t zstep = konst ? 0u : (uint32_t)(2 * ZC * 8 * sizeof(T));
+  const uint32_t zlane = konst ? (uint32_t)((reinterpret_cast<char*>(cst) - smem) + (c == 16 ? 0 : 8 * sizeof(T)))
+                               : (uint32_t)((stage0 - smem) + (QE + (g * ZC + c) * 8) * sizeof(T));
+  const int rt_full = p.M / 32;
+
+  int seq = 0;  // stages consumed by this workgroup (buffer seq & 1)
+  for (; t < total; t += gridDim.x) {
+    const int b = t / nblk;
+    const int xrow = (t % nblk) * TOK + wave * 32 + c;
+    const bool xok = xrow < p.N;
+    const int tn = t + gridDim.x;  // the next token block of this workgroup
+    F yf[KSC];                     // decoded tokens, oldest group first (shift register)
+    bool xpending = false;         // the next block's X loads are in flight
+    for (int hg = 0; hg < HG; ++hg) {
+      // key projection of the group's heads from the resident W_K slice
+      f32x16 ka[GB];
+#pragma unroll
+      for (int cb = 0; cb < GB; ++cb) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) ka[cb][e] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KSC; ++ks)
+          mma(ka[cb], load_frag(wk_l + hg * WELEMS + ((cb * KSC + ks) * 64 + lane) * 8), xf[ks]);
+      }
+      F kf[HPG][KS];
+#pragma unroll
+      for (int hh = 0; hh < HPG; ++hh)
+#pragma unroll
+        for (int js = 0; js < KS; ++js) {
+          const int fi = hh * KS + js;
+          kf[hh][js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
+        }
+#pragma unroll
+      for (int u = 0; u + GKS < KSC; ++u) yf[u] = yf[u + GKS];
+#pragma unroll
+      for (int hh = 0; hh < HPG; ++hh) {
+        const int h = hg * HPG + hh;
+        // This head's stage has landed (every wave's share of the copy) and
+        // every wave is done with the previous one, whose buffer takes the
+        // next.  Only the KSC loads of the next block's X rows (issued after
+        // the copy, see below) may stay in flight across the barrier.
+        if (xpending) {
+          asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(KSC) : "memory");
+        } else {
+          asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        }
+        const int buf = seq & 1;
+        ++seq;
+        if (h + 1 < H) persist_stage_issue<T, D, KSC>(p, stage0 + (buf ^ 1) * SB, b * H + h + 1);
+        else if (tn < total) persist_stage_issue<T, D, KSC>(p, stage0 + (buf ^ 1) * SB, (tn / nblk) * H);
+        // X is no longer needed once the last group is projected: the next
+        // token block's rows are loaded behind the first copy issued after it
+        if (hg == HG - 1 && hh == 0 && tn < total) {
+          asm volatile("" ::: "memory");  // the loads stay behind the copy: vmcnt(KSC) covers it
+          load_x(tn);
+          xpending = true;
+        }
+        const char* st = stage0 + buf * SB;
+        // |score| bound: token-key norms x the head's route-query norm bound
+        float qmax = 0.f;
+        {
+          const float* qn = reinterpret_cast<const float*>(st + 2 * (size_t)QE * sizeof(T));
+          for (int i = lane; i < Mp / 4; i += 64) qmax = fmaxf(qmax, qn[i]);
+          qmax = wave_max_nonneg(qmax);
+        }
+        const bool fast = uniform(frag_rows_max_sq<T, KS>(kf[hh]) * qmax <= p.fast_lim);
+        const T* qst = reinterpret_cast<const T*>(st);
+        const uint32_t zb = zlane + (konst ? 0u : (uint32_t)(buf * SB));
+        f32x16 acc[RB];
+        float m = -INFINITY, ls = 0.f;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[rb][e] = 0.f;
+        auto score = [&](int rt, int) __attribute__((always_inline)) {
+          f32x16 sc;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+#pragma unroll
+          for (int js = 0; js < KS; ++js) mma(sc, load_frag(qst + ((rt * KS + js) * 64 + lane) * 8), kf[hh][js]);
+          return sc;
+        };
+        auto routes = [&](auto sf) __attribute__((always_inline)) {
+          constexpr bool SF = decltype(sf)::value;
+          auto finish = [&](int rt, int, const f32x16& sc, auto mask) __attribute__((always_inline)) {
+            constexpr bool MASK = decltype(mask)::value;
+            const int nvalid = MASK ? p.M - rt * 32 : 32;
+            F zv[2][RB];
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+              for (int rb = 0; rb < RB; ++rb)
+                zv[hf][rb] = *reinterpret_cast<const F*>(smem + zb + zstep * ((rt * 2 + hf) * RB + rb));
+            if (SF) tile_shift_free<T, RB, ONES_ROW, MASK>(acc, ls, sc, zv, nvalid, lane);
+            else tile_online<T, RB, ONES_ROW, MASK>(acc, m, ls, sc, zv, nvalid, lane);
+          };
+          pipelined_routes2<1>(RT, rt_full, score, finish);
+        };
+        if (fast) routes(std::true_type{});
+        else routes(std::false_type{});
+        const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc, ls, lane));
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf)
+            if (rb * 32 + 16 * hf < D) yf[KSC - GKS + hh * KS + 2 * rb + hf] = cvt8<T>(acc[rb], 8 * hf, inv);
+        if (p.y && xok) {
+          T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + h * D;
+          constexpr int NQ4 = ONES_ROW ? 2 : 4;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < NQ4; ++q)
+              store4(yp + rb * 32 + 8 * q + 4 * g, acc[rb][4 * q] * inv, acc[rb][4 * q + 1] * inv,
+                     acc[rb][4 * q + 2] * inv, acc[rb][4 * q + 3] * inv);
+        }
+      }
+    }
+    // merge: output block cb of O^T = sum over the groups of W_O^T rows x Y^T
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      f32x16 oc;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) oc[e] = 0.f;
+#pragma unroll
+      for (int u = 0; u < HG; ++u)
+#pragma unroll
+        for (int j = 0; j < KPG; ++j)
+          mma(oc, load_frag(wo_l + (((u * CB + cb) * KPG + j) * 64 + lane) * 8), yf[u * KPG + j]);
+      if (xok) {
+        const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cb;
+        T* op = (T*)p.o + oo;
+        const T* rp = p.res ? (const T*)p.res + oo : nullptr;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, oc[4 * q], oc[4 * q + 1], oc[4 * q + 2],
+                     oc[4 * q + 3]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 template <typename T, int D, int KSC, int NQW, int W>
@@ -1782,6 +2016,23 @@ static hipError_t dec_launch(const DecFusedParams& p, hipStream_t s) {
   } else {
     constexpr int NW = dec_waves(16 * KSC);
     const unsigned grid = (unsigned)((int64_t)p.B * ((p.N + 32 * NW - 1) / (32 * NW)));
+    if constexpr (sizeof(T) == 2 && (D == 16 || D == 32) && KSC <= 8) {
+      if (p.kind == kDecodePersist) {  // one persistent workgroup per CU
+        const size_t lds = persist_lds_bytes(16 * KSC, D, p.Mp, sizeof(T));
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_persist<T, D, KSC>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        int dev = 0, ncu = 0;
+        e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
+        e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        const unsigned pgrid = (unsigned)std::min<int64_t>((int64_t)grid, std::max(ncu, 1));
+        k_decode_persist<T, D, KSC><<<pgrid, 64 * NW, lds, s>>>(p);
+        return hipGetLastError();
+      }
+    }
+    if (p.kind == kDecodePersist) return hipErrorInvalidValue;
     if constexpr (16 * KSC <= 128) {  // per-group stages (k_decode2)
       if constexpr (sizeof(T) == 2 && (D == 16 || (D == 32 && KSC <= 4))) {
         const int rt = p.Mp / 32;

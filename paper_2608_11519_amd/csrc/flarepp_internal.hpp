@@ -185,8 +185,13 @@ bool decode_fused_fits(int C, int D, int Mp, int elem_bytes);
 // Decode kernels: k_decode_fused (per-group stages of keys and routes, W_O
 // staged by output block at the end), k_decode2 with per-group stages that
 // also carry the group's W_O rows (two alternating buffers, or all resident).
-enum DecodeKind { kDecodeStaged = 0, kDecodeGroupsStaged = 1, kDecodeGroupsResident = 2 };
+// k_decode_persist: persistent workgroups with W_K and W_O resident in LDS and
+// the route operands of one head at a time in two alternating stages.
+enum DecodeKind { kDecodeStaged = 0, kDecodeGroupsStaged = 1, kDecodeGroupsResident = 2, kDecodePersist = 3 };
 int decode_kind(int C, int D, int Mp, int elem_bytes);
+bool decode_kind_fits(int kind, int C, int D, int Mp, int elem_bytes);
+size_t persist_stage_bytes(int D, int Mp, int elem_bytes);
+size_t persist_lds_bytes(int C, int D, int Mp, int elem_bytes);
 size_t dec2_stage_bytes(int C, int D, int Mp, int elem_bytes);
 size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res);
 

@@ -75,7 +75,7 @@ def test_block_unfused_path(monkeypatch, dtype):
     _check_block(w, inp.make_inputs(w, 15, seed_scale=4.0), f"unfused-{dtype}")
 
 
-@pytest.mark.parametrize("kind", [0, 1, 2])
+@pytest.mark.parametrize("kind", [0, 1, 2, 3])
 def test_block_every_decode_kernel(monkeypatch, kind):
     monkeypatch.setenv("FLAREPP_DECODE_KIND", str(kind))
     w = inp.Workload("block-deckind", 2, 1500, 128, 8, 64, "bf16", "normal")

@@ -129,6 +129,14 @@ def test_flare_empty_chunks_with_very_negative_row_maxima(monkeypatch):
     _check_flare(w, d, "offset-R40")
 
 
+@pytest.mark.parametrize("M", [96, 512])
+def test_flare_persistent_decode(monkeypatch, M):
+    # the persistent decode on the fixed queries (natural at M = 512)
+    monkeypatch.setenv("FLAREPP_DECODE_KIND", "3")
+    w = inp.Workload("flare-persist", 2, 3000, 128, 8, M, "bf16", "normal")
+    _check_flare(w, inp.make_inputs(w, 44, seed_scale=6.0), f"persist-M{M}")
+
+
 def test_flare_online_max_path(monkeypatch):
     monkeypatch.setenv("FLAREPP_NO_FAST_PATH", "1")
     w = inp.Workload("flare-online", 2, 900, 64, 4, 40, "f32", "normal")

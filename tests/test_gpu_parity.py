@@ -123,7 +123,7 @@ def test_odd_route_block_counts_bf16(M):
     _check_mixer(w, inp.make_inputs(w, 13, seed_scale=4.0), f"oddblocks-M{M}")
 
 
-@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("kind", [0, 1, 3])
 @pytest.mark.parametrize("M", [64, 80])
 def test_every_decode_kernel(monkeypatch, kind, M):
     # the decode kernels with smaller LDS footprints than the one the shape
@@ -196,15 +196,40 @@ def _assert_fused(w):
     assert fp.flarepp_mixer_path(dt, w.B, w.N, w.C, w.H, w.M) == fp.PATH_FUSED
 
 
-@pytest.mark.parametrize("seed_scale", [1.0, 8.0])
-def test_m512_c128_full_comparison(seed_scale):
+@pytest.mark.parametrize("seed_scale,kind", [(1.0, None), (8.0, None), (8.0, 0)])
+def test_m512_c128_full_comparison(monkeypatch, seed_scale, kind):
     """The 2^20-token workload's shape (C=128, H=8, M=512) at N=65536, compared
     element by element on every stage: the same fused encode instance (two
-    query blocks per wave) and the output-block-staged decode as at 2^20
-    tokens, at the workload's seeds and with sharp ones (seeds x8)."""
+    query blocks per wave) and decode as at 2^20 tokens (the persistent one),
+    at the workload's seeds and with sharp ones (seeds x8); and the
+    output-block-staged decode (kind 0) at this shape."""
+    if kind is not None:
+        monkeypatch.setenv("FLAREPP_DECODE_KIND", str(kind))
     w = inp.Workload("m512", 1, 65536, 128, 8, 512, "bf16", "normal")
     _assert_fused(w)
-    _check_mixer(w, inp.make_inputs(w, 30, seed_scale=seed_scale), f"m512-seeds{seed_scale:g}")
+    _check_mixer(w, inp.make_inputs(w, 30, seed_scale=seed_scale), f"m512-seeds{seed_scale:g}-kind{kind}")
+
+
+# The persistent decode (W_K and W_O resident, one head's route operands per
+# stage): natural for C <= 128 when the route operands of all heads do not fit
+# in LDS together (M = 512 at C = 128), forced (FLAREPP_DECODE_KIND=3) on other
+# shapes: D = 32, C = 64, a partial route tile, token tails, the online path,
+# and more token blocks than workgroups, crossing batch entries.
+@pytest.mark.parametrize("B,N,C,H,M,variant", [
+    (2, 1500, 128, 8, 64, "sharp"),
+    (3, 777, 128, 8, 500, "sharp"),
+    (2, 2000, 128, 4, 96, "sharp"),
+    (1, 33, 64, 4, 40, "sharp"),
+    (2, 3000, 128, 8, 160, "nofast"),
+    (2, 150000, 128, 8, 96, "sharp"),
+])
+def test_persistent_decode(monkeypatch, B, N, C, H, M, variant):
+    monkeypatch.setenv("FLAREPP_DECODE_KIND", "3")
+    if variant == "nofast":
+        monkeypatch.setenv("FLAREPP_NO_FAST_PATH", "1")
+    w = inp.Workload("persist", B, N, C, H, M, "bf16", "normal")
+    _assert_fused(w)
+    _check_mixer(w, inp.make_inputs(w, 35, seed_scale=6.0), f"persist-{variant}")
 
 
 # C = 256, H = 8 (D = 32), M = 256: the irregular-mesh workload's kernels, with
