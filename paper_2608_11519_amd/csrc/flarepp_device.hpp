@@ -128,8 +128,27 @@ __device__ __forceinline__ void store4_res(T* p, const T* rp, float a, float b, 
 }
 
 // ---- cross-lane helpers ------------------------------------------------------
+// v_permlane32_swap of x with itself: .lo = x of lanes 0..31 in both halves,
+// .hi = x of lanes 32..63 in both halves (one VALU instruction, no LDS).
+struct HalfPair { float lo, hi; };
+__device__ __forceinline__ HalfPair half_pair(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
 // Value held by lane l ^ 32 (the other half of the wave).
-__device__ __forceinline__ float other_half(float x) { return __shfl_xor(x, 32, 64); }
+__device__ __forceinline__ float other_half(float x) {
+  const HalfPair p = half_pair(x);
+  return (threadIdx.x & 32) ? p.lo : p.hi;
+}
+// x of lane l plus x of lane l ^ 32, and their maximum, in every lane.
+__device__ __forceinline__ float halves_sum(float x) {
+  const HalfPair p = half_pair(x);
+  return p.lo + p.hi;
+}
+__device__ __forceinline__ float halves_max(float x) {
+  const HalfPair p = half_pair(x);
+  return fmaxf(p.lo, p.hi);
+}
 
 // Maximum of a non-negative float over each 32-lane half of the wave, summed
 // over the two halves (an upper bound on max_c (x[c] + x[c+32])).  The result
@@ -221,7 +240,7 @@ __device__ __forceinline__ void tile_online(f32x16 (&acc)[RB], float& m, float& 
   float mx = s[0];
 #pragma unroll
   for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[e]);
-  mx = fmaxf(mx, other_half(mx));
+  mx = halves_max(mx);
   const float mn = fmaxf(m, mx);
   const float alpha = __builtin_amdgcn_exp2f(m - mn);  // m = -inf -> 0
 #pragma unroll
@@ -259,12 +278,8 @@ __device__ __forceinline__ void softmax_pv_tile(f32x16 (&acc)[RB], float& m, flo
 // value product (ONES_ROW), else the two halves' partial sums.
 template <int RB, bool ONES_ROW>
 __device__ __forceinline__ float softmax_denominator(const f32x16 (&acc)[RB], float ls, int lane) {
-  if (ONES_ROW) {
-    const float a8 = acc[0][8];
-    const float o = other_half(a8);
-    return (lane >> 5) == 0 ? a8 : o;
-  }
-  return ls + other_half(ls);
+  if (ONES_ROW) return half_pair(acc[0][8]).lo;  // row 16 lives in the lanes of half 0
+  return halves_sum(ls);
 }
 
 // Upper bound on the squared norm of the rows a fragment set holds (rows are

@@ -1156,9 +1156,9 @@ size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res) {
 }
 
 // LDS of k_decode_persist: [W_K fragments][W_O fragments][2 head stages]
-// [16 constant elements]; a head stage is [q][z][route-norm bounds].
+// [16 constant elements]; a head stage is [q][z].
 size_t persist_stage_bytes(int D, int Mp, int elem_bytes) {
-  return (size_t)2 * Mp * D * elem_bytes + (size_t)Mp;  // + Mp / 4 floats
+  return (size_t)2 * Mp * D * elem_bytes;
 }
 size_t persist_lds_bytes(int C, int D, int Mp, int elem_bytes) {
   return (size_t)2 * C * C * elem_bytes + 2 * persist_stage_bytes(D, Mp, elem_bytes) + 16 * elem_bytes;
@@ -1740,7 +1740,8 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 // of one head at a time ([q][z][route-norm bounds], one batch entry's head)
 // go through two alternating stages, so the stage sequence runs on across
 // token blocks: while head h is routed, the copy of the next head (or of head
-// 0 of the next token block) is in flight.  The X rows of the next token
+// 0 of the next token block) is in flight.  The route-norm bound of every head
+// is reduced once per batch entry, from the combine's per-wave maxima.  The X rows of the next token
 // block are loaded once the last head group has been projected.  Per token
 // block: HG key projections, H route loops, one merge O^T = W_O^T Y^T from
 // the resident W_O (no barrier), and one barrier per head.
@@ -1752,7 +1753,6 @@ __device__ __forceinline__ void persist_stage_issue(const DecFusedParams& p, cha
   const int QE = Mp * D, ZE = (int)z_frag_elems_per_head(Mp, D);
   copy_to_lds((const T*)p.q_op + (int64_t)bh * QE, dst, QE / PER16, NT);
   copy_to_lds((const T*)p.z_op + (int64_t)bh * ZE, dst + (size_t)QE * sizeof(T), ZE / PER16, NT);
-  copy_to_lds(p.qnorm2 + (int64_t)bh * (Mp / 4), dst + (size_t)(QE + ZE) * sizeof(T), Mp / 16, NT);
 }
 
 template <typename T, int D, int KSC>
@@ -1804,8 +1804,20 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
   const int rt_full = p.M / 32;
 
   int seq = 0;  // stages consumed by this workgroup (buffer seq & 1)
+  int bq = -1;  // the batch entry whose route-norm bounds qmax holds
+  float qmax[H];
   for (; t < total; t += gridDim.x) {
     const int b = t / nblk;
+    if (b != bq) {  // max over a head's routes of |scaled q|^2, wave-uniform
+#pragma unroll
+      for (int h = 0; h < H; ++h) {
+        const float* qn = p.qnorm2 + ((int64_t)b * H + h) * (Mp / 4);
+        float v = 0.f;
+        for (int i = lane; i < Mp / 4; i += 64) v = fmaxf(v, qn[i]);
+        qmax[h] = wave_max_nonneg(v);
+      }
+      bq = b;
+    }
     const int xrow = (t % nblk) * TOK + wave * 32 + c;
     const bool xok = xrow < p.N;
     const int tn = t + gridDim.x;  // the next token block of this workgroup
@@ -1857,13 +1869,11 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
         }
         const char* st = stage0 + buf * SB;
         // |score| bound: token-key norms x the head's route-query norm bound
-        float qmax = 0.f;
-        {
-          const float* qn = reinterpret_cast<const float*>(st + 2 * (size_t)QE * sizeof(T));
-          for (int i = lane; i < Mp / 4; i += 64) qmax = fmaxf(qmax, qn[i]);
-          qmax = wave_max_nonneg(qmax);
-        }
-        const bool fast = uniform(frag_rows_max_sq<T, KS>(kf[hh]) * qmax <= p.fast_lim);
+        // (h is wave-uniform: the selection runs on scalar registers)
+        float qh = qmax[0];
+#pragma unroll
+        for (int i = 1; i < H; ++i) qh = (h == i) ? qmax[i] : qh;
+        const bool fast = uniform(frag_rows_max_sq<T, KS>(kf[hh]) * qh <= p.fast_lim);
         const T* qst = reinterpret_cast<const T*>(st);
         const uint32_t zb = zlane + (konst ? 0u : (uint32_t)(buf * SB));
         f32x16 acc[RB];
