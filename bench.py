@@ -32,8 +32,8 @@ METRIC = "FLARE++ mixer fwd tokens/sec (B·N/s) at 1 GPU + % bf16 MFMA peak"
 PEAK_MFMA_BF16_TFLOPS = 2500.0
 PEAK_MFMA_F32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
-# v_exp_f32 issue rate: 256 CUs x 2.4 GHz x 32 per clock per CU (half the
-# 64-lane fp32 vector rate; see the derivation in the design notes)
+# v_exp_f32 issue rate: 256 CUs x 2.4 GHz x 32 lanes per clock per CU, half
+# the fp32 FMA rate (a wave64 v_exp_f32 occupies a 16-lane SIMD for 8 clocks)
 PEAK_EXP_TPS = 256 * 2.4e9 * 32 / 1e12  # Texp/s
 
 
@@ -126,11 +126,12 @@ def roofline(work, ms, dtype):
 
 # Kernels (symbol substrings) that can carry each stage on the fused path, for
 # the counter tables; for C <= 128 the decode is k_decode3 or k_decode2 when
-# the head-group stages fit, otherwise k_decode_fused.
+# the head-group stages fit, else k_decode_persist when one head's route
+# operands fit beside the weights, otherwise k_decode_fused.
 STAGE_KERNELS_FUSED = {"call1_encode": ("k_encode_fused",),
                        "call1_combine": ("k_combine_par",), "call2_encode": ("k_encode_fused",),
                        "call2_combine": ("k_combine_par",),
-                       "call3_decode": ("k_decode3", "k_decode2", "k_decode_fused")}
+                       "call3_decode": ("k_decode3", "k_decode2", "k_decode_persist", "k_decode_fused")}
 
 
 def sources_digest():
