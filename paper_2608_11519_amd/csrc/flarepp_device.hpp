@@ -11,6 +11,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <stdint.h>
 
 namespace flarepp {
@@ -206,7 +207,8 @@ template <typename T, int RB, bool ONES_ROW>
 __device__ __forceinline__ void pv_product(f32x16 (&acc)[RB], float& ls, const f32x16& s,
                                            const typename Frag<T>::type (&vf)[2][RB]) {
   using F = typename Frag<T>::type;
-  if (!ONES_ROW) {
+  constexpr bool BF16 = std::is_same<T, __bf16>::value;
+  if (!ONES_ROW && !BF16) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) ls += s[e];
   }
@@ -215,6 +217,17 @@ __device__ __forceinline__ void pv_product(f32x16 (&acc)[RB], float& ls, const f
   for (int e = 0; e < 8; ++e) {
     p0[e] = from_f32<T>(s[e]);
     p1[e] = from_f32<T>(s[8 + e]);
+  }
+  if constexpr (!ONES_ROW && BF16) {
+    // the denominators sum the numerators the value product uses (the bf16
+    // ones), two per instruction: a dot product of each packed pair with (1, 1)
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 one2 = {(__bf16)1.f, (__bf16)1.f};
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      ls = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p0[e], p0[e + 1]}, one2, ls, false);
+      ls = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p1[e], p1[e + 1]}, one2, ls, false);
+    }
   }
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
