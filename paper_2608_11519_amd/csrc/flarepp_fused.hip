@@ -951,7 +951,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
   constexpr int HPG = (D == 16) ? 2 : 1, GB = (D == 64) ? 2 : 1;
   constexpr int KS = D / 16, RB = (D + 31) / 32;
   constexpr bool ONES_ROW = (D == 16);
-  constexpr int C = KSC * 16, CB = C / 32, HG = CB / GB;
+  constexpr int C = KSC * 16, CB = C / 32, HG = CB / GB, H = C / D;
   constexpr int WELEMS = GB * KSC * kFrag;  // key weight slice of one head group
   constexpr int NW = dec_waves(C), TOK = 32 * NW;
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -978,29 +978,32 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 #pragma unroll
   for (int ks = 0; ks < KSC; ++ks)
     xf[ks] = load_frag((const T*)p.x + ((int64_t)b * p.N + min(xrow, p.N - 1)) * C + 16 * ks + 8 * g);
-  lds_wait_barrier();
-
-  // route-query norm bound of each head of a group (this lane's share of the
-  // max over the combine's per-wave entries), loaded one group ahead
-  auto load_qn2 = [&](int hg, float (&v)[HPG]) __attribute__((always_inline)) {
+  // Route-query norm bound of every head (max over its routes of |scaled
+  // q|^2, from the combine's per-wave entries), loaded once here behind
+  // stage 0 and X.  A load issued inside the group loop is consumed at once,
+  // and with in-order completion that wait would drain the stage copy issued
+  // just before it.  Head h's bound ends up in lane h of qtab.
+  int qtab = 0;
+  {
+    float qv[H];
 #pragma unroll
-    for (int hh = 0; hh < HPG; ++hh) {
-      const float* qp = p.qnorm2 + ((int64_t)b * p.H + hg * HPG + hh) * (Mp / 4);
-      v[hh] = 0.f;
-      for (int i = lane; i < Mp / 4; i += 64) v[hh] = fmaxf(v[hh], qp[i]);
+    for (int h = 0; h < H; ++h) qv[h] = 0.f;
+    for (int i = lane; i < Mp / 4; i += 64) {
+      float t[H];
+#pragma unroll
+      for (int h = 0; h < H; ++h) t[h] = p.qnorm2[((int64_t)b * p.H + h) * (Mp / 4) + i];
+#pragma unroll
+      for (int h = 0; h < H; ++h) qv[h] = fmaxf(qv[h], t[h]);
     }
-  };
-  float qn2_next[HPG];
-  load_qn2(0, qn2_next);
+    lds_wait_barrier();
+#pragma unroll
+    for (int h = 0; h < H; ++h) qtab = lane == h ? __float_as_int(wave_max_nonneg(qv[h])) : qtab;
+  }
 
   F yf[KSC];  // decoded tokens, merge B operands (16 channels per k step)
 #pragma unroll
   for (int hg = 0; hg < HG; ++hg) {
     decode_stage_issue<T, D, KSC>(p, smem, SE, b, hg + 1);
-    float qn2[HPG];
-#pragma unroll
-    for (int hh = 0; hh < HPG; ++hh) qn2[hh] = qn2_next[hh];
-    if (hg + 1 < HG) load_qn2(hg + 1, qn2_next);
     const T* sb = bufs + (hg & 1) * SE;
     f32x16 ka[GB];
 #pragma unroll
@@ -1022,7 +1025,8 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
         const int fi = hh * KS + js;
         kf[hh][js] = cvt8<T>(ka[fi >> 1], 8 * (fi & 1));
       }
-      bnd = fmaxf(bnd, frag_rows_max_sq<T, KS>(kf[hh]) * wave_max_nonneg(qn2[hh]));
+      bnd = fmaxf(bnd, frag_rows_max_sq<T, KS>(kf[hh]) *
+                           __int_as_float(__builtin_amdgcn_readlane(qtab, hg * HPG + hh)));
     }
     const bool fast = uniform(bnd <= p.fast_lim);
     // z operand addresses (bytes into LDS): lanes of value rows walk the
@@ -1120,9 +1124,38 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
   }
 
   // ---- merge: O^T = W_O^T Y^T, one 32-channel output block per stage ----
+  // A block's stores are issued after the next barrier, and its residual is
+  // loaded before its stage's copy: the barrier's wait for the next stage's
+  // copy then covers both instead of draining the copy at each use.
+  using Half = typename Frag<T>::half;
+  auto load_res = [&](int cbo, Half (&r)[4]) __attribute__((always_inline)) {
+    if (p.res && xok) {
+      const T* rp = (const T*)p.res + ((int64_t)b * p.N + xrow) * C + 32 * cbo;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[q] = load_half(rp + 8 * q + 4 * g);
+    }
+  };
+  auto store_o = [&](int cbo, const f32x16& o, const Half (&r)[4]) __attribute__((always_inline)) {
+    if (xok) {
+      T* op = (T*)p.o + ((int64_t)b * p.N + xrow) * C + 32 * cbo;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4] = {o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]};
+        if (p.res) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += to_f32(r[q][e]);
+        }
+        store4(op + 8 * q + 4 * g, v[0], v[1], v[2], v[3]);
+      }
+    }
+  };
+  f32x16 o_prev;
+  Half r_prev[4], r_cur[4];
 #pragma unroll
   for (int cbo = 0; cbo < CB; ++cbo) {
     const int s = HG + cbo;
+    if (cbo > 0) store_o(cbo - 1, o_prev, r_prev);
+    load_res(cbo, r_cur);
     if (cbo + 1 < CB) decode_stage_issue<T, D, KSC>(p, smem, SE, b, s + 1);
     const T* sb = bufs + (s & 1) * SE;
     f32x16 o;
@@ -1130,16 +1163,12 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
     for (int e = 0; e < 16; ++e) o[e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KSC; ++ks) mma(o, load_frag(sb + (ks * 64 + lane) * 8), yf[ks]);
-    if (xok) {
-      const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cbo;
-      T* op = (T*)p.o + oo;
-      const T* rp = p.res ? (const T*)p.res + oo : nullptr;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
-    }
     if (cbo + 1 < CB) lds_wait_barrier();
+    o_prev = o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r_prev[q] = r_cur[q];
   }
+  store_o(CB - 1, o_prev, r_prev);
 }
 
 // ---------------------------------------------------------------------------
