@@ -117,15 +117,31 @@ __device__ __forceinline__ void store4(__bf16* p, float a, float b, float c, flo
   *reinterpret_cast<bf16x4*>(p) = v;
 }
 
-// store4 of a + r, b + r', ... where r.. are the 4 values at rp (the block's
-// residual), or of a, b, c, d when rp is null
+// One 32-channel output block of this lane's row in the 32x32 accumulator
+// layout (channels 8 q + 4 g .. + 3 hold o[4 q .. 4 q + 3]).  The residual
+// is loaded by load_res16 ahead of use, so that a merge issues all its
+// residual loads before it waits for any, and store16 adds it (when has_res)
+// and stores the block.
 template <typename T>
-__device__ __forceinline__ void store4_res(T* p, const T* rp, float a, float b, float c, float d) {
-  if (rp) {
-    const typename Frag<T>::half r = load_half(rp);
-    a += to_f32(r[0]); b += to_f32(r[1]); c += to_f32(r[2]); d += to_f32(r[3]);
+struct Res16 {
+  typename Frag<T>::half r[4];
+};
+template <typename T>
+__device__ __forceinline__ void load_res16(Res16<T>& res, const T* rp, int g) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) res.r[q] = load_half(rp + 8 * q + 4 * g);
+}
+template <typename T>
+__device__ __forceinline__ void store16(T* op, const f32x16& o, const Res16<T>& res, bool has_res, int g) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float v[4] = {o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]};
+    if (has_res) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] += to_f32(res.r[q][e]);
+    }
+    store4(op + 8 * q + 4 * g, v[0], v[1], v[2], v[3]);
   }
-  store4(p, a, b, c, d);
 }
 
 // ---- cross-lane helpers ------------------------------------------------------

@@ -1433,16 +1433,14 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode2(DecFusedPa
   }
 
   if (xok) {
+    const int64_t oo = ((int64_t)b * p.N + xrow) * C;
+    Res16<T> res[CB];
+    if (p.res) {
 #pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
-      const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cb;
-      T* op = (T*)p.o + oo;
-      const T* rp = p.res ? (const T*)p.res + oo : nullptr;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, o[cb][4 * q], o[cb][4 * q + 1],
-                   o[cb][4 * q + 2], o[cb][4 * q + 3]);
+      for (int cb = 0; cb < CB; ++cb) load_res16(res[cb], (const T*)p.res + oo + 32 * cb, g);
     }
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) store16((T*)p.o + oo + 32 * cb, o[cb], res[cb], p.res != nullptr, g);
   }
 }
 
@@ -1746,6 +1744,13 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
     }
   }
   // merge: output block cb of O^T = sum over the groups of W_O^T rows x Y^T
+  // (the residual of every block is loaded before the first MFMA)
+  const int64_t oo = ((int64_t)b * p.N + xrow) * C;
+  Res16<T> res[CB];
+  if (p.res && xok) {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) load_res16(res[cb], (const T*)p.res + oo + 32 * cb, g);
+  }
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     f32x16 oc;
@@ -1757,15 +1762,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
 #pragma unroll
       for (int j = 0; j < KPG; ++j) mma(oc, load_frag(wo + ((cb * KPG + j) * 64 + lane) * 8), yall[u][j]);
     }
-    if (xok) {
-      const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cb;
-      T* op = (T*)p.o + oo;
-      const T* rp = p.res ? (const T*)p.res + oo : nullptr;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, oc[4 * q], oc[4 * q + 1], oc[4 * q + 2],
-                   oc[4 * q + 3]);
-    }
+    if (xok) store16((T*)p.o + oo + 32 * cb, oc, res[cb], p.res != nullptr, g);
   }
 }
 
@@ -1964,6 +1961,13 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
       }
     }
     // merge: output block cb of O^T = sum over the groups of W_O^T rows x Y^T
+    // (the residual of every block is loaded before the first MFMA)
+    const int64_t oo = ((int64_t)b * p.N + xrow) * C;
+    Res16<T> res[CB];
+    if (p.res && xok) {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) load_res16(res[cb], (const T*)p.res + oo + 32 * cb, g);
+    }
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
       f32x16 oc;
@@ -1974,15 +1978,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
 #pragma unroll
         for (int j = 0; j < KPG; ++j)
           mma(oc, load_frag(wo_l + (((u * CB + cb) * KPG + j) * 64 + lane) * 8), yf[u * KPG + j]);
-      if (xok) {
-        const int64_t oo = ((int64_t)b * p.N + xrow) * C + 32 * cb;
-        T* op = (T*)p.o + oo;
-        const T* rp = p.res ? (const T*)p.res + oo : nullptr;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          store4_res(op + 8 * q + 4 * g, rp ? rp + 8 * q + 4 * g : nullptr, oc[4 * q], oc[4 * q + 1], oc[4 * q + 2],
-                     oc[4 * q + 3]);
-      }
+      if (xok) store16((T*)p.o + oo + 32 * cb, oc, res[cb], p.res != nullptr, g);
     }
   }
 }

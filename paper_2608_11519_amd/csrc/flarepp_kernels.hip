@@ -151,6 +151,17 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
   }
   T* out = (T*)p.out[w];
   const int D = p.D;
+  // the residual of every block is loaded before the first store uses it
+  const bool has_res = layout == kPlain && p.res && xok;
+  Res16<T> res[kProjBlocks];
+  if (has_res) {
+#pragma unroll
+    for (int q = 0; q < kProjBlocks; ++q) {
+      const int cb = cg * kProjBlocks + q;
+      if (cb >= CB) break;  // wave-uniform
+      load_res16(res[q], (const T*)p.res + ((int64_t)b * p.N + xrow) * p.C + 32 * cb, g);
+    }
+  }
 #pragma unroll
   for (int q = 0; q < kProjBlocks; ++q) {
     const int cb = cg * kProjBlocks + q;
@@ -161,21 +172,15 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4)
         store4(o + 8 * r4 + 4 * g, acc[q][4 * r4], acc[q][4 * r4 + 1], acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
+    } else if (layout == kPlain && xok) {
+      store16(out + ((int64_t)b * p.N + xrow) * p.C + 32 * cb, acc[q], res[q], has_res, g);
     } else if (xok) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int col = 32 * cb + 8 * r4 + 4 * g;
-        T* o;
-        const T* rp = nullptr;
-        if (layout == kPlain) {
-          const int64_t oo = ((int64_t)b * p.N + xrow) * p.C + col;
-          o = out + oo;
-          if (p.res) rp = (const T*)p.res + oo;
-        } else {
-          const int h = col / D, d = col % D;
-          o = out + (((int64_t)b * p.H + h) * p.N + xrow) * D + d;
-        }
-        store4_res(o, rp, acc[q][4 * r4], acc[q][4 * r4 + 1], acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
+        const int h = col / D, d = col % D;
+        store4(out + (((int64_t)b * p.H + h) * p.N + xrow) * D + d, acc[q][4 * r4], acc[q][4 * r4 + 1],
+               acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
       }
     }
   }
