@@ -116,6 +116,41 @@ def test_backward_many_routes_in_windows(dtype):
     _check(w, inp.make_inputs(w, 12, seed_scale=4.0), "M300")
 
 
+def _golden_backward():
+    """The stored float64-oracle gradients at 2^18 tokens and the script that
+    wrote them (its workload and seeds)."""
+    import importlib.util
+    import os
+    here = os.path.join(os.path.dirname(__file__), "golden")
+    spec = importlib.util.spec_from_file_location("make_backward_expected",
+                                                  os.path.join(here, "make_backward_expected.py"))
+    mk = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mk)
+    return mk, np.load(mk.OUT, allow_pickle=False)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_backward_quarter_million_tokens_against_stored_oracle(dtype):
+    # N = 2^18 tokens, C = 128, H = 8, M = 128: the seed gradient, the five
+    # weight gradients, dZ, dQ and dX at one token of every 512-token block
+    # against float64 oracle values stored by
+    # tests/golden/make_backward_expected.py (the oracle takes a few minutes
+    # here).  Both storage types read the same bf16-rounded inputs.
+    mk, ref = _golden_backward()
+    wb = mk.workload()
+    w = wb.replace(dtype=dtype)
+    print(f"[case] backward stored-oracle {inp.describe(w)}", flush=True)
+    d = inp.make_inputs(wb, mk.INPUT_SEED)
+    dO = inp.make_tensor((wb.B, wb.N, wb.C), mk.DO_SEED, wb.dtype)
+    got = _run(w, d, dO)
+    tol = TOL[dtype]
+    tok = ref["tokens"]
+    assert len(tok) >= w.N // mk.BLOCK
+    for k in ("dseeds", "dWk", "dWv", "dWkt", "dWvt", "dWo", "dZ", "dQ"):
+        assert_close(k, got[k], ref[k], tol, "quartermega")
+    assert_close("dX[tokens]", got["dX"][:, tok], ref["dX"], tol, "quartermega")
+
+
 def test_value_gradients_keep_their_token_part_at_half_a_million_tokens(monkeypatch):
     # N = 2^19, M = 512: the encoders' softmaxes over the tokens are near
     # uniform, so a value gradient P^T dOut is a large common part plus a
