@@ -624,6 +624,7 @@ int gemm_splits(int64_t T, int64_t C, int* kchunk) {
 
 struct BwdWs {
   void *wf[4], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *Y, *q_op, *z_op;
+  void *fwf[2], *fq_op;  // fused encodes: W_K (key order), W_V fragments; Q(X) in q fragment order
   float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2, *L3;
   float *dZf, *dQf, *c1, *c2, *l1, *l2, *pa, *pg, *pq, *gpart;
   void *dY, *dK, *dV, *dKt, *dVt;
@@ -649,6 +650,12 @@ bool bwd_lo_parts(int dtype) {
   return !(f && std::atoi(f) != 0);
 }
 
+// The backward's forward runs calls 1 and 2 on the fused encodes (which
+// project inside the routing kernel) when the fused path covers the shape;
+// K, V, K~, V~ are still materialised for the reverse pass, and call 3 stays
+// on the unfused decode, which writes Y and the per-token log-normaliser.
+bool bwd_fused_encodes(int dtype, const MixerPlan& pl) { return pl.fused && dtype == FLAREPP_BF16; }
+
 BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
   const int64_t D = C / H, Mp = round_up(M, 32), Np = round_up(N, 32), DB = cdiv(D, 32);
   const size_t bs = dtype_bytes(dtype), f4 = sizeof(float);
@@ -665,8 +672,17 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
   w.Y = cv.take(bs * T * C);
   w.q_op = cv.take(bs * BH * Mp * D);
   w.z_op = cv.take(bs * BH * D * Mp);
-  w.part_ml = (float*)cv.take(f4 * e.nchunks * BH * Mp * 2);
-  w.part_acc = (float*)cv.take(f4 * e.nchunks * BH * Mp * D);
+  // the encodes' partials: the unfused route's chunks or the fused encode's
+  const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
+  const bool fused = bwd_fused_encodes(dtype, pl);
+  const int64_t Rp = std::max<int64_t>(e.nchunks, fused ? pl.nchunks : 1);
+  if (fused) {
+    w.fwf[0] = cv.take(bs * C * C);
+    w.fwf[1] = cv.take(bs * C * C);
+    w.fq_op = cv.take(bs * BH * Mp * D);
+  }
+  w.part_ml = (float*)cv.take(f4 * Rp * BH * Mp * 2);
+  w.part_acc = (float*)cv.take(f4 * Rp * BH * Mp * D);
   w.Qf = (float*)cv.take(f4 * BH * M * D);
   w.Zf = (float*)cv.take(f4 * BH * M * D);
   w.L1 = (float*)cv.take(f4 * BH * M);
@@ -751,10 +767,6 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   for (int i = 0; i < 4; ++i) { wp.w[i] = w_in[i]; wp.out[i] = w.wf[i]; }
   wp.nw = 4;
   HIPTRY(launch_weight_frags<T>(wp, s));
-  RoutePrepParams sp{};
-  sp.src = seeds; sp.src_bstride = 0; sp.B = 1; sp.H = (int)H; sp.M = (int)M; sp.Mp = (int)Mp;
-  sp.D = (int)D; sp.qscale = qscale; sp.q_op = w.seeds_op; sp.z_op = nullptr;
-  HIPTRY((launch_route_prep<T, T>(sp, s)));
   ProjParams pp{};
   pp.x = X; pp.B = (int)B; pp.N = (int)N; pp.Np = (int)Np; pp.C = (int)C; pp.H = (int)H; pp.D = (int)D;
   pp.nw = 4;
@@ -763,6 +775,41 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   pp.wf[2] = w.wf[2]; pp.out[2] = w.Kt;   pp.layout[2] = kHeadsTokenMajor;
   pp.wf[3] = w.wf[3]; pp.out[3] = w.Vtdm; pp.layout[3] = kHeadsDMajor;
   HIPTRY(launch_project<T>(pp, s));
+  const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
+  if (bwd_fused_encodes(dtype, pl)) {
+    // calls 1 and 2 on the fused encodes, as in the forward; the combines
+    // also write the route operands of the unfused decode (rows of Q(X)
+    // scaled, Z d-major)
+    PrepFusedParams fp{};
+    fp.C = (int)C;
+    fp.w[0] = Wk; fp.wf[0] = w.fwf[0]; fp.mode[0] = kFragKeyPerm;
+    fp.w[1] = Wv; fp.wf[1] = w.fwf[1]; fp.mode[1] = kFragPlain;
+    fp.nw = 2;
+    fp.seeds = seeds; fp.H = (int)H; fp.M = (int)M; fp.Mp = (int)Mp; fp.D = (int)D; fp.qscale = qscale;
+    EncFusedParams ep{};
+    ep.x = X; ep.wk_raw = Wkt; ep.wv_raw = Wvt; ep.seeds_raw = seeds;
+    ep.q_sb = 0; ep.M = (int)M; ep.qscale = qscale;
+    ep.B = (int)B; ep.N = (int)N; ep.C = (int)C; ep.H = (int)H; ep.Mp = (int)Mp; ep.QB = (int)(Mp / 32);
+    ep.nqw = pl.nqw; ep.qgroups = pl.qgroups; ep.chunk = pl.chunk; ep.nchunks = pl.nchunks;
+    ep.fast_lim = fast_limit(); ep.part_ml = w.part_ml; ep.part_acc = w.part_acc;
+    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));
+    CombineParams cp{};
+    cp.part_ml = w.part_ml; cp.part_acc = w.part_acc; cp.BH = BH; cp.R = pl.nchunks;
+    cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale; cp.frag = 1;
+    cp.out32 = w.Qf; cp.lse = w.L1; cp.q_op = w.fq_op; cp.q_rows = w.q_op;
+    cp.prep = fp; cp.prep_n = prep_fused_items(fp);
+    HIPTRY(launch_combine_par<T>(cp, s));
+    ep.wk_raw = ep.wv_raw = ep.seeds_raw = nullptr;
+    ep.wkf = w.fwf[0]; ep.wvf = w.fwf[1]; ep.q_op = w.fq_op; ep.q_sb = H * Mp * D;
+    HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));
+    cp.out32 = w.Zf; cp.lse = w.L2; cp.q_op = nullptr; cp.q_rows = nullptr; cp.z_rows = w.z_op;
+    cp.prep_n = 0;
+    HIPTRY(launch_combine_par<T>(cp, s));
+  } else {
+  RoutePrepParams sp{};
+  sp.src = seeds; sp.src_bstride = 0; sp.B = 1; sp.H = (int)H; sp.M = (int)M; sp.Mp = (int)Mp;
+  sp.D = (int)D; sp.qscale = qscale; sp.q_op = w.seeds_op; sp.z_op = nullptr;
+  HIPTRY((launch_route_prep<T, T>(sp, s)));
   RouteParams r1 = encode_params(e, B, H, N, Mp, D);
   r1.ka = w.Kt; r1.ka_sb = tokBS; r1.ka_sh = tokHS; r1.ka_rows = (int)N;
   r1.va = w.Vtdm; r1.va_sb = dmBS; r1.va_sh = dmHS; r1.va_ld = (int)Np;
@@ -781,6 +828,7 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   CombineParams c2 = c1;
   c2.out32 = w.Zf; c2.lse = w.L2; c2.q_op = nullptr; c2.z_op = w.z_op;
   HIPTRY(launch_combine_par<T>(c2, s));
+  }
   RouteParams r3 = decode_params(B, H, N, M, D);
   r3.ka = w.q_op; r3.ka_sb = rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
   r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;

@@ -839,6 +839,8 @@ __global__ __launch_bounds__(256) void k_combine_par(CombineParams p) {
       if (k == d) v = a[k];
     const float out = v * inv;
     if (valid && p.out32) p.out32[(bh * p.M + qrow) * D + d] = out;
+    if (p.q_rows) ((T*)p.q_rows)[(bh * p.Mp + qrow) * D + d] = from_f32<T>(out * p.qscale);
+    if (p.z_rows) ((T*)p.z_rows)[(bh * D + d) * p.Mp + qrow] = from_f32<T>(out);
     if (!p.frag) {
       if (p.q_op) ((T*)p.q_op)[(bh * p.Mp + qrow) * D + d] = from_f32<T>(out * p.qscale);
       if (p.z_op) ((T*)p.z_op)[(bh * D + d) * p.Mp + qrow] = from_f32<T>(out);

@@ -107,6 +107,10 @@ struct CombineParams {
   void* z_op;
   float* qnorm2;  // frag == 1 with q_op: [BH][Mp / 4] max of |scaled q|^2 over
                   // each group of 4 routes (one entry per wave), or null
+  // the frag == 0 layouts as well, whatever frag is (the backward's unfused
+  // decode after fused encodes): q_rows [BH][Mp][D] scaled, z_rows [BH][D][Mp]
+  void* q_rows;
+  void* z_rows;
   // fragment conversion for the later kernels (prep_n items), spread over the
   // threads: each issues its item's loads first and stores it at the end
   PrepFusedParams prep;
