@@ -55,41 +55,6 @@ __device__ __forceinline__ int key_perm(int rho) {
   return 16 * (rho >> 4) + 8 * ((rho >> 2) & 1) + 4 * ((rho & 15) >> 3) + (rho & 3);
 }
 
-__device__ __forceinline__ void lds_wait_barrier() {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-}
-
-// Workgroup barrier over LDS traffic only.  __syncthreads() also waits for
-// every global load the wave has in flight (vmcnt counts loads too), which
-// would drain a prefetch issued before it; here only this wave's LDS
-// operations are waited for.  Use it where the barrier orders LDS accesses
-// and nothing written to global memory by another wave is read afterwards.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// Copy n16 16-byte chunks src -> LDS dst with direct buffer -> LDS loads by
-// all nt threads of the block (each wave fills 1 KiB per step).  The source
-// is a raw buffer resource over exactly the n16 chunks (uniform, in scalar
-// registers); a step's address is one 32-bit per-thread offset shared by
-// every step plus the step's scalar offset, so no per-step 64-bit address
-// registers are kept live.
-__device__ __forceinline__ void copy_to_lds(const void* src, char* dst, int n16, int nt) {
-  if (n16 <= 0) return;
-  const int wave = wave_id();
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(src), (short)0, n16 * 16,
-                                        0x00020000);  // descriptor word 3: 32-bit data format, raw access
-  const int toff = (int)threadIdx.x * 16;
-  for (int k = 0; k * nt < n16; ++k) {
-    if (k * nt + (int)threadIdx.x < n16)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rsrc, (__attribute__((address_space(3))) void*)(dst + (size_t)(k * nt + wave * 64) * 16), 16, toff,
-          k * nt * 16, 0, 0);
-  }
-}
-
 // ---- small helpers -----------------------------------------------------------
 template <typename T>
 __device__ __forceinline__ typename Frag<T>::type cvt8(const f32x16& a, int off, float scale = 1.f) {

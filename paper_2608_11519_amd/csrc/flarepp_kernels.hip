@@ -100,18 +100,17 @@ __global__ void k_dmajor(DmajorParams p) {
 // blocks at once (independent accumulators), the token fragments loaded once.
 constexpr int kProjBlocks = 4;
 
+template <typename T, int NQ = kProjBlocks, int LAYOUT = -1>
+__device__ __forceinline__ void proj_store(const ProjParams& p, int b, int n0, int w, int cg,
+                                           const f32x16 (&acc)[NQ]);
+
+// One unit: tokens [n0, n0 + 32) of batch entry b times column group cg of
+// weight w, whose fragments start at wf (global memory or an LDS copy).
 template <typename T>
-__global__ __launch_bounds__(256) void k_project(ProjParams p) {
+__device__ __forceinline__ void proj_unit(const ProjParams& p, int b, int n0, int w, int cg, const T* wf) {
   using F = typename Frag<T>::type;
   const int lane = lane_id(), g = lane >> 5, c = lane & 31;
-  const int CB = p.C / 32, KS = p.C / 16, NB = p.Np / 32, CG = (CB + kProjBlocks - 1) / kProjBlocks;
-  const int64_t u = (int64_t)blockIdx.x * 4 + wave_id();
-  const int64_t total = (int64_t)p.B * NB * CG * p.nw;
-  if (u >= total) return;
-  const int cg = (int)(u % CG);
-  const int w = (int)((u / CG) % p.nw);
-  const int64_t bn = u / ((int64_t)CG * p.nw);
-  const int b = (int)(bn / NB), n0 = (int)(bn % NB) * 32;
+  const int CB = p.C / 32, KS = p.C / 16;
   const int layout = p.layout[w];
   const T* X = (const T*)p.x + ((int64_t)b * p.N) * p.C;
   const int xrow = n0 + c;
@@ -125,7 +124,7 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
   // rows past N load row N - 1 and are zeroed (the d-major layout stores them
   // as the zero padding)
   const T* xr = X + (int64_t)min(xrow, p.N - 1) * p.C + 8 * g;
-  const T* wr = (const T*)p.wf[w] + (int64_t)cg * kProjBlocks * KS * 512 + lane * 8;
+  const T* wr = wf + (int64_t)cg * kProjBlocks * KS * 512 + lane * 8;
   const int nq = min(kProjBlocks, CB - cg * kProjBlocks);  // wave-uniform
   F xn = load_frag(xr), wn[kProjBlocks];
 #pragma unroll
@@ -149,22 +148,41 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
       else mma(acc[q], wv[q], xf);                          // rows = channels, cols = tokens
     }
   }
+  proj_store<T>(p, b, n0, w, cg, acc);
+}
+
+// Stores the (up to) NQ result blocks acc of one unit (tokens [n0, n0 + 32)
+// of batch entry b, column group cg of weight w) in weight w's layout, adding
+// the residual for the plain layout when there is one.  LAYOUT is weight w's
+// layout when known at compile time, else -1.
+template <typename T, int NQ, int LAYOUT>
+__device__ __forceinline__ void proj_store(const ProjParams& p, int b, int n0, int w, int cg,
+                                           const f32x16 (&acc)[NQ]) {
+  int lane = lane_id();
+  // computed again at each call: kept from being hoisted out of a caller's
+  // loops, where the per-lane store offsets would occupy registers throughout
+  asm volatile("" : "+v"(lane));
+  const int g = lane >> 5, c = lane & 31;
+  const int CB = p.C / 32;
+  const int layout = LAYOUT >= 0 ? LAYOUT : p.layout[w];
+  const int xrow = n0 + c;
+  const bool xok = xrow < p.N;
   T* out = (T*)p.out[w];
   const int D = p.D;
   // the residual of every block is loaded before the first store uses it
   const bool has_res = layout == kPlain && p.res && xok;
-  Res16<T> res[kProjBlocks];
+  Res16<T> res[NQ];
   if (has_res) {
 #pragma unroll
-    for (int q = 0; q < kProjBlocks; ++q) {
-      const int cb = cg * kProjBlocks + q;
+    for (int q = 0; q < NQ; ++q) {
+      const int cb = cg * NQ + q;
       if (cb >= CB) break;  // wave-uniform
       load_res16(res[q], (const T*)p.res + ((int64_t)b * p.N + xrow) * p.C + 32 * cb, g);
     }
   }
 #pragma unroll
-  for (int q = 0; q < kProjBlocks; ++q) {
-    const int cb = cg * kProjBlocks + q;
+  for (int q = 0; q < NQ; ++q) {
+    const int cb = cg * NQ + q;
     if (cb >= CB) break;  // wave-uniform
     if (layout == kHeadsDMajor) {
       const int col = 32 * cb + c, h = col / D, d = col % D;
@@ -183,6 +201,131 @@ __global__ __launch_bounds__(256) void k_project(ProjParams p) {
                acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
       }
     }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_project(ProjParams p) {
+  const int CB = p.C / 32, NB = p.Np / 32, CG = (CB + kProjBlocks - 1) / kProjBlocks;
+  const int64_t u = (int64_t)blockIdx.x * 4 + wave_id();
+  const int64_t total = (int64_t)p.B * NB * CG * p.nw;
+  if (u >= total) return;
+  const int cg = (int)(u % CG);
+  const int w = (int)((u / CG) % p.nw);
+  const int64_t bn = u / ((int64_t)CG * p.nw);
+  proj_unit<T>(p, (int)(bn / NB), (int)(bn % NB) * 32, w, cg, (const T*)p.wf[w]);
+}
+
+// One unit of the persistent form: the tile's X fragments xf times weight w
+// (fragments in LDS at wl), all CB = C / 32 column blocks, then the stores.
+// The d-major layout takes result rows = tokens, the others rows = channels.
+template <int KS, int LAYOUT>
+__device__ __forceinline__ void proj_lds_unit(const ProjParams& p, int b, int n0, int w, const __bf16* wl,
+                                              const bf16x8 (&xf)[KS]) {
+  constexpr int CB = KS / 2;
+  const __bf16* wr = wl + lane_id() * 8;
+  f32x16 acc[CB];
+#pragma unroll
+  for (int q = 0; q < CB; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[q][r] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int q = 0; q < CB; ++q) {
+      const bf16x8 wv = load_frag(wr + (q * KS + ks) * 512);
+      if (LAYOUT == kHeadsDMajor) mma(acc[q], xf[ks], wv);
+      else mma(acc[q], wv, xf[ks]);
+    }
+  // issue order: the LDS reads of k step ks + 1 go out before the products
+  // of step ks, and no further ahead (all of them hoisted would hold KS CB
+  // fragments in registers)
+  __builtin_amdgcn_sched_group_barrier(0x100, CB, 0);
+#pragma unroll
+  for (int ks = 1; ks < KS; ++ks) {
+    __builtin_amdgcn_sched_group_barrier(0x100, CB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, CB, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, CB, 0);
+  proj_store<__bf16, CB, LAYOUT>(p, b, n0, w, 0, acc);
+}
+
+// Weight layout patterns of the persistent form (fixed at compile time so a
+// tile's units are straight-line code): K, V (, K~, V~) as the mixer projects
+// them, token-major outputs only, or one plain output (with residual).
+enum ProjPattern { kPatKV = 0, kPatTok = 1, kPatPlain = 2 };
+
+// Persistent form for bf16 when every weight's fragments fit in LDS together
+// (C = 16 KS <= 128): a workgroup of 8 waves per CU copies them in once, then
+// each wave walks 32-token tiles (tile = blockIdx.x * 8 + wave, + 8
+// gridDim.x, ...).  A tile's rows of X stay in registers for all its units
+// (KS fragments) and the next tile's rows are loaded while the current one is
+// computed, so a wave keeps a whole tile's X reads in flight instead of one
+// fragment per k step.  kPatKV: weights alternate token-major, d-major
+// (nw = 2 or 4); kPatTok: nw token-major; kPatPlain: nw = 1, plain.
+template <int KS, int PAT>
+__global__ __launch_bounds__(512) void k_project_lds(ProjParams p) {
+  using T = __bf16;
+  using F = Frag<T>::type;
+  constexpr int C = 16 * KS, CB = C / 32;  // one column group: CB <= kProjBlocks
+  static_assert(CB >= 1 && CB <= kProjBlocks, "C = 32 .. 32 kProjBlocks");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  for (int w = 0; w < p.nw; ++w)
+    copy_to_lds(p.wf[w], smem + (size_t)w * C * C * sizeof(T), C * C * (int)sizeof(T) / 16, 512);
+  const int lane = lane_id(), g = lane >> 5, c = lane & 31;
+  const int NB = p.Np / 32;
+  const int64_t tiles = (int64_t)p.B * NB, stride = (int64_t)gridDim.x * 8;
+  int64_t t = (int64_t)blockIdx.x * 8 + wave_id();
+  const __bf16* wl = reinterpret_cast<const __bf16*>(smem);
+  // rows past N load row N - 1 and are zeroed before use (the d-major layout
+  // stores them as the zero padding)
+  auto load_tile = [&](F (&xf)[KS], int64_t tile) {
+    const int bb = (int)(tile / NB), row = min((int)(tile % NB) * 32 + c, p.N - 1);
+    const T* xr = (const T*)p.x + ((int64_t)bb * p.N + row) * C + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) xf[ks] = load_frag(xr + 16 * ks);
+  };
+  // one tile: this tile's rows (loaded one tile earlier) are waited for
+  // first (the empty asm reads them, so the wait sits here, ahead of the next
+  // tile's loads, and not in the units), then the next tile's rows go out,
+  // then every weight's unit
+  auto tile = [&](F (&xf)[KS], F (&xn)[KS], int64_t tt) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("; x tile %0" : "+v"(xf[ks]));
+    if (tt + stride < tiles) load_tile(xn, tt + stride);
+    const int b = (int)(tt / NB), n0 = (int)(tt % NB) * 32;
+    if (n0 + c >= p.N) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) xf[ks] = zero_frag<T>();
+    }
+    if constexpr (PAT == kPatKV) {
+      proj_lds_unit<KS, kHeadsTokenMajor>(p, b, n0, 0, wl, xf);
+      proj_lds_unit<KS, kHeadsDMajor>(p, b, n0, 1, wl + C * C, xf);
+      if (p.nw == 4) {
+        proj_lds_unit<KS, kHeadsTokenMajor>(p, b, n0, 2, wl + 2 * C * C, xf);
+        proj_lds_unit<KS, kHeadsDMajor>(p, b, n0, 3, wl + 3 * C * C, xf);
+      }
+    } else if constexpr (PAT == kPatTok) {
+      for (int w = 0; w < p.nw; ++w) proj_lds_unit<KS, kHeadsTokenMajor>(p, b, n0, w, wl + w * C * C, xf);
+    } else {
+      proj_lds_unit<KS, kPlain>(p, b, n0, 0, wl, xf);
+    }
+  };
+  // two register sets, alternating (no copies between tiles)
+  F xa[KS], xb[KS];
+  if (t < tiles) load_tile(xa, t);
+  lds_wait_barrier();
+  // the first tile's rows are complete here; reading them in the empty asm
+  // tells the compiler so, which keeps the loop's waits at the distance of a
+  // whole tile of stores
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) asm volatile("; x tile %0" : "+v"(xa[ks]));
+  while (t < tiles) {
+    tile(xa, xb, t);
+    t += stride;
+    if (t >= tiles) break;
+    tile(xb, xa, t);
+    t += stride;
   }
 }
 
@@ -528,6 +671,35 @@ hipError_t launch_layernorm_bwd(const LayerNormBwdParams& p, hipStream_t s) {
 
 template <typename T>
 hipError_t launch_project(const ProjParams& p, hipStream_t s) {
+  // the persistent form: bf16, C = 64 or 128, every weight in LDS, and one
+  // of its layout patterns
+  int pat = -1;
+  {
+    bool kv = (p.nw == 2 || p.nw == 4), tok = true;
+    for (int w = 0; w < p.nw; ++w) {
+      kv = kv && p.layout[w] == ((w & 1) ? kHeadsDMajor : kHeadsTokenMajor);
+      tok = tok && p.layout[w] == kHeadsTokenMajor;
+    }
+    pat = kv ? kPatKV : tok ? kPatTok : (p.nw == 1 && p.layout[0] == kPlain) ? kPatPlain : -1;
+  }
+  const size_t lds = (size_t)p.nw * p.C * p.C * sizeof(T);
+  if (std::is_same<T, __bf16>::value && (p.C == 64 || p.C == 128) && lds <= 160 * 1024 && pat >= 0) {
+    using Kern = void (*)(ProjParams);
+    static const Kern kerns[2][3] = {
+        {&k_project_lds<4, kPatKV>, &k_project_lds<4, kPatTok>, &k_project_lds<4, kPatPlain>},
+        {&k_project_lds<8, kPatKV>, &k_project_lds<8, kPatTok>, &k_project_lds<8, kPatPlain>}};
+    const Kern fn = kerns[p.C == 128][pat];
+    int dev = 0, ncu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    const int64_t tiles = (int64_t)p.B * (p.Np / 32);
+    const unsigned grid = (unsigned)std::min<int64_t>(blocks_for(tiles, 8), std::max(ncu, 1));
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(512), lds, s, p);
+    return hipGetLastError();
+  }
   const int64_t units = (int64_t)p.B * (p.Np / 32) * ((p.C / 32 + kProjBlocks - 1) / kProjBlocks) * p.nw;
   k_project<T><<<blocks_for(units, 4), 256, 0, s>>>(p);
   return hipGetLastError();
