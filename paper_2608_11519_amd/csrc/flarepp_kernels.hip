@@ -100,6 +100,39 @@ __global__ void k_dmajor(DmajorParams p) {
 // blocks at once (independent accumulators), the token fragments loaded once.
 constexpr int kProjBlocks = 4;
 
+// Lane (c, g) of a 32x32 result block holds rows 8 (j / 4) + 4 g + j % 4 of
+// column c (j = 0..15): runs of 4 rows.  Swapping runs between the two lane
+// halves (v_permlane32_swap; lanes c and c + 32 exchange) leaves lane (c, g)
+// with rows 16 pr + 8 g .. + 7 in r[pr], pr = 0, 1: runs of 8 rows, one
+// 16-byte (bf16) store each instead of two 8-byte ones, so a store
+// instruction covers half as many memory segments.  All 64 lanes take part.
+__device__ __forceinline__ void runs8(const f32x16& acc, float (&r)[2][8]) {
+#pragma unroll
+  for (int pr = 0; pr < 2; ++pr)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      // lanes 0-31 keep their rows 4 g + e and take the other half's; lanes
+      // 32-63 take the other half's rows 8 + e and keep their own 12 + e
+      const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[8 * pr + e]),
+                                                      __float_as_uint(acc[8 * pr + 4 + e]), false, false);
+      r[pr][e] = __uint_as_float(s[0]);
+      r[pr][4 + e] = __uint_as_float(s[1]);
+    }
+}
+__device__ __forceinline__ void store8(__bf16* p, const float (&v)[8]) {
+  bf16x8 w;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) w[i] = (__bf16)v[i];
+  *reinterpret_cast<bf16x8*>(p) = w;
+}
+__device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
+  f32x4 a, b;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { a[i] = v[i]; b[i] = v[4 + i]; }
+  reinterpret_cast<f32x4*>(p)[0] = a;
+  reinterpret_cast<f32x4*>(p)[1] = b;
+}
+
 template <typename T, int NQ = kProjBlocks, int LAYOUT = -1>
 __device__ __forceinline__ void proj_store(const ProjParams& p, int b, int n0, int w, int cg,
                                            const f32x16 (&acc)[NQ]);
@@ -185,13 +218,26 @@ __device__ __forceinline__ void proj_store(const ProjParams& p, int b, int n0, i
     const int cb = cg * NQ + q;
     if (cb >= CB) break;  // wave-uniform
     if (layout == kHeadsDMajor) {
+      // rows = tokens: two runs of 8 tokens per lane, 16-byte (bf16) stores
+      float r[2][8];
+      runs8(acc[q], r);
       const int col = 32 * cb + c, h = col / D, d = col % D;
-      T* o = out + (((int64_t)b * p.H + h) * D + d) * p.Np + n0;
+      T* o = out + (((int64_t)b * p.H + h) * D + d) * p.Np + n0 + 8 * g;
+      store8(o, r[0]);
+      store8(o + 16, r[1]);
+    } else if (layout == kPlain) {
+      if (xok) store16(out + ((int64_t)b * p.N + xrow) * p.C + 32 * cb, acc[q], res[q], has_res, g);
+    } else if (D % 8 == 0) {
+      // rows = channels: two runs of 8 channels of one head per lane
+      float r[2][8];
+      runs8(acc[q], r);
+      if (xok) {
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4)
-        store4(o + 8 * r4 + 4 * g, acc[q][4 * r4], acc[q][4 * r4 + 1], acc[q][4 * r4 + 2], acc[q][4 * r4 + 3]);
-    } else if (layout == kPlain && xok) {
-      store16(out + ((int64_t)b * p.N + xrow) * p.C + 32 * cb, acc[q], res[q], has_res, g);
+        for (int pr = 0; pr < 2; ++pr) {
+          const int col = 32 * cb + 16 * pr + 8 * g, h = col / D, d = col % D;
+          store8(out + (((int64_t)b * p.H + h) * p.N + xrow) * D + d, r[pr]);
+        }
+      }
     } else if (xok) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {

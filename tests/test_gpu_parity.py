@@ -328,6 +328,26 @@ def test_project_entry_point(dtype):
     assert torch.equal(V2, V)
 
 
+@pytest.mark.parametrize("C,H", [(64, 4), (128, 8)])
+def test_project_entry_point_many_tiles_per_wave(C, H):
+    # bf16 at C = 64 and 128 takes the persistent projection (weights in
+    # LDS, one workgroup per CU walking 32-token tiles): 3 batch entries of
+    # 44101 tokens are 4137 tiles, so each of the 2048 waves of a 256-CU
+    # launch walks two or three of them, across batch boundaries and the
+    # token tails; four weights, then one
+    w = inp.Workload("proj-many", 3, 44101, C, H, 8, "bf16", "normal")
+    d = inp.make_inputs(w, 21)
+    t = upload(d, w)
+    outs = fp.flarepp_project(t["X"], t["Wk"], t["Wv"], t["Wkt"], t["Wvt"], H=w.H)
+    torch.cuda.synchronize()
+    for name, W, got in zip(("K", "V", "Kt", "Vt"), ("Wk", "Wv", "Wkt", "Wvt"), outs):
+        assert_close(name, got.float().cpu().numpy(), orc.project(d["X"], d[W], w.H), TOL["bf16"] / 2,
+                     f"project-many-C{C}")
+    _, _, Kt1, _ = fp.flarepp_project(t["X"], Wkt=t["Wkt"], H=w.H)
+    torch.cuda.synchronize()
+    assert torch.equal(Kt1, outs[2])
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shared", [True, False])
 def test_route_encode_entry_point(dtype, shared):
