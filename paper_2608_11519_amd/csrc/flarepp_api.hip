@@ -873,10 +873,10 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   BwdPrepParams bp{};
   bp.M = (int)M; bp.Mp = (int)Mp; bp.D = (int)D; bp.njobs = 3;
   bp.job[0].src = w.Qf; bp.job[0].src_is_f32 = 1; bp.job[0].O = (int)BH;
-  bp.job[0].rows = w.Qr; bp.job[0].tfrag = w.Qt;
+  bp.job[0].rows = w.Qr; bp.job[0].tfrag = w.Qt; bp.job[0].rows_scale = sc * 1.4426950408889634f;
   bp.job[1].src = w.Zf; bp.job[1].src_is_f32 = 1; bp.job[1].O = (int)BH; bp.job[1].rows = w.Zr;
   bp.job[2].src = seeds; bp.job[2].src_is_f32 = f32 ? 1 : 0; bp.job[2].O = (int)H;
-  bp.job[2].rows = w.Sr; bp.job[2].tfrag = w.St;
+  bp.job[2].rows = w.Sr; bp.job[2].tfrag = w.St; bp.job[2].rows_scale = sc * 1.4426950408889634f;
   HIPTRY(launch_bwd_prep<T>(bp, s));
 
   // ---- call 3 (decode): queries K, keys Q, values Z ----

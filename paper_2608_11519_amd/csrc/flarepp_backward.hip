@@ -398,12 +398,30 @@ __device__ __forceinline__ void load_short(ShortBlock<T, D, DEC>& s, const T* as
     }
 }
 
+// bf16 at D = 16 keeps two waves per SIMD (two workgroups per CU)
 template <typename T, int D, bool DEC>
-__global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
+__global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_attn_bwd(AttnBwdParams p) {
   using F = typename Frag<T>::type;
   constexpr int KS = D / 16, DB = (D + 31) / 32, TBP = tb_pitch<T>();
+  // bf16: dS (and P in the decode) change layout on the MFMA (times a
+  // permutation matrix) instead of through LDS; fp32 keeps the LDS transpose
+  constexpr bool MT = std::is_same<T, __bf16>::value;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
+  // position of element j of the lane's k = position fragment kk in the
+  // short-side products: 16 kk + 8 g + j with the LDS transpose; with the
+  // MFMA one it is the accumulator's row order, 16 kk + 8 (j / 4) + 4 g + j % 4
+  auto short_k_pos = [&](int kk, int gg, int j) __attribute__((always_inline)) {
+    return MT ? 16 * kk + 8 * (j >> 2) + 4 * gg + (j & 3) : 16 * kk + 8 * gg + j;
+  };
+  // B operands of the layout change: perm[kk][k = 8 g + j][col = c] = 1 when
+  // route 16 kk + 8 (j / 4) + 4 g + j % 4 (the route that the accumulator's
+  // element 8 kk + j of lane (., g) holds) is c
+  F perm[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) perm[kk][j] = from_f32<T>(short_k_pos(kk, g, j) == c ? 1.f : 0.f);
   const int W = blockDim.x >> 6;
   const int bh = blockIdx.x / p.R, r = blockIdx.x % p.R;
   const int b = bh / p.H, h = bh % p.H;
@@ -412,14 +430,14 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
   float* slot_a = reinterpret_cast<float*>(smem) + wave * slot_floats;
   float* slot_g = slot_a + D * SP;
   T* tb = reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) + wave * 32 * TBP;
-  // encode: the routes' L (log2) and c of this (b, h), [2][Mp], after the
-  // waves' transpose tiles
+  // encode: the routes' -L (log2) and -c of this (b, h), [2][Mp], after the
+  // waves' transpose tiles (the initial values of the S and dP accumulators)
   float* lc_lds = reinterpret_cast<float*>(reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) +
                                            W * 32 * TBP);
   for (int i = lane; i < slot_floats; i += 64) slot_a[i] = 0.f;
   if constexpr (!DEC) {
     for (int i = threadIdx.x; i < 2 * p.Mp; i += blockDim.x)
-      lc_lds[i] = i < p.Mp ? p.lrow[(int64_t)bh * p.Mp + i] : p.crow[(int64_t)bh * p.Mp + i - p.Mp];
+      lc_lds[i] = -(i < p.Mp ? p.lrow[(int64_t)bh * p.Mp + i] : p.crow[(int64_t)bh * p.Mp + i - p.Mp]);
     __syncthreads();
   }
 
@@ -484,7 +502,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            const int pos = 16 * kk + 8 * g + j;
+            const int pos = short_k_pos(kk, g, j);
             const T v = tb[pos * TBP + c];
             out[kk][db][j] = n0 + pos < p.Nl ? v : from_f32<T>(0.f);
           }
@@ -503,7 +521,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         for (int db = 0; db < DB; ++db)
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            const int nn = n0 + 16 * kk + 8 * g + j, d = 32 * db + c;
+            const int nn = n0 + short_k_pos(kk, g, j), d = 32 * db + c;
             const bool ok = nn < p.Nl && d < D;
             const int64_t at = (int64_t)min(nn, p.Nl - 1) * p.blo_sn + (int64_t)min(d, D - 1) * p.blo_sd;
             const T kv = blo[at];
@@ -535,44 +553,54 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.f;
+    // initial accumulators of route block sb: encode -L and -c of the block's
+    // routes (rows), so that S' = s log2(e) S - L and dP' = dP - c come out
+    // of the MFMAs; decode zero (L and c belong to the column there).  The
+    // ash rows are scaled by s log2(e) beforehand.
+    auto load_init = [&](int sb, f32x16& si, f32x16& di) __attribute__((always_inline)) {
+      if constexpr (!DEC) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lc_lds + 32 * (SB0 + sb) + 8 * a + 4 * g);
+          const f32x4 c4 = *reinterpret_cast<const f32x4*>(lc_lds + p.Mp + 32 * (SB0 + sb) + 8 * a + 4 * g);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) { si[4 * a + q] = l4[q]; di[4 * a + q] = c4[q]; }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) si[e] = di[e] = 0.f;
+      }
+    };
     // one block of 32 routes; the operands of the next block are loaded into
     // the other buffer first (the last block again at the end, so the same
-    // number of loads is in flight on every block)
-    auto route_block = [&](const ShortBlock<T, D, DEC>& cb, int sb) __attribute__((always_inline)) {
-      f32x16 sc, dp;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) sc[e] = dp[e] = 0.f;
+    // number of loads is in flight on every block), and its initial
+    // accumulators at the end
+    auto route_block = [&](const ShortBlock<T, D, DEC>& cb, int sb, f32x16& si, f32x16& di) __attribute__((always_inline)) {
+      f32x16 sc = si, dp = di;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         mma(sc, cb.a[ks], kb[ks]);
         mma(dp, cb.gr[ks], gb[ks]);
       }
-      // P = exp(s S - L), dS = P (dP - c); rows past M and columns past the
-      // long length are zero
+      // P = exp2(S'), dS = P dP' (encode; decode: the column's L and c
+      // subtracted here); rows past M and columns past the long length are
+      // zero
       f32x16 P, dS;
-      // encode: L (log2) and c of this lane's 16 routes, from LDS
-      f32x4 lq[4], cq[4];
-      if constexpr (!DEC) {
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          lq[a] = *reinterpret_cast<const f32x4*>(lc_lds + 32 * (SB0 + sb) + 8 * a + 4 * g);
-          cq[a] = *reinterpret_cast<const f32x4*>(lc_lds + p.Mp + 32 * (SB0 + sb) + 8 * a + 4 * g);
-        }
-      }
       auto softmax_grad = [&](auto masked) __attribute__((always_inline)) {
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
-          float L, cc;
+          float pv, dd;
           if constexpr (DEC) {
-            L = Ll; cc = cl;
+            pv = __builtin_amdgcn_exp2f(sc[rr] - Ll);
+            dd = dp[rr] - cl;
           } else {
-            L = lq[rr >> 2][rr & 3]; cc = cq[rr >> 2][rr & 3];
+            pv = __builtin_amdgcn_exp2f(sc[rr]);
+            dd = dp[rr];
           }
-          float pv = __builtin_amdgcn_exp2f(sc[rr] * p.sl2 - L);
           if constexpr (decltype(masked)::value)
             if (!(nok && 32 * (SB0 + sb) + acc_row(lane, rr) < p.M)) pv = 0.f;
           P[rr] = pv;
-          dS[rr] = pv * (dp[rr] - cc);
+          dS[rr] = pv * dd;
         }
       };
       if (full_tile && 32 * (SB0 + sb + 1) <= p.M) softmax_grad(std::false_type{});  // wave-uniform
@@ -594,27 +622,48 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
           mma(dk[db], cb.at[kk][db], dsb[kk]);
           if constexpr (!DEC) mma(dv[db], cb.gt[kk][db], pb[kk]);
         }
-      // short side: dS (then P in the decode) transposed through the wave's
-      // LDS tile [position][route]
+      // short side: dS (then P in the decode) with rows = routes along the
+      // lanes and k = positions in the registers
       F dsa[2], pa[2];
+      if constexpr (MT) {
+        // (dS^T)^T on the MFMA: A = dS^T (rows = positions, k = routes in the
+        // accumulator's order, exactly the B operand dsb already built) times
+        // the permutation perm gives dS with lane = route and the positions
+        // in the accumulator's row order; exact (one product of 1 per sum)
+        auto relayout = [&](const F (&src)[2], F (&dst)[2]) __attribute__((always_inline)) {
+          f32x16 t;
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
-        store4(tb + c * TBP + 8 * a + 4 * g, dS[4 * a], dS[4 * a + 1], dS[4 * a + 2], dS[4 * a + 3]);
-      __builtin_amdgcn_wave_barrier();
+          for (int e = 0; e < 16; ++e) t[e] = 0.f;
+          mma(t, src[0], perm[0]);
+          mma(t, src[1], perm[1]);
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
+          for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) dsa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
-      if constexpr (DEC) {
-        __builtin_amdgcn_wave_barrier();
+            for (int j = 0; j < 8; ++j) dst[kk][j] = from_f32<T>(t[8 * kk + j]);
+        };
+        relayout(dsb, dsa);
+        if constexpr (DEC) relayout(pb, pa);
+      } else {
+        // through the wave's LDS tile [position][route]
 #pragma unroll
         for (int a = 0; a < 4; ++a)
-          store4(tb + c * TBP + 8 * a + 4 * g, P[4 * a], P[4 * a + 1], P[4 * a + 2], P[4 * a + 3]);
+          store4(tb + c * TBP + 8 * a + 4 * g, dS[4 * a], dS[4 * a + 1], dS[4 * a + 2], dS[4 * a + 3]);
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-          for (int j = 0; j < 8; ++j) pa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
+          for (int j = 0; j < 8; ++j) dsa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
+        if constexpr (DEC) {
+          __builtin_amdgcn_wave_barrier();
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+            store4(tb + c * TBP + 8 * a + 4 * g, P[4 * a], P[4 * a + 1], P[4 * a + 2], P[4 * a + 3]);
+          __builtin_amdgcn_wave_barrier();
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) pa[kk][j] = tb[(16 * kk + 8 * g + j) * TBP + c];
+        }
       }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -645,15 +694,18 @@ __global__ __launch_bounds__(256) void k_attn_bwd(AttnBwdParams p) {
         }
       }
       __builtin_amdgcn_wave_barrier();
+      load_init(min(sb + 1, NS - 1), si, di);
     };
     ShortBlock<T, D, DEC> b0, b1;
+    f32x16 si, di;
     load_short(b0, ash, gsh, asht, gsht, SB0, lane);
+    load_init(0, si, di);
     for (int sb = 0; sb < NS; sb += 2) {
       load_short(b1, ash, gsh, asht, gsht, SB0 + min(sb + 1, NS - 1), lane);
-      route_block(b0, sb);
+      route_block(b0, sb, si, di);
       if (sb + 1 < NS) {  // wave-uniform
         load_short(b0, ash, gsh, asht, gsht, SB0 + min(sb + 2, NS - 1), lane);
-        route_block(b1, sb + 1);
+        route_block(b1, sb + 1, si, di);
       }
     }
     // long-side results for this wave's 32 positions: rows d, column = lane
@@ -745,7 +797,13 @@ __global__ __launch_bounds__(256) void k_bwd_prep(BwdPrepParams p) {
             for (int j = 0; j < 8; ++j) cs += v[j] * w[j];
           }
         }
-        if (J.rows) store8(static_cast<T*>(J.rows) + i * D + d0, v);
+        if (J.rows) {
+          const float rs = J.rows_scale != 0.f ? J.rows_scale : 1.f;
+          float u[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) u[j] = v[j] * rs;
+          store8(static_cast<T*>(J.rows) + i * D + d0, u);
+        }
       }
       if (J.c) J.c[i] = cs;
       if (J.l2) J.l2[i] = m < p.M ? J.lse[(int64_t)o * p.M + m] * kLog2e : 0.f;

@@ -247,7 +247,7 @@ struct GemmParams {
 struct AttnBwdParams {
   int B, H, Nl, M, Mp, R, tpw;   // long length, routes, chunks per (b, h), long tiles per wave
   int sb0, nsb;                  // the window of route blocks [sb0, sb0 + nsb) of this launch
-  float s, sl2;                  // 1/sqrt(D), and times log2(e)
+  float s, sl2;                  // 1/sqrt(D), and times log2(e) (the route rows ash come scaled by sl2)
   // short side, per (b, h) at b * sb + h * sh (elements)
   const void* ash; int64_t ash_sb, ash_sh;    // rows [Mp][D]
   const void* asht; int64_t asht_sb, asht_sh; // A fragments of A_sh^T
@@ -294,6 +294,7 @@ struct BwdPrepJob {
   const float* lse;
   int O;
   void* rows; void* tfrag; float* c; float* l2;
+  float rows_scale;  // rows are stored times this (0 is taken as 1)
 };
 struct BwdPrepParams {
   int M, Mp, D, njobs;
