@@ -450,6 +450,39 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
   T* dout_b = static_cast<T*>(p.dout_b);
   T* dout_g = static_cast<T*>(p.dout_g);
 
+  // bf16 encode at D = 16 with token-major keys and d-major values: a tile's
+  // long-side rows (32 key rows [32][16], then the 16 value rows of its 32
+  // positions [16][32]; 1 KiB each) are copied into the wave's tile buffer
+  // one tile ahead by direct buffer -> LDS loads, issued as soon as the
+  // current tile's rows have been read out, so no tile waits on its loads.
+  // Rows past the long length read as zero (buffer bounds; the d-major
+  // values are zero-padded).
+  constexpr bool STG = MT && D == 16 && !DEC;
+  const bool stg = STG && p.blo_sd == 1 && p.blo_sn == D && p.glo_sn == 1;  // uniform
+  auto stage_issue = [&](int i) __attribute__((always_inline)) {
+    if (i >= p.tpw) return;
+    const int n0i = ((r * p.tpw + i) * W + wave) * 32;  // wave-uniform
+    if (n0i >= p.Nl) return;
+    constexpr int EB = (int)sizeof(T);
+    const int kbytes = (int)std::min<int64_t>((int64_t)p.Nl * D * EB, 0x7fffffff);
+    const int vbytes = (int)std::min<int64_t>((int64_t)D * p.glo_sd * EB, 0x7fffffff);
+    const __amdgpu_buffer_rsrc_t rk =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(blo), (short)0, kbytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(glo), (short)0, vbytes, 0x00020000);
+    // lane l: key row n0i + l / 2, half l % 2; value row l / 4, positions
+    // n0i + 8 (l % 4) .. + 7; each lands at byte 16 l of its KiB
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (__attribute__((address_space(3))) void*)tb, 16,
+                                             (n0i * D + 8 * lane) * EB, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (__attribute__((address_space(3))) void*)(tb + 32 * D), 16,
+                                             ((lane >> 2) * (int)p.glo_sd + n0i + 8 * (lane & 3)) * EB, 0, 0, 0);
+    asm volatile("" ::: "memory");  // the copies go out ahead of the tile's route-operand loads
+  };
+  if (stg) {
+    stage_issue(0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+
   for (int i = 0; i < p.tpw; ++i) {
     const int n0 = ((r * p.tpw + i) * W + wave) * 32;  // wave-uniform
     if (n0 >= p.Nl) break;
@@ -459,78 +492,100 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
     const bool full_tile = n0 + 32 <= p.Nl;  // wave-uniform: no position masked
     // long-side B operands of S (keys) and dP (values), one lane per position
     F kb[KS], gb[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kb[ks] = long_frag(blo, p.blo_sn, p.blo_sd, nc, 16 * ks + 8 * g, nok);
-    if (D == 32 && p.glo_sn == 1) {  // wave-uniform (at D = 16 the staging would cost the second wave per SIMD)
-      // d-major values (each head's rows padded to whole 32-position tiles):
-      // the tile's D rows of 32 positions go through the wave's transpose
-      // tile with 16-byte loads (chunk r: row r / 4, positions 8 (r % 4) ..
-      // + 7), then each lane reads its position's column
-#pragma unroll
-      for (int r0 = 0; r0 < D * 4; r0 += 64) {
-        const int r = r0 + lane, d = r >> 2, q = r & 3;
-        store_frag8(tb + d * TBP + 8 * q, load_frag(glo + (int64_t)d * p.glo_sd + n0 + 8 * q));
-      }
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const T v = tb[(16 * ks + 8 * g + j) * TBP + c];
-          gb[ks][j] = nok ? v : from_f32<T>(0.f);
-        }
-      __builtin_amdgcn_wave_barrier();
-    } else {
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) gb[ks] = long_frag(glo, p.glo_sn, p.glo_sd, nc, 16 * ks + 8 * g, nok);
-    }
     // long-side B operands of the short-side products (k = position, n = d)
     F kt[2][DB], gt[2][DB];
-    // row-major long side (unit stride along d): each lane stores its
-    // position's row of 32 columns into the wave's transpose tile with
-    // 16-byte loads, then reads one column (d = 32 db + c) of it
-    auto transpose_long = [&](const T* x, int64_t sn, F (&out)[2][DB]) __attribute__((always_inline)) {
+    if (stg) {
+      // from the staged rows (landed at the end of the previous tile)
+      // (the lane index is re-read here so that the per-lane LDS offsets are
+      // computed per tile rather than held in registers across the loop)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      const int lg = ln >> 5, lc = ln & 31;
+      const T* sk = tb;           // [32 positions][D]
+      const T* sv = tb + 32 * D;  // [D][32 positions]
+      kb[0] = load_frag(sk + lc * D + 8 * lg);
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int d0 = 32 * db + 16 * g + 8 * h;  // D is a multiple of 16: d0 < D means d0 + 8 <= D
-          store_frag8(tb + c * TBP + 16 * g + 8 * h, d0 < D ? load_frag(x + (int64_t)nc * sn + d0) : zero_frag<T>());
-        }
-        __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int pos = short_k_pos(kk, g, j);
-            const T v = tb[pos * TBP + c];
-            out[kk][db][j] = n0 + pos < p.Nl ? v : from_f32<T>(0.f);
-          }
-        __builtin_amdgcn_wave_barrier();
-      }
-    };
-    // (D = 64 keeps the element loads: the staged rows would add to a
-    // register budget that is already full there)
-    if (D <= 32 && p.blo_sd == 1 && (!DEC || p.glo_sd == 1)) {  // wave-uniform
-      transpose_long(blo, p.blo_sn, kt);
-      if constexpr (DEC) transpose_long(glo, p.glo_sn, gt);
-    } else {
+      for (int j = 0; j < 8; ++j) gb[0][j] = sv[(8 * lg + j) * 32 + lc];
+      // columns d = lc >= D of the short-side product are never stored:
+      // those lanes read a valid (finite) key of another column
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+        for (int j = 0; j < 8; ++j) kt[kk][0][j] = sk[short_k_pos(kk, lg, j) * D + (lc & (D - 1))];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // read out before the next tile's rows land
+      stage_issue(i + 1);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kb[ks] = long_frag(blo, p.blo_sn, p.blo_sd, nc, 16 * ks + 8 * g, nok);
+      if (D == 32 && p.glo_sn == 1) {  // wave-uniform (at D = 16 the staging would cost the second wave per SIMD)
+        // d-major values (each head's rows padded to whole 32-position tiles):
+        // the tile's D rows of 32 positions go through the wave's transpose
+        // tile with 16-byte loads (chunk r: row r / 4, positions 8 (r % 4) ..
+        // + 7), then each lane reads its position's column
+#pragma unroll
+        for (int r0 = 0; r0 < D * 4; r0 += 64) {
+          const int r = r0 + lane, d = r >> 2, q = r & 3;
+          store_frag8(tb + d * TBP + 8 * q, load_frag(glo + (int64_t)d * p.glo_sd + n0 + 8 * q));
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            const int nn = n0 + short_k_pos(kk, g, j), d = 32 * db + c;
-            const bool ok = nn < p.Nl && d < D;
-            const int64_t at = (int64_t)min(nn, p.Nl - 1) * p.blo_sn + (int64_t)min(d, D - 1) * p.blo_sd;
-            const T kv = blo[at];
-            kt[kk][db][j] = ok ? kv : from_f32<T>(0.f);
-            if (DEC) {
-              const T gv = glo[(int64_t)min(nn, p.Nl - 1) * p.glo_sn + (int64_t)min(d, D - 1) * p.glo_sd];
-              gt[kk][db][j] = ok ? gv : from_f32<T>(0.f);
-            }
+            const T v = tb[(16 * ks + 8 * g + j) * TBP + c];
+            gb[ks][j] = nok ? v : from_f32<T>(0.f);
           }
+        __builtin_amdgcn_wave_barrier();
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) gb[ks] = long_frag(glo, p.glo_sn, p.glo_sd, nc, 16 * ks + 8 * g, nok);
+      }
+      // row-major long side (unit stride along d): each lane stores its
+      // position's row of 32 columns into the wave's transpose tile with
+      // 16-byte loads, then reads one column (d = 32 db + c) of it
+      auto transpose_long = [&](const T* x, int64_t sn, F (&out)[2][DB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int d0 = 32 * db + 16 * g + 8 * h;  // D is a multiple of 16: d0 < D means d0 + 8 <= D
+            store_frag8(tb + c * TBP + 16 * g + 8 * h, d0 < D ? load_frag(x + (int64_t)nc * sn + d0) : zero_frag<T>());
+          }
+          __builtin_amdgcn_wave_barrier();
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              const int pos = short_k_pos(kk, g, j);
+              const T v = tb[pos * TBP + c];
+              out[kk][db][j] = n0 + pos < p.Nl ? v : from_f32<T>(0.f);
+            }
+          __builtin_amdgcn_wave_barrier();
+        }
+      };
+      // (D = 64 keeps the element loads: the staged rows would add to a
+      // register budget that is already full there)
+      if (D <= 32 && p.blo_sd == 1 && (!DEC || p.glo_sd == 1)) {  // wave-uniform
+        transpose_long(blo, p.blo_sn, kt);
+        if constexpr (DEC) transpose_long(glo, p.glo_sn, gt);
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              const int nn = n0 + short_k_pos(kk, g, j), d = 32 * db + c;
+              const bool ok = nn < p.Nl && d < D;
+              const int64_t at = (int64_t)min(nn, p.Nl - 1) * p.blo_sn + (int64_t)min(d, D - 1) * p.blo_sd;
+              const T kv = blo[at];
+              kt[kk][db][j] = ok ? kv : from_f32<T>(0.f);
+              if (DEC) {
+                const T gv = glo[(int64_t)min(nn, p.Nl - 1) * p.glo_sn + (int64_t)min(d, D - 1) * p.glo_sd];
+                gt[kk][db][j] = ok ? gv : from_f32<T>(0.f);
+              }
+            }
+      }
     }
     // decode: c = <dY_n, Y_n> over the head's channels, and the token's
     // log-normaliser over the routes (log2 units) from the forward
@@ -708,6 +763,10 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
         route_block(b1, sb + 1, si, di);
       }
     }
+    // the next tile's staged rows (issued at this tile's start, ahead of all
+    // its route-operand loads) have landed; waited for here, before this
+    // tile's stores, so the wait covers loads only
+    if (stg) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     // long-side results for this wave's 32 positions: rows d, column = lane
     if (nok) {
       const int64_t row = ((int64_t)b * p.Nl + n) * (int64_t)(p.H * D) + h * D;
