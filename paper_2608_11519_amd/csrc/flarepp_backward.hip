@@ -322,9 +322,16 @@ __global__ __launch_bounds__(256) void k_sum_splits(const float* part, SumOuts o
 // tile [32][32 + 16 bytes] of T (dS, then P in the decode); per workgroup
 // (encode) the routes' L and c.
 template <typename T> constexpr int tb_pitch() { return 32 + 16 / (int)sizeof(T); }
+// Bytes of a wave's tile buffer: the transpose tile, or for the bf16 decode
+// at D = 16 its staged long-side rows (keys, dY, Y: 1 KiB each, then 32
+// log-normalisers), whichever is larger.
+constexpr size_t attn_bwd_tile_bytes(int D, bool dec, int elem_bytes) {
+  const size_t tile = (size_t)32 * (32 + 16 / elem_bytes) * elem_bytes;
+  const size_t staged = (dec && elem_bytes == 2 && D == 16) ? 3 * 1024 + 128 : 0;
+  return tile > staged ? tile : staged;
+}
 size_t attn_bwd_wave_bytes(int D, int nsb, bool dec, int elem_bytes) {
-  const int tbp = 32 + 16 / elem_bytes;
-  return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (32 * nsb + 4) + (size_t)32 * tbp * elem_bytes;
+  return sizeof(float) * (size_t)(dec ? 2 : 1) * D * (32 * nsb + 4) + attn_bwd_tile_bytes(D, dec, elem_bytes);
 }
 
 // Fragment of a long-side row: element j = x[n * sn + (d0 + j) * sd] (one
@@ -403,6 +410,7 @@ template <typename T, int D, bool DEC>
 __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_attn_bwd(AttnBwdParams p) {
   using F = typename Frag<T>::type;
   constexpr int KS = D / 16, DB = (D + 31) / 32, TBP = tb_pitch<T>();
+  constexpr int TBE = (int)(attn_bwd_tile_bytes(D, DEC, (int)sizeof(T)) / sizeof(T));  // tile buffer elements
   // bf16: dS (and P in the decode) change layout on the MFMA (times a
   // permutation matrix) instead of through LDS; fp32 keeps the LDS transpose
   constexpr bool MT = std::is_same<T, __bf16>::value;
@@ -429,11 +437,11 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
   const int slot_floats = (DEC ? 2 : 1) * D * SP;
   float* slot_a = reinterpret_cast<float*>(smem) + wave * slot_floats;
   float* slot_g = slot_a + D * SP;
-  T* tb = reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) + wave * 32 * TBP;
+  T* tb = reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) + wave * TBE;
   // encode: the routes' -L (log2) and -c of this (b, h), [2][Mp], after the
   // waves' transpose tiles (the initial values of the S and dP accumulators)
   float* lc_lds = reinterpret_cast<float*>(reinterpret_cast<T*>(reinterpret_cast<float*>(smem) + W * slot_floats) +
-                                           W * 32 * TBP);
+                                           W * TBE);
   for (int i = lane; i < slot_floats; i += 64) slot_a[i] = 0.f;
   if constexpr (!DEC) {
     for (int i = threadIdx.x; i < 2 * p.Mp; i += blockDim.x)
@@ -450,15 +458,18 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
   T* dout_b = static_cast<T*>(p.dout_b);
   T* dout_g = static_cast<T*>(p.dout_g);
 
-  // bf16 encode at D = 16 with token-major keys and d-major values: a tile's
-  // long-side rows (32 key rows [32][16], then the 16 value rows of its 32
-  // positions [16][32]; 1 KiB each) are copied into the wave's tile buffer
-  // one tile ahead by direct buffer -> LDS loads, issued as soon as the
-  // current tile's rows have been read out, so no tile waits on its loads.
+  // bf16 at D = 16 with token-major keys: a tile's long-side rows are copied
+  // into the wave's tile buffer one tile ahead by direct buffer -> LDS loads,
+  // issued as soon as the current tile's rows have been read out, so no tile
+  // waits on its loads.  Encode: the 32 key rows [32][16], then the 16 d-major
+  // value rows of its 32 positions [16][32]; decode: key rows, dY rows, Y rows
+  // ([32][16] each), then the 32 log-normalisers; 1 KiB per block of rows.
   // Rows past the long length read as zero (buffer bounds; the d-major
   // values are zero-padded).
-  constexpr bool STG = MT && D == 16 && !DEC;
-  const bool stg = STG && p.blo_sd == 1 && p.blo_sn == D && p.glo_sn == 1;  // uniform
+  constexpr bool STG = MT && D == 16;
+  const bool stg = STG && p.blo_sd == 1 && p.blo_sn == D &&
+                   (DEC ? (p.glo_sd == 1 && p.ylo_sn == p.glo_sn) : p.glo_sn == 1);  // uniform
+  const T* ylo = DEC ? static_cast<const T*>(p.ylo) + b * p.ylo_sb + h * p.ylo_sh : nullptr;
   auto stage_issue = [&](int i) __attribute__((always_inline)) {
     if (i >= p.tpw) return;
     const int n0i = ((r * p.tpw + i) * W + wave) * 32;  // wave-uniform
@@ -468,14 +479,34 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
     const int vbytes = (int)std::min<int64_t>((int64_t)D * p.glo_sd * EB, 0x7fffffff);
     const __amdgpu_buffer_rsrc_t rk =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(blo), (short)0, kbytes, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(glo), (short)0, vbytes, 0x00020000);
-    // lane l: key row n0i + l / 2, half l % 2; value row l / 4, positions
-    // n0i + 8 (l % 4) .. + 7; each lands at byte 16 l of its KiB
+    // lane l: key row n0i + l / 2, half l % 2 (likewise dY and Y rows);
+    // value row l / 4, positions n0i + 8 (l % 4) .. + 7; each lands at byte
+    // 16 l of its KiB
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (__attribute__((address_space(3))) void*)tb, 16,
                                              (n0i * D + 8 * lane) * EB, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (__attribute__((address_space(3))) void*)(tb + 32 * D), 16,
-                                             ((lane >> 2) * (int)p.glo_sd + n0i + 8 * (lane & 3)) * EB, 0, 0, 0);
+    if constexpr (DEC) {
+      const int sn = (int)p.glo_sn;
+      const int rbytes = (int)std::min<int64_t>((int64_t)p.Nl * sn * EB, 0x7fffffff);
+      const __amdgpu_buffer_rsrc_t rg =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(glo), (short)0, rbytes, 0x00020000);
+      const __amdgpu_buffer_rsrc_t ry =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(ylo), (short)0, rbytes, 0x00020000);
+      const int roff = ((n0i + (lane >> 1)) * sn + 8 * (lane & 1)) * EB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (__attribute__((address_space(3))) void*)(tb + 32 * D), 16, roff, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, (__attribute__((address_space(3))) void*)(tb + 64 * D), 16, roff, 0, 0, 0);
+      if (lane < 8) {  // 32 log-normalisers, 4 per lane
+        const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(p.lcol + (int64_t)bh * p.Nl), (short)0,
+            (int)std::min<int64_t>((int64_t)p.Nl * 4, 0x7fffffff), 0x00020000);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (__attribute__((address_space(3))) void*)(tb + 96 * D), 16,
+                                                 (n0i + 4 * lane) * 4, 0, 0, 0);
+      }
+    } else {
+      const __amdgpu_buffer_rsrc_t rv =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(glo), (short)0, vbytes, 0x00020000);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (__attribute__((address_space(3))) void*)(tb + 32 * D), 16,
+                                               ((lane >> 2) * (int)p.glo_sd + n0i + 8 * (lane & 3)) * EB, 0, 0, 0);
+    }
     asm volatile("" ::: "memory");  // the copies go out ahead of the tile's route-operand loads
   };
   if (stg) {
@@ -494,6 +525,8 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
     F kb[KS], gb[KS];
     // long-side B operands of the short-side products (k = position, n = d)
     F kt[2][DB], gt[2][DB];
+    // decode: c = <dY_n, Y_n> and the token's log-normaliser
+    float Ll = 0.f, cl = 0.f;
     if (stg) {
       // from the staged rows (landed at the end of the previous tile)
       // (the lane index is re-read here so that the per-lane LDS offsets are
@@ -502,16 +535,32 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
       asm volatile("" : "+v"(ln));
       const int lg = ln >> 5, lc = ln & 31;
       const T* sk = tb;           // [32 positions][D]
-      const T* sv = tb + 32 * D;  // [D][32 positions]
+      const T* sv = tb + 32 * D;  // encode: [D][32 positions]; decode: dY [32 positions][D]
       kb[0] = load_frag(sk + lc * D + 8 * lg);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) gb[0][j] = sv[(8 * lg + j) * 32 + lc];
-      // columns d = lc >= D of the short-side product are never stored:
-      // those lanes read a valid (finite) key of another column
+      // columns d = lc >= D of the short-side products are never stored:
+      // those lanes read a valid (finite) value of another column
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
         for (int j = 0; j < 8; ++j) kt[kk][0][j] = sk[short_k_pos(kk, lg, j) * D + (lc & (D - 1))];
+      if constexpr (DEC) {
+        gb[0] = load_frag(sv + lc * D + 8 * lg);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) gt[kk][0][j] = sv[short_k_pos(kk, lg, j) * D + (lc & (D - 1))];
+        // c = <dY_n, Y_n> over the head's channels and the token's
+        // log-normaliser (log2 units), from the staged rows
+        const F yf = load_frag(tb + 64 * D + lc * D + 8 * lg);
+        float sacc = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sacc += to_f32(gb[0][j]) * to_f32(yf[j]);
+        cl = sacc + other_half(sacc);
+        Ll = reinterpret_cast<const float*>(tb + 96 * D)[lc];
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) gb[0][j] = sv[(8 * lg + j) * 32 + lc];
+      }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // read out before the next tile's rows land
       stage_issue(i + 1);
     } else {
@@ -589,9 +638,8 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
     }
     // decode: c = <dY_n, Y_n> over the head's channels, and the token's
     // log-normaliser over the routes (log2 units) from the forward
-    float Ll = 0.f, cl = 0.f;
-    if constexpr (DEC) {
-      const T* y = static_cast<const T*>(p.ylo) + b * p.ylo_sb + h * p.ylo_sh;
+    if (DEC && !stg) {
+      const T* y = ylo;
       float sacc = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
