@@ -75,6 +75,16 @@ def test_backward_tails_and_route_counts(N, M):
     _check(w, inp.make_inputs(w, 3, seed_scale=4.0), f"N{N}-M{M}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_backward_several_tiles_per_wave_with_tail(dtype):
+    # two heads over 40,013 tokens: 1,251 position tiles per (b, h), so each
+    # wave of the SDPA backward walks two of them (in bf16 at D = 16 the
+    # second tile's rows are staged through LDS during the first), and the
+    # last tile holds 13 positions
+    w = inp.Workload("bwd-tiles", 1, 40013, 32, 2, 40, dtype, "normal")
+    _check(w, inp.make_inputs(w, 11, seed_scale=4.0), "tiles-tail")
+
+
 @pytest.mark.parametrize("D,dtype", [(32, "bf16"), (64, "bf16"), (32, "f32"), (64, "f32")])
 def test_backward_head_widths(D, dtype):
     w = inp.Workload("bwd-width", 2, 600, 2 * D, 2, 40, dtype, "normal")
