@@ -778,7 +778,38 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
           mma(o, dsa[kk], kt[kk][db]);
           if (DEC) mma(o2, pa[kk], gt[kk][db]);
         }
-        if (32 * db + c < D) {
+        if constexpr (D == 16) {
+          // only columns c < 16 are real: lanes c >= 16 take rows 16 .. 31
+          // (accumulator entries 8 .. 15) of column c - 16 by a swap of
+          // 16-lane rows, so every lane adds two runs of 4 routes instead
+          // of half the lanes adding four
+          float v[8], u[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const auto so = __builtin_amdgcn_permlane16_swap(__float_as_uint(o[e]), __float_as_uint(o[e + 8]), false, false);
+            v[e] = __uint_as_float(so[0]);
+            if (DEC) {
+              const auto s2 = __builtin_amdgcn_permlane16_swap(__float_as_uint(o2[e]), __float_as_uint(o2[e + 8]), false, false);
+              u[e] = __uint_as_float(s2[0]);
+            }
+          }
+          const int off = (c & 15) * SP + 32 * sb + (c & 16) + 4 * g;
+#pragma unroll
+          for (int a = 0; a < 2; ++a) {
+            f32x4* pa4 = reinterpret_cast<f32x4*>(slot_a + off + 8 * a);
+            f32x4 x = *pa4;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) x[q] += v[4 * a + q];
+            *pa4 = x;
+            if (DEC) {
+              f32x4* pg4 = reinterpret_cast<f32x4*>(slot_g + off + 8 * a);
+              f32x4 y = *pg4;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) y[q] += u[4 * a + q];
+              *pg4 = y;
+            }
+          }
+        } else if (32 * db + c < D) {
           float* sa = slot_a + (32 * db + c) * SP + 32 * sb + 4 * g;
           float* sg = slot_g + (32 * db + c) * SP + 32 * sb + 4 * g;
 #pragma unroll
