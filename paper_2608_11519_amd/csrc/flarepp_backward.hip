@@ -213,7 +213,17 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
   __shared__ __attribute__((aligned(16))) T Bs[TN * PITCH];
   const int lane = lane_id(), wave = wave_id(), g = lane >> 5, c = lane & 31;
   const int m0 = blockIdx.y * TM, n0 = blockIdx.x * TN;
-  const int prob = blockIdx.z / p.splits, z = blockIdx.z % p.splits;
+  int prob = blockIdx.z / p.splits, z = blockIdx.z % p.splits;
+  if (p.nprob > 1 && gridDim.x * gridDim.y == 1) {
+    // one output tile per problem (C <= 128): the problems of one token
+    // chunk go to the same XCD (workgroups are dealt to the 8 XCDs in turn),
+    // close together in time, so the X rows they share come from that
+    // XCD's L2 after the first read; z runs over the chunks rounded up to 8
+    const int L = blockIdx.z, xcd = L & 7, r = L >> 3;
+    prob = r % p.nprob;
+    z = (r / p.nprob) * 8 + xcd;
+    if (z >= p.splits) return;  // whole workgroup, before any barrier
+  }
   const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
   const int mw = wave >> 1, nw = wave & 1;
   f32x16 acc[MT][NT];
@@ -996,7 +1006,9 @@ int gemm_tile(int n) { return n >= 128 ? 128 : 64; }
 template <typename T>
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   const int tm = gemm_tile(p.M), tn = gemm_tile(p.N);
-  dim3 grid((p.N + tn - 1) / tn, (p.M + tm - 1) / tm, p.nprob * p.splits);
+  const bool one_tile = (p.N + tn - 1) / tn == 1 && (p.M + tm - 1) / tm == 1;
+  const int nz = p.nprob > 1 && one_tile ? p.nprob * ((p.splits + 7) / 8 * 8) : p.nprob * p.splits;
+  dim3 grid((p.N + tn - 1) / tn, (p.M + tm - 1) / tm, nz);
   if (tm == 128 && tn == 128) k_gemm<T, 128, 128><<<grid, 256, 0, s>>>(p);
   else if (tm == 128) k_gemm<T, 128, 64><<<grid, 256, 0, s>>>(p);
   else if (tn == 128) k_gemm<T, 64, 128><<<grid, 256, 0, s>>>(p);
