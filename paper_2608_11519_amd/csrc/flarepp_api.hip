@@ -625,6 +625,8 @@ int gemm_splits(int64_t T, int64_t C, int* kchunk) {
 struct BwdWs {
   void *wf[4], *seeds_op, *K, *Kt, *Vdm, *Vtdm, *Y, *q_op, *z_op;
   void *fwf[2], *fq_op;  // fused encodes: W_K (key order), W_V fragments; Q(X) in q fragment order
+  void *fwo, *fz_op;     // fused decode: W_O merge fragments, Z in z fragment order
+  float* fqnorm2;        // fused decode: route-norm bounds of Q(X)
   float *part_ml, *part_acc, *Qf, *Zf, *L1, *L2, *L3;
   float *dZf, *dQf, *c1, *c2, *l1, *l2, *pa, *pg, *pq, *gpart;
   void *dY, *dK, *dV, *dKt, *dVt;
@@ -650,10 +652,10 @@ bool bwd_lo_parts(int dtype) {
   return !(f && std::atoi(f) != 0);
 }
 
-// The backward's forward runs calls 1 and 2 on the fused encodes (which
-// project inside the routing kernel) when the fused path covers the shape;
-// K, V, K~, V~ are still materialised for the reverse pass, and call 3 stays
-// on the unfused decode, which writes Y and the per-token log-normaliser.
+// The backward's forward runs its three calls on the fused kernels (which
+// project inside the routing kernel) when the fused path covers the shape:
+// the decode also writes Y and the per-token log-normaliser; K, V, K~, V~
+// are still materialised for the reverse pass.
 bool bwd_fused_encodes(int dtype, const MixerPlan& pl) { return pl.fused && dtype == FLAREPP_BF16; }
 
 BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t M) {
@@ -680,6 +682,9 @@ BwdWs bwd_ws(void* base, int dtype, int64_t B, int64_t N, int64_t C, int64_t H, 
     w.fwf[0] = cv.take(bs * C * C);
     w.fwf[1] = cv.take(bs * C * C);
     w.fq_op = cv.take(bs * BH * Mp * D);
+    w.fwo = cv.take(bs * C * C);
+    w.fz_op = cv.take(bs * BH * flarepp::z_frag_elems_per_head((int)Mp, (int)D));
+    w.fqnorm2 = (float*)cv.take(f4 * BH * (Mp / 4));
   }
   w.part_ml = (float*)cv.take(f4 * Rp * BH * Mp * 2);
   w.part_acc = (float*)cv.take(f4 * Rp * BH * Mp * D);
@@ -776,15 +781,33 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   pp.wf[3] = w.wf[3]; pp.out[3] = w.Vtdm; pp.layout[3] = kHeadsDMajor;
   HIPTRY(launch_project<T>(pp, s));
   const MixerPlan pl = mixer_plan(dtype, B, N, C, H, M);
+  // call 3 on the unfused decode (route operands as rows of Q(X) scaled and
+  // Z d-major), which writes Y and the per-token log-normaliser
+  auto unfused_call3 = [&]() -> int {
+    RouteParams r3 = decode_params(B, H, N, M, D);
+    r3.ka = w.q_op; r3.ka_sb = rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
+    r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;
+    r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
+    r3.y = w.Y; r3.y_sb = N * C; r3.y_row = C; r3.lse2 = w.L3;
+    HIPTRY(launch_route<T>(r3, (int)D, true, s));
+    return FLAREPP_OK;
+  };
   if (bwd_fused_encodes(dtype, pl)) {
-    // calls 1 and 2 on the fused encodes, as in the forward; the combines
-    // also write the route operands of the unfused decode (rows of Q(X)
-    // scaled, Z d-major)
+    // calls 1 and 2 on the fused encodes, as in the forward.  Call 3 on the
+    // fused decode where it has the per-group stages (C <= 128; the first
+    // combine then also writes W_O's merge fragments): it writes Y and the
+    // per-token log-normaliser for the reverse pass, and O (the training
+    // forward's output; otherwise into dY's buffer, which the merge gradient
+    // overwrites).  At C = 256 the unfused decode is the faster one here (no
+    // projection or merge to repeat): the combines write its route operands.
+    const int dkind = decode_kind_for((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype));
+    const bool fdec = dkind != kDecodeStaged;
     PrepFusedParams fp{};
     fp.C = (int)C;
     fp.w[0] = Wk; fp.wf[0] = w.fwf[0]; fp.mode[0] = kFragKeyPerm;
     fp.w[1] = Wv; fp.wf[1] = w.fwf[1]; fp.mode[1] = kFragPlain;
-    fp.nw = 2;
+    fp.w[2] = Wo; fp.wf[2] = w.fwo; fp.mode[2] = dkind == kDecodeStaged ? kFragMerge : kFragMergeHg;
+    fp.nw = fdec ? 3 : 2;
     fp.seeds = seeds; fp.H = (int)H; fp.M = (int)M; fp.Mp = (int)Mp; fp.D = (int)D; fp.qscale = qscale;
     EncFusedParams ep{};
     ep.x = X; ep.wk_raw = Wkt; ep.wv_raw = Wvt; ep.seeds_raw = seeds;
@@ -796,15 +819,32 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
     CombineParams cp{};
     cp.part_ml = w.part_ml; cp.part_acc = w.part_acc; cp.BH = BH; cp.R = pl.nchunks;
     cp.M = (int)M; cp.Mp = (int)Mp; cp.D = (int)D; cp.qscale = qscale; cp.frag = 1;
-    cp.out32 = w.Qf; cp.lse = w.L1; cp.q_op = w.fq_op; cp.q_rows = w.q_op;
+    cp.out32 = w.Qf; cp.lse = w.L1; cp.q_op = w.fq_op;
+    cp.qnorm2 = fdec ? w.fqnorm2 : nullptr; cp.q_rows = fdec ? nullptr : w.q_op;
     cp.prep = fp; cp.prep_n = prep_fused_items(fp);
     HIPTRY(launch_combine_par<T>(cp, s));
     ep.wk_raw = ep.wv_raw = ep.seeds_raw = nullptr;
     ep.wkf = w.fwf[0]; ep.wvf = w.fwf[1]; ep.q_op = w.fq_op; ep.q_sb = H * Mp * D;
     HIPTRY(launch_encode_fused<T>(ep, (int)D, pl.waves, s));
-    cp.out32 = w.Zf; cp.lse = w.L2; cp.q_op = nullptr; cp.q_rows = nullptr; cp.z_rows = w.z_op;
+    cp.out32 = w.Zf; cp.lse = w.L2; cp.q_op = nullptr; cp.qnorm2 = nullptr; cp.q_rows = nullptr;
+    cp.z_op = fdec ? w.fz_op : nullptr; cp.z_rows = fdec ? nullptr : w.z_op;
     cp.prep_n = 0;
     HIPTRY(launch_combine_par<T>(cp, s));
+    if (!fdec) {
+      TRY(unfused_call3());
+    } else {
+    DecFusedParams dp{};
+    dp.x = X; dp.wkf = w.fwf[0]; dp.wof = w.fwo; dp.q_op = w.fq_op; dp.z_op = w.fz_op; dp.qnorm2 = w.fqnorm2;
+    dp.B = (int)B; dp.N = (int)N; dp.C = (int)C; dp.H = (int)H; dp.M = (int)M; dp.Mp = (int)Mp;
+    dp.fast_lim = fast_limit(); dp.y = w.Y; dp.lse2 = w.L3;
+    dp.o = mode == kBwdForward ? O : w.dY; dp.res = nullptr;
+    dp.stage_elems = decode_stage_elems((int)C, (int)D, (int)Mp);
+    dp.stage_bytes = (int)(dkind == kDecodePersist ? persist_stage_bytes((int)D, (int)Mp, (int)dtype_bytes(dtype))
+                                                   : dec2_stage_bytes((int)C, (int)D, (int)Mp, (int)dtype_bytes(dtype)));
+    dp.kind = dkind;
+    HIPTRY(launch_decode_fused<T>(dp, (int)D, s));
+    if (mode == kBwdForward) return ok();
+    }
   } else {
   RoutePrepParams sp{};
   sp.src = seeds; sp.src_bstride = 0; sp.B = 1; sp.H = (int)H; sp.M = (int)M; sp.Mp = (int)Mp;
@@ -828,15 +868,10 @@ int backward_impl(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int64_t
   CombineParams c2 = c1;
   c2.out32 = w.Zf; c2.lse = w.L2; c2.q_op = nullptr; c2.z_op = w.z_op;
   HIPTRY(launch_combine_par<T>(c2, s));
+  TRY(unfused_call3());
   }
-  RouteParams r3 = decode_params(B, H, N, M, D);
-  r3.ka = w.q_op; r3.ka_sb = rtBS; r3.ka_sh = rtHS; r3.ka_rows = (int)Mp;
-  r3.va = w.z_op; r3.va_sb = H * D * Mp; r3.va_sh = D * Mp; r3.va_ld = (int)Mp;
-  r3.qs = w.K; r3.qs_sb = tokBS; r3.qs_sh = tokHS; r3.qs_rows = (int)N;
-  r3.y = w.Y; r3.y_sb = N * C; r3.y_row = C; r3.lse2 = w.L3;
-  HIPTRY(launch_route<T>(r3, (int)D, true, s));
   }
-  if (mode == kBwdForward) {  // the training forward's output O = Y W_O
+  if (mode == kBwdForward) {  // the training forward's output O = Y W_O (the fused decode returned above)
     GemmParams go{};
     go.M = (int)NT; go.N = (int)C; go.K = (int)C; go.nseg = 1; go.nprob = 1; go.splits = 1;
     go.a[0] = w.Y; go.a_m = C; go.a_k = 1;

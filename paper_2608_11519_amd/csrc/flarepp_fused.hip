@@ -1070,12 +1070,16 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_fused(DecFu
 #pragma unroll
     for (int hh = 0; hh < HPG; ++hh) {
       const int h = hg * HPG + hh;
-      const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane));
+      const float den = softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane);
+      const float inv = __builtin_amdgcn_rcpf(den);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
           if (rb * 32 + 16 * hf < D) yf[KSC - GKS + hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
+      // log2 of the softmax normaliser over the routes (0 is the shift of the
+      // shift-free tiles), for the backward
+      if (p.lse2 && xok && g == 0) p.lse2[((int64_t)b * H + (h)) * p.N + xrow] = (fast ? 0.f : m[hh]) + __log2f(den);
       if (p.y && xok) {
         T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + h * D;
         constexpr int NQ4 = ONES_ROW ? 2 : 4;
@@ -1375,12 +1379,16 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode2(DecFusedPa
     F yg[KPG];
 #pragma unroll
     for (int hh = 0; hh < HPG; ++hh) {
-      const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane));
+      const float den = softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane);
+      const float inv = __builtin_amdgcn_rcpf(den);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
           if (rb * 32 + 16 * hf < D) yg[hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
+      // log2 of the softmax normaliser over the routes (0 is the shift of the
+      // shift-free tiles), for the backward
+      if (p.lse2 && xok && g == 0) p.lse2[((int64_t)b * p.H + (hg * HPG + hh)) * p.N + xrow] = (fast ? 0.f : m[hh]) + __log2f(den);
       if (p.y && xok) {
         T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + (hg * HPG + hh) * D;
         constexpr int NQ4 = ONES_ROW ? 2 : 4;
@@ -1692,12 +1700,16 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode3(DecFusedPa
       for (int j = 0; j < KPG; ++j) yall[u][j] = yall[u + 1][j];
 #pragma unroll
     for (int hh = 0; hh < HPG; ++hh) {
-      const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane));
+      const float den = softmax_denominator<RB, ONES_ROW>(acc[hh], ls[hh], lane);
+      const float inv = __builtin_amdgcn_rcpf(den);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
           if (rb * 32 + 16 * hf < D) yall[HG - 1][hh * KS + 2 * rb + hf] = cvt8<T>(acc[hh][rb], 8 * hf, inv);
+      // log2 of the softmax normaliser over the routes (0 is the shift of the
+      // shift-free tiles), for the backward
+      if (p.lse2 && xok && g == 0) p.lse2[((int64_t)b * p.H + (hg * HPG + hh)) * p.N + xrow] = (fast ? 0.f : m[hh]) + __log2f(den);
       if (p.y && xok) {
         T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + (hg * HPG + hh) * D;
         constexpr int NQ4 = ONES_ROW ? 2 : 4;
@@ -1909,12 +1921,16 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
         };
         if (fast) routes(std::true_type{});
         else routes(std::false_type{});
-        const float inv = __builtin_amdgcn_rcpf(softmax_denominator<RB, ONES_ROW>(acc, ls, lane));
+        const float den = softmax_denominator<RB, ONES_ROW>(acc, ls, lane);
+        const float inv = __builtin_amdgcn_rcpf(den);
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
           for (int hf = 0; hf < 2; ++hf)
             if (rb * 32 + 16 * hf < D) yf[KSC - GKS + hh * KS + 2 * rb + hf] = cvt8<T>(acc[rb], 8 * hf, inv);
+        // log2 of the softmax normaliser over the routes (0 is the shift of the
+        // shift-free tiles), for the backward
+        if (p.lse2 && xok && g == 0) p.lse2[((int64_t)b * H + (h)) * p.N + xrow] = (fast ? 0.f : m) + __log2f(den);
         if (p.y && xok) {
           T* yp = (T*)p.y + ((int64_t)b * p.N + xrow) * C + h * D;
           constexpr int NQ4 = ONES_ROW ? 2 : 4;

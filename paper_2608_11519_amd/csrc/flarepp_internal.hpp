@@ -164,6 +164,7 @@ struct DecFusedParams {
   int B, N, C, H, M, Mp;
   float fast_lim;
   void* y;            // [B][N][C] decoded tokens, or null
+  float* lse2;        // [B][H][N] log2 softmax normaliser of each token's scaled scores, or null
   void* o;            // [B][N][C]
   const void* res;    // [B][N][C] added to O (the block's residual), or null
   int stage_elems;    // elements per LDS stage buffer (k_decode_fused)
