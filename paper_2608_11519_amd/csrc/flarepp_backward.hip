@@ -520,6 +520,11 @@ __global__ __launch_bounds__(256, (sizeof(T) == 2 && D == 16) ? 2 : 1) void k_at
     asm volatile("" ::: "memory");  // the copies go out ahead of the tile's route-operand loads
   };
   if (stg) {
+    // zero the tile buffer first: rows past the long length hold zeros (or,
+    // after a full tile, that tile's finite rows) whatever the bounds-checked
+    // copies leave there, so no NaN of earlier LDS contents reaches a sum
+    for (int i = 8 * lane; i < TBE; i += 8 * 64) store_frag8(tb + i, zero_frag<T>());
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     stage_issue(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
