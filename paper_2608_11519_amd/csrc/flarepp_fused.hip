@@ -1163,8 +1163,12 @@ size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res) {
   return (res ? hg : 2) * dec2_stage_bytes(C, D, Mp, elem_bytes) + 16 * elem_bytes;
 }
 
-// LDS of k_decode_persist: [W_K fragments][W_O fragments][2 head stages]
-// [16 constant elements]; a head stage is [q][z].
+// LDS of k_decode_persist: [2 head stages][W_K fragments][W_O fragments]
+// [16 constant elements]; a head stage is [q][z].  The kernel declares the
+// whole 160 KB statically (one workgroup per CU in any case): a static array
+// has a known address, so the route loop's LDS addresses need no add of the
+// dynamic-LDS base, and the stages, first, are reached with the 16-bit
+// immediate offsets of the LDS reads.
 size_t persist_stage_bytes(int D, int Mp, int elem_bytes) {
   return (size_t)2 * Mp * D * elem_bytes;
 }
@@ -1177,7 +1181,7 @@ bool decode_kind_fits(int kind, int C, int D, int Mp, int elem_bytes) {
     case kDecodeGroupsResident: return C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, true) <= 160 * 1024;
     case kDecodeGroupsStaged: return C <= 128 && dec2_lds_bytes(C, D, Mp, elem_bytes, false) <= 160 * 1024;
     case kDecodePersist:
-      return elem_bytes == 2 && C <= 128 && (D == 16 || D == 32) && persist_lds_bytes(C, D, Mp, elem_bytes) <= 160 * 1024;
+      return elem_bytes == 2 && C <= 128 && (D == 16 || D == 32) && persist_lds_bytes(C, D, Mp, elem_bytes) <= kPersistLdsBytes;
     case kDecodeStaged: {
       const size_t se = (size_t)decode_stage_elems(C, D, Mp) * elem_bytes;
       return 2 * se + 16 * elem_bytes <= 160 * 1024;
@@ -1780,13 +1784,13 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
   constexpr int ZC = D < 32 ? D : 32;
   constexpr int GKS = HPG * KS;  // decoded-token fragments per head group
   static_assert(C <= 128 && GKS == KPG, "");
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ __attribute__((aligned(16))) char smem[kPersistLdsBytes];
   const int Mp = p.Mp, RT = Mp / 32, QE = Mp * D;
-  const int SB = p.stage_bytes;
-  T* wk_l = reinterpret_cast<T*>(smem);
+  const int SB = p.stage_bytes;  // the host keeps 2 SB + 2 C^2 + 16 elements within the array
+  char* stage0 = smem;
+  T* wk_l = reinterpret_cast<T*>(smem + 2 * SB);
   T* wo_l = wk_l + C * C;
-  char* stage0 = smem + (size_t)2 * C * C * sizeof(T);
-  T* cst = reinterpret_cast<T*>(stage0 + 2 * SB);  // 8 ones (row 16), 8 zeros
+  T* cst = wo_l + C * C;  // 8 ones (row 16), 8 zeros
 
   const int lane = lane_id(), g = lane >> 5, c = lane & 31, wave = wave_id();
   const int nblk = (p.N + TOK - 1) / TOK;
@@ -1795,7 +1799,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
   if (t >= total) return;  // whole workgroup, before any barrier
 
   // resident weights, the first head's stage and the first block's X
-  copy_to_lds(p.wkf, smem, C * C * (int)sizeof(T) / 16, 64 * NW);
+  copy_to_lds(p.wkf, reinterpret_cast<char*>(wk_l), C * C * (int)sizeof(T) / 16, 64 * NW);
   copy_to_lds(p.wof, reinterpret_cast<char*>(wo_l), C * C * (int)sizeof(T) / 16, 64 * NW);
   persist_stage_issue<T, D, KSC>(p, stage0, (t / nblk) * H);
   if (ONES_ROW && threadIdx.x < 2) store_frag<T>(cst + 8 * threadIdx.x, threadIdx.x == 0 ? fill_frag<T>(1.f) : zero_frag<T>());
@@ -2043,18 +2047,17 @@ static hipError_t dec_launch(const DecFusedParams& p, hipStream_t s) {
     constexpr int NW = dec_waves(16 * KSC);
     const unsigned grid = (unsigned)((int64_t)p.B * ((p.N + 32 * NW - 1) / (32 * NW)));
     if constexpr (sizeof(T) == 2 && (D == 16 || D == 32) && KSC <= 8) {
-      if (p.kind == kDecodePersist) {  // one persistent workgroup per CU
-        const size_t lds = persist_lds_bytes(16 * KSC, D, p.Mp, sizeof(T));
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_persist<T, D, KSC>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
+      if (p.kind == kDecodePersist) {  // one persistent workgroup per CU, static LDS
+        if (persist_lds_bytes(16 * KSC, D, p.Mp, sizeof(T)) > kPersistLdsBytes ||
+            p.stage_bytes != (int)persist_stage_bytes(D, p.Mp, sizeof(T)))
+          return hipErrorInvalidValue;
         int dev = 0, ncu = 0;
-        e = hipGetDevice(&dev);
+        hipError_t e = hipGetDevice(&dev);
         if (e != hipSuccess) return e;
         e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
         const unsigned pgrid = (unsigned)std::min<int64_t>((int64_t)grid, std::max(ncu, 1));
-        k_decode_persist<T, D, KSC><<<pgrid, 64 * NW, lds, s>>>(p);
+        k_decode_persist<T, D, KSC><<<pgrid, 64 * NW, 0, s>>>(p);
         return hipGetLastError();
       }
     }

@@ -197,6 +197,7 @@ int decode_kind(int C, int D, int Mp, int elem_bytes);
 bool decode_kind_fits(int kind, int C, int D, int Mp, int elem_bytes);
 size_t persist_stage_bytes(int D, int Mp, int elem_bytes);
 size_t persist_lds_bytes(int C, int D, int Mp, int elem_bytes);
+constexpr size_t kPersistLdsBytes = 160 * 1024;  // static LDS of k_decode_persist
 size_t dec2_stage_bytes(int C, int D, int Mp, int elem_bytes);
 size_t dec2_lds_bytes(int C, int D, int Mp, int elem_bytes, bool res);
 
