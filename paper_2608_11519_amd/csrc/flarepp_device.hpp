@@ -93,11 +93,16 @@ __device__ __forceinline__ typename Frag<T>::type join(typename Frag<T>::half a,
   for (int i = 0; i < 4; ++i) { r[i] = a[i]; r[4 + i] = b[i]; }
   return r;
 }
-// Sum of squares of one fragment's elements, in fp32.
+// Sum of squares of one fragment's elements, in fp32 (bf16: one packed dot
+// product per element pair; the squares of bf16 values are exact in fp32).
 __device__ __forceinline__ float sumsq(const bf16x8& f) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) { float x = (float)f[i]; s = __builtin_fmaf(x, x, s); }
+  for (int i = 0; i < 8; i += 2) {
+    const bf16x2 v = {f[i], f[i + 1]};
+    s = __builtin_amdgcn_fdot2_f32_bf16(v, v, s, false);
+  }
   return s;
 }
 __device__ __forceinline__ float sumsq(const f32x8& f) {
@@ -211,10 +216,10 @@ __device__ __forceinline__ float halves_max(float x) {
 // reduction runs on integers through DPP row operations and lane reads.
 __device__ __forceinline__ float halfmax_sum_nonneg(float x) {
   int v = __float_as_int(x);
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false)); // row_half_mirror
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false)); // row_mirror
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true));  // quad_perm [1,0,3,2]
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true));  // quad_perm [2,3,0,1]
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, true)); // row_half_mirror
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, true)); // row_mirror
   int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
   int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
   const float s = __int_as_float(max(r0, r1)) + __int_as_float(max(r2, r3));
@@ -224,10 +229,10 @@ __device__ __forceinline__ float halfmax_sum_nonneg(float x) {
 // Maximum of a non-negative float over the whole wave, wave-uniform.
 __device__ __forceinline__ float wave_max_nonneg(float x) {
   int v = __float_as_int(x);
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false)); // row_half_mirror
-  v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false)); // row_mirror
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true));  // quad_perm [1,0,3,2]
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true));  // quad_perm [2,3,0,1]
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, true)); // row_half_mirror
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, true)); // row_mirror
   const int r = max(max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
                     max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
   return __int_as_float(__builtin_amdgcn_readfirstlane(r));
