@@ -396,7 +396,6 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   // spread over the NT route tiles); after the last full super-tile of a
   // chunk without a tail that projection is of clamped rows and unused.
   constexpr int NT = W * NQW;
-  const bool all_slots = slot0 + NQW <= nslots;
   auto consume_v = [&](auto sf, auto mask, auto all, int it, int t0) __attribute__((always_inline)) {
     constexpr bool SF = decltype(sf)::value, MASK = decltype(mask)::value, ALL = decltype(all)::value;
     const int buf = it & 1;
@@ -638,9 +637,11 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
       }
     }
   };
+  // Every wave runs all NQW slots: a slot past the last query block holds a
+  // zero query (its tiles are wasted work, and its partial is never stored),
+  // and the waves of a workgroup meet at every super-tile anyway.
   auto consume = [&](auto sf, auto mask, int it, int t0) __attribute__((always_inline)) {
-    if (all_slots) consume_v(sf, mask, std::true_type{}, it, t0);
-    else consume_v(sf, mask, std::false_type{}, it, t0);
+    consume_v(sf, mask, std::true_type{}, it, t0);
   };
 
   // Full super-tiles: shift-free while every score of the super-tile is
@@ -650,7 +651,7 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
   const int nfull = (k1 - k0) / STEP;
   const bool tail = (k1 - k0) % STEP != 0;
   const int nst = nfull + (tail ? 1 : 0);
-  bool fast = true, used = false;
+  bool used = false;
   auto go_online = [&]() __attribute__((always_inline)) {
     if (!used) {
 #pragma unroll
@@ -658,23 +659,46 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
       used = true;
     }
   };
-  int t0 = k0;
-  for (int it = 0; it < nfull; ++it, t0 += STEP) {
-    if (fast) {
-      float kb = 0.f;
-      for (int j = 0; j < W * HPG; ++j) kb = fmaxf(kb, kmx[(it & 1) * W * HPG + j]);
-      fast = uniform(qmax2 * kb <= p.fast_lim);
-    }
-    if (fast) {
-      consume(std::true_type{}, std::false_type{}, it, t0);
-      used = true;
-    } else {
-      go_online();
-      consume(std::false_type{}, std::false_type{}, it, t0);
-    }
+  // The shift-free super-tiles run in a loop of their own, so that its body
+  // is a single path: with the shift-free and online bodies in one loop the
+  // register allocator placed the loop-carried X rows differently in each
+  // and copied them at every iteration, behind a wait for the X loads still
+  // in flight.
+  auto fast_at = [&](int it) __attribute__((always_inline)) {
+    float kb = 0.f;
+    for (int j = 0; j < W * HPG; ++j) kb = fmaxf(kb, kmx[(it & 1) * W * HPG + j]);
+    return uniform(qmax2 * kb <= p.fast_lim);
+  };
+  auto next_super_tile = [&](int it) __attribute__((always_inline)) {
     if (it + 1 < nst) {  // the next super-tile, projected during this one
       proj_store((it + 1) & 1);
       lds_barrier();
+    }
+  };
+  int t0 = k0, it = 0;
+  if constexpr (!(D == 32 && KSC == 16)) {
+    for (; it < nfull && fast_at(it); ++it, t0 += STEP) {
+      consume(std::true_type{}, std::false_type{}, it, t0);
+      used = true;
+      next_super_tile(it);
+    }
+    if (it < nfull) go_online();
+    for (; it < nfull; ++it, t0 += STEP) {
+      consume(std::false_type{}, std::false_type{}, it, t0);
+      next_super_tile(it);
+    }
+  } else {  // C = 256, D = 32: the two loops run out of registers; one loop
+    bool fast = true;
+    for (; it < nfull; ++it, t0 += STEP) {
+      if (fast) fast = fast_at(it);
+      if (fast) {
+        consume(std::true_type{}, std::false_type{}, it, t0);
+        used = true;
+      } else {
+        go_online();
+        consume(std::false_type{}, std::false_type{}, it, t0);
+      }
+      next_super_tile(it);
     }
   }
   if (tail) {
