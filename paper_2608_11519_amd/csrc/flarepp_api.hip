@@ -212,7 +212,7 @@ MixerPlan mixer_plan(int dtype, int64_t B, int64_t N, int64_t C, int64_t H, int6
              !(off && std::atoi(off) != 0);
   pl.enc = encode_plan(B, H, N, Mp, D);
   if (pl.fused) {
-    pl.nqw = (int)std::min<int64_t>(flarepp::enc_nqw_cap((int)D, pl.waves), next_pow2(cdiv(slots, pl.waves)));
+    pl.nqw = (int)std::min<int64_t>(flarepp::enc_nqw_cap((int)D, pl.waves, (int)bs), next_pow2(cdiv(slots, pl.waves)));
     // every wave's query slots must belong to one head of the group
     while (hpg > 1 && (Mp / 32) % pl.nqw != 0) pl.nqw /= 2;
     pl.qgroups = (int)cdiv(slots, (int64_t)pl.waves * pl.nqw);

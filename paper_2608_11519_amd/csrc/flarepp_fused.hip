@@ -1999,7 +1999,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
 // ---------------------------------------------------------------------------
 template <typename T, int D, int KSC, int NQW, int W>
 static hipError_t enc_one(const EncFusedParams& p, hipStream_t s) {
-  if constexpr (NQW > enc_nqw_cap(D, W) || (W == 8 && !((D == 16 && KSC <= 8) || (D == 32 && KSC == 16))) ||
+  if constexpr (NQW > enc_nqw_cap(D, W, (int)sizeof(T)) || (W == 8 && !((D == 16 && KSC <= 8) || (D == 32 && KSC == 16))) ||
                 !fused_width_ok(16 * KSC, sizeof(T))) {
     return hipErrorInvalidValue;
   } else {

@@ -174,12 +174,17 @@ struct DecFusedParams {
 
 // Fused path coverage.  bf16: C in {64, 128, 256}; fp32 (a correctness path):
 // C = 64.  Query blocks per wave of the fused encode: a power of two up to
-// enc_nqw_cap; waves per encode workgroup: enc_waves (eight, two per SIMD,
-// where the registers allow it with at least eight query slots).
+// enc_nqw_cap (bf16 at D = 16: four, so that one eight-wave workgroup holds
+// all 32 query slots of a head group at M = 512 and the K, V of a token chunk
+// are projected once instead of once per query group); waves per encode
+// workgroup: enc_waves (eight, two per SIMD, where the registers allow it
+// with at least eight query slots).
 constexpr bool fused_width_ok(int C, int elem_bytes) {
   return elem_bytes == 2 ? (C == 64 || C == 128 || C == 256) : C == 64;
 }
-constexpr int enc_nqw_cap(int D, int waves) { return D == 16 ? (waves == 8 ? 2 : 4) : (D == 32 ? 2 : 1); }
+constexpr int enc_nqw_cap(int D, int waves, int elem_bytes) {
+  return D == 16 ? (waves == 8 && elem_bytes == 4 ? 2 : 4) : (D == 32 ? 2 : 1);
+}
 constexpr int enc_waves(int D, int C, int slots) {
   return ((D == 16 && C <= 128) || (D == 32 && C == 256)) && slots >= 8 ? 8 : 4;
 }

@@ -199,7 +199,7 @@ def _assert_fused(w):
 @pytest.mark.parametrize("seed_scale,kind", [(1.0, None), (8.0, None), (8.0, 0)])
 def test_m512_c128_full_comparison(monkeypatch, seed_scale, kind):
     """The 2^20-token workload's shape (C=128, H=8, M=512) at N=65536, compared
-    element by element on every stage: the same fused encode instance (two
+    element by element on every stage: the same fused encode instance (four
     query blocks per wave) and decode as at 2^20 tokens (the persistent one),
     at the workload's seeds and with sharp ones (seeds x8); and the
     output-block-staged decode (kind 0) at this shape."""
@@ -208,6 +208,22 @@ def test_m512_c128_full_comparison(monkeypatch, seed_scale, kind):
     w = inp.Workload("m512", 1, 65536, 128, 8, 512, "bf16", "normal")
     _assert_fused(w)
     _check_mixer(w, inp.make_inputs(w, 30, seed_scale=seed_scale), f"m512-seeds{seed_scale:g}-kind{kind}")
+
+
+# Four query blocks per wave of the D = 16 encode (bf16, M > 256): C = 64 and
+# C = 128, token tails, and M = 384, where the last two waves of the workgroup
+# hold only slots past the last query block (zero queries, partials unstored).
+@pytest.mark.parametrize("B,N,C,H,M,variant", [
+    (1, 3001, 128, 8, 384, "sharp"),
+    (2, 1000, 64, 4, 512, "sharp"),
+    (1, 2999, 128, 8, 512, "nofast"),
+])
+def test_encode_four_query_blocks(monkeypatch, B, N, C, H, M, variant):
+    if variant == "nofast":
+        monkeypatch.setenv("FLAREPP_NO_FAST_PATH", "1")
+    w = inp.Workload("nqw4", B, N, C, H, M, "bf16", "normal")
+    _assert_fused(w)
+    _check_mixer(w, inp.make_inputs(w, 37, seed_scale=6.0), f"nqw4-{C}-{M}-{variant}")
 
 
 # The persistent decode (W_K and W_O resident, one head's route operands per
