@@ -390,14 +390,16 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
 
   // Run the wave's query slots over every sub-tile of the super-tile at t0
   // (LDS buffer it & 1): shift-free (SF) or with the online maximum; MASK
-  // only for the last, partial super-tile of a chunk; ALL when every slot of
-  // the wave is a real one (no per-slot branch inside the tile sequence).
-  // Unmasked runs also project the super-tile after this one (the k-steps
-  // spread over the NT route tiles); after the last full super-tile of a
-  // chunk without a tail that projection is of clamped rows and unused.
+  // only for the last, partial super-tile of a chunk.  Every wave runs all
+  // NQW slots: a slot past the last query block holds a zero query (its
+  // tiles are wasted work, its partial is never stored), and the waves of a
+  // workgroup meet at every super-tile anyway, so no tile sequence branches
+  // per slot.  Unmasked runs also project the super-tile after this one (the
+  // k-steps spread over the NT route tiles); after the last full super-tile
+  // of a chunk without a tail that projection is of clamped rows and unused.
   constexpr int NT = W * NQW;
-  auto consume_v = [&](auto sf, auto mask, auto all, int it, int t0) __attribute__((always_inline)) {
-    constexpr bool SF = decltype(sf)::value, MASK = decltype(mask)::value, ALL = decltype(all)::value;
+  auto consume = [&](auto sf, auto mask, int it, int t0) __attribute__((always_inline)) {
+    constexpr bool SF = decltype(sf)::value, MASK = decltype(mask)::value;
     const int buf = it & 1;
     if (!MASK) proj_zero();
     auto hooks = [&](int n) __attribute__((always_inline)) {
@@ -406,7 +408,7 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
         for (int ks = n * KSC / NT; ks < (n + 1) * KSC / NT; ++ks) proj_step(ks, t0 + 2 * STEP);
       }
     };
-    if constexpr (ALL && !MASK && SF) {
+    if constexpr (!MASK && SF) {
       // Shift-free tiles n = j * NQW + i (sub-tile j, slot i), software
       // pipelined so that every MFMA is issued between groups of
       // exponentials whose inputs are long ready (a wave issues in order: an
@@ -564,7 +566,7 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
       }
       return;
     }
-    if constexpr (ALL && !MASK) {
+    if constexpr (!MASK) {
       // Tiles n = j * NQW + i (sub-tile j, slot i); the score MFMA of tile
       // n + 1 is issued before the softmax of tile n, so its latency (and any
       // wait for the matrix pipe) is hidden behind the exponentials.
@@ -624,7 +626,7 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
           vf[hf][rb] = load_frag(tl + (KFR + (hh * RB + rb) * 2 + hf) * kFrag + lane * 8);
 #pragma unroll
       for (int i = 0; i < NQW; ++i) {
-        if (ALL || slot0 + i < nslots) {
+        {
           f32x16 sc;
 #pragma unroll
           for (int e = 0; e < 16; ++e) sc[e] = 0.f;
@@ -636,12 +638,6 @@ __global__ __launch_bounds__(64 * W) void k_encode_fused(EncFusedParams p) {
         hooks(j * NQW + i);
       }
     }
-  };
-  // Every wave runs all NQW slots: a slot past the last query block holds a
-  // zero query (its tiles are wasted work, and its partial is never stored),
-  // and the waves of a workgroup meet at every super-tile anyway.
-  auto consume = [&](auto sf, auto mask, int it, int t0) __attribute__((always_inline)) {
-    consume_v(sf, mask, std::true_type{}, it, t0);
   };
 
   // Full super-tiles: shift-free while every score of the super-tile is
