@@ -1806,7 +1806,7 @@ __global__ __launch_bounds__(64 * dec_waves(16 * KSC)) void k_decode_persist(Dec
   static_assert(C <= 128 && GKS == KPG, "");
   __shared__ __attribute__((aligned(16))) char smem[kPersistLdsBytes];
   const int Mp = p.Mp, RT = Mp / 32, QE = Mp * D;
-  const int SB = p.stage_bytes;  // the host keeps 2 SB + 2 C^2 + 16 elements within the array
+  const int SB = p.stage_bytes;  // the host keeps 2 SB bytes + (2 C^2 + 16) elements within the array
   char* stage0 = smem;
   T* wk_l = reinterpret_cast<T*>(smem + 2 * SB);
   T* wo_l = wk_l + C * C;
